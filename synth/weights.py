@@ -1,0 +1,50 @@
+"""Seeded random-init weights for the probability model.
+
+Layout (fp32, row-major, shared by every consumer):
+  conv_w[l]  [27][C_in][C_out]   offset k = (dx+1) + 3(dy+1) + 9(dz+1)
+  conv_b[l]  [C_out]
+  head_w     [C][256]
+  head_b     [256]
+with C_in = 11 for the first layer and C for the rest.  Kaiming-normal:
+std = sqrt(2 / fan_in), fan_in = 27 * C_in for a conv and C for the head.
+Biases are zero unless ``bias_std`` is given (tests use non-zero biases so
+that the bias path is exercised).
+"""
+from __future__ import annotations
+
+import numpy as np
+
+from . import rng
+
+IN_FEATURES = 11
+SYMBOLS = 256
+KVOL = 27
+_W_STREAM = 21
+
+
+def gen_weights(channels: int, layers: int, seed: int = 2, bias_std: float = 0.0,
+                head_scale: float = 1.0, in_features: int = IN_FEATURES) -> dict:
+    draw = [0]
+
+    def normals(n):
+        out = rng.normal(seed, _W_STREAM, draw[0], n)
+        draw[0] += n
+        return out
+
+    conv_w, conv_b = [], []
+    c_in = in_features
+    for _ in range(layers):
+        fan_in = KVOL * c_in
+        w = normals(KVOL * c_in * channels) * np.sqrt(2.0 / fan_in)
+        conv_w.append(w.reshape(KVOL, c_in, channels).astype(np.float32))
+        b = normals(channels) * bias_std
+        conv_b.append(b.astype(np.float32))
+        c_in = channels
+    hw = normals(channels * SYMBOLS) * np.sqrt(2.0 / channels) * head_scale
+    hb = normals(SYMBOLS) * bias_std * head_scale
+    return {
+        "c_in": in_features, "channels": channels, "layers": layers,
+        "conv_w": conv_w, "conv_b": conv_b,
+        "head_w": hw.reshape(channels, SYMBOLS).astype(np.float32),
+        "head_b": hb.astype(np.float32),
+    }
