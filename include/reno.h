@@ -1,0 +1,186 @@
+/*
+ * reno.h - C ABI of the MI355X (gfx950) hot path of the RENO LiDAR geometry
+ * codec (You et al., "RENO: Real-Time Neural Compression for 3D LiDAR Point
+ * Clouds", CVPR 2025).
+ *
+ * The library turns one LiDAR frame into a multiscale sparse tensor
+ * (Sec. 3, Eq. 1), derives the 8-bit occupancy code of every voxel (FOG,
+ * Sec. 3.1), evaluates the target occupancy predictor on the occupied voxels
+ * of each scale (TOP, Sec. 3.2, Eq. 5) to a 256-way distribution and an ideal
+ * code length (Eq. 4), and on the decoder side expands codes into the next
+ * scale (FCG, Sec. 3.1).  Arithmetic coding stays on the host; a host rANS
+ * coder is exported for round-trip validation.
+ *
+ * Conventions (apply to every call unless stated otherwise):
+ *  - Scales are bit depths.  A frame has scales b0 .. B (b0 = min_bit_depth,
+ *    B = the frame's bit depth); scale b has N_b voxels V_b on a 2^b grid.
+ *    Codes O_b exist for b0 <= b < B.  The model scales are b0 < b < B
+ *    (Eq. 3 conditions O^d on scale d-1 for d = 1 .. D-1; the initial state
+ *    (C^0, O^0) is coded raw).
+ *  - Voxel order inside a scale is ascending Morton key
+ *    key(x,y,z) = sum_i x_i 2^(3i) + y_i 2^(3i+1) + z_i 2^(3i+2), so that the
+ *    children of v are 8*key(v) + delta with delta = dx + 2dy + 4dz (Eq. 8)
+ *    and the sorted finer scale equals the FCG expansion order.
+ *  - Array arguments are DEVICE pointers (hipMalloc or torch memory) unless
+ *    the name ends in _host.  The caller owns them and keeps them alive until
+ *    the context stream has passed the call.
+ *  - Every call enqueues on the context's HIP stream and returns without
+ *    waiting, except calls that write a _host value, which synchronise.
+ *  - Sizes produced on the device (N_b) stay on the device; output buffers
+ *    must hold the capacity stated for each call.
+ *  - Errors are returned as reno_status, never thrown or aborted; the message
+ *    is available from reno_last_error.  Data errors found by kernels
+ *    (non-finite point, zero code, capacity overflow, ...) are latched on the
+ *    device and reported by the next synchronising call (RENO_E_INPUT or
+ *    RENO_E_CAPACITY); the frame's outputs are then undefined.
+ *  - One context per stream; contexts are independent and may run
+ *    concurrently on different streams.  A context is not thread-safe.
+ */
+#ifndef RENO_H
+#define RENO_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef struct reno_ctx reno_ctx;
+
+typedef enum {
+  RENO_OK = 0,
+  RENO_E_INVALID = -1,  /* bad argument (null pointer, out-of-range scale or size) */
+  RENO_E_STATE = -2,    /* call out of order (e.g. predict before the scale exists) */
+  RENO_E_NOMEM = -3,    /* device allocation failed at create time */
+  RENO_E_HIP = -4,      /* a HIP runtime call failed */
+  RENO_E_CAPACITY = -5, /* a frame exceeded the capacities given at create time */
+  RENO_E_INPUT = -6     /* bad data found on the device (non-finite point, zero
+                           code, unsorted or duplicate base voxels) */
+} reno_status;
+
+#define RENO_MAX_LAYERS 8
+#define RENO_SYMBOLS 256
+#define RENO_KVOL 27
+#define RENO_IN_FEATURES 11
+#define RENO_MAX_BIT_DEPTH 21
+#define RENO_ALL_SCALES (-1)
+
+/* Capacities and model shape, fixed for the life of a context. */
+typedef struct {
+  int64_t max_points;        /* raw points per frame; also the per-scale voxel capacity */
+  int64_t max_model_voxels;  /* sum of N_b over the model scales; 0 selects 3*max_points */
+  int max_bit_depth;         /* largest B accepted, <= RENO_MAX_BIT_DEPTH (keys use 3B bits) */
+  int min_bit_depth;         /* b0, the coarsest scale, 0 <= b0 < B */
+  double range_m;            /* R: the grid covers [-R, R) on each axis */
+  int in_features;           /* must be RENO_IN_FEATURES */
+  int channels;              /* C: 16 or 32 */
+  int layers;                /* L: 1 .. RENO_MAX_LAYERS sparse conv layers */
+} reno_params;
+
+/* Model weights (fp32, device memory, row-major).  Layout:
+ *   conv_w[l]  [27][C_in][C]   C_in = 11 for l = 0, C otherwise;
+ *              offset k = (dx+1) + 3(dy+1) + 9(dz+1)
+ *   conv_b[l]  [C]
+ *   head_w     [C][256]
+ *   head_b     [256]                                                        */
+typedef struct {
+  const float* conv_w[RENO_MAX_LAYERS];
+  const float* conv_b[RENO_MAX_LAYERS];
+  const float* head_w;
+  const float* head_b;
+} reno_weights;
+
+/* Creates a context on the current HIP device that enqueues on `hip_stream`
+ * (a hipStream_t; NULL = the null stream).  Allocates every device buffer
+ * the context needs for the given capacities; no later call allocates. */
+reno_status reno_create(const reno_params* params, void* hip_stream, reno_ctx** out);
+reno_status reno_destroy(reno_ctx* ctx);
+/* Message of the last failed call on this context ("" if none).  With a NULL
+ * context, the message of the last failed reno_create on this thread. */
+const char* reno_last_error(const reno_ctx* ctx);
+/* Waits for the context stream and reports latched device errors. */
+reno_status reno_sync(reno_ctx* ctx);
+
+/* Copies the model weights into the context's operand layout (Sec. 3.2:
+ * one parameter set shared by all scales).  Must precede predict_probs. */
+reno_status reno_set_weights(reno_ctx* ctx, const reno_weights* w);
+
+/* ENCODER (Sec. 3, Eq. 1; Sec. 3.1 FOG).  points: fp32 xyz [n][3].
+ * Quantises each coordinate to the 2^bit_depth grid over [-R, R)
+ * (u = ((p + R) * 2^B) / (2R) in fp64, floor, clamp to [0, 2^B - 1]),
+ * removes duplicates, builds V_b for b = b0 .. B, the codes O_b for
+ * b0 <= b < B (bit delta of O_b[v] set iff child 2v + delta is occupied) and
+ * the parent links.  n may be 0.  Requires b0 < bit_depth <= max_bit_depth
+ * and n <= max_points. */
+reno_status reno_build_pyramid(reno_ctx* ctx, const float* points, int64_t n, int bit_depth);
+
+/* DECODER start (Eq. 2: the initial state (C^0, O^0)).  Sets scale b0 of a
+ * frame of bit depth `bit_depth` to the n voxels xyz int32 [n][3] (strictly
+ * ascending Morton order, coordinates in [0, 2^b0)) with codes [n] (1..255). */
+reno_status reno_set_base(reno_ctx* ctx, int bit_depth, const int32_t* xyz, const uint8_t* codes,
+                          int64_t n);
+
+/* DECODER step (Sec. 3.1 FCG).  Records O_scale := codes[N_scale] (codes may
+ * be NULL when O_scale is already known: set_base, or an encoder context)
+ * and builds V_{scale+1} by keeping, for each voxel in order, the children
+ * whose code bit is set, in ascending delta.  b0 <= scale < B. */
+reno_status reno_expand(reno_ctx* ctx, int scale, const uint8_t* codes);
+
+/* Number of voxels of a scale (synchronises). */
+reno_status reno_num_voxels(reno_ctx* ctx, int scale, int64_t* n_host);
+/* Voxels of a scale: xyz int32 [N][3] and/or Morton keys uint64 [N] (either may be NULL). */
+reno_status reno_coords(reno_ctx* ctx, int scale, int32_t* xyz, uint64_t* keys);
+/* Occupancy codes O_scale uint8 [N_scale], b0 <= scale < B (Eq. 1). */
+reno_status reno_occupancy_codes(reno_ctx* ctx, int scale, uint8_t* codes);
+/* Row of each voxel's parent in scale-1, int32 [N_scale] (-1 at b0). */
+reno_status reno_parent_rows(reno_ctx* ctx, int scale, int32_t* parent);
+
+/* TOP (Sec. 3.2, Eq. 5, in the configured form): on the voxels of `scale`
+ * (b0 < scale < B), input features [delta bits 0..2, bits 0..7 of the parent's
+ * code] (target embedding, Eqs. 7-8), L submanifold 3x3x3 sparse conv + ReLU
+ * layers on the target coordinates (Eq. 9), a linear head to 256 logits and
+ * the softmax normaliser (Eq. 10; 256 classes indexed by code value).
+ * Needs V_scale and O_{scale-1}; does NOT need O_scale, so a decoder calls it
+ * before the codes of the scale are known.  RENO_ALL_SCALES runs every model
+ * scale in one batch (all scales must exist).  logits: optional fp32
+ * [N_scale][256] (for RENO_ALL_SCALES, the scales concatenated in increasing
+ * order).  weights: NULL uses the weights of the last reno_set_weights;
+ * otherwise they are set first. */
+reno_status reno_predict_probs(reno_ctx* ctx, int scale, const reno_weights* weights, float* logits);
+
+/* Ideal code length (Eq. 4): for a model scale, bits_v = -log2 p(O_scale[v])
+ * under the distribution of the last predict_probs of that scale; for
+ * scale == b0 the raw cost of the initial state, 32 + N_b0 * (3*b0 + 8) bits.
+ * bits_per_voxel: optional fp32 [N_scale] (NULL for b0).  total_host:
+ * optional, synchronises; the sum in double.  RENO_ALL_SCALES: the whole
+ * frame (base + every model scale); bits_per_voxel then holds the model
+ * scales concatenated. */
+reno_status reno_code_length(reno_ctx* ctx, int scale, float* bits_per_voxel, double* total_host);
+
+/* Neighbour map of a model scale, int32 [N_scale][27]: entry k is the row in
+ * V_scale of v + (dx,dy,dz), k = (dx+1) + 3(dy+1) + 9(dz+1), or -1 when absent
+ * or outside [0, 2^scale)^3.  Available after predict_probs of that scale. */
+reno_status reno_neighbor_map(reno_ctx* ctx, int scale, int32_t* map);
+
+/* Quantised distribution for the host coder, uint16 [N_scale][256]:
+ * f_s = 1 + floor(p_s * 65024) with p_s = exp(z_s - lse) in fp32, and the
+ * 65536 - sum leftover added to the lowest-index largest f_s (so sum f = 2^16).
+ * Deterministic: an encoder and a decoder context that computed the same
+ * distribution produce identical tables. */
+reno_status reno_symbol_freqs(reno_ctx* ctx, int scale, uint16_t* freq);
+
+/* Host rANS coder (Duda, arXiv:1311.2540) for one scale's stream; HOST
+ * pointers.  64-bit state in [2^31, 2^63), 32-bit renormalisation words.
+ * encode: symbols sym[n], frequency tables freq [n][256] (sum 2^16); writes at
+ * most cap words to out and their count to *nwords_host.  decode: the
+ * inverse; fails with RENO_E_INPUT on a corrupt or truncated stream. */
+reno_status reno_rans_encode(const uint8_t* sym, const uint16_t* freq, int64_t n, uint32_t* out,
+                             int64_t cap, int64_t* nwords_host);
+reno_status reno_rans_decode(const uint32_t* in, int64_t nwords, const uint16_t* freq, int64_t n,
+                             uint8_t* sym);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* RENO_H */

@@ -1,0 +1,281 @@
+"""MI355X (gfx950) hot path of the RENO LiDAR geometry codec.
+
+Thin ctypes binding over the C ABI of libreno.so (declared in include/reno.h):
+argument marshalling only.  Device memory and streams come from PyTorch; every
+step of the codec runs in the library's HIP kernels.  Importing works without
+a GPU; creating a context needs one, and the library must have been built
+(``python -m paper_2503_12382_amd.build``) -- there is no fallback path.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libreno.so")
+
+RENO_OK = 0
+RENO_E_INVALID = -1
+RENO_E_STATE = -2
+RENO_E_NOMEM = -3
+RENO_E_HIP = -4
+RENO_E_CAPACITY = -5
+RENO_E_INPUT = -6
+RENO_MAX_LAYERS = 8
+RENO_ALL_SCALES = -1
+SYMBOLS = 256
+
+_STATUS = {0: "RENO_OK", -1: "RENO_E_INVALID", -2: "RENO_E_STATE", -3: "RENO_E_NOMEM",
+           -4: "RENO_E_HIP", -5: "RENO_E_CAPACITY", -6: "RENO_E_INPUT"}
+
+
+class RenoError(RuntimeError):
+    def __init__(self, status: int, msg: str):
+        super().__init__(f"{_STATUS.get(status, status)}: {msg}")
+        self.status = status
+
+
+class reno_params(ctypes.Structure):
+    _fields_ = [("max_points", ctypes.c_int64), ("max_model_voxels", ctypes.c_int64),
+                ("max_bit_depth", ctypes.c_int), ("min_bit_depth", ctypes.c_int),
+                ("range_m", ctypes.c_double), ("in_features", ctypes.c_int),
+                ("channels", ctypes.c_int), ("layers", ctypes.c_int)]
+
+
+class reno_weights(ctypes.Structure):
+    _fields_ = [("conv_w", ctypes.c_void_p * RENO_MAX_LAYERS),
+                ("conv_b", ctypes.c_void_p * RENO_MAX_LAYERS),
+                ("head_w", ctypes.c_void_p), ("head_b", ctypes.c_void_p)]
+
+
+# exported symbol -> (restype, argtypes); exactly the functions of include/reno.h
+_vp, _i64, _int = ctypes.c_void_p, ctypes.c_int64, ctypes.c_int
+_SIGS = {
+    "reno_create": (_int, [ctypes.POINTER(reno_params), _vp, ctypes.POINTER(_vp)]),
+    "reno_destroy": (_int, [_vp]),
+    "reno_last_error": (ctypes.c_char_p, [_vp]),
+    "reno_sync": (_int, [_vp]),
+    "reno_set_weights": (_int, [_vp, ctypes.POINTER(reno_weights)]),
+    "reno_build_pyramid": (_int, [_vp, _vp, _i64, _int]),
+    "reno_set_base": (_int, [_vp, _int, _vp, _vp, _i64]),
+    "reno_expand": (_int, [_vp, _int, _vp]),
+    "reno_num_voxels": (_int, [_vp, _int, ctypes.POINTER(_i64)]),
+    "reno_coords": (_int, [_vp, _int, _vp, _vp]),
+    "reno_occupancy_codes": (_int, [_vp, _int, _vp]),
+    "reno_parent_rows": (_int, [_vp, _int, _vp]),
+    "reno_predict_probs": (_int, [_vp, _int, ctypes.POINTER(reno_weights), _vp]),
+    "reno_code_length": (_int, [_vp, _int, _vp, ctypes.POINTER(ctypes.c_double)]),
+    "reno_neighbor_map": (_int, [_vp, _int, _vp]),
+    "reno_symbol_freqs": (_int, [_vp, _int, _vp]),
+    "reno_rans_encode": (_int, [_vp, _vp, _i64, _vp, _i64, ctypes.POINTER(_i64)]),
+    "reno_rans_decode": (_int, [_vp, _i64, _vp, _i64, _vp]),
+}
+
+_lib = None
+
+
+def lib():
+    """The loaded C library; raises if it has not been built."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise RuntimeError(f"{LIB_PATH} is missing: build it with "
+                               "`python -m paper_2503_12382_amd.build` (no CPU fallback exists)")
+        L = ctypes.CDLL(LIB_PATH)
+        for name, (res, args) in _SIGS.items():
+            f = getattr(L, name)
+            f.restype = res
+            f.argtypes = args
+        _lib = L
+    return _lib
+
+
+def _ptr(t):
+    return None if t is None else ctypes.c_void_p(t.data_ptr())
+
+
+class Context:
+    """One codec context (reno_ctx) bound to a torch device and stream."""
+
+    def __init__(self, max_points: int, max_bit_depth: int, min_bit_depth: int, range_m: float,
+                 channels: int, layers: int, max_model_voxels: int = 0, stream=None):
+        import torch
+        self.torch = torch
+        self.device = torch.device("cuda", torch.cuda.current_device())
+        self.stream = stream if stream is not None else torch.cuda.current_stream()
+        p = reno_params(max_points, max_model_voxels, max_bit_depth, min_bit_depth, range_m, 11,
+                        channels, layers)
+        h = ctypes.c_void_p()
+        rc = lib().reno_create(ctypes.byref(p), ctypes.c_void_p(self.stream.cuda_stream),
+                               ctypes.byref(h))
+        if rc != RENO_OK:
+            raise RenoError(rc, lib().reno_last_error(None).decode())
+        self._h = h
+        self.params = p
+        self.b0 = min_bit_depth
+        self.channels = channels
+        self.layers = layers
+        self.B = 0
+        self._keep = []
+
+    def close(self):
+        if getattr(self, "_h", None):
+            lib().reno_destroy(self._h)
+            self._h = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+    def _check(self, rc):
+        if rc != RENO_OK:
+            raise RenoError(rc, lib().reno_last_error(self._h).decode())
+
+    def _empty(self, shape, dtype):
+        return self.torch.empty(shape, dtype=dtype, device=self.device)
+
+    # ---- C ABI calls -------------------------------------------------------------------------
+    def sync(self):
+        self._check(lib().reno_sync(self._h))
+
+    def set_weights(self, weights: dict):
+        """weights: dict of fp32 device tensors conv_w[l], conv_b[l], head_w, head_b."""
+        w = reno_weights()
+        keep = []
+        for l in range(self.layers):
+            cw = weights["conv_w"][l].contiguous()
+            cb = weights["conv_b"][l].contiguous()
+            keep += [cw, cb]
+            w.conv_w[l] = cw.data_ptr()
+            w.conv_b[l] = cb.data_ptr()
+        hw = weights["head_w"].contiguous()
+        hb = weights["head_b"].contiguous()
+        keep += [hw, hb]
+        w.head_w = hw.data_ptr()
+        w.head_b = hb.data_ptr()
+        self._check(lib().reno_set_weights(self._h, ctypes.byref(w)))
+        self._keep = keep        # alive until the next set_weights (stream-ordered)
+
+    def build_pyramid(self, points, bit_depth: int):
+        n = int(points.shape[0])
+        pts = points.contiguous()
+        self._check(lib().reno_build_pyramid(self._h, _ptr(pts) if n else None, n, bit_depth))
+        self._points = pts
+        self.B = bit_depth
+
+    def set_base(self, bit_depth: int, xyz, codes):
+        n = int(xyz.shape[0])
+        x = xyz.contiguous()
+        c = codes.contiguous()
+        self._check(lib().reno_set_base(self._h, bit_depth, _ptr(x) if n else None,
+                                        _ptr(c) if n else None, n))
+        self._base = (x, c)
+        self.B = bit_depth
+
+    def expand(self, scale: int, codes=None):
+        c = codes.contiguous() if codes is not None else None
+        self._check(lib().reno_expand(self._h, scale, _ptr(c)))
+        if c is not None:
+            self._last_codes = c
+
+    def num_voxels(self, scale: int) -> int:
+        n = ctypes.c_int64()
+        self._check(lib().reno_num_voxels(self._h, scale, ctypes.byref(n)))
+        return n.value
+
+    def coords(self, scale: int):
+        n = self.num_voxels(scale)
+        xyz = self._empty((max(n, 1), 3), self.torch.int32)
+        keys = self._empty((max(n, 1),), self.torch.int64)
+        self._check(lib().reno_coords(self._h, scale, _ptr(xyz), _ptr(keys)))
+        return xyz[:n], keys[:n]
+
+    def occupancy_codes(self, scale: int):
+        n = self.num_voxels(scale)
+        out = self._empty((max(n, 1),), self.torch.uint8)
+        self._check(lib().reno_occupancy_codes(self._h, scale, _ptr(out)))
+        return out[:n]
+
+    def parent_rows(self, scale: int):
+        n = self.num_voxels(scale)
+        out = self._empty((max(n, 1),), self.torch.int32)
+        self._check(lib().reno_parent_rows(self._h, scale, _ptr(out)))
+        return out[:n]
+
+    def predict_probs(self, scale: int, weights: dict | None = None, logits: bool = False):
+        if weights is not None:
+            self.set_weights(weights)
+        out = None
+        if logits:
+            if scale == RENO_ALL_SCALES:
+                n = sum(self.num_voxels(b) for b in range(self.b0 + 1, self.B))
+            else:
+                n = self.num_voxels(scale)
+            out = self._empty((max(n, 1), SYMBOLS), self.torch.float32)
+        self._check(lib().reno_predict_probs(self._h, scale, None, _ptr(out)))
+        if logits:
+            return out[:n]
+        return None
+
+    def code_length(self, scale: int, per_voxel: bool = True, total: bool = True):
+        out = None
+        if per_voxel:
+            if scale == RENO_ALL_SCALES:
+                n = sum(self.num_voxels(b) for b in range(self.b0 + 1, self.B))
+            else:
+                n = self.num_voxels(scale)
+            out = self._empty((max(n, 1),), self.torch.float32)
+        tot = ctypes.c_double()
+        self._check(lib().reno_code_length(self._h, scale, _ptr(out),
+                                           ctypes.byref(tot) if total else None))
+        return (out[:n] if per_voxel else None), (tot.value if total else None)
+
+    def neighbor_map(self, scale: int):
+        n = self.num_voxels(scale)
+        out = self._empty((max(n, 1), 27), self.torch.int32)
+        self._check(lib().reno_neighbor_map(self._h, scale, _ptr(out)))
+        return out[:n]
+
+    def symbol_freqs(self, scale: int):
+        n = self.num_voxels(scale)
+        out = self._empty((max(n, 1), SYMBOLS), self.torch.int16)
+        self._check(lib().reno_symbol_freqs(self._h, scale, _ptr(out)))
+        return out[:n]
+
+
+def rans_encode(sym: np.ndarray, freq: np.ndarray) -> np.ndarray:
+    """Host rANS encode of one scale's symbols with per-symbol frequency tables."""
+    s = np.ascontiguousarray(sym, dtype=np.uint8)
+    f = np.ascontiguousarray(freq, dtype=np.uint16).reshape(-1, SYMBOLS)
+    cap = s.size + 16
+    out = np.empty(cap, dtype=np.uint32)
+    nw = ctypes.c_int64()
+    rc = lib().reno_rans_encode(s.ctypes.data_as(_vp), f.ctypes.data_as(_vp), s.size,
+                                out.ctypes.data_as(_vp), cap, ctypes.byref(nw))
+    if rc != RENO_OK:
+        raise RenoError(rc, "rANS encode failed")
+    return out[:nw.value].copy()
+
+
+def rans_decode(words: np.ndarray, freq: np.ndarray, n: int) -> np.ndarray:
+    w = np.ascontiguousarray(words, dtype=np.uint32)
+    f = np.ascontiguousarray(freq, dtype=np.uint16).reshape(-1, SYMBOLS)
+    out = np.empty(n, dtype=np.uint8)
+    rc = lib().reno_rans_decode(w.ctypes.data_as(_vp), w.size, f.ctypes.data_as(_vp), n,
+                                out.ctypes.data_as(_vp))
+    if rc != RENO_OK:
+        raise RenoError(rc, "rANS decode failed")
+    return out
+
+
+def weights_to_device(w: dict, device="cuda") -> dict:
+    """numpy weight dict (synth layout) -> fp32 device tensors."""
+    import torch
+    return {"conv_w": [torch.from_numpy(np.ascontiguousarray(x)).to(device) for x in w["conv_w"]],
+            "conv_b": [torch.from_numpy(np.ascontiguousarray(x)).to(device) for x in w["conv_b"]],
+            "head_w": torch.from_numpy(np.ascontiguousarray(w["head_w"])).to(device),
+            "head_b": torch.from_numpy(np.ascontiguousarray(w["head_b"])).to(device)}

@@ -1,0 +1,406 @@
+// C ABI of the codec hot path: argument checks, call-order state, buffer
+// ownership and device-error reporting.  Every compute step is a HIP kernel
+// enqueued on the context stream (see the k_*.hip files).
+
+#include <cmath>
+#include <cstring>
+#include <string>
+
+#include "ctx.h"
+
+struct reno_ctx : reno::Ctx {};
+
+namespace {
+
+using reno::Ctx;
+thread_local std::string g_create_err;
+
+reno_status fail(Ctx* c, reno_status s, const std::string& msg) {
+  if (c)
+    c->err = msg;
+  else
+    g_create_err = msg;
+  return s;
+}
+
+#define RENO_HIP(c, expr)                                                                  \
+  do {                                                                                     \
+    hipError_t e_ = (expr);                                                                \
+    if (e_ != hipSuccess)                                                                  \
+      return fail((c), RENO_E_HIP, std::string(#expr) + ": " + hipGetErrorString(e_));     \
+  } while (0)
+
+size_t round256(size_t n) { return (n + 255) & ~size_t(255); }
+
+template <typename T>
+hipError_t dalloc(T** p, size_t count) {
+  return hipMalloc(reinterpret_cast<void**>(p), round256(count * sizeof(T) + 16));
+}
+
+bool has(uint32_t mask, int b) { return b >= 0 && b < 32 && ((mask >> b) & 1u); }
+uint32_t bits_range(int lo, int hi) {  // bits lo..hi inclusive
+  uint32_t m = 0;
+  for (int b = lo; b <= hi; ++b) m |= 1u << b;
+  return m;
+}
+
+void free_all(Ctx* c) {
+  void* ptrs[] = {c->keys_a,  c->keys_b,    c->lv_key,   c->lv_code,  c->lv_parent, c->lv_fc,
+                  c->lv_feat, c->d_count,   c->d_moff,   c->d_err,    c->d_hist,    c->d_ticket,
+                  c->d_status, c->d_hash,   c->h_a,      c->h_b,      c->d_nbr,     c->d_lse,
+                  c->d_partial, c->d_total, c->w_head,   c->w_hbias,  c->w_head_plain};
+  for (void* p : ptrs)
+    if (p) (void)hipFree(p);
+  for (int l = 0; l < RENO_MAX_LAYERS; ++l) {
+    if (c->w_conv[l]) (void)hipFree(c->w_conv[l]);
+    if (c->w_bias[l]) (void)hipFree(c->w_bias[l]);
+  }
+  if (c->h_total) (void)hipHostFree(c->h_total);
+  if (c->h_count) (void)hipHostFree(c->h_count);
+  if (c->h_err) (void)hipHostFree(c->h_err);
+}
+
+// Waits for the stream and turns latched device errors into a status.
+reno_status sync_check(Ctx* c) {
+  RENO_HIP(c, hipMemcpyAsync(c->h_err, c->d_err, sizeof(uint32_t), hipMemcpyDeviceToHost, c->stream));
+  RENO_HIP(c, hipStreamSynchronize(c->stream));
+  const uint32_t e = *c->h_err;
+  if (e == 0) return RENO_OK;
+  std::string msg = "device reported:";
+  if (e & reno::ERR_NONFINITE) msg += " non-finite input coordinate;";
+  if (e & reno::ERR_ZERO_CODE) msg += " zero occupancy code;";
+  if (e & reno::ERR_BASE_ORDER) msg += " base voxels not strictly ascending in Morton order;";
+  if (e & reno::ERR_BASE_RANGE) msg += " base voxel outside the base grid;";
+  if (e & reno::ERR_CAPACITY) msg += " frame exceeds the context capacity;";
+  if (e & reno::ERR_HASH_FULL) msg += " coordinate hash full;";
+  if (e & reno::ERR_SPIN) msg += " internal: look-back wait bound exceeded;";
+  if (e & reno::ERR_DUP_KEY) msg += " internal: duplicate hash key;";
+  if (e & reno::ERR_INTERNAL) msg += " internal: consistency check failed;";
+  if (e & (reno::ERR_CAPACITY | reno::ERR_HASH_FULL)) return fail(c, RENO_E_CAPACITY, msg);
+  if (e & (reno::ERR_SPIN | reno::ERR_DUP_KEY | reno::ERR_INTERNAL)) return fail(c, RENO_E_HIP, msg);
+  return fail(c, RENO_E_INPUT, msg);
+}
+
+// Zeroes the per-frame counters, tickets, look-back state and hash.
+reno_status frame_init(Ctx* c) {
+  void* p[8] = {c->d_err, c->d_count, c->d_moff, c->d_hist, c->d_ticket, c->d_status, c->d_hash};
+  size_t n[8] = {16,
+                 sizeof(int32_t) * reno::NLEV,
+                 sizeof(int32_t) * (reno::NLEV + 1),
+                 sizeof(uint32_t) * reno::MAX_PASSES * reno::RADIX,
+                 sizeof(uint32_t) * reno::TICKETS,
+                 sizeof(uint32_t) * (size_t)c->status_words,
+                 sizeof(reno::HashSlot) << c->hash_lg};
+  RENO_HIP(c, reno::launch_zero(*c, p, n, 7));
+  return RENO_OK;
+}
+
+bool model_scale(const Ctx* c, int b) { return c->B > 0 && b > c->b0() && b < c->B; }
+
+}  // namespace
+
+extern "C" {
+
+const char* reno_last_error(const reno_ctx* ctx) {
+  return ctx ? ctx->err.c_str() : g_create_err.c_str();
+}
+
+reno_status reno_create(const reno_params* p, void* hip_stream, reno_ctx** out) {
+  if (!p || !out) return fail(nullptr, RENO_E_INVALID, "null argument");
+  *out = nullptr;
+  if (p->max_points < 1 || p->max_points >= (int64_t(1) << 30))
+    return fail(nullptr, RENO_E_INVALID, "max_points must be in [1, 2^30)");
+  if (p->max_bit_depth < 1 || p->max_bit_depth > RENO_MAX_BIT_DEPTH)
+    return fail(nullptr, RENO_E_INVALID, "max_bit_depth must be in [1, 21]");
+  if (p->min_bit_depth < 0 || p->min_bit_depth >= p->max_bit_depth)
+    return fail(nullptr, RENO_E_INVALID, "min_bit_depth must be in [0, max_bit_depth)");
+  if (!(p->range_m > 0.0) || !std::isfinite(p->range_m))
+    return fail(nullptr, RENO_E_INVALID, "range_m must be positive and finite");
+  if (p->in_features != RENO_IN_FEATURES)
+    return fail(nullptr, RENO_E_INVALID, "in_features must be 11");
+  if (p->channels != 16 && p->channels != 32)
+    return fail(nullptr, RENO_E_INVALID, "channels must be 16 or 32");
+  if (p->layers < 1 || p->layers > RENO_MAX_LAYERS)
+    return fail(nullptr, RENO_E_INVALID, "layers must be in [1, 8]");
+  int64_t cap_model = p->max_model_voxels > 0 ? p->max_model_voxels : 3 * p->max_points;
+  if (cap_model >= (int64_t(1) << 30))
+    return fail(nullptr, RENO_E_INVALID, "max_model_voxels must be below 2^30");
+
+  reno_ctx* c = new reno_ctx();
+  c->p = *p;
+  c->p.max_model_voxels = cap_model;
+  c->stream = static_cast<hipStream_t>(hip_stream);
+  if (hipGetDevice(&c->device) != hipSuccess) {
+    delete c;
+    return fail(nullptr, RENO_E_HIP, "no HIP device");
+  }
+  c->cap_pts = p->max_points;
+  c->cap_model = cap_model;
+  c->nlv = p->max_bit_depth - p->min_bit_depth + 1;
+  int lg = 10;
+  while ((int64_t(1) << lg) * 3 < cap_model * 4 && lg < 31) ++lg;  // load factor <= 3/4
+  c->hash_lg = lg;
+  c->sort_tiles = (c->cap_pts + reno::SORT_TILE - 1) / reno::SORT_TILE;
+  c->pyr_tiles = (c->cap_pts + reno::PYR_TILE - 1) / reno::PYR_TILE;
+  c->exp_tiles = (c->cap_pts + reno::EXP_TILE - 1) / reno::EXP_TILE;
+  c->status_words = (int64_t)reno::MAX_PASSES * c->sort_tiles * reno::RADIX +
+                    c->pyr_tiles * reno::NLEV + (int64_t)reno::NLEV * c->exp_tiles;
+  const int C = p->channels;
+  const size_t lvn = (size_t)c->nlv * c->cap_pts;
+  hipError_t e = hipSuccess;
+  auto A = [&](hipError_t r) {
+    if (e == hipSuccess) e = r;
+  };
+  A(dalloc(&c->keys_a, c->cap_pts));
+  A(dalloc(&c->keys_b, c->cap_pts));
+  A(dalloc(&c->lv_key, lvn));
+  A(dalloc(&c->lv_code, lvn));
+  A(dalloc(&c->lv_parent, lvn));
+  A(dalloc(&c->lv_fc, lvn));
+  A(dalloc(&c->lv_feat, lvn));
+  A(dalloc(&c->d_count, reno::NLEV));
+  A(dalloc(&c->d_moff, reno::NLEV + 1));
+  A(dalloc(&c->d_err, 4));
+  A(dalloc(&c->d_hist, reno::MAX_PASSES * reno::RADIX));
+  A(dalloc(&c->d_ticket, reno::TICKETS));
+  A(dalloc(&c->d_status, (size_t)c->status_words));
+  A(dalloc(&c->d_hash, size_t(1) << c->hash_lg));
+  A(dalloc(&c->h_a, (size_t)cap_model * C));
+  A(dalloc(&c->h_b, (size_t)cap_model * C));
+  A(dalloc(&c->d_nbr, (size_t)cap_model * 27));
+  A(dalloc(&c->d_lse, (size_t)cap_model));
+  A(dalloc(&c->d_partial, (size_t)reno::NLEV * reno::RED_BLOCKS));
+  A(dalloc(&c->d_total, reno::NLEV));
+  int c_in = RENO_IN_FEATURES;
+  for (int l = 0; l < p->layers; ++l) {
+    const int KS = (c_in + 3) / 4, KSP = (KS + 3) & ~3;
+    A(dalloc(&c->w_conv[l], (size_t)27 * (C / 16) * 64 * KSP));
+    A(dalloc(&c->w_bias[l], (size_t)C));
+    c_in = C;
+  }
+  A(dalloc(&c->w_head, (size_t)16 * 64 * (C / 4)));
+  A(dalloc(&c->w_hbias, 256));
+  A(dalloc(&c->w_head_plain, (size_t)C * 256));
+  A(hipHostMalloc(reinterpret_cast<void**>(&c->h_total), sizeof(double) * reno::NLEV, 0));
+  A(hipHostMalloc(reinterpret_cast<void**>(&c->h_count), sizeof(int32_t) * reno::NLEV, 0));
+  A(hipHostMalloc(reinterpret_cast<void**>(&c->h_err), 64, 0));
+  if (e != hipSuccess) {
+    const std::string msg = std::string("allocation failed: ") + hipGetErrorString(e);
+    free_all(c);
+    delete c;
+    return fail(nullptr, e == hipErrorOutOfMemory ? RENO_E_NOMEM : RENO_E_HIP, msg);
+  }
+  // reduction done-counters start at zero and reset themselves after use
+  e = hipMemsetAsync(c->d_ticket, 0, sizeof(uint32_t) * reno::TICKETS, c->stream);
+  if (e == hipSuccess) e = hipStreamSynchronize(c->stream);
+  if (e != hipSuccess) {
+    const std::string msg = std::string("init failed: ") + hipGetErrorString(e);
+    free_all(c);
+    delete c;
+    return fail(nullptr, RENO_E_HIP, msg);
+  }
+  *out = c;
+  return RENO_OK;
+}
+
+reno_status reno_destroy(reno_ctx* c) {
+  if (!c) return RENO_E_INVALID;
+  (void)hipStreamSynchronize(c->stream);
+  free_all(c);
+  delete c;
+  return RENO_OK;
+}
+
+reno_status reno_sync(reno_ctx* c) {
+  if (!c) return RENO_E_INVALID;
+  return sync_check(c);
+}
+
+reno_status reno_set_weights(reno_ctx* c, const reno_weights* w) {
+  if (!c || !w) return fail(c, RENO_E_INVALID, "null argument");
+  for (int l = 0; l < c->p.layers; ++l)
+    if (!w->conv_w[l] || !w->conv_b[l]) return fail(c, RENO_E_INVALID, "missing conv weights");
+  if (!w->head_w || !w->head_b) return fail(c, RENO_E_INVALID, "missing head weights");
+  RENO_HIP(c, reno::launch_pack_weights(*c, *w));
+  c->have_weights = true;
+  return RENO_OK;
+}
+
+reno_status reno_build_pyramid(reno_ctx* c, const float* points, int64_t n, int bit_depth) {
+  if (!c) return RENO_E_INVALID;
+  if (n < 0 || n > c->cap_pts) return fail(c, RENO_E_INVALID, "point count out of range");
+  if (n > 0 && !points) return fail(c, RENO_E_INVALID, "null points");
+  if (bit_depth <= c->b0() || bit_depth > c->p.max_bit_depth)
+    return fail(c, RENO_E_INVALID, "bit_depth must be in (min_bit_depth, max_bit_depth]");
+  const int B = bit_depth;
+  c->B = B;
+  c->encoder = true;
+  c->npoints = n;
+  c->have_level = bits_range(c->b0(), B);
+  c->have_codes = bits_range(c->b0(), B - 1);
+  c->have_pred = 0;
+  reno_status s = frame_init(c);
+  if (s != RENO_OK) return s;
+  if (n == 0) return RENO_OK;
+  const int passes = (3 * B + reno::RADIX_BITS - 1) / reno::RADIX_BITS;
+  RENO_HIP(c, reno::launch_quantize(*c, points, n, B, passes));
+  uint64_t* src = c->keys_a;
+  uint64_t* dst = c->keys_b;
+  for (int ps = 0; ps < passes; ++ps) {
+    RENO_HIP(c, reno::launch_sort_pass(*c, src, dst, n, ps));
+    uint64_t* t = src;
+    src = dst;
+    dst = t;
+  }
+  RENO_HIP(c, reno::launch_pyramid(*c, src, n, B));
+  RENO_HIP(c, reno::launch_codes(*c, B));
+  return RENO_OK;
+}
+
+reno_status reno_set_base(reno_ctx* c, int bit_depth, const int32_t* xyz, const uint8_t* codes,
+                          int64_t n) {
+  if (!c) return RENO_E_INVALID;
+  if (bit_depth <= c->b0() || bit_depth > c->p.max_bit_depth)
+    return fail(c, RENO_E_INVALID, "bit_depth must be in (min_bit_depth, max_bit_depth]");
+  const int64_t grid = int64_t(1) << (3 * c->b0());
+  if (n < 0 || n > c->cap_pts || n > grid) return fail(c, RENO_E_INVALID, "base count out of range");
+  if (n > 0 && (!xyz || !codes)) return fail(c, RENO_E_INVALID, "null base arrays");
+  c->B = bit_depth;
+  c->encoder = false;
+  c->npoints = 0;
+  c->have_level = 1u << c->b0();
+  c->have_codes = 1u << c->b0();
+  c->have_pred = 0;
+  reno_status s = frame_init(c);
+  if (s != RENO_OK) return s;
+  RENO_HIP(c, reno::launch_set_base(*c, xyz, codes, n, bit_depth));
+  return RENO_OK;
+}
+
+reno_status reno_expand(reno_ctx* c, int scale, const uint8_t* codes) {
+  if (!c) return RENO_E_INVALID;
+  if (c->B == 0) return fail(c, RENO_E_STATE, "no frame");
+  if (scale < c->b0() || scale >= c->B) return fail(c, RENO_E_INVALID, "scale out of range");
+  if (!has(c->have_level, scale)) return fail(c, RENO_E_STATE, "scale not built yet");
+  if (has(c->have_level, scale + 1))
+    return fail(c, RENO_E_STATE, "the next scale already exists in this frame");
+  if (!codes && !has(c->have_codes, scale)) return fail(c, RENO_E_STATE, "codes of the scale unknown");
+  RENO_HIP(c, reno::launch_expand(*c, scale, codes, c->B));
+  c->have_codes |= 1u << scale;
+  c->have_level |= 1u << (scale + 1);
+  return RENO_OK;
+}
+
+reno_status reno_num_voxels(reno_ctx* c, int scale, int64_t* n_host) {
+  if (!c || !n_host) return fail(c, RENO_E_INVALID, "null argument");
+  if (!has(c->have_level, scale)) return fail(c, RENO_E_STATE, "scale not built");
+  RENO_HIP(c, hipMemcpyAsync(c->h_count, c->d_count, sizeof(int32_t) * reno::NLEV,
+                             hipMemcpyDeviceToHost, c->stream));
+  reno_status s = sync_check(c);
+  if (s != RENO_OK) return s;
+  *n_host = c->h_count[scale];
+  return RENO_OK;
+}
+
+reno_status reno_coords(reno_ctx* c, int scale, int32_t* xyz, uint64_t* keys) {
+  if (!c) return RENO_E_INVALID;
+  if (!has(c->have_level, scale)) return fail(c, RENO_E_STATE, "scale not built");
+  if (!xyz && !keys) return RENO_OK;
+  RENO_HIP(c, reno::launch_coords(*c, scale, xyz, keys));
+  return RENO_OK;
+}
+
+reno_status reno_occupancy_codes(reno_ctx* c, int scale, uint8_t* codes) {
+  if (!c || !codes) return fail(c, RENO_E_INVALID, "null argument");
+  if (!has(c->have_codes, scale)) return fail(c, RENO_E_STATE, "codes of the scale unknown");
+  RENO_HIP(c, reno::launch_copy_level_u8(*c, scale, codes));
+  return RENO_OK;
+}
+
+reno_status reno_parent_rows(reno_ctx* c, int scale, int32_t* parent) {
+  if (!c || !parent) return fail(c, RENO_E_INVALID, "null argument");
+  if (!has(c->have_level, scale)) return fail(c, RENO_E_STATE, "scale not built");
+  RENO_HIP(c, reno::launch_copy_level_i32(*c, scale, c->lv_parent + c->lv(scale), parent));
+  return RENO_OK;
+}
+
+reno_status reno_predict_probs(reno_ctx* c, int scale, const reno_weights* weights, float* logits) {
+  if (!c) return RENO_E_INVALID;
+  if (c->B == 0) return fail(c, RENO_E_STATE, "no frame");
+  if (weights) {
+    reno_status s = reno_set_weights(c, weights);
+    if (s != RENO_OK) return s;
+  }
+  if (!c->have_weights) return fail(c, RENO_E_STATE, "no weights set");
+  int lo, hi;
+  if (scale == RENO_ALL_SCALES) {
+    lo = c->b0() + 1;
+    hi = c->B - 1;
+    if (lo > hi) return RENO_OK;
+    for (int b = lo; b <= hi; ++b)
+      if (!has(c->have_level, b) || !has(c->have_codes, b - 1))
+        return fail(c, RENO_E_STATE, "every model scale and its parent codes must exist");
+  } else {
+    if (!model_scale(c, scale)) return fail(c, RENO_E_INVALID, "not a model scale");
+    if (!has(c->have_level, scale) || !has(c->have_codes, scale - 1))
+      return fail(c, RENO_E_STATE, "scale or the codes of its parent scale unknown");
+    lo = hi = scale;
+  }
+  RENO_HIP(c, reno::launch_model(*c, lo, hi, logits));
+  c->have_pred |= bits_range(lo, hi);
+  return RENO_OK;
+}
+
+reno_status reno_code_length(reno_ctx* c, int scale, float* bits_per_voxel, double* total_host) {
+  if (!c) return RENO_E_INVALID;
+  if (c->B == 0) return fail(c, RENO_E_STATE, "no frame");
+  const int b0 = c->b0();
+  double base_bits = 0.0;
+  bool with_base = false;
+  int lo = 0, hi = -1;
+  if (scale == RENO_ALL_SCALES) {
+    with_base = true;
+    lo = b0 + 1;
+    hi = c->B - 1;
+    for (int b = lo; b <= hi; ++b)
+      if (!has(c->have_pred, b) || !has(c->have_codes, b))
+        return fail(c, RENO_E_STATE, "every model scale needs predict_probs and its codes");
+  } else if (scale == b0) {
+    if (bits_per_voxel) return fail(c, RENO_E_INVALID, "the base scale has no per-voxel bits");
+    with_base = true;
+  } else {
+    if (!model_scale(c, scale)) return fail(c, RENO_E_INVALID, "not a model scale");
+    if (!has(c->have_pred, scale) || !has(c->have_codes, scale))
+      return fail(c, RENO_E_STATE, "scale needs predict_probs and its codes");
+    lo = hi = scale;
+  }
+  if (lo <= hi) RENO_HIP(c, reno::launch_code_length(*c, lo, hi, bits_per_voxel));
+  if (!total_host) return RENO_OK;
+  RENO_HIP(c, hipMemcpyAsync(c->h_total, c->d_total, sizeof(double) * reno::NLEV,
+                             hipMemcpyDeviceToHost, c->stream));
+  RENO_HIP(c, hipMemcpyAsync(c->h_count, c->d_count, sizeof(int32_t) * reno::NLEV,
+                             hipMemcpyDeviceToHost, c->stream));
+  reno_status s = sync_check(c);
+  if (s != RENO_OK) return s;
+  if (with_base) base_bits = 32.0 + (double)c->h_count[b0] * (3.0 * b0 + 8.0);
+  double t = base_bits;
+  for (int b = lo; b <= hi; ++b) t += c->h_total[b];
+  *total_host = t;
+  return RENO_OK;
+}
+
+reno_status reno_neighbor_map(reno_ctx* c, int scale, int32_t* map) {
+  if (!c || !map) return fail(c, RENO_E_INVALID, "null argument");
+  if (!has(c->have_pred, scale)) return fail(c, RENO_E_STATE, "predict_probs of the scale not run");
+  RENO_HIP(c, reno::launch_neighbor_map(*c, scale, map));
+  return RENO_OK;
+}
+
+reno_status reno_symbol_freqs(reno_ctx* c, int scale, uint16_t* freq) {
+  if (!c || !freq) return fail(c, RENO_E_INVALID, "null argument");
+  if (!has(c->have_pred, scale)) return fail(c, RENO_E_STATE, "predict_probs of the scale not run");
+  RENO_HIP(c, reno::launch_symbol_freqs(*c, scale, freq));
+  return RENO_OK;
+}
+
+}  // extern "C"

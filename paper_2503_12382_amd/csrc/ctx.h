@@ -1,0 +1,130 @@
+// Context of one codec stream: capacities, device buffers and the host-side
+// call-order state.  Shared by the C-ABI layer (api.cpp) and the kernel
+// launchers.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include <string>
+
+#include "../../include/reno.h"
+#include "dev.h"
+
+namespace reno {
+
+constexpr int NLEV = RENO_MAX_BIT_DEPTH + 1;   // bit depths 0 .. 21
+constexpr int SORT_THREADS = 256;
+constexpr int SORT_KPT = 4;                     // keys per thread per sort tile
+constexpr int SORT_TILE = SORT_THREADS * SORT_KPT;
+constexpr int RADIX_BITS = 8;
+constexpr int RADIX = 1 << RADIX_BITS;
+constexpr int MAX_PASSES = (3 * RENO_MAX_BIT_DEPTH + RADIX_BITS - 1) / RADIX_BITS;
+constexpr int PYR_THREADS = 256;
+constexpr int PYR_KPT = 4;
+constexpr int PYR_TILE = PYR_THREADS * PYR_KPT;
+constexpr int EXP_THREADS = 256;
+constexpr int EXP_KPT = 4;
+constexpr int EXP_TILE = EXP_THREADS * EXP_KPT;
+constexpr int RED_BLOCKS = 32;                  // partial sums per scale in the bits reduction
+constexpr int TICKETS = 64;
+
+// ticket slots
+constexpr int TK_SORT = 0;        // + pass
+constexpr int TK_PYR = 16;
+constexpr int TK_EXPAND = 17;     // + scale (decoder: one per expand call)
+constexpr int TK_RED = 40;        // + scale slot (reduction done-counters, self-resetting)
+
+struct Ctx {
+  reno_params p{};
+  hipStream_t stream = nullptr;
+  int device = 0;
+  std::string err;
+
+  // capacities
+  int64_t cap_pts = 0;      // voxels per scale and raw points
+  int64_t cap_model = 0;    // sum of model-scale voxels
+  int nlv = 0;              // allocated scales: b0 .. max_bit_depth
+  int hash_lg = 0;
+  int64_t sort_tiles = 0;   // max tiles of one sort pass
+  int64_t status_words = 0; // look-back status capacity (uint32)
+
+  // per-scale regions: scale b lives at (b - b0) * cap_pts
+  uint64_t* keys_a = nullptr;   // sort ping-pong [cap_pts]
+  uint64_t* keys_b = nullptr;
+  uint64_t* lv_key = nullptr;   // Morton keys of V_b
+  uint8_t* lv_code = nullptr;   // O_b
+  int32_t* lv_parent = nullptr; // row of the parent in V_{b-1}
+  int32_t* lv_fc = nullptr;     // row of the first child in V_{b+1}
+  uint16_t* lv_feat = nullptr;  // delta | O_{b-1}[parent] << 3  (layer-1 input bits)
+
+  // device scalars / small arrays
+  int32_t* d_count = nullptr;   // [NLEV] N_b
+  int32_t* d_moff = nullptr;    // [NLEV] first packed model row of scale b
+  uint32_t* d_err = nullptr;    // [1] latched error bits
+  uint32_t* d_hist = nullptr;   // [MAX_PASSES][RADIX]
+  uint32_t* d_ticket = nullptr; // [TICKETS]
+  uint32_t* d_status = nullptr; // look-back status words
+  HashSlot* d_hash = nullptr;   // [1 << hash_lg]
+
+  // model buffers (packed model rows: scale b at d_moff[b] ..)
+  float* h_a = nullptr;         // [cap_model][C]
+  float* h_b = nullptr;
+  int32_t* d_nbr = nullptr;     // [cap_model][27]
+  float* d_lse = nullptr;       // [cap_model]
+  double* d_partial = nullptr;  // [NLEV][RED_BLOCKS]
+  double* d_total = nullptr;    // [NLEV]
+  double* h_total = nullptr;    // pinned host mirror [NLEV]
+  int32_t* h_count = nullptr;   // pinned host mirror [NLEV]
+  uint32_t* h_err = nullptr;    // pinned host mirror [1]
+
+  // packed weights (operand layouts of the conv/head kernels)
+  float* w_conv[RENO_MAX_LAYERS] = {};
+  float* w_bias[RENO_MAX_LAYERS] = {};
+  float* w_head = nullptr;
+  float* w_hbias = nullptr;
+  float* w_head_plain = nullptr;  // [C][256] as given, for code lengths and symbol tables
+  bool have_weights = false;
+
+  // frame state
+  int B = 0;                    // bit depth of the current frame (0 = none)
+  bool encoder = false;
+  uint32_t have_level = 0;      // bit b: V_b built
+  uint32_t have_codes = 0;      // bit b: O_b known
+  uint32_t have_pred = 0;       // bit b: TOP evaluated on V_b
+  int64_t npoints = 0;
+
+  int64_t pyr_tiles = 0;    // max tiles of the pyramid pass
+  int64_t exp_tiles = 0;    // max tiles of one expansion
+
+  // look-back status layout: [sort passes][sort_tiles][RADIX] | [pyr_tiles][NLEV] | [NLEV][exp_tiles]
+  uint32_t* st_sort(int pass) const { return d_status + (size_t)pass * sort_tiles * RADIX; }
+  uint32_t* st_pyr() const { return d_status + (size_t)MAX_PASSES * sort_tiles * RADIX; }
+  uint32_t* st_exp(int b) const {
+    return st_pyr() + (size_t)pyr_tiles * NLEV + (size_t)b * exp_tiles;
+  }
+
+  int b0() const { return p.min_bit_depth; }
+  int64_t lv(int b) const { return (int64_t)(b - p.min_bit_depth) * cap_pts; }
+  // buffer that holds the last conv layer's output (h_L), per the ping-pong
+  float* hlast() const { return (p.layers & 1) ? h_a : h_b; }
+};
+
+// ---- kernel launchers (each enqueues on ctx.stream; return hipError_t) ----
+hipError_t launch_zero(Ctx& c, void* const* ptrs, const size_t* bytes, int n);
+hipError_t launch_quantize(Ctx& c, const float* pts, int64_t n, int B, int passes);
+hipError_t launch_sort_pass(Ctx& c, const uint64_t* in, uint64_t* out, int64_t n, int pass);
+hipError_t launch_pyramid(Ctx& c, const uint64_t* sorted, int64_t n, int B);
+hipError_t launch_codes(Ctx& c, int B);
+hipError_t launch_set_base(Ctx& c, const int32_t* xyz, const uint8_t* codes, int64_t n, int B);
+hipError_t launch_expand(Ctx& c, int b, const uint8_t* codes, int B);
+hipError_t launch_pack_weights(Ctx& c, const reno_weights& w);
+hipError_t launch_model(Ctx& c, int b_lo, int b_hi, float* logits);
+hipError_t launch_code_length(Ctx& c, int b_lo, int b_hi, float* bits);
+hipError_t launch_symbol_freqs(Ctx& c, int b, uint16_t* freq);
+hipError_t launch_coords(Ctx& c, int b, int32_t* xyz, uint64_t* keys);
+hipError_t launch_copy_level_u8(Ctx& c, int b, uint8_t* out);
+hipError_t launch_copy_level_i32(Ctx& c, int b, const int32_t* src, int32_t* out);
+hipError_t launch_neighbor_map(Ctx& c, int b, int32_t* out);
+
+}  // namespace reno

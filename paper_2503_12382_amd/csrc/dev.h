@@ -1,0 +1,166 @@
+// Device-side helpers shared by the HIP kernels of the codec hot path:
+// Morton bit spreading, error latching, wavefront primitives, the decoupled
+// look-back used by every single-pass scan, and the open-addressing
+// coordinate hash.  gfx950 (CDNA4) only: wave64, 64-bit ballots.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace reno {
+
+// ---- error latch (ctx device word), reported by the next synchronising call ----
+enum : uint32_t {
+  ERR_NONFINITE = 1u,    // a non-finite input coordinate
+  ERR_CAPACITY = 2u,     // a scale or the model batch exceeded the context capacity
+  ERR_HASH_FULL = 4u,    // coordinate hash ran out of slots
+  ERR_ZERO_CODE = 8u,    // a code of 0 given to the decoder (codes lie in [1, 255])
+  ERR_BASE_ORDER = 16u,  // base voxels not strictly ascending
+  ERR_BASE_RANGE = 32u,  // base voxel outside [0, 2^b0)
+  ERR_SPIN = 64u,        // a look-back wait exceeded its bound (never expected)
+  ERR_DUP_KEY = 128u,    // the same key inserted twice (never expected: keys are a set)
+  ERR_INTERNAL = 256u,   // an internal consistency check failed (never expected)
+};
+
+__device__ __forceinline__ void latch(uint32_t* err, uint32_t bit) { atomicOr(err, bit); }
+
+// ---- Morton keys: x bit i -> key bit 3i, y -> 3i+1, z -> 3i+2 (21 bits per axis) ----
+__device__ __forceinline__ uint64_t spread3(uint64_t x) {
+  x &= 0x1fffffull;
+  x = (x | (x << 32)) & 0x001f00000000ffffull;
+  x = (x | (x << 16)) & 0x001f0000ff0000ffull;
+  x = (x | (x << 8)) & 0x100f00f00f00f00full;
+  x = (x | (x << 4)) & 0x10c30c30c30c30c3ull;
+  x = (x | (x << 2)) & 0x1249249249249249ull;
+  return x;
+}
+
+__device__ __forceinline__ uint32_t compact3(uint64_t x) {
+  x &= 0x1249249249249249ull;
+  x = (x ^ (x >> 2)) & 0x10c30c30c30c30c3ull;
+  x = (x ^ (x >> 4)) & 0x100f00f00f00f00full;
+  x = (x ^ (x >> 8)) & 0x001f0000ff0000ffull;
+  x = (x ^ (x >> 16)) & 0x001f00000000ffffull;
+  x = (x ^ (x >> 32)) & 0x1fffffull;
+  return (uint32_t)x;
+}
+
+__device__ __forceinline__ uint64_t morton3(uint32_t x, uint32_t y, uint32_t z) {
+  return spread3(x) | (spread3(y) << 1) | (spread3(z) << 2);
+}
+
+// ---- wavefront primitives (wave64) ----
+__device__ __forceinline__ int lane_id() { return (int)(threadIdx.x & 63); }
+
+// number of set bits of `mask` below this lane
+__device__ __forceinline__ uint32_t rank_below(uint64_t mask) {
+  return __builtin_amdgcn_mbcnt_hi((uint32_t)(mask >> 32),
+                                   __builtin_amdgcn_mbcnt_lo((uint32_t)mask, 0u));
+}
+
+__device__ __forceinline__ uint32_t wave_or(uint32_t v) {
+  for (int o = 32; o > 0; o >>= 1) v |= (uint32_t)__shfl_xor((int)v, o);
+  return v;
+}
+
+// ---- agent-scope relaxed atomics on look-back status words ----
+__device__ __forceinline__ uint32_t ld_status(const uint32_t* p) {
+  return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ void st_status(uint32_t* p, uint32_t v) {
+  __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+// Decoupled look-back (single-pass prefix over tiles processed in ticket
+// order).  Status word = 2 flag bits | 30-bit count; 0 = not yet published.
+constexpr uint32_t LB_AGG = 1u << 30;
+constexpr uint32_t LB_INC = 2u << 30;
+constexpr uint32_t LB_VAL = (1u << 30) - 1u;
+constexpr uint32_t LB_SPIN_LIMIT = 1u << 24;
+
+// The calling thread owns counter `c` of tile `tile` (status row stride
+// `width`).  Publishes the tile aggregate, walks back over earlier tiles until
+// an inclusive prefix is found, publishes its own inclusive prefix and returns
+// the exclusive one.  Earlier tiles took their tickets earlier and are
+// therefore already running; each publishes its aggregate without waiting, so
+// every wait ends.  A bound on the wait latches ERR_SPIN instead of hanging.
+__device__ __forceinline__ uint32_t lookback(uint32_t* status, int width, int tile, int c,
+                                             uint32_t agg, uint32_t* err) {
+  uint32_t* mine = status + (size_t)tile * width + c;
+  if (tile == 0) {
+    st_status(mine, LB_INC | agg);
+    return 0;
+  }
+  st_status(mine, LB_AGG | agg);
+  uint32_t excl = 0;
+  uint32_t spins = 0;
+  for (int t = tile - 1; t >= 0;) {
+    uint32_t v = ld_status(status + (size_t)t * width + c);
+    uint32_t f = v & ~LB_VAL;
+    if (f == 0) {
+      if (++spins > LB_SPIN_LIMIT) {
+        latch(err, ERR_SPIN);
+        break;
+      }
+      __builtin_amdgcn_s_sleep(1);
+      continue;
+    }
+    excl += v & LB_VAL;
+    if (f == LB_INC) break;
+    --t;
+  }
+  st_status(mine, LB_INC | (excl + agg));
+  return excl;
+}
+
+// ---- open-addressing coordinate hash in HBM ----
+// One table serves every scale of a frame: a scale-b key is tagged with a
+// sentinel bit at position 3b (key < 2^{3b}), which makes tagged keys of
+// different scales distinct and never 0 (0 marks an empty slot).
+struct alignas(16) HashSlot {
+  unsigned long long key;
+  int32_t row;
+  int32_t pad;
+};
+
+__device__ __forceinline__ uint64_t tag_key(uint64_t key, int b) { return key | (1ull << (3 * b)); }
+
+__device__ __forceinline__ uint32_t hash_home(uint64_t tk, int lg) {
+  return (uint32_t)((tk * 0x9E3779B97F4A7C15ull) >> (64 - lg));
+}
+
+// Inserts tagged key -> row with linear probing (64-bit CAS on the key).
+__device__ __forceinline__ void hash_insert(HashSlot* tab, int lg, uint64_t tk, int32_t row,
+                                            uint32_t* err) {
+  const uint32_t mask = (1u << lg) - 1u;
+  uint32_t h = hash_home(tk, lg);
+  for (uint32_t step = 0; step <= mask; ++step) {
+    unsigned long long prev = atomicCAS(&tab[h].key, 0ull, (unsigned long long)tk);
+    if (prev == 0ull) {
+      tab[h].row = row;
+      return;
+    }
+    if (prev == tk) {
+      latch(err, ERR_DUP_KEY);
+      return;
+    }
+    h = (h + 1u) & mask;
+  }
+  latch(err, ERR_HASH_FULL);
+}
+
+// Row of a tagged key, or -1.  The table was built by an earlier kernel.
+__device__ __forceinline__ int32_t hash_find(const HashSlot* tab, int lg, uint64_t tk) {
+  const uint32_t mask = (1u << lg) - 1u;
+  uint32_t h = hash_home(tk, lg);
+  for (uint32_t step = 0; step <= mask; ++step) {
+    const uint4 s = *reinterpret_cast<const uint4*>(&tab[h]);
+    const uint64_t k = ((uint64_t)s.y << 32) | s.x;
+    if (k == tk) return (int32_t)s.z;
+    if (k == 0ull) return -1;
+    h = (h + 1u) & mask;
+  }
+  return -1;
+}
+
+}  // namespace reno

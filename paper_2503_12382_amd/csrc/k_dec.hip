@@ -1,0 +1,198 @@
+// Decoder side on gfx950: the initial state (C^0, O^0) of Eq. 2 and the FCG
+// expansion of Sec. 3.1 (expand each code to 8 bits, keep the children whose
+// bit is set), as a single-pass popcount scan with decoupled look-back.  The
+// children of a scale come out in ascending Morton order, identical to the
+// encoder's sorted scale, and are inserted into the coordinate hash.
+
+#include "ctx.h"
+
+namespace reno {
+namespace {
+
+// Scale b0 from int32 xyz (strictly ascending Morton order) and codes.
+__global__ void __launch_bounds__(256) k_set_base(const int32_t* __restrict__ xyz,
+                                                  const uint8_t* __restrict__ codes, int64_t n,
+                                                  int b0, uint64_t* __restrict__ key,
+                                                  uint8_t* __restrict__ code,
+                                                  int32_t* __restrict__ parent, int32_t* count,
+                                                  int32_t* moff, uint32_t* err) {
+  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i == 0) {
+    count[b0] = (int32_t)n;
+    moff[b0 + 1] = 0;
+  }
+  if (i >= n) return;
+  const int32_t lim = 1 << b0;
+  uint32_t q[3], qp[3];
+  bool range_ok = true;
+  for (int a = 0; a < 3; ++a) {
+    const int32_t v = xyz[3 * i + a];
+    range_ok = range_ok && v >= 0 && v < lim;
+    q[a] = (uint32_t)v & (uint32_t)(lim - 1);
+  }
+  if (!range_ok) latch(err, ERR_BASE_RANGE);
+  const uint64_t k = morton3(q[0], q[1], q[2]);
+  if (i > 0) {
+    for (int a = 0; a < 3; ++a) qp[a] = (uint32_t)xyz[3 * (i - 1) + a] & (uint32_t)(lim - 1);
+    if (morton3(qp[0], qp[1], qp[2]) >= k) latch(err, ERR_BASE_ORDER);
+  }
+  const uint8_t c = codes[i];
+  if (c == 0) latch(err, ERR_ZERO_CODE);
+  key[i] = k;
+  code[i] = c;
+  parent[i] = -1;
+}
+
+struct ExpArgs {
+  const uint8_t* codes_in;  // caller codes for O_b, or null (already recorded)
+  int b, B;
+  int64_t cap_pts;
+  int64_t cap_model;
+  const uint64_t* key_b;
+  uint8_t* code_b;
+  int32_t* fc_b;
+  uint64_t* key_n;    // scale b+1
+  int32_t* parent_n;
+  uint16_t* feat_n;
+  int32_t* count;
+  int32_t* moff;
+  uint32_t* status;
+  uint32_t* ticket;
+  HashSlot* hash;
+  int hash_lg;
+  uint32_t* err;
+};
+
+__global__ void __launch_bounds__(EXP_THREADS) k_expand(ExpArgs a) {
+  __shared__ uint32_t s_tile;
+  __shared__ uint32_t s_wtot[4];
+  __shared__ uint32_t s_base;
+  const int tid = threadIdx.x, w = tid >> 6, lane = tid & 63;
+  const int64_t np = a.count[a.b];
+  const int64_t ntiles = (np + EXP_TILE - 1) / EXP_TILE;
+  const int bn = a.b + 1;
+  if (ntiles == 0) {
+    if (blockIdx.x == 0 && tid == 0) {
+      a.count[bn] = 0;
+      if (bn < a.B) a.moff[bn + 1] = a.moff[bn];
+    }
+    return;
+  }
+  if (tid == 0) s_tile = atomicAdd(a.ticket, 1u);
+  __syncthreads();
+  const int64_t tile = s_tile;
+  if (tile >= ntiles) return;
+  const int64_t base = tile * EXP_TILE;
+
+  uint32_t code[EXP_KPT], incl[EXP_KPT];
+  uint32_t run = 0;  // wave running total before element j
+#pragma unroll
+  for (int j = 0; j < EXP_KPT; ++j) {
+    const int64_t p = base + (int64_t)w * 64 * EXP_KPT + j * 64 + lane;
+    uint32_t c = 0;
+    if (p < np) {
+      c = a.codes_in ? a.codes_in[p] : a.code_b[p];
+      if (a.codes_in) a.code_b[p] = (uint8_t)c;
+      if (c == 0u) latch(a.err, ERR_ZERO_CODE);
+    }
+    code[j] = c;
+    uint32_t x = (uint32_t)__popc(c);
+#pragma unroll
+    for (int o = 1; o < 64; o <<= 1) {
+      const uint32_t y = (uint32_t)__shfl_up((int)x, o);
+      if (lane >= o) x += y;
+    }
+    incl[j] = run + x;
+    run += (uint32_t)__shfl((int)x, 63);
+  }
+  if (lane == 0) s_wtot[w] = run;
+  __syncthreads();
+  if (tid == 0) {
+    const uint32_t t0 = s_wtot[0], t1 = s_wtot[1], t2 = s_wtot[2], t3 = s_wtot[3];
+    const uint32_t tot = t0 + t1 + t2 + t3;
+    const uint32_t ex = lookback(a.status, 1, (int)tile, 0, tot, a.err);
+    s_base = ex;
+    s_wtot[0] = 0;
+    s_wtot[1] = t0;
+    s_wtot[2] = t0 + t1;
+    s_wtot[3] = t0 + t1 + t2;
+    if (tile == ntiles - 1) {
+      int64_t nn = (int64_t)ex + tot;
+      if (nn > a.cap_pts) {
+        latch(a.err, ERR_CAPACITY);
+        nn = a.cap_pts;
+      }
+      a.count[bn] = (int32_t)nn;
+      if (bn < a.B) {
+        const int64_t mo = (int64_t)a.moff[bn] + nn;
+        if (mo > a.cap_model) latch(a.err, ERR_CAPACITY);
+        a.moff[bn + 1] = (int32_t)mo;
+      }
+    }
+  }
+  __syncthreads();
+  const int64_t wbase = (int64_t)s_base + s_wtot[w];
+  const bool model = bn < a.B;
+#pragma unroll
+  for (int j = 0; j < EXP_KPT; ++j) {
+    const int64_t p = base + (int64_t)w * 64 * EXP_KPT + j * 64 + lane;
+    if (p >= np) continue;
+    const uint32_t c = code[j];
+    int64_t q = wbase + incl[j] - (uint32_t)__popc(c);
+    a.fc_b[p] = (int32_t)q;
+    const uint64_t kp = a.key_b[p] << 3;
+    for (uint32_t d = 0; d < 8; ++d) {
+      if (!((c >> d) & 1u)) continue;
+      if (q >= a.cap_pts) {
+        latch(a.err, ERR_CAPACITY);
+        break;
+      }
+      const uint64_t kc = kp | d;
+      a.key_n[q] = kc;
+      a.parent_n[q] = (int32_t)p;
+      a.feat_n[q] = (uint16_t)(d | (c << 3));
+      if (model) hash_insert(a.hash, a.hash_lg, tag_key(kc, bn), (int32_t)q, a.err);
+      ++q;
+    }
+  }
+}
+
+}  // namespace
+
+hipError_t launch_set_base(Ctx& c, const int32_t* xyz, const uint8_t* codes, int64_t n, int B) {
+  (void)B;
+  const int b0 = c.b0();
+  int64_t blocks = (n + 255) / 256;
+  if (blocks < 1) blocks = 1;
+  hipLaunchKernelGGL(k_set_base, dim3((unsigned)blocks), dim3(256), 0, c.stream, xyz, codes, n, b0,
+                     c.lv_key + c.lv(b0), c.lv_code + c.lv(b0), c.lv_parent + c.lv(b0), c.d_count,
+                     c.d_moff, c.d_err);
+  return hipGetLastError();
+}
+
+hipError_t launch_expand(Ctx& c, int b, const uint8_t* codes, int B) {
+  ExpArgs a;
+  a.codes_in = codes;
+  a.b = b;
+  a.B = B;
+  a.cap_pts = c.cap_pts;
+  a.cap_model = c.cap_model;
+  a.key_b = c.lv_key + c.lv(b);
+  a.code_b = c.lv_code + c.lv(b);
+  a.fc_b = c.lv_fc + c.lv(b);
+  a.key_n = c.lv_key + c.lv(b + 1);
+  a.parent_n = c.lv_parent + c.lv(b + 1);
+  a.feat_n = c.lv_feat + c.lv(b + 1);
+  a.count = c.d_count;
+  a.moff = c.d_moff;
+  const int64_t max_tiles = c.exp_tiles;
+  a.status = c.st_exp(b);
+  a.ticket = c.d_ticket + TK_EXPAND + b;
+  a.hash = c.d_hash;
+  a.hash_lg = c.hash_lg;
+  a.err = c.d_err;
+  hipLaunchKernelGGL(k_expand, dim3((unsigned)max_tiles), dim3(EXP_THREADS), 0, c.stream, a);
+  return hipGetLastError();
+}
+
+}  // namespace reno

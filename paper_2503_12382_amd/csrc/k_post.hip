@@ -1,0 +1,207 @@
+// Code lengths (Eq. 4), the quantised distributions handed to the host
+// arithmetic coder, and the getters that copy per-scale arrays out of the
+// context.  All sizes are read from the device.
+
+#include "ctx.h"
+
+namespace reno {
+namespace {
+
+constexpr float INV_LN2 = 1.4426950408889634f;
+
+// bits_v = (lse_v - z_{O_b[v]}) / ln 2 with z_o = hb[o] + sum_c H[c][o] h_L[v][c]
+// (fp32, channel order), per-scale sums in double: RED_BLOCKS partial sums per
+// scale, reduced in index order by the last block to finish (deterministic).
+__global__ void __launch_bounds__(256) k_code_length(
+    int b_lo, int b0, const int32_t* __restrict__ count, const int32_t* __restrict__ moff,
+    int64_t cap_pts, int64_t cap_model, const uint8_t* __restrict__ lv_code, const float* __restrict__ hL, int C,
+    const float* __restrict__ H, const float* __restrict__ hb, const float* __restrict__ lse,
+    float* __restrict__ bits_out, double* partial, double* total, uint32_t* done) {
+  __shared__ double s_red[256];
+  __shared__ bool s_last;
+  const int b = b_lo + blockIdx.y;
+  const int64_t mo = moff[b];
+  int64_t n = count[b];
+  if (mo + n > cap_model) n = 0;  // capacity overflow, latched where the size was made
+  const int64_t out0 = mo - moff[b_lo];
+  const uint8_t* code = lv_code + (int64_t)(b - b0) * cap_pts;
+  double acc = 0.0;
+  for (int64_t v = (int64_t)blockIdx.x * 256 + threadIdx.x; v < n; v += (int64_t)RED_BLOCKS * 256) {
+    const int o = code[v];
+    const float* h = hL + (mo + v) * C;
+    float z = hb[o];
+    for (int c = 0; c < C; ++c) z = fmaf(H[c * 256 + o], h[c], z);
+    const float bt = (lse[mo + v] - z) * INV_LN2;
+    if (bits_out) bits_out[out0 + v] = bt;
+    acc += (double)bt;
+  }
+  s_red[threadIdx.x] = acc;
+  __syncthreads();
+  for (int s = 128; s > 0; s >>= 1) {
+    if (threadIdx.x < s) s_red[threadIdx.x] += s_red[threadIdx.x + s];
+    __syncthreads();
+  }
+  if (threadIdx.x == 0) {
+    partial[b * RED_BLOCKS + blockIdx.x] = s_red[0];
+    __threadfence();
+    const uint32_t prev = atomicAdd(&done[b], 1u);
+    s_last = prev == RED_BLOCKS - 1;
+  }
+  __syncthreads();
+  if (s_last && threadIdx.x == 0) {
+    __threadfence();
+    double t = 0.0;
+    for (int i = 0; i < RED_BLOCKS; ++i) t += __hip_atomic_load(&partial[b * RED_BLOCKS + i],
+                                                                __ATOMIC_RELAXED,
+                                                                __HIP_MEMORY_SCOPE_AGENT);
+    total[b] = t;
+    done[b] = 0u;  // ready for the next call
+  }
+}
+
+// One wavefront per voxel: logits recomputed from h_L, p = exp(z - lse),
+// f = 1 + floor(p * 65024) in fp32, the leftover of 65536 - sum f added to the
+// lowest-index largest f.
+__global__ void __launch_bounds__(256) k_symbol_freqs(const int32_t* __restrict__ count,
+                                                      const int32_t* __restrict__ moff, int b,
+                                                      int64_t cap_model,
+                                                      const float* __restrict__ hL, int C,
+                                                      const float* __restrict__ H,
+                                                      const float* __restrict__ hb,
+                                                      const float* __restrict__ lse,
+                                                      uint16_t* __restrict__ out) {
+  const int lane = threadIdx.x & 63;
+  const int64_t mo = moff[b];
+  int64_t n = count[b];
+  if (mo + n > cap_model) n = 0;
+  const int64_t wstride = (int64_t)gridDim.x * (blockDim.x / 64);
+  for (int64_t v = (int64_t)blockIdx.x * (blockDim.x / 64) + (threadIdx.x >> 6); v < n; v += wstride) {
+    const float* h = hL + (mo + v) * C;
+    const float l = lse[mo + v];
+    uint32_t f[4];
+    uint32_t sum = 0, best = 0;
+    int besti = 0;
+    for (int e = 0; e < 4; ++e) {
+      const int s = lane * 4 + e;
+      float z = hb[s];
+      for (int c = 0; c < C; ++c) z = fmaf(H[c * 256 + s], h[c], z);
+      const float p = __expf(z - l);
+      f[e] = 1u + (uint32_t)floorf(p * 65024.0f);
+      sum += f[e];
+      if (f[e] > best) {
+        best = f[e];
+        besti = s;
+      }
+    }
+    for (int o = 32; o > 0; o >>= 1) {
+      sum += (uint32_t)__shfl_xor((int)sum, o);
+      const uint32_t ob = (uint32_t)__shfl_xor((int)best, o);
+      const int oi = __shfl_xor(besti, o);
+      if (ob > best || (ob == best && oi < besti)) {
+        best = ob;
+        besti = oi;
+      }
+    }
+    const uint32_t left = 65536u - sum;
+    uint16_t* dst = out + v * 256 + lane * 4;
+    for (int e = 0; e < 4; ++e) {
+      const int s = lane * 4 + e;
+      dst[e] = (uint16_t)(f[e] + (s == besti ? left : 0u));
+    }
+  }
+}
+
+__global__ void k_coords(const uint64_t* __restrict__ key, const int32_t* __restrict__ count, int b,
+                         int32_t* __restrict__ xyz, uint64_t* __restrict__ keys) {
+  const int64_t n = count[b];
+  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n;
+       i += (int64_t)gridDim.x * blockDim.x) {
+    const uint64_t k = key[i];
+    if (keys) keys[i] = k;
+    if (xyz) {
+      xyz[3 * i + 0] = (int32_t)compact3(k);
+      xyz[3 * i + 1] = (int32_t)compact3(k >> 1);
+      xyz[3 * i + 2] = (int32_t)compact3(k >> 2);
+    }
+  }
+}
+
+__global__ void k_copy_u8(const uint8_t* __restrict__ src, const int32_t* __restrict__ count, int b,
+                          uint8_t* __restrict__ dst) {
+  const int64_t n = count[b];
+  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n;
+       i += (int64_t)gridDim.x * blockDim.x)
+    dst[i] = src[i];
+}
+
+__global__ void k_copy_i32(const int32_t* __restrict__ src, const int32_t* __restrict__ count,
+                           int b, int mult, int32_t* __restrict__ dst) {
+  const int64_t n = (int64_t)count[b] * mult;
+  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n;
+       i += (int64_t)gridDim.x * blockDim.x)
+    dst[i] = src[i];
+}
+
+// neighbour map rows of scale b start at its packed model row (device value)
+__global__ void k_copy_map(const int32_t* __restrict__ nbr, const int32_t* __restrict__ moff,
+                           const int32_t* __restrict__ count, int b, int64_t cap_model,
+                           int32_t* __restrict__ dst) {
+  int64_t n = (int64_t)count[b];
+  if (moff[b] + n > cap_model) n = 0;
+  n *= 27;
+  const int64_t o = (int64_t)moff[b] * 27;
+  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n;
+       i += (int64_t)gridDim.x * blockDim.x)
+    dst[i] = nbr[o + i];
+}
+
+unsigned grid_for(int64_t cap, int per_block) {
+  int64_t g = (cap + per_block - 1) / per_block;
+  if (g > 2048) g = 2048;
+  if (g < 1) g = 1;
+  return (unsigned)g;
+}
+
+}  // namespace
+
+hipError_t launch_code_length(Ctx& c, int b_lo, int b_hi, float* bits) {
+  hipLaunchKernelGGL(k_code_length, dim3(RED_BLOCKS, b_hi - b_lo + 1), dim3(256), 0, c.stream, b_lo,
+                     c.b0(), c.d_count, c.d_moff, c.cap_pts, c.cap_model, c.lv_code, c.hlast(), c.p.channels,
+                     c.w_head_plain, c.w_hbias, c.d_lse, bits, c.d_partial, c.d_total,
+                     c.d_ticket + TK_RED);
+  return hipGetLastError();
+}
+
+hipError_t launch_symbol_freqs(Ctx& c, int b, uint16_t* freq) {
+  hipLaunchKernelGGL(k_symbol_freqs, dim3(grid_for(c.cap_pts, 4)), dim3(256), 0, c.stream,
+                     c.d_count, c.d_moff, b, c.cap_model, c.hlast(), c.p.channels, c.w_head_plain,
+                     c.w_hbias,
+                     c.d_lse, freq);
+  return hipGetLastError();
+}
+
+hipError_t launch_coords(Ctx& c, int b, int32_t* xyz, uint64_t* keys) {
+  hipLaunchKernelGGL(k_coords, dim3(grid_for(c.cap_pts, 256)), dim3(256), 0, c.stream,
+                     c.lv_key + c.lv(b), c.d_count, b, xyz, keys);
+  return hipGetLastError();
+}
+
+hipError_t launch_copy_level_u8(Ctx& c, int b, uint8_t* out) {
+  hipLaunchKernelGGL(k_copy_u8, dim3(grid_for(c.cap_pts, 256)), dim3(256), 0, c.stream,
+                     c.lv_code + c.lv(b), c.d_count, b, out);
+  return hipGetLastError();
+}
+
+hipError_t launch_copy_level_i32(Ctx& c, int b, const int32_t* src, int32_t* out) {
+  hipLaunchKernelGGL(k_copy_i32, dim3(grid_for(c.cap_pts, 256)), dim3(256), 0, c.stream, src,
+                     c.d_count, b, 1, out);
+  return hipGetLastError();
+}
+
+hipError_t launch_neighbor_map(Ctx& c, int b, int32_t* out) {
+  hipLaunchKernelGGL(k_copy_map, dim3(grid_for(c.cap_pts * 27, 256)), dim3(256), 0, c.stream,
+                     c.d_nbr, c.d_moff, c.d_count, b, c.cap_model, out);
+  return hipGetLastError();
+}
+
+}  // namespace reno

@@ -1,0 +1,104 @@
+"""C ABI: the library loads, exports every function include/reno.h declares,
+rejects bad arguments before touching the GPU, and its host rANS coder round
+trips.  Runs on the CPU (no kernel is launched)."""
+import ctypes
+import os
+import re
+
+import numpy as np
+import pytest
+
+import paper_2503_12382_amd as reno
+
+HEADER = os.path.join(os.path.dirname(os.path.dirname(__file__)), "include", "reno.h")
+
+pytestmark = pytest.mark.skipif(not os.path.exists(reno.LIB_PATH),
+                                reason="libreno.so not built (run __graft_entry__.build())")
+
+
+def declared_functions():
+    src = open(HEADER).read()
+    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+    return set(re.findall(r"\b(reno_[a-z_0-9]+)\s*\(", src))
+
+
+def test_header_and_binding_agree():
+    decl = declared_functions()
+    assert decl == set(reno._SIGS), decl ^ set(reno._SIGS)
+    assert len(decl) == 18
+
+
+def test_every_symbol_exported():
+    L = ctypes.CDLL(reno.LIB_PATH)
+    for name in declared_functions():
+        assert hasattr(L, name), name
+
+
+def test_create_rejects_bad_params_without_gpu():
+    L = reno.lib()
+    h = ctypes.c_void_p()
+    assert L.reno_create(None, None, ctypes.byref(h)) == reno.RENO_E_INVALID
+    good = dict(max_points=1000, max_model_voxels=0, max_bit_depth=12, min_bit_depth=4,
+                range_m=131.0, in_features=11, channels=32, layers=3)
+    bad_cases = [dict(max_points=0), dict(max_bit_depth=22), dict(min_bit_depth=12),
+                 dict(range_m=-1.0), dict(range_m=float("inf")), dict(in_features=8),
+                 dict(channels=24), dict(layers=0), dict(layers=9), dict(max_points=1 << 30)]
+    for bad in bad_cases:
+        p = reno.reno_params(**{**good, **bad})
+        rc = L.reno_create(ctypes.byref(p), None, ctypes.byref(h))
+        assert rc == reno.RENO_E_INVALID, bad
+        assert L.reno_last_error(None)                 # a message is set
+
+
+def test_null_context_calls():
+    L = reno.lib()
+    assert L.reno_destroy(None) == reno.RENO_E_INVALID
+    assert L.reno_sync(None) == reno.RENO_E_INVALID
+    assert L.reno_build_pyramid(None, None, 0, 10) == reno.RENO_E_INVALID
+    assert L.reno_expand(None, 4, None) == reno.RENO_E_INVALID
+    assert L.reno_predict_probs(None, 5, None, None) == reno.RENO_E_INVALID
+    assert L.reno_code_length(None, 5, None, None) == reno.RENO_E_INVALID
+
+
+def _random_tables(rs, n, peaked):
+    logits = rs.normal(size=(n, 256)) * (6.0 if peaked else 1.0)
+    p = np.exp(logits - logits.max(1, keepdims=True))
+    p /= p.sum(1, keepdims=True)
+    f = 1 + np.floor(p.astype(np.float32) * np.float32(65024)).astype(np.int64)
+    f[np.arange(n), f.argmax(1)] += 65536 - f.sum(1)
+    assert np.all(f.sum(1) == 65536)
+    return p, f.astype(np.uint16)
+
+
+@pytest.mark.parametrize("peaked", [False, True])
+def test_host_rans_round_trip(peaked):
+    rs = np.random.default_rng(31 + peaked)
+    n = 30000
+    p, f = _random_tables(rs, n, peaked)
+    sym = np.array([rs.choice(256, p=pi) for pi in p], dtype=np.uint8)
+    words = reno.rans_encode(sym, f)
+    assert np.array_equal(reno.rans_decode(words, f, n), sym)
+    ideal = -np.log2(f[np.arange(n), sym].astype(np.float64) / 65536.0).sum()
+    coded = 32.0 * words.size
+    assert abs(coded - ideal) <= n * np.log2(1 + 2.0 ** -15) + 96
+
+
+def test_host_rans_errors():
+    rs = np.random.default_rng(5)
+    n = 100
+    _, f = _random_tables(rs, n, False)
+    sym = rs.integers(0, 256, n).astype(np.uint8)
+    words = reno.rans_encode(sym, f)
+    with pytest.raises(reno.RenoError):
+        reno.rans_decode(words[:-1], f, n)            # truncated
+    bad = f.copy()
+    bad[3, 0] += 1                                     # table no longer sums to 2^16
+    with pytest.raises(reno.RenoError):
+        reno.rans_encode(sym, bad)
+
+
+def test_host_rans_empty_stream():
+    f = np.zeros((0, 256), np.uint16)
+    words = reno.rans_encode(np.zeros(0, np.uint8), f)
+    assert words.size == 2
+    assert reno.rans_decode(words, f, 0).size == 0
