@@ -69,7 +69,10 @@ typedef enum {
 /* Capacities and model shape, fixed for the life of a context. */
 typedef struct {
   int64_t max_points;        /* raw points per frame; also the per-scale voxel capacity */
-  int64_t max_model_voxels;  /* sum of N_b over the model scales; 0 selects 3*max_points */
+  int64_t max_model_voxels;  /* sum of N_b over the model scales; 0 selects
+                                (max_bit_depth - min_bit_depth - 1) * max_points, which
+                                always suffices; a tighter value saves memory and the
+                                per-frame hash clear */
   int max_bit_depth;         /* largest B accepted, <= RENO_MAX_BIT_DEPTH (keys use 3B bits) */
   int min_bit_depth;         /* b0, the coarsest scale, 0 <= b0 < B */
   double range_m;            /* R: the grid covers [-R, R) on each axis */
@@ -122,9 +125,12 @@ reno_status reno_set_base(reno_ctx* ctx, int bit_depth, const int32_t* xyz, cons
                           int64_t n);
 
 /* DECODER step (Sec. 3.1 FCG).  Records O_scale := codes[N_scale] (codes may
- * be NULL when O_scale is already known: set_base, or an encoder context)
- * and builds V_{scale+1} by keeping, for each voxel in order, the children
- * whose code bit is set, in ascending delta.  b0 <= scale < B. */
+ * be NULL when O_scale is already known, i.e. for the base scale after
+ * set_base) and builds V_{scale+1} by keeping, for each voxel in order, the
+ * children whose code bit is set, in ascending delta.  b0 <= scale < B;
+ * V_scale must exist and V_{scale+1} must not (RENO_E_STATE otherwise; an
+ * encoder context already holds every scale).  A zero code latches
+ * RENO_E_INPUT. */
 reno_status reno_expand(reno_ctx* ctx, int scale, const uint8_t* codes);
 
 /* Number of voxels of a scale (synchronises). */

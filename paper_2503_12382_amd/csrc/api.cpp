@@ -122,7 +122,10 @@ reno_status reno_create(const reno_params* p, void* hip_stream, reno_ctx** out) 
     return fail(nullptr, RENO_E_INVALID, "channels must be 16 or 32");
   if (p->layers < 1 || p->layers > RENO_MAX_LAYERS)
     return fail(nullptr, RENO_E_INVALID, "layers must be in [1, 8]");
-  int64_t cap_model = p->max_model_voxels > 0 ? p->max_model_voxels : 3 * p->max_points;
+  // N_b <= N_{b+1} <= max_points, so (model scales) x max_points always suffices
+  const int64_t nmodel = p->max_bit_depth - p->min_bit_depth - 1 > 0
+                             ? p->max_bit_depth - p->min_bit_depth - 1 : 1;
+  int64_t cap_model = p->max_model_voxels > 0 ? p->max_model_voxels : nmodel * p->max_points;
   if (cap_model >= (int64_t(1) << 30))
     return fail(nullptr, RENO_E_INVALID, "max_model_voxels must be below 2^30");
 
