@@ -1,0 +1,244 @@
+#!/usr/bin/env python3
+"""Throughput of the RENO codec hot path on one MI355X.
+
+One step = one frame encoded and decoded through the C ABI:
+  encode: build_pyramid (quantise, sort, all scales, FOG codes)
+          -> predict_probs on every model scale in one batch -> code_length
+  decode: set_base (initial state) -> for each scale: expand, predict_probs
+          -> final expand -> code_length
+The decoder's symbols are injected from the encoder (a stand-in for an
+instant entropy decoder; the host rANS round trip is covered by the tests).
+Inputs are resident in device memory before the timed region.  The default
+timed region replays the step as one HIP graph; --mode eager launches it
+call by call.
+
+Prints ONE JSON line (rank 0, N=1).
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+PEAK_FP32_MFMA_TFLOPS = 157.3
+PEAK_HBM_GBS = 8000.0
+
+
+def log(*a):
+    print("[bench]", *a, file=sys.stderr, flush=True)
+
+
+def main():
+    ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawTextHelpFormatter)
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=200)
+    ap.add_argument("--warmup", type=int, default=10)
+    ap.add_argument("--config", default="hdl64_b14")
+    ap.add_argument("--mode", choices=["graph", "eager"], default="graph")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(f"bench.py runs on one GPU only (got --gpus {args.gpus}): frames are independent, "
+              "so multi-GPU throughput is N independent copies of this line; no multi-GPU "
+              "path is built.", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    import paper_2503_12382_amd as reno
+    from synth import BY_NAME, gen_scan, gen_weights
+
+    cfg = BY_NAME[args.config]
+    B, b0, C, L = cfg.bit_depth, cfg.min_bit_depth, cfg.channels, cfg.layers
+    log("generating", cfg.name)
+    pts_np = gen_scan(cfg)
+    M = pts_np.shape[0]
+    w_np = gen_weights(C, L, seed=cfg.weight_seed)
+    dev = torch.device("cuda", 0)
+    torch.cuda.set_device(dev)
+    stream = torch.cuda.Stream(device=dev)
+    pts = torch.from_numpy(pts_np).to(dev)
+    wd = reno.weights_to_device(w_np, dev)
+
+    # probe pass with the always-sufficient capacity to learn this sensor's
+    # model-voxel count; the timed contexts are sized to it (+12.5 %)
+    with torch.cuda.stream(stream):
+        probe = reno.Context(M, B, b0, cfg.range_m, C, L, stream=stream)
+        probe.build_pyramid(pts, B)
+        counts = [probe.num_voxels(b) for b in range(b0, B + 1)]
+        probe.close()
+    model_vox = sum(counts[1:-1])
+    cap_model = (model_vox + model_vox // 8 + 4095) // 4096 * 4096
+    log("N_b", counts, "model voxels", model_vox, "capacity", cap_model)
+
+    with torch.cuda.stream(stream):
+        enc = reno.Context(M, B, b0, cfg.range_m, C, L, max_model_voxels=cap_model, stream=stream)
+        dec = reno.Context(M, B, b0, cfg.range_m, C, L, max_model_voxels=cap_model, stream=stream)
+        enc.set_weights(wd)
+        dec.set_weights(wd)
+        # decoder inputs (resident before timing): initial state and every scale's codes
+        enc.build_pyramid(pts, B)
+        base_xyz, _ = enc.coords(b0)
+        base_xyz = base_xyz.clone()
+        codes = {b: enc.occupancy_codes(b).clone() for b in range(b0, B)}
+        enc.predict_probs(reno.RENO_ALL_SCALES)
+        _, enc_total = enc.code_length(reno.RENO_ALL_SCALES, per_voxel=False)
+        pairs = {b: int((enc.neighbor_map(b) >= 0).sum().item()) for b in range(b0 + 1, B)}
+        stream.synchronize()
+
+    def step():
+        enc.build_pyramid(pts, B)
+        enc.predict_probs(reno.RENO_ALL_SCALES)
+        enc.code_length(reno.RENO_ALL_SCALES, per_voxel=False, total=False)
+        dec.set_base(B, base_xyz, codes[b0])
+        for b in range(b0 + 1, B):
+            dec.expand(b - 1, None if b - 1 == b0 else codes[b - 1])
+            dec.predict_probs(b)
+        dec.expand(B - 1, codes[B - 1])
+        dec.code_length(reno.RENO_ALL_SCALES, per_voxel=False, total=False)
+
+    with torch.cuda.stream(stream):
+        for _ in range(args.warmup):
+            step()
+        stream.synchronize()
+        _, dec_total = dec.code_length(reno.RENO_ALL_SCALES, per_voxel=False)
+        _, enc_total2 = enc.code_length(reno.RENO_ALL_SCALES, per_voxel=False)
+    if not (dec_total == enc_total == enc_total2):
+        log("decoder/encoder bit totals differ", dec_total, enc_total, enc_total2)
+        sys.exit(1)
+
+    graph = None
+    if args.mode == "graph":
+        graph = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(graph, stream=stream):
+            step()
+        with torch.cuda.stream(stream):
+            for _ in range(args.warmup):
+                graph.replay()
+        stream.synchronize()
+
+    # ---- timed region ----
+    t0 = torch.cuda.Event(enable_timing=True)
+    t1 = torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    wall0 = time.perf_counter()
+    with torch.cuda.stream(stream):
+        t0.record(stream)
+        for _ in range(args.steps):
+            if graph is not None:
+                graph.replay()
+            else:
+                step()
+        t1.record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - wall0
+    ms_total = t0.elapsed_time(t1)
+    ms_step = ms_total / args.steps
+    fps = 1000.0 / ms_step
+    log(f"{args.mode}: {ms_step * 1000:.1f} us/frame, {fps:.1f} frames/s (wall {wall:.3f} s)")
+    # results of the last replayed frame are still consistent
+    with torch.cuda.stream(stream):
+        _, chk = dec.code_length(reno.RENO_ALL_SCALES, per_voxel=False)
+    if chk != enc_total:
+        log("post-timing check failed", chk, enc_total)
+        sys.exit(1)
+
+    # ---- live kernel timing of the dominant kernel (HIP events on the same stream) ----
+    with torch.cuda.stream(stream):
+        enc.profile(["conv_last"])
+        dec.profile(["conv_last"])
+        for _ in range(args.steps):
+            step()
+        pe = enc.profile_read()
+        pd = dec.profile_read()
+        # per-kind breakdown of one eager frame (all kernels bracketed)
+        kinds = reno.KERNELS
+        enc.profile(kinds)
+        dec.profile(kinds)
+        nb = 20
+        for _ in range(nb):
+            step()
+        be, bd = enc.profile_read(), dec.profile_read()
+        enc.profile([])
+        dec.profile([])
+    breakdown = {}
+    for k in kinds:
+        ms = be.get(k, (0.0, 0))[0] + bd.get(k, (0.0, 0))[0]
+        n = be.get(k, (0.0, 0))[1] + bd.get(k, (0.0, 0))[1]
+        if n:
+            breakdown[k] = {"us_per_frame": round(1000.0 * ms / nb, 2), "launches_per_frame": n // nb}
+    cl_ms = pe["conv_last"][0] + pd["conv_last"][0]
+    cl_launches = pe["conv_last"][1] + pd["conv_last"][1]
+    # algorithmic flops of the last conv layer + head: per voxel, 2*C*C per
+    # occupied neighbour (the conv) and 2*C*256 (the head); encoder + decoder
+    flops_frame = 2 * sum(2 * C * C * pairs[b] + 2 * C * 256 * counts[b - b0] for b in pairs)
+    achieved_tflops = flops_frame * args.steps / (cl_ms * 1e-3) / 1e12
+    log(f"conv_last: {cl_launches} launches, {1000 * cl_ms / cl_launches:.1f} us avg, "
+        f"{achieved_tflops:.2f} TFLOP/s algorithmic")
+
+    # ---- CPU baseline: the oracle, single-threaded, one frame encode + decode ----
+    cpu = None
+    oracle_bpp = None
+    if not args.no_cpu_baseline:
+        import oracle
+        t = time.perf_counter()
+        P = oracle.Pyramid.from_points(pts_np, B, b0, cfg.range_m)
+        T_enc, _ = P.totals(w_np)
+        t_enc = time.perf_counter() - t
+        t = time.perf_counter()
+        D = oracle.Pyramid.from_codes(P.xyz(b0), b0, B, [P.codes(b) for b in range(b0, B)])
+        T_dec, _ = D.totals(w_np)
+        t_dec = time.perf_counter() - t
+        oracle_bpp = T_enc / M
+        cpu = {"value": round(1.0 / (t_enc + t_dec), 4), "unit": "frames/s", "cores": 1,
+               "kind": "oracle",
+               "sample": f"one {cfg.name} frame ({M} points): oracle encode {t_enc:.1f} s "
+                         f"(pyramid, codes, model, bits) + decode {t_dec:.1f} s "
+                         f"(FCG expansion, model, bits), single-threaded C++ in fp64"}
+        log("cpu baseline", cpu)
+
+    voxels_frame = sum(counts)
+    out = {
+        "metric": "frames/s + Mvoxels/s, encode+decode model path, 14-bit 64-beam scan; bits/pt",
+        "value": round(fps, 2),
+        "unit": "frames/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_step, 5),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f32",
+        "data": "synthetic",
+        "mvoxels_per_s": round(fps * voxels_frame / 1e6, 2),
+        "bits_per_point": round(enc_total / M, 4),
+        "oracle_bits_per_point": None if oracle_bpp is None else round(oracle_bpp, 4),
+        "config": {"workload": f"{cfg.name}: synthetic {cfg.beams}-beam x {cfg.azimuth_steps}-azimuth "
+                               f"LiDAR scan, {B}-bit grid over +-{cfg.range_m} m, pyramid {B}->{b0}, "
+                               f"random-init predictor C={C} L={L}, one frame encoded + decoded "
+                               "per step",
+                   "points": M, "voxels_per_frame": voxels_frame, "model_voxels": model_vox,
+                   "mode": args.mode},
+        "roofline": {"bound": "mfma", "kernel": "conv_last (last sparse conv + 256-way head)",
+                     "achieved": round(achieved_tflops, 3), "peak": PEAK_FP32_MFMA_TFLOPS,
+                     "unit": "TFLOP/s", "frac": round(achieved_tflops / PEAK_FP32_MFMA_TFLOPS, 4),
+                     "traffic": None,
+                     "avg_launch_us": round(1000 * cl_ms / cl_launches, 2),
+                     "launches": cl_launches},
+        "cpu_baseline": cpu,
+        "kernels": breakdown,
+    }
+    print(json.dumps(out), flush=True)
+    enc.close()
+    dec.close()
+
+
+if __name__ == "__main__":
+    main()

@@ -186,6 +186,32 @@ reno_status reno_rans_encode(const uint8_t* sym, const uint16_t* freq, int64_t n
 reno_status reno_rans_decode(const uint32_t* in, int64_t nwords, const uint16_t* freq, int64_t n,
                              uint8_t* sym);
 
+/* Kernel timing for measurement.  While a kind's bit is set in `kind_mask`,
+ * every launch of that kind is bracketed by two HIP events recorded on the
+ * context stream (event pairs come from a pool created by this call; launches
+ * beyond the pool are not timed).  reno_profile resets the accumulators;
+ * reno_profile_read synchronises and returns, per kind, the summed
+ * event-to-event milliseconds and the number of timed launches (arrays of
+ * RENO_K_COUNT).  Launches captured into a HIP graph are not timed. */
+typedef enum {
+  RENO_K_ZERO = 0,      /* per-frame clear of counters, look-back state and hash */
+  RENO_K_QUANTIZE,      /* quantisation, Morton keys, digit histograms */
+  RENO_K_SORT,          /* one radix-sort pass */
+  RENO_K_PYRAMID,       /* all scales, parents, first children, hash inserts */
+  RENO_K_CODES,         /* FOG codes and layer-1 input bits */
+  RENO_K_SET_BASE,      /* decoder initial state */
+  RENO_K_EXPAND,        /* FCG expansion of one scale */
+  RENO_K_CONV_FIRST,    /* first conv layer with the hash probes */
+  RENO_K_CONV_MID,      /* a middle conv layer */
+  RENO_K_CONV_LAST,     /* last conv layer fused with the 256-way head and softmax normaliser */
+  RENO_K_CODE_LENGTH,   /* ideal bits and per-scale sums */
+  RENO_K_OTHER,         /* weight packing, getters, symbol tables */
+  RENO_K_COUNT
+} reno_kernel;
+
+reno_status reno_profile(reno_ctx* ctx, uint32_t kind_mask);
+reno_status reno_profile_read(reno_ctx* ctx, double* ms_host, int64_t* launches_host);
+
 #ifdef __cplusplus
 }
 #endif

@@ -71,7 +71,12 @@ _SIGS = {
     "reno_symbol_freqs": (_int, [_vp, _int, _vp]),
     "reno_rans_encode": (_int, [_vp, _vp, _i64, _vp, _i64, ctypes.POINTER(_i64)]),
     "reno_rans_decode": (_int, [_vp, _i64, _vp, _i64, _vp]),
+    "reno_profile": (_int, [_vp, ctypes.c_uint32]),
+    "reno_profile_read": (_int, [_vp, _vp, _vp]),
 }
+
+KERNELS = ["zero", "quantize", "sort", "pyramid", "codes", "set_base", "expand", "conv_first",
+           "conv_mid", "conv_last", "code_length", "other"]
 
 _lib = None
 
@@ -80,6 +85,10 @@ def lib():
     """The loaded C library; raises if it has not been built."""
     global _lib
     if _lib is None:
+        try:                      # load torch's HIP runtime first so that both share it
+            import torch  # noqa: F401
+        except ImportError:
+            pass
         if not os.path.exists(LIB_PATH):
             raise RuntimeError(f"{LIB_PATH} is missing: build it with "
                                "`python -m paper_2503_12382_amd.build` (no CPU fallback exists)")
@@ -239,6 +248,19 @@ class Context:
         out = self._empty((max(n, 1), 27), self.torch.int32)
         self._check(lib().reno_neighbor_map(self._h, scale, _ptr(out)))
         return out[:n]
+
+    def profile(self, kinds=()):
+        """Time the launches of the named kernel kinds (see KERNELS) with HIP events."""
+        mask = 0
+        for k in kinds:
+            mask |= 1 << KERNELS.index(k)
+        self._check(lib().reno_profile(self._h, mask))
+
+    def profile_read(self) -> dict:
+        ms = np.zeros(len(KERNELS), np.float64)
+        n = np.zeros(len(KERNELS), np.int64)
+        self._check(lib().reno_profile_read(self._h, ms.ctypes.data_as(_vp), n.ctypes.data_as(_vp)))
+        return {k: (float(ms[i]), int(n[i])) for i, k in enumerate(KERNELS) if n[i]}
 
     def symbol_freqs(self, scale: int):
         n = self.num_voxels(scale)

@@ -58,6 +58,8 @@ void free_all(Ctx* c) {
   if (c->h_total) (void)hipHostFree(c->h_total);
   if (c->h_count) (void)hipHostFree(c->h_count);
   if (c->h_err) (void)hipHostFree(c->h_err);
+  for (hipEvent_t ev : c->prof_pool) (void)hipEventDestroy(ev);
+  c->prof_pool.clear();
 }
 
 // Waits for the stream and turns latched device errors into a status.
@@ -403,6 +405,40 @@ reno_status reno_symbol_freqs(reno_ctx* c, int scale, uint16_t* freq) {
   if (!c || !freq) return fail(c, RENO_E_INVALID, "null argument");
   if (!has(c->have_pred, scale)) return fail(c, RENO_E_STATE, "predict_probs of the scale not run");
   RENO_HIP(c, reno::launch_symbol_freqs(*c, scale, freq));
+  return RENO_OK;
+}
+
+reno_status reno_profile(reno_ctx* c, uint32_t kind_mask) {
+  if (!c) return RENO_E_INVALID;
+  if (kind_mask >> RENO_K_COUNT) return fail(c, RENO_E_INVALID, "unknown kernel kind");
+  RENO_HIP(c, hipStreamSynchronize(c->stream));
+  const size_t pool = 2 * 16384;
+  while (kind_mask && c->prof_pool.size() < pool) {
+    hipEvent_t ev;
+    RENO_HIP(c, hipEventCreate(&ev));
+    c->prof_pool.push_back(ev);
+  }
+  c->prof_mask = kind_mask;
+  c->prof_used = 0;
+  c->prof_recs.clear();
+  return RENO_OK;
+}
+
+reno_status reno_profile_read(reno_ctx* c, double* ms_host, int64_t* launches_host) {
+  if (!c || !ms_host || !launches_host) return fail(c, RENO_E_INVALID, "null argument");
+  RENO_HIP(c, hipStreamSynchronize(c->stream));
+  for (int k = 0; k < RENO_K_COUNT; ++k) {
+    ms_host[k] = 0.0;
+    launches_host[k] = 0;
+  }
+  for (const reno::ProfRec& r : c->prof_recs) {
+    float ms = 0.0f;
+    RENO_HIP(c, hipEventElapsedTime(&ms, r.a, r.b));
+    ms_host[r.kind] += ms;
+    launches_host[r.kind] += 1;
+  }
+  c->prof_used = 0;
+  c->prof_recs.clear();
   return RENO_OK;
 }
 

@@ -7,6 +7,7 @@
 #include <stdint.h>
 
 #include <string>
+#include <vector>
 
 #include "../../include/reno.h"
 #include "dev.h"
@@ -34,6 +35,11 @@ constexpr int TK_SORT = 0;        // + pass
 constexpr int TK_PYR = 16;
 constexpr int TK_EXPAND = 17;     // + scale (decoder: one per expand call)
 constexpr int TK_RED = 40;        // + scale slot (reduction done-counters, self-resetting)
+
+struct ProfRec {
+  int kind;
+  hipEvent_t a, b;
+};
 
 struct Ctx {
   reno_params p{};
@@ -94,6 +100,12 @@ struct Ctx {
   uint32_t have_pred = 0;       // bit b: TOP evaluated on V_b
   int64_t npoints = 0;
 
+  // kernel timing (reno_profile)
+  uint32_t prof_mask = 0;
+  std::vector<hipEvent_t> prof_pool;
+  size_t prof_used = 0;
+  std::vector<ProfRec> prof_recs;
+
   int64_t pyr_tiles = 0;    // max tiles of the pyramid pass
   int64_t exp_tiles = 0;    // max tiles of one expansion
 
@@ -108,6 +120,24 @@ struct Ctx {
   int64_t lv(int b) const { return (int64_t)(b - p.min_bit_depth) * cap_pts; }
   // buffer that holds the last conv layer's output (h_L), per the ping-pong
   float* hlast() const { return (p.layers & 1) ? h_a : h_b; }
+};
+
+// Brackets the launches made during its lifetime with a pair of events when
+// the kind is being profiled.
+struct ProfScope {
+  Ctx& c;
+  int kind;
+  hipEvent_t end = nullptr;
+  ProfScope(Ctx& ctx, int k) : c(ctx), kind(k) {
+    if (!((c.prof_mask >> kind) & 1u) || c.prof_used + 2 > c.prof_pool.size()) return;
+    hipEvent_t a = c.prof_pool[c.prof_used++];
+    end = c.prof_pool[c.prof_used++];
+    (void)hipEventRecord(a, c.stream);
+    c.prof_recs.push_back(ProfRec{kind, a, end});
+  }
+  ~ProfScope() {
+    if (end) (void)hipEventRecord(end, c.stream);
+  }
 };
 
 // ---- kernel launchers (each enqueues on ctx.stream; return hipError_t) ----

@@ -160,6 +160,7 @@ __global__ void __launch_bounds__(EXP_THREADS) k_expand(ExpArgs a) {
 }  // namespace
 
 hipError_t launch_set_base(Ctx& c, const int32_t* xyz, const uint8_t* codes, int64_t n, int B) {
+  ProfScope ps_(c, RENO_K_SET_BASE);
   (void)B;
   const int b0 = c.b0();
   int64_t blocks = (n + 255) / 256;
@@ -171,6 +172,7 @@ hipError_t launch_set_base(Ctx& c, const int32_t* xyz, const uint8_t* codes, int
 }
 
 hipError_t launch_expand(Ctx& c, int b, const uint8_t* codes, int B) {
+  ProfScope ps_(c, RENO_K_EXPAND);
   ExpArgs a;
   a.codes_in = codes;
   a.b = b;

@@ -106,7 +106,6 @@ __global__ void __launch_bounds__(CONV_THREADS) k_conv(ConvArgs a) {
   __shared__ __attribute__((aligned(16))) float s_h[HSZ];
   __shared__ int32_t s_map[CONV_WAVES][16 * 28];
   __shared__ int64_t s_tpre[NLEV + 1];
-  __shared__ int32_t s_roff[NLEV + 1];
 
   const int tid = threadIdx.x, w = tid >> 6, lane = tid & 63;
   const int r = lane & 15, g = lane >> 4;
@@ -322,6 +321,7 @@ hipError_t run_layer(Ctx& c, bool first, bool last, const ConvArgs& a) {
 }  // namespace
 
 hipError_t launch_pack_weights(Ctx& c, const reno_weights& w) {
+  ProfScope ps_(c, RENO_K_OTHER);
   const int C = c.p.channels;
   int c_in = RENO_IN_FEATURES;
   for (int l = 0; l < c.p.layers; ++l) {
@@ -366,6 +366,7 @@ hipError_t launch_model(Ctx& c, int b_lo, int b_hi, float* logits) {
     a.bias = c.w_bias[l];
     a.logits = (l == L - 1) ? logits : nullptr;
     const bool first = l == 0, last = l == L - 1;
+    ProfScope ps_(c, last ? RENO_K_CONV_LAST : (first ? RENO_K_CONV_FIRST : RENO_K_CONV_MID));
     e = (c.p.channels == 32) ? run_layer<32>(c, first, last, a) : run_layer<16>(c, first, last, a);
   }
   return e;

@@ -165,6 +165,7 @@ unsigned grid_for(int64_t cap, int per_block) {
 }  // namespace
 
 hipError_t launch_code_length(Ctx& c, int b_lo, int b_hi, float* bits) {
+  ProfScope ps_(c, RENO_K_CODE_LENGTH);
   hipLaunchKernelGGL(k_code_length, dim3(RED_BLOCKS, b_hi - b_lo + 1), dim3(256), 0, c.stream, b_lo,
                      c.b0(), c.d_count, c.d_moff, c.cap_pts, c.cap_model, c.lv_code, c.hlast(), c.p.channels,
                      c.w_head_plain, c.w_hbias, c.d_lse, bits, c.d_partial, c.d_total,
@@ -173,6 +174,7 @@ hipError_t launch_code_length(Ctx& c, int b_lo, int b_hi, float* bits) {
 }
 
 hipError_t launch_symbol_freqs(Ctx& c, int b, uint16_t* freq) {
+  ProfScope ps_(c, RENO_K_OTHER);
   hipLaunchKernelGGL(k_symbol_freqs, dim3(grid_for(c.cap_pts, 4)), dim3(256), 0, c.stream,
                      c.d_count, c.d_moff, b, c.cap_model, c.hlast(), c.p.channels, c.w_head_plain,
                      c.w_hbias,
@@ -181,24 +183,28 @@ hipError_t launch_symbol_freqs(Ctx& c, int b, uint16_t* freq) {
 }
 
 hipError_t launch_coords(Ctx& c, int b, int32_t* xyz, uint64_t* keys) {
+  ProfScope ps_(c, RENO_K_OTHER);
   hipLaunchKernelGGL(k_coords, dim3(grid_for(c.cap_pts, 256)), dim3(256), 0, c.stream,
                      c.lv_key + c.lv(b), c.d_count, b, xyz, keys);
   return hipGetLastError();
 }
 
 hipError_t launch_copy_level_u8(Ctx& c, int b, uint8_t* out) {
+  ProfScope ps_(c, RENO_K_OTHER);
   hipLaunchKernelGGL(k_copy_u8, dim3(grid_for(c.cap_pts, 256)), dim3(256), 0, c.stream,
                      c.lv_code + c.lv(b), c.d_count, b, out);
   return hipGetLastError();
 }
 
 hipError_t launch_copy_level_i32(Ctx& c, int b, const int32_t* src, int32_t* out) {
+  ProfScope ps_(c, RENO_K_OTHER);
   hipLaunchKernelGGL(k_copy_i32, dim3(grid_for(c.cap_pts, 256)), dim3(256), 0, c.stream, src,
                      c.d_count, b, 1, out);
   return hipGetLastError();
 }
 
 hipError_t launch_neighbor_map(Ctx& c, int b, int32_t* out) {
+  ProfScope ps_(c, RENO_K_OTHER);
   hipLaunchKernelGGL(k_copy_map, dim3(grid_for(c.cap_pts * 27, 256)), dim3(256), 0, c.stream,
                      c.d_nbr, c.d_moff, c.d_count, b, c.cap_model, out);
   return hipGetLastError();

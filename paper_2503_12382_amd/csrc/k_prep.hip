@@ -344,6 +344,7 @@ __global__ void __launch_bounds__(256) k_codes(const uint64_t* __restrict__ key,
 }  // namespace
 
 hipError_t launch_zero(Ctx& c, void* const* ptrs, const size_t* bytes, int n) {
+  ProfScope ps_(c, RENO_K_ZERO);
   ZeroArgs a{};
   uint64_t most = 0;
   for (int i = 0; i < n && i < 8; ++i) {
@@ -360,6 +361,7 @@ hipError_t launch_zero(Ctx& c, void* const* ptrs, const size_t* bytes, int n) {
 }
 
 hipError_t launch_quantize(Ctx& c, const float* pts, int64_t n, int B, int passes) {
+  ProfScope ps_(c, RENO_K_QUANTIZE);
   int64_t blocks = (n + 255) / 256;
   if (blocks > 1024) blocks = 1024;
   if (blocks < 1) blocks = 1;
@@ -369,6 +371,7 @@ hipError_t launch_quantize(Ctx& c, const float* pts, int64_t n, int B, int passe
 }
 
 hipError_t launch_sort_pass(Ctx& c, const uint64_t* in, uint64_t* out, int64_t n, int pass) {
+  ProfScope ps_(c, RENO_K_SORT);
   const int64_t tiles = (n + SORT_TILE - 1) / SORT_TILE;
   uint32_t* status = c.st_sort(pass);
   hipLaunchKernelGGL(k_sort_pass, dim3((unsigned)tiles), dim3(SORT_THREADS), 0, c.stream, in, out,
@@ -378,6 +381,7 @@ hipError_t launch_sort_pass(Ctx& c, const uint64_t* in, uint64_t* out, int64_t n
 }
 
 hipError_t launch_pyramid(Ctx& c, const uint64_t* sorted, int64_t n, int B) {
+  ProfScope ps_(c, RENO_K_PYRAMID);
   PyrArgs a;
   a.S = sorted;
   a.n = n;
@@ -402,6 +406,7 @@ hipError_t launch_pyramid(Ctx& c, const uint64_t* sorted, int64_t n, int B) {
 }
 
 hipError_t launch_codes(Ctx& c, int B) {
+  ProfScope ps_(c, RENO_K_CODES);
   int64_t work = (int64_t)(B - c.b0()) * c.npoints;
   int64_t blocks = (work + 255) / 256;
   if (blocks > 2048) blocks = 2048;
