@@ -162,7 +162,7 @@ reno_status reno_create(const reno_params* p, void* hip_stream, reno_ctx** out) 
   A(dalloc(&c->lv_code, lvn));
   A(dalloc(&c->lv_parent, lvn));
   A(dalloc(&c->lv_fc, lvn));
-  A(dalloc(&c->lv_feat, lvn));
+  A(dalloc(&c->lv_feat, lvn + 8));  // entry lvn stays zero: absent-neighbour input
   A(dalloc(&c->d_count, reno::NLEV));
   A(dalloc(&c->d_moff, reno::NLEV + 1));
   A(dalloc(&c->d_err, 4));
@@ -170,11 +170,11 @@ reno_status reno_create(const reno_params* p, void* hip_stream, reno_ctx** out) 
   A(dalloc(&c->d_ticket, reno::TICKETS));
   A(dalloc(&c->d_status, (size_t)c->status_words));
   A(dalloc(&c->d_hash, size_t(1) << c->hash_lg));
-  A(dalloc(&c->h_a, (size_t)cap_model * C));
-  A(dalloc(&c->h_b, (size_t)cap_model * C));
-  A(dalloc(&c->d_nbr, (size_t)cap_model * 27));
+  A(dalloc(&c->h_a, (size_t)(cap_model + 1) * C));  // row cap_model stays zero
+  A(dalloc(&c->h_b, (size_t)(cap_model + 1) * C));
+  A(dalloc(&c->d_nbr, (size_t)cap_model * reno::NBR_STRIDE));
   A(dalloc(&c->d_lse, (size_t)cap_model));
-  A(dalloc(&c->d_partial, (size_t)reno::NLEV * reno::RED_BLOCKS));
+  A(dalloc(&c->d_partial, (size_t)reno::NLEV * ((c->cap_pts + 1023) / 1024)));
   A(dalloc(&c->d_total, reno::NLEV));
   int c_in = RENO_IN_FEATURES;
   for (int l = 0; l < p->layers; ++l) {
@@ -195,8 +195,15 @@ reno_status reno_create(const reno_params* p, void* hip_stream, reno_ctx** out) 
     delete c;
     return fail(nullptr, e == hipErrorOutOfMemory ? RENO_E_NOMEM : RENO_E_HIP, msg);
   }
-  // reduction done-counters start at zero and reset themselves after use
+  // reduction done-counters start at zero and reset themselves after use; the
+  // reserved zero row of each feature buffer and the zero input-bit entry are
+  // never written afterwards
   e = hipMemsetAsync(c->d_ticket, 0, sizeof(uint32_t) * reno::TICKETS, c->stream);
+  if (e == hipSuccess)
+    e = hipMemsetAsync(c->h_a + (size_t)cap_model * C, 0, sizeof(float) * C, c->stream);
+  if (e == hipSuccess)
+    e = hipMemsetAsync(c->h_b + (size_t)cap_model * C, 0, sizeof(float) * C, c->stream);
+  if (e == hipSuccess) e = hipMemsetAsync(c->lv_feat + lvn, 0, 16, c->stream);
   if (e == hipSuccess) e = hipStreamSynchronize(c->stream);
   if (e != hipSuccess) {
     const std::string msg = std::string("init failed: ") + hipGetErrorString(e);

@@ -24,11 +24,11 @@ constexpr int MAX_PASSES = (3 * RENO_MAX_BIT_DEPTH + RADIX_BITS - 1) / RADIX_BIT
 constexpr int PYR_THREADS = 256;
 constexpr int PYR_KPT = 4;
 constexpr int PYR_TILE = PYR_THREADS * PYR_KPT;
-constexpr int EXP_THREADS = 256;
-constexpr int EXP_KPT = 4;
+constexpr int EXP_THREADS = 512;
+constexpr int EXP_KPT = 2;
 constexpr int EXP_TILE = EXP_THREADS * EXP_KPT;
-constexpr int RED_BLOCKS = 32;                  // partial sums per scale in the bits reduction
 constexpr int TICKETS = 64;
+constexpr int NBR_STRIDE = 32;                  // neighbour-map row: 27 offsets + 5 padding
 
 // ticket slots
 constexpr int TK_SORT = 0;        // + pass
@@ -76,9 +76,9 @@ struct Ctx {
   // model buffers (packed model rows: scale b at d_moff[b] ..)
   float* h_a = nullptr;         // [cap_model][C]
   float* h_b = nullptr;
-  int32_t* d_nbr = nullptr;     // [cap_model][27]
+  int32_t* d_nbr = nullptr;     // [cap_model][NBR_STRIDE]
   float* d_lse = nullptr;       // [cap_model]
-  double* d_partial = nullptr;  // [NLEV][RED_BLOCKS]
+  double* d_partial = nullptr;  // [NLEV][ceil(cap_pts / 1024)] per-chunk bit sums
   double* d_total = nullptr;    // [NLEV]
   double* h_total = nullptr;    // pinned host mirror [NLEV]
   int32_t* h_count = nullptr;   // pinned host mirror [NLEV]

@@ -81,9 +81,14 @@ constexpr uint32_t LB_SPIN_LIMIT = 1u << 24;
 // The calling thread owns counter `c` of tile `tile` (status row stride
 // `width`).  Publishes the tile aggregate, walks back over earlier tiles until
 // an inclusive prefix is found, publishes its own inclusive prefix and returns
-// the exclusive one.  Earlier tiles took their tickets earlier and are
-// therefore already running; each publishes its aggregate without waiting, so
-// every wait ends.  A bound on the wait latches ERR_SPIN instead of hanging.
+// the exclusive one.  The walk reads LB_BATCH predecessors per round trip and
+// consumes them in order, stopping at the first inclusive prefix or retrying
+// from the first one not yet published.  Earlier tiles took their tickets
+// earlier and are therefore already running; each publishes its aggregate
+// without waiting, so every wait ends.  A bound on the wait latches ERR_SPIN
+// instead of hanging.
+constexpr int LB_BATCH = 8;
+
 __device__ __forceinline__ uint32_t lookback(uint32_t* status, int width, int tile, int c,
                                              uint32_t agg, uint32_t* err) {
   uint32_t* mine = status + (size_t)tile * width + c;
@@ -95,32 +100,93 @@ __device__ __forceinline__ uint32_t lookback(uint32_t* status, int width, int ti
   uint32_t excl = 0;
   uint32_t spins = 0;
   for (int t = tile - 1; t >= 0;) {
-    uint32_t v = ld_status(status + (size_t)t * width + c);
-    uint32_t f = v & ~LB_VAL;
-    if (f == 0) {
+    uint32_t v[LB_BATCH];
+#pragma unroll
+    for (int i = 0; i < LB_BATCH; ++i)
+      v[i] = (t - i >= 0) ? ld_status(status + (size_t)(t - i) * width + c) : LB_INC;
+    int used = 0;
+    bool done = false, wait = false;
+#pragma unroll
+    for (int i = 0; i < LB_BATCH; ++i) {
+      if (done || wait) continue;
+      const uint32_t f = v[i] & ~LB_VAL;
+      if (f == 0) {
+        wait = true;
+        continue;
+      }
+      excl += v[i] & LB_VAL;
+      ++used;
+      if (f == LB_INC) done = true;
+    }
+    if (done) break;
+    t -= used;
+    if (wait) {
       if (++spins > LB_SPIN_LIMIT) {
         latch(err, ERR_SPIN);
         break;
       }
       __builtin_amdgcn_s_sleep(1);
-      continue;
     }
-    excl += v & LB_VAL;
-    if (f == LB_INC) break;
-    --t;
   }
   st_status(mine, LB_INC | (excl + agg));
   return excl;
 }
 
+// Single-counter look-back run by all 64 lanes of one wavefront: lane i reads
+// predecessor t-i, so one round trip covers 64 tiles.  Returns the exclusive
+// prefix (same value in every lane).
+__device__ __forceinline__ uint32_t lookback_wave(uint32_t* status, int tile, uint32_t agg,
+                                                  uint32_t* err) {
+  const int lane = (int)(threadIdx.x & 63);
+  if (tile == 0) {
+    if (lane == 0) st_status(status, LB_INC | agg);
+    return 0;
+  }
+  if (lane == 0) st_status(status + tile, LB_AGG | agg);
+  uint32_t excl = 0;
+  uint32_t spins = 0;
+  for (int t = tile - 1; t >= 0;) {
+    const int my = t - lane;
+    const uint32_t v = my >= 0 ? ld_status(status + my) : LB_INC;
+    const uint32_t f = v & ~LB_VAL;
+    const uint64_t notready = __ballot(f == 0);
+    const uint64_t inc = __ballot(f == LB_INC);
+    const uint64_t stop = notready | inc;
+    // lanes before the first stopping lane hold aggregates to consume; an
+    // inclusive prefix there ends the walk, an unpublished one is retried
+    const int first = stop ? __builtin_ctzll(stop) : 64;
+    const bool take_inc = first < 64 && ((inc >> first) & 1ull);
+    const int ntake = first + (take_inc ? 1 : 0);
+    uint32_t x = lane < ntake ? (v & LB_VAL) : 0u;
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) x += (uint32_t)__shfl_xor((int)x, o);
+    excl += x;
+    if (take_inc) break;
+    t -= ntake;
+    if (first < 64) {  // a predecessor has not published yet
+      if (++spins > LB_SPIN_LIMIT) {
+        latch(err, ERR_SPIN);
+        break;
+      }
+      __builtin_amdgcn_s_sleep(1);
+    }
+  }
+  if (lane == 0) st_status(status + tile, LB_INC | (excl + agg));
+  return excl;
+}
+
 // ---- open-addressing coordinate hash in HBM ----
-// One table serves every scale of a frame: a scale-b key is tagged with a
-// sentinel bit at position 3b (key < 2^{3b}), which makes tagged keys of
-// different scales distinct and never 0 (0 marks an empty slot).
+// Maps a voxel of a parent scale to its occupancy code and the row of its
+// first child, so that any cell of the next scale can be resolved from one
+// probe: the child with octant d exists iff bit d of the code is set, and its
+// row is first + popcount(code & ((1 << d) - 1)) (the FCG order).  One table
+// serves every scale of a frame: a scale-b key is tagged with a sentinel bit
+// at position 3b (key < 2^{3b}), which makes tagged keys of different scales
+// distinct and never 0 (0 marks an empty slot).
 struct alignas(16) HashSlot {
   unsigned long long key;
-  int32_t row;
-  int32_t pad;
+  int32_t first;   // row of the first child in the next scale
+  uint32_t code;   // occupancy code of the voxel
 };
 
 __device__ __forceinline__ uint64_t tag_key(uint64_t key, int b) { return key | (1ull << (3 * b)); }
@@ -129,15 +195,16 @@ __device__ __forceinline__ uint32_t hash_home(uint64_t tk, int lg) {
   return (uint32_t)((tk * 0x9E3779B97F4A7C15ull) >> (64 - lg));
 }
 
-// Inserts tagged key -> row with linear probing (64-bit CAS on the key).
-__device__ __forceinline__ void hash_insert(HashSlot* tab, int lg, uint64_t tk, int32_t row,
-                                            uint32_t* err) {
+// Inserts tagged key -> (first, code) with linear probing (64-bit CAS on the key).
+__device__ __forceinline__ void hash_insert(HashSlot* tab, int lg, uint64_t tk, int32_t first,
+                                            uint32_t code, uint32_t* err) {
   const uint32_t mask = (1u << lg) - 1u;
   uint32_t h = hash_home(tk, lg);
   for (uint32_t step = 0; step <= mask; ++step) {
     unsigned long long prev = atomicCAS(&tab[h].key, 0ull, (unsigned long long)tk);
     if (prev == 0ull) {
-      tab[h].row = row;
+      tab[h].first = first;
+      tab[h].code = code;
       return;
     }
     if (prev == tk) {
@@ -149,18 +216,41 @@ __device__ __forceinline__ void hash_insert(HashSlot* tab, int lg, uint64_t tk, 
   latch(err, ERR_HASH_FULL);
 }
 
-// Row of a tagged key, or -1.  The table was built by an earlier kernel.
-__device__ __forceinline__ int32_t hash_find(const HashSlot* tab, int lg, uint64_t tk) {
+// (first, code) of a tagged key; code 0 (no children) when absent.  The
+// table was built by an earlier kernel.
+__device__ __forceinline__ uint2 hash_find(const HashSlot* tab, int lg, uint64_t tk) {
   const uint32_t mask = (1u << lg) - 1u;
   uint32_t h = hash_home(tk, lg);
   for (uint32_t step = 0; step <= mask; ++step) {
     const uint4 s = *reinterpret_cast<const uint4*>(&tab[h]);
     const uint64_t k = ((uint64_t)s.y << 32) | s.x;
-    if (k == tk) return (int32_t)s.z;
-    if (k == 0ull) return -1;
+    if (k == tk) return make_uint2(s.z, s.w);
+    if (k == 0ull) return make_uint2(0u, 0u);
     h = (h + 1u) & mask;
   }
-  return -1;
+  return make_uint2(0u, 0u);
+}
+
+// N lookups at once (tk == 0: no query, result code 0): the home slots of all
+// queries are loaded together, so a lane pays one memory round trip unless a
+// query lands on a slot holding another key.
+template <int N>
+__device__ __forceinline__ void hash_find_n(const HashSlot* tab, int lg, const uint64_t* tk,
+                                            uint2* out) {
+  uint4 s[N];
+#pragma unroll
+  for (int j = 0; j < N; ++j)
+    s[j] = *reinterpret_cast<const uint4*>(&tab[hash_home(tk[j] ? tk[j] : 1ull, lg)]);
+#pragma unroll
+  for (int j = 0; j < N; ++j) {
+    const uint64_t k = ((uint64_t)s[j].y << 32) | s[j].x;
+    out[j] = make_uint2(0u, 0u);
+    if (!tk[j]) continue;
+    if (k == tk[j])
+      out[j] = make_uint2(s[j].z, s[j].w);
+    else if (k != 0ull)  // collision: continue linear probing from the home slot
+      out[j] = hash_find(tab, lg, tk[j]);
+  }
 }
 
 }  // namespace reno

@@ -65,8 +65,9 @@ struct ExpArgs {
 
 __global__ void __launch_bounds__(EXP_THREADS) k_expand(ExpArgs a) {
   __shared__ uint32_t s_tile;
-  __shared__ uint32_t s_wtot[4];
+  __shared__ uint32_t s_wtot[EXP_THREADS / 64];
   __shared__ uint32_t s_base;
+  constexpr int NW = EXP_THREADS / 64;
   const int tid = threadIdx.x, w = tid >> 6, lane = tid & 63;
   const int64_t np = a.count[a.b];
   const int64_t ntiles = (np + EXP_TILE - 1) / EXP_TILE;
@@ -84,8 +85,9 @@ __global__ void __launch_bounds__(EXP_THREADS) k_expand(ExpArgs a) {
   if (tile >= ntiles) return;
   const int64_t base = tile * EXP_TILE;
 
+  // popcount scan over the tile's parents (element j of wave w: w*64*KPT + j*64 + lane)
   uint32_t code[EXP_KPT], incl[EXP_KPT];
-  uint32_t run = 0;  // wave running total before element j
+  uint32_t run = 0;
 #pragma unroll
   for (int j = 0; j < EXP_KPT; ++j) {
     const int64_t p = base + (int64_t)w * 64 * EXP_KPT + j * 64 + lane;
@@ -107,32 +109,35 @@ __global__ void __launch_bounds__(EXP_THREADS) k_expand(ExpArgs a) {
   }
   if (lane == 0) s_wtot[w] = run;
   __syncthreads();
-  if (tid == 0) {
-    const uint32_t t0 = s_wtot[0], t1 = s_wtot[1], t2 = s_wtot[2], t3 = s_wtot[3];
-    const uint32_t tot = t0 + t1 + t2 + t3;
-    const uint32_t ex = lookback(a.status, 1, (int)tile, 0, tot, a.err);
-    s_base = ex;
-    s_wtot[0] = 0;
-    s_wtot[1] = t0;
-    s_wtot[2] = t0 + t1;
-    s_wtot[3] = t0 + t1 + t2;
-    if (tile == ntiles - 1) {
-      int64_t nn = (int64_t)ex + tot;
-      if (nn > a.cap_pts) {
-        latch(a.err, ERR_CAPACITY);
-        nn = a.cap_pts;
+  if (w == 0) {
+    uint32_t tot = 0;
+    for (int i = 0; i < NW; ++i) tot += s_wtot[i];
+    const uint32_t ex = lookback_wave(a.status, (int)tile, tot, a.err);
+    if (lane == 0) {
+      s_base = ex;
+      uint32_t acc = 0;
+      for (int i = 0; i < NW; ++i) {
+        const uint32_t t = s_wtot[i];
+        s_wtot[i] = acc;
+        acc += t;
       }
-      a.count[bn] = (int32_t)nn;
-      if (bn < a.B) {
-        const int64_t mo = (int64_t)a.moff[bn] + nn;
-        if (mo > a.cap_model) latch(a.err, ERR_CAPACITY);
-        a.moff[bn + 1] = (int32_t)mo;
+      if (tile == ntiles - 1) {
+        int64_t nn = (int64_t)ex + tot;
+        if (nn > a.cap_pts) {
+          latch(a.err, ERR_CAPACITY);
+          nn = a.cap_pts;
+        }
+        a.count[bn] = (int32_t)nn;
+        if (bn < a.B) {
+          const int64_t mo = (int64_t)a.moff[bn] + nn;
+          if (mo > a.cap_model) latch(a.err, ERR_CAPACITY);
+          a.moff[bn + 1] = (int32_t)mo;
+        }
       }
     }
   }
   __syncthreads();
   const int64_t wbase = (int64_t)s_base + s_wtot[w];
-  const bool model = bn < a.B;
 #pragma unroll
   for (int j = 0; j < EXP_KPT; ++j) {
     const int64_t p = base + (int64_t)w * 64 * EXP_KPT + j * 64 + lane;
@@ -147,13 +152,21 @@ __global__ void __launch_bounds__(EXP_THREADS) k_expand(ExpArgs a) {
         latch(a.err, ERR_CAPACITY);
         break;
       }
-      const uint64_t kc = kp | d;
-      a.key_n[q] = kc;
+      a.key_n[q] = kp | d;
       a.parent_n[q] = (int32_t)p;
       a.feat_n[q] = (uint16_t)(d | (c << 3));
-      if (model) hash_insert(a.hash, a.hash_lg, tag_key(kc, bn), (int32_t)q, a.err);
       ++q;
     }
+  }
+  // the parents (scale b) go into the coordinate hash with their code and
+  // first child when scale b+1 is a model scale
+  if (bn >= a.B) return;
+#pragma unroll
+  for (int j = 0; j < EXP_KPT; ++j) {
+    const int64_t p = base + (int64_t)w * 64 * EXP_KPT + j * 64 + lane;
+    if (p >= np) continue;
+    const int64_t q = wbase + incl[j] - (uint32_t)__popc(code[j]);
+    hash_insert(a.hash, a.hash_lg, tag_key(a.key_b[p], a.b), (int32_t)q, code[j], a.err);
   }
 }
 

@@ -24,9 +24,9 @@ namespace {
 
 typedef float f4 __attribute__((ext_vector_type(4)));
 
-constexpr int CONV_THREADS = 512;
+constexpr int CONV_THREADS = 1024;
 constexpr int CONV_WAVES = CONV_THREADS / 64;
-constexpr int KCH = 4;  // offsets whose gathers are in flight together
+constexpr int KCH = 8;  // offsets whose gathers are in flight together
 
 __device__ __forceinline__ f4 mfma4(float a, float b, f4 c) {
   return __builtin_amdgcn_mfma_f32_16x16x4f32(a, b, c, 0, 0, 0);
@@ -82,8 +82,9 @@ struct ConvArgs {
   const uint16_t* lv_feat;
   const HashSlot* hash;
   int hash_lg;
-  int32_t* nbr;           // [cap_model][27]
-  const float* h_in;      // [cap_model][C_in] (unused by the first layer)
+  int32_t* nbr;           // [cap_model][NBR_STRIDE], entries 27.. are -1
+  const float* h_in;      // [cap_model + 1][C_in], row cap_model all zero (unused by layer 1)
+  int64_t zero_feat;      // index of a zero entry of lv_feat
   float* h_out;           // [cap_model][C]
   const float* w;         // packed conv weights
   const float* bias;      // [C]
@@ -93,6 +94,38 @@ struct ConvArgs {
   float* logits;          // optional [rows][256], row = packed row - moff[b_lo]
   uint32_t* err;
 };
+
+// Entry j (wave-uniform) of the 8 neighbour rows a lane holds in two int4,
+// as a branch-free select tree.
+__device__ __forceinline__ int32_t pick8(const int4& lo, const int4& hi, int j) {
+  const bool b0 = j & 1, b1 = j & 2, b2 = j & 4;
+  const int32_t l01 = b0 ? lo.y : lo.x, l23 = b0 ? lo.w : lo.z;
+  const int32_t h01 = b0 ? hi.y : hi.x, h23 = b0 ? hi.w : hi.z;
+  const int32_t l = b1 ? l23 : l01, h = b1 ? h23 : h01;
+  return b2 ? h : l;
+}
+
+// Copies n16 16-byte words from global memory to LDS, all loads of a thread
+// issued before its stores.
+template <int N16, int THREADS>
+__device__ __forceinline__ void stage_lds(const f4* __restrict__ src, f4* dst, int tid) {
+  constexpr int PER = (N16 + THREADS - 1) / THREADS;
+  constexpr int BATCH = PER < 12 ? PER : 12;
+#pragma unroll
+  for (int b0 = 0; b0 < PER; b0 += BATCH) {
+    f4 v[BATCH];
+#pragma unroll
+    for (int i = 0; i < BATCH; ++i) {
+      const int idx = (b0 + i) * THREADS + tid;
+      if (b0 + i < PER && idx < N16) v[i] = src[idx];
+    }
+#pragma unroll
+    for (int i = 0; i < BATCH; ++i) {
+      const int idx = (b0 + i) * THREADS + tid;
+      if (b0 + i < PER && idx < N16) dst[idx] = v[i];
+    }
+  }
+}
 
 template <int C, bool FIRST, bool LAST>
 __global__ void __launch_bounds__(CONV_THREADS) k_conv(ConvArgs a) {
@@ -104,8 +137,10 @@ __global__ void __launch_bounds__(CONV_THREADS) k_conv(ConvArgs a) {
   constexpr int HSZ = LAST ? 16 * 64 * KT : 4;
   __shared__ __attribute__((aligned(16))) float s_w[WSZ];
   __shared__ __attribute__((aligned(16))) float s_h[HSZ];
-  __shared__ int32_t s_map[CONV_WAVES][16 * 28];
+  __shared__ uint64_t s_par[FIRST ? CONV_WAVES : 1][16][8];  // per wave: parent cells (code<<32|first)
   __shared__ int64_t s_tpre[NLEV + 1];
+  __shared__ int64_t s_nv[NLEV];   // N_b of the launch's scales
+  __shared__ int64_t s_mo[NLEV];   // first packed row of each scale
 
   const int tid = threadIdx.x, w = tid >> 6, lane = tid & 63;
   const int r = lane & 15, g = lane >> 4;
@@ -120,8 +155,9 @@ __global__ void __launch_bounds__(CONV_THREADS) k_conv(ConvArgs a) {
     if (mo + nb > a.cap_model) nb = 0;  // overflow was latched where the size was made
     total_tiles += (nb + 15) / 16;
   }
-  const int64_t first_tile = (int64_t)blockIdx.x * CONV_WAVES;
-  if (first_tile >= total_tiles) return;  // whole block idle: skip the weight staging
+  // tile t runs on block t % grid, so a small scale spreads over many CUs
+  // instead of queueing its tiles on one CU's matrix pipes
+  if ((int64_t)blockIdx.x >= total_tiles) return;  // whole block idle: skip the weight staging
   if (tid == 0) {
     int64_t acc = 0;
     for (int i = 0; i < nsc; ++i) {
@@ -129,80 +165,101 @@ __global__ void __launch_bounds__(CONV_THREADS) k_conv(ConvArgs a) {
       int64_t nb = a.count[b];
       if (a.moff[b] + nb > a.cap_model) nb = 0;
       s_tpre[i] = acc;
+      s_nv[i] = nb;
+      s_mo[i] = a.moff[b];
       acc += (nb + 15) / 16;
     }
     s_tpre[nsc] = acc;
   }
-  // stage the weights (and head weights) in LDS
-  {
-    const f4* src = reinterpret_cast<const f4*>(a.w);
-    f4* dst = reinterpret_cast<f4*>(s_w);
-    for (int i = tid; i < WSZ / 4; i += CONV_THREADS) dst[i] = src[i];
-    if (LAST) {
-      const f4* hs = reinterpret_cast<const f4*>(a.hw);
-      f4* hd = reinterpret_cast<f4*>(s_h);
-      for (int i = tid; i < HSZ / 4; i += CONV_THREADS) hd[i] = hs[i];
-    }
-  }
+  stage_lds<WSZ / 4, CONV_THREADS>(reinterpret_cast<const f4*>(a.w), reinterpret_cast<f4*>(s_w), tid);
+  if (LAST)
+    stage_lds<HSZ / 4, CONV_THREADS>(reinterpret_cast<const f4*>(a.hw), reinterpret_cast<f4*>(s_h),
+                                     tid);
   __syncthreads();
 
   const int64_t wave_stride = (int64_t)gridDim.x * CONV_WAVES;
-  for (int64_t tile = first_tile + w; tile < total_tiles; tile += wave_stride) {
+  for (int64_t tile = (int64_t)w * gridDim.x + blockIdx.x; tile < total_tiles; tile += wave_stride) {
     int si = 0;
     while (si + 1 < nsc && s_tpre[si + 1] <= tile) ++si;
     const int b = a.b_lo + si;
-    const int64_t nvox = a.count[b];
-    const int64_t mo = a.moff[b];
-    const int64_t row0 = (tile - s_tpre[si]) * 16;
-    const int64_t row = row0 + r;
+    const int64_t nvox = s_nv[si];
+    const int64_t mo = s_mo[si];
+    const int64_t row = (tile - s_tpre[si]) * 16 + r;
     const bool valid = row < nvox;
-    const int64_t prow = mo + row;
+    const int64_t prow = mo + (valid ? row : nvox - 1);  // idle lanes read a real row
     const int64_t lvb = (int64_t)(b - a.b0) * a.cap_pts;
-    int32_t* map = s_map[w];
 
-    // ---- neighbour rows of the tile: probe the hash (first layer) or load the map
-    uint32_t present = 0;
+    // ---- neighbour rows: lane (r, g) holds offsets k = 8g .. 8g+7 of voxel r
+    int4 nlo, nhi;
     if (FIRST) {
-      const uint64_t key = valid ? a.lv_key[lvb + row] : 0ull;
+      // The 27 cells around v lie in at most 8 cells of the parent scale: the
+      // parent p and, per axis, the neighbour of p on v's side.  Lane (r, g)
+      // probes cells e = 2g and 2g+1 (e = ex + 2ey + 4ez) of voxel r; each
+      // hit gives the cell's code and first-child row, from which every
+      // neighbour row follows by the FCG order.
+      const uint64_t key = a.lv_key[lvb + (prow - mo)];
       const int x = (int)compact3(key), y = (int)compact3(key >> 1), z = (int)compact3(key >> 2);
-      const int lim = 1 << b;
+      const int px = x >> 1, py = y >> 1, pz = z >> 1;
+      const int sx = (x & 1) ? 1 : -1, sy = (y & 1) ? 1 : -1, sz = (z & 1) ? 1 : -1;
+      const int plim = 1 << (b - 1);
+      uint64_t tk[2];
 #pragma unroll
-      for (int j = 0; j < 7; ++j) {
-        const int k = 7 * g + j;
-        if (k >= 27) break;
-        int32_t nbv = -1;
-        if (valid) {
-          if (k == 13) {
-            nbv = (int32_t)row;
-          } else {
-            const int xx = x + (k % 3) - 1, yy = y + (k / 3) % 3 - 1, zz = z + k / 9 - 1;
-            if (xx >= 0 && yy >= 0 && zz >= 0 && xx < lim && yy < lim && zz < lim)
-              nbv = hash_find(a.hash, a.hash_lg,
-                              tag_key(morton3((uint32_t)xx, (uint32_t)yy, (uint32_t)zz), b));
-          }
-          a.nbr[prow * 27 + k] = nbv;
+      for (int i = 0; i < 2; ++i) {
+        const int e = 2 * g + i;
+        const int cx = px + ((e & 1) ? sx : 0), cy = py + ((e & 2) ? sy : 0),
+                  cz = pz + ((e & 4) ? sz : 0);
+        tk[i] = (cx >= 0 && cy >= 0 && cz >= 0 && cx < plim && cy < plim && cz < plim)
+                    ? tag_key(morton3((uint32_t)cx, (uint32_t)cy, (uint32_t)cz), b - 1)
+                    : 0ull;
+      }
+      uint2 hit[2];
+      hash_find_n<2>(a.hash, a.hash_lg, tk, hit);
+      // cross-lane exchange through LDS (volatile: every read goes to LDS)
+      volatile uint64_t* par = s_par[w][r];
+      par[2 * g] = ((uint64_t)hit[0].y << 32) | hit[0].x;
+      par[2 * g + 1] = ((uint64_t)hit[1].y << 32) | hit[1].x;
+      __builtin_amdgcn_wave_barrier();
+      const int lim = 1 << b;
+      int32_t nb[8];
+#pragma unroll
+      for (int j = 0; j < 8; ++j) {
+        const int k = 8 * g + j;
+        const int ux = x + (k % 3) - 1, uy = y + (k / 3) % 3 - 1, uz = z + (k / 9) % 3 - 1;
+        nb[j] = -1;
+        if (k < 27 && ux >= 0 && uy >= 0 && uz >= 0 && ux < lim && uy < lim && uz < lim) {
+          const int e = ((ux >> 1) != px ? 1 : 0) | ((uy >> 1) != py ? 2 : 0) | ((uz >> 1) != pz ? 4 : 0);
+          const uint64_t pc = par[e];
+          const uint32_t first = (uint32_t)pc, code = (uint32_t)(pc >> 32);
+          const uint32_t d = (uint32_t)((ux & 1) | ((uy & 1) << 1) | ((uz & 1) << 2));
+          if ((code >> d) & 1u) nb[j] = (int32_t)first + __popc(code & ((1u << d) - 1u));
         }
-        map[r * 28 + k] = nbv;
-        present |= (nbv >= 0 ? 1u : 0u) << k;
+      }
+      nlo = make_int4(nb[0], nb[1], nb[2], nb[3]);
+      nhi = make_int4(nb[4], nb[5], nb[6], nb[7]);
+      if (valid) {
+        int4* dst = reinterpret_cast<int4*>(a.nbr + prow * NBR_STRIDE + 8 * g);
+        dst[0] = nlo;
+        dst[1] = nhi;
       }
     } else {
-#pragma unroll
-      for (int j = 0; j < 7; ++j) {
-        const int k = 7 * g + j;
-        if (k >= 27) break;
-        const int32_t nbv = valid ? a.nbr[prow * 27 + k] : -1;
-        map[r * 28 + k] = nbv;
-        present |= (nbv >= 0 ? 1u : 0u) << k;
-      }
+      const int4* src = reinterpret_cast<const int4*>(a.nbr + prow * NBR_STRIDE + 8 * g);
+      nlo = src[0];
+      nhi = src[1];
+    }
+    uint32_t present = 0;
+    if (valid) {
+      present = (uint32_t)(nlo.x >= 0) | ((uint32_t)(nlo.y >= 0) << 1) |
+                ((uint32_t)(nlo.z >= 0) << 2) | ((uint32_t)(nlo.w >= 0) << 3) |
+                ((uint32_t)(nhi.x >= 0) << 4) | ((uint32_t)(nhi.y >= 0) << 5) |
+                ((uint32_t)(nhi.z >= 0) << 6) | ((uint32_t)(nhi.w >= 0) << 7);
+      present = (present << (8 * g)) & 0x7FFFFFFu;  // the 5 padding entries are -1 anyway
     }
     uint32_t offs = (uint32_t)__builtin_amdgcn_readfirstlane((int)wave_or(present));
 
-    // ---- accumulate over the occupied offsets
+    // ---- accumulate over the occupied offsets, KCH gathers in flight
     f4 acc[NCB];
 #pragma unroll
-    for (int cb = 0; cb < NCB; ++cb) {
-      acc[cb] = *reinterpret_cast<const f4*>(a.bias + 16 * cb + 4 * g);
-    }
+    for (int cb = 0; cb < NCB; ++cb) acc[cb] = *reinterpret_cast<const f4*>(a.bias + 16 * cb + 4 * g);
     while (offs) {
       int ks[KCH];
 #pragma unroll
@@ -214,26 +271,25 @@ __global__ void __launch_bounds__(CONV_THREADS) k_conv(ConvArgs a) {
 #pragma unroll
       for (int c = 0; c < KCH; ++c) {
         if (ks[c] < 0) break;
-        const int32_t n = map[r * 28 + ks[c]];
+        int32_t n = __shfl(pick8(nlo, nhi, ks[c] & 7), r + 16 * (ks[c] >> 3));
+        if (!valid) n = -1;
         if (FIRST) {
-          const uint32_t word = n >= 0 ? (uint32_t)a.lv_feat[lvb + n] : 0u;
+          // absent neighbours read the reserved zero entry: no select on loaded data
+          const uint32_t word = n >= 0 ? a.lv_feat[lvb + n] : a.lv_feat[a.zero_feat];
 #pragma unroll
           for (int s = 0; s < KSP; ++s) bsrc[c][s] = (float)((word >> (g * KS + s)) & 1u);
-          // the fourth slot (s = 3) is padding and its weights are zero
+          // slot s = KS (padding) meets zero weights
         } else {
-          if (n >= 0) {
-            const f4* src = reinterpret_cast<const f4*>(a.h_in + (mo + n) * C + g * KS);
+          // absent neighbours read the reserved all-zero row cap_model
+          const int64_t srow = n >= 0 ? mo + n : a.cap_model;
+          const f4* src = reinterpret_cast<const f4*>(a.h_in + srow * C + g * KS);
 #pragma unroll
-            for (int q = 0; q < KSP / 4; ++q) {
-              const f4 v = src[q];
-              bsrc[c][4 * q + 0] = v[0];
-              bsrc[c][4 * q + 1] = v[1];
-              bsrc[c][4 * q + 2] = v[2];
-              bsrc[c][4 * q + 3] = v[3];
-            }
-          } else {
-#pragma unroll
-            for (int s = 0; s < KSP; ++s) bsrc[c][s] = 0.0f;
+          for (int q = 0; q < KSP / 4; ++q) {
+            const f4 v = src[q];
+            bsrc[c][4 * q + 0] = v[0];
+            bsrc[c][4 * q + 1] = v[1];
+            bsrc[c][4 * q + 2] = v[2];
+            bsrc[c][4 * q + 3] = v[3];
           }
         }
       }
@@ -264,41 +320,52 @@ __global__ void __launch_bounds__(CONV_THREADS) k_conv(ConvArgs a) {
     }
 
     if (LAST) {
-      // ---- head: z^T[256][16] = H^T h^T, B operand = the conv accumulators
-      f4 zz[16];
+      // ---- head: z^T[256][16] = H^T h^T with the conv accumulators as the B
+      // operand; 64 symbols at a time with a running (max, sum of exp)
+      float m = -INFINITY, ssum = 0.0f;
+      float* lo = (a.logits && valid) ? a.logits + (prow - s_mo[0]) * 256 + 4 * g : nullptr;
+#pragma unroll 1
+      for (int grp = 0; grp < 4; ++grp) {
+        f4 zz[4];
 #pragma unroll
-      for (int sb = 0; sb < 16; ++sb) {
-        zz[sb] = *reinterpret_cast<const f4*>(a.hb + 16 * sb + 4 * g);
-        const f4* hp = reinterpret_cast<const f4*>(s_h + (sb * 64 + lane) * KT);
+        for (int q4 = 0; q4 < 4; ++q4) {
+          const int sb = grp * 4 + q4;
+          zz[q4] = *reinterpret_cast<const f4*>(a.hb + 16 * sb + 4 * g);
+          const f4* hp = reinterpret_cast<const f4*>(s_h + (sb * 64 + lane) * KT);
 #pragma unroll
-        for (int q = 0; q < KT / 4; ++q) {
-          const f4 hv = hp[q];
+          for (int q = 0; q < KT / 4; ++q) {
+            const f4 hv = hp[q];
 #pragma unroll
-          for (int e = 0; e < 4; ++e) zz[sb] = mfma4(hv[e], acc[q][e], zz[sb]);
+            for (int e = 0; e < 4; ++e) zz[q4] = mfma4(hv[e], acc[q][e], zz[q4]);
+          }
+        }
+        float gm = zz[0][0];
+#pragma unroll
+        for (int q4 = 0; q4 < 4; ++q4)
+#pragma unroll
+          for (int e = 0; e < 4; ++e) gm = fmaxf(gm, zz[q4][e]);
+        const float mn = fmaxf(m, gm);
+        float part = 0.0f;
+#pragma unroll
+        for (int q4 = 0; q4 < 4; ++q4)
+#pragma unroll
+          for (int e = 0; e < 4; ++e) part += __expf(zz[q4][e] - mn);
+        ssum = ssum * __expf(m - mn) + part;
+        m = mn;
+        if (lo) {
+#pragma unroll
+          for (int q4 = 0; q4 < 4; ++q4) *reinterpret_cast<f4*>(lo + 16 * (grp * 4 + q4)) = zz[q4];
         }
       }
-      // lane holds symbols 16*sb + 4*g + e of voxel r; the 4 lanes r, r+16,
-      // r+32, r+48 together hold all 256
-      float m = zz[0][0];
+      // the 4 lanes r, r+16, r+32, r+48 hold the 4 quarters of voxel r's symbols
 #pragma unroll
-      for (int sb = 0; sb < 16; ++sb)
-#pragma unroll
-        for (int e = 0; e < 4; ++e) m = fmaxf(m, zz[sb][e]);
-      m = fmaxf(m, __shfl_xor(m, 16));
-      m = fmaxf(m, __shfl_xor(m, 32));
-      float s = 0.0f;
-#pragma unroll
-      for (int sb = 0; sb < 16; ++sb)
-#pragma unroll
-        for (int e = 0; e < 4; ++e) s += __expf(zz[sb][e] - m);
-      s += __shfl_xor(s, 16);
-      s += __shfl_xor(s, 32);
-      if (valid && g == 0) a.lse[prow] = m + __logf(s);
-      if (a.logits && valid) {
-        float* lo = a.logits + (prow - a.moff[a.b_lo]) * 256 + 4 * g;
-#pragma unroll
-        for (int sb = 0; sb < 16; ++sb) *reinterpret_cast<f4*>(lo + 16 * sb) = zz[sb];
+      for (int o = 16; o <= 32; o <<= 1) {
+        const float om = __shfl_xor(m, o), os = __shfl_xor(ssum, o);
+        const float mn = fmaxf(m, om);
+        ssum = ssum * __expf(m - mn) + os * __expf(om - mn);
+        m = mn;
       }
+      if (valid && g == 0) a.lse[prow] = m + __logf(ssum);
     }
   }
 }
@@ -353,6 +420,7 @@ hipError_t launch_model(Ctx& c, int b_lo, int b_hi, float* logits) {
   a.hash = c.d_hash;
   a.hash_lg = c.hash_lg;
   a.nbr = c.d_nbr;
+  a.zero_feat = (int64_t)c.nlv * c.cap_pts;
   a.hb = c.w_hbias;
   a.hw = c.w_head;
   a.lse = c.d_lse;

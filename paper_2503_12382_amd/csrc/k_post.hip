@@ -10,52 +10,105 @@ namespace {
 constexpr float INV_LN2 = 1.4426950408889634f;
 
 // bits_v = (lse_v - z_{O_b[v]}) / ln 2 with z_o = hb[o] + sum_c H[c][o] h_L[v][c]
-// (fp32, channel order), per-scale sums in double: RED_BLOCKS partial sums per
-// scale, reduced in index order by the last block to finish (deterministic).
-__global__ void __launch_bounds__(256) k_code_length(
+// (fp32, channel order).  Block (chunk, scale) handles 1024 voxels of one
+// scale with H staged in LDS; per-chunk sums in double are reduced in chunk
+// order by the last block of the scale to finish (deterministic).
+constexpr int CL_THREADS = 256;
+constexpr int CL_CHUNK = 1024;
+
+template <int C>
+__global__ void __launch_bounds__(CL_THREADS) k_code_length(
     int b_lo, int b0, const int32_t* __restrict__ count, const int32_t* __restrict__ moff,
-    int64_t cap_pts, int64_t cap_model, const uint8_t* __restrict__ lv_code, const float* __restrict__ hL, int C,
-    const float* __restrict__ H, const float* __restrict__ hb, const float* __restrict__ lse,
-    float* __restrict__ bits_out, double* partial, double* total, uint32_t* done) {
-  __shared__ double s_red[256];
+    int64_t cap_pts, int64_t cap_model, const uint8_t* __restrict__ lv_code,
+    const float* __restrict__ hL, const float* __restrict__ H, const float* __restrict__ hb,
+    const float* __restrict__ lse, float* __restrict__ bits_out, double* partial, int max_chunks,
+    double* total, uint32_t* done) {
+  __shared__ float s_H[C * 256];
+  __shared__ float s_hb[256];
+  __shared__ double s_red[CL_THREADS / 64];
   __shared__ bool s_last;
   const int b = b_lo + blockIdx.y;
   const int64_t mo = moff[b];
   int64_t n = count[b];
   if (mo + n > cap_model) n = 0;  // capacity overflow, latched where the size was made
+  const int64_t nchunks = (n + CL_CHUNK - 1) / CL_CHUNK;
+  if (nchunks == 0) {
+    if (blockIdx.x == 0 && threadIdx.x == 0) total[b] = 0.0;
+    return;
+  }
+  if ((int64_t)blockIdx.x >= nchunks) return;
+  {  // stage the head in LDS, every load of a thread issued before its stores
+    constexpr int PER = C * 256 / 4 / CL_THREADS;
+    float4 v[PER];
+    const float4* src = reinterpret_cast<const float4*>(H);
+#pragma unroll
+    for (int i = 0; i < PER; ++i) v[i] = src[i * CL_THREADS + threadIdx.x];
+    const float hbv = hb[threadIdx.x];
+#pragma unroll
+    for (int i = 0; i < PER; ++i) reinterpret_cast<float4*>(s_H)[i * CL_THREADS + threadIdx.x] = v[i];
+    s_hb[threadIdx.x] = hbv;
+  }
+  __syncthreads();
   const int64_t out0 = mo - moff[b_lo];
   const uint8_t* code = lv_code + (int64_t)(b - b0) * cap_pts;
   double acc = 0.0;
-  for (int64_t v = (int64_t)blockIdx.x * 256 + threadIdx.x; v < n; v += (int64_t)RED_BLOCKS * 256) {
-    const int o = code[v];
-    const float* h = hL + (mo + v) * C;
-    float z = hb[o];
-    for (int c = 0; c < C; ++c) z = fmaf(H[c * 256 + o], h[c], z);
-    const float bt = (lse[mo + v] - z) * INV_LN2;
-    if (bits_out) bits_out[out0 + v] = bt;
-    acc += (double)bt;
+  constexpr int PV = CL_CHUNK / CL_THREADS;  // voxels per thread
+  int64_t vv[PV];
+  int oo[PV];
+  float ll[PV];
+#pragma unroll
+  for (int i = 0; i < PV; ++i) {  // clamped rows: every load is issued up front
+    const int64_t v = (int64_t)blockIdx.x * CL_CHUNK + i * CL_THREADS + threadIdx.x;
+    vv[i] = v < n ? v : n - 1;
+    oo[i] = code[vv[i]];
+    ll[i] = lse[mo + vv[i]];
   }
-  s_red[threadIdx.x] = acc;
+#pragma unroll
+  for (int i = 0; i < PV; ++i) {
+    const int64_t v = (int64_t)blockIdx.x * CL_CHUNK + i * CL_THREADS + threadIdx.x;
+    const int o = oo[i];
+    const float4* h = reinterpret_cast<const float4*>(hL + (mo + vv[i]) * C);
+    float z = s_hb[o];
+#pragma unroll
+    for (int c4 = 0; c4 < C / 4; ++c4) {
+      const float4 hv = h[c4];
+      z = fmaf(s_H[(4 * c4 + 0) * 256 + o], hv.x, z);
+      z = fmaf(s_H[(4 * c4 + 1) * 256 + o], hv.y, z);
+      z = fmaf(s_H[(4 * c4 + 2) * 256 + o], hv.z, z);
+      z = fmaf(s_H[(4 * c4 + 3) * 256 + o], hv.w, z);
+    }
+    const float bt = (ll[i] - z) * INV_LN2;
+    if (v < n) {
+      if (bits_out) bits_out[out0 + v] = bt;
+      acc += (double)bt;
+    }
+  }
+  for (int o = 32; o > 0; o >>= 1) acc += __shfl_xor(acc, o);
+  if ((threadIdx.x & 63) == 0) s_red[threadIdx.x >> 6] = acc;
   __syncthreads();
-  for (int s = 128; s > 0; s >>= 1) {
-    if (threadIdx.x < s) s_red[threadIdx.x] += s_red[threadIdx.x + s];
-    __syncthreads();
-  }
   if (threadIdx.x == 0) {
-    partial[b * RED_BLOCKS + blockIdx.x] = s_red[0];
+    double t = 0.0;
+    for (int i = 0; i < CL_THREADS / 64; ++i) t += s_red[i];
+    partial[(int64_t)b * max_chunks + blockIdx.x] = t;
     __threadfence();
     const uint32_t prev = atomicAdd(&done[b], 1u);
-    s_last = prev == RED_BLOCKS - 1;
+    s_last = prev == (uint32_t)(nchunks - 1);
   }
   __syncthreads();
-  if (s_last && threadIdx.x == 0) {
+  if (s_last && threadIdx.x < 64) {
+    // the first wave sums the chunk partials: lane i takes chunks i, i+64, ...
+    // in order, then a fixed xor tree; the same result whatever the arrival order
     __threadfence();
+    const int lane = threadIdx.x;
     double t = 0.0;
-    for (int i = 0; i < RED_BLOCKS; ++i) t += __hip_atomic_load(&partial[b * RED_BLOCKS + i],
-                                                                __ATOMIC_RELAXED,
-                                                                __HIP_MEMORY_SCOPE_AGENT);
-    total[b] = t;
-    done[b] = 0u;  // ready for the next call
+    for (int64_t i = lane; i < nchunks; i += 64)
+      t += __hip_atomic_load(&partial[(int64_t)b * max_chunks + i], __ATOMIC_RELAXED,
+                             __HIP_MEMORY_SCOPE_AGENT);
+    for (int o = 32; o > 0; o >>= 1) t += __shfl_xor(t, o);
+    if (lane == 0) {
+      total[b] = t;
+      done[b] = 0u;  // ready for the next call
+    }
   }
 }
 
@@ -149,10 +202,10 @@ __global__ void k_copy_map(const int32_t* __restrict__ nbr, const int32_t* __res
   int64_t n = (int64_t)count[b];
   if (moff[b] + n > cap_model) n = 0;
   n *= 27;
-  const int64_t o = (int64_t)moff[b] * 27;
+  const int64_t o = (int64_t)moff[b] * NBR_STRIDE;
   for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n;
        i += (int64_t)gridDim.x * blockDim.x)
-    dst[i] = nbr[o + i];
+    dst[i] = nbr[o + (i / 27) * NBR_STRIDE + i % 27];
 }
 
 unsigned grid_for(int64_t cap, int per_block) {
@@ -166,10 +219,18 @@ unsigned grid_for(int64_t cap, int per_block) {
 
 hipError_t launch_code_length(Ctx& c, int b_lo, int b_hi, float* bits) {
   ProfScope ps_(c, RENO_K_CODE_LENGTH);
-  hipLaunchKernelGGL(k_code_length, dim3(RED_BLOCKS, b_hi - b_lo + 1), dim3(256), 0, c.stream, b_lo,
-                     c.b0(), c.d_count, c.d_moff, c.cap_pts, c.cap_model, c.lv_code, c.hlast(), c.p.channels,
-                     c.w_head_plain, c.w_hbias, c.d_lse, bits, c.d_partial, c.d_total,
-                     c.d_ticket + TK_RED);
+  const int max_chunks = (int)((c.cap_pts + CL_CHUNK - 1) / CL_CHUNK);
+  const dim3 grid(max_chunks, b_hi - b_lo + 1);
+  if (c.p.channels == 32)
+    hipLaunchKernelGGL(k_code_length<32>, grid, dim3(CL_THREADS), 0, c.stream, b_lo, c.b0(),
+                       c.d_count, c.d_moff, c.cap_pts, c.cap_model, c.lv_code, c.hlast(),
+                       c.w_head_plain, c.w_hbias, c.d_lse, bits, c.d_partial, max_chunks,
+                       c.d_total, c.d_ticket + TK_RED);
+  else
+    hipLaunchKernelGGL(k_code_length<16>, grid, dim3(CL_THREADS), 0, c.stream, b_lo, c.b0(),
+                       c.d_count, c.d_moff, c.cap_pts, c.cap_model, c.lv_code, c.hlast(),
+                       c.w_head_plain, c.w_hbias, c.d_lse, bits, c.d_partial, max_chunks,
+                       c.d_total, c.d_ticket + TK_RED);
   return hipGetLastError();
 }
 

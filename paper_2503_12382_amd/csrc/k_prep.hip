@@ -33,6 +33,30 @@ __global__ void __launch_bounds__(256) k_zero(ZeroArgs a) {
 }
 
 // ---------------------------------------------------------------------------
+// Histogram update of every sort pass's digit of key k in LDS, aggregated over
+// the lanes of the wave that share a digit (one LDS atomic per distinct digit:
+// the coarse digits of Morton keys are few, so unaggregated atomics serialise).
+__device__ __forceinline__ void digit_count(uint32_t dig, bool valid, uint32_t* h) {
+  uint64_t peers = __ballot(valid);
+#pragma unroll
+  for (int bit = 0; bit < RADIX_BITS; ++bit) {
+    const bool set = (dig >> bit) & 1u;
+    const uint64_t bm = __ballot(set);
+    peers &= set ? bm : ~bm;
+  }
+  if (valid && rank_below(peers) == 0u) atomicAdd(&h[dig], (uint32_t)__popcll(peers));
+}
+
+__device__ __forceinline__ void digits_of(uint64_t k, int passes, uint32_t* sh) {
+  for (int ps = 0; ps < passes; ++ps)
+    digit_count((uint32_t)(k >> (RADIX_BITS * ps)) & (RADIX - 1), true, sh + ps * RADIX);
+}
+
+__device__ __forceinline__ void digits_of_idle(int passes, uint32_t* sh) {
+  for (int ps = 0; ps < passes; ++ps) digit_count(0u, false, sh + ps * RADIX);
+}
+
+// ---------------------------------------------------------------------------
 // Quantise + Morton + digit histograms of every sort pass.
 //   u = ((p + R) * 2^B) / (2R) in fp64, q = clamp(floor(u), 0, 2^B - 1).
 __global__ void __launch_bounds__(256) k_quantize(const float* __restrict__ pts, int64_t n, int B,
@@ -47,7 +71,15 @@ __global__ void __launch_bounds__(256) k_quantize(const float* __restrict__ pts,
   const double top = (double)((int64_t(1) << B) - 1);
   bool bad = false;
   const int64_t stride = (int64_t)gridDim.x * blockDim.x;
-  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += stride) {
+  // every lane of a wave runs the same number of iterations so that the
+  // wave-wide digit matching below sees all lanes; idle lanes carry no key
+  const int64_t nwaves_iter = (n + stride - 1) / stride;
+  for (int64_t it = 0; it < nwaves_iter; ++it) {
+    const int64_t i = it * stride + (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (i >= n) {
+      digits_of_idle(passes, sh);
+      continue;
+    }
     uint32_t q[3];
 #pragma unroll
     for (int a = 0; a < 3; ++a) {
@@ -65,8 +97,7 @@ __global__ void __launch_bounds__(256) k_quantize(const float* __restrict__ pts,
     }
     const uint64_t k = morton3(q[0], q[1], q[2]);
     keys[i] = k;
-    for (int ps = 0; ps < passes; ++ps)
-      atomicAdd(&sh[ps * RADIX + (uint32_t)((k >> (RADIX_BITS * ps)) & (RADIX - 1))], 1u);
+    digits_of(k, passes, sh);
   }
   if (bad) latch(err, ERR_NONFINITE);
   __syncthreads();
@@ -135,9 +166,12 @@ __global__ void __launch_bounds__(SORT_THREADS) k_sort_pass(const uint64_t* __re
       const uint64_t bm = __ballot(set);
       peers &= set ? bm : ~bm;
     }
+    // the leader lane updates the count that every lane of the group has just
+    // read; volatile keeps the compiler from reusing a value across slots
+    volatile uint32_t* cnt = &s_wh[w][dig[j]];
     const uint32_t below = rank_below(peers);
-    const uint32_t before = s_wh[w][dig[j]];
-    if (ok[j] && below == 0u) s_wh[w][dig[j]] = before + (uint32_t)__popcll(peers);
+    const uint32_t before = *cnt;
+    if (ok[j] && below == 0u) *cnt = before + (uint32_t)__popcll(peers);
     rnk[j] = before + below;
   }
   __syncthreads();
@@ -176,8 +210,7 @@ __global__ void __launch_bounds__(SORT_THREADS) k_sort_pass(const uint64_t* __re
 // iff lv(i) <= b - b0, where lv(i) = max(0, B - floor(h/3) - b0), h = highest
 // bit of S[i] ^ S[i-1] (lv(0) = 0; duplicates never start a run).  Its row in
 // V_b is the number of such elements before it, found with per-scale ballots
-// and a look-back over tiles.  Also writes parent rows, first-child rows and
-// inserts the model scales into the coordinate hash.
+// and a look-back over tiles.  Also writes parent rows and first-child rows.
 struct PyrArgs {
   const uint64_t* S;
   int64_t n;
@@ -201,7 +234,7 @@ __global__ void __launch_bounds__(PYR_THREADS) k_pyramid(PyrArgs a) {
   __shared__ uint32_t s_wc[4][NLEV];     // per-wave counts -> exclusive offsets
   __shared__ uint32_t s_gb[NLEV];        // global exclusive base of the tile per scale
   __shared__ uint32_t s_tot[NLEV];       // inclusive totals (last tile)
-  __shared__ uint32_t s_run[4][NLEV];    // running rows per wave
+  __shared__ uint32_t s_jex[4][PYR_KPT][NLEV];  // per wave: elements before slot j
   const int tid = threadIdx.x, w = tid >> 6, lane = tid & 63;
   const int nl = a.nl;
   if (tid == 0) s_tile = atomicAdd(a.ticket, 1u);
@@ -232,11 +265,15 @@ __global__ void __launch_bounds__(PYR_THREADS) k_pyramid(PyrArgs a) {
     lvj[j] = lv;
     kj[j] = k;
   }
-  // phase 1: per-wave counts per scale
+  // phase 1: per-wave counts per scale, and per element slot j (read-only in
+  // phase 2, so no lane ever depends on another lane's LDS update)
   for (int l = 0; l < nl; ++l) {
     uint32_t c = 0;
 #pragma unroll
-    for (int j = 0; j < PYR_KPT; ++j) c += (uint32_t)__popcll(__ballot(lvj[j] <= l));
+    for (int j = 0; j < PYR_KPT; ++j) {
+      if (lane == 0) s_jex[w][j][l] = c;
+      c += (uint32_t)__popcll(__ballot(lvj[j] <= l));
+    }
     if (lane == 0) s_wc[w][l] = c;
   }
   __syncthreads();
@@ -253,10 +290,8 @@ __global__ void __launch_bounds__(PYR_THREADS) k_pyramid(PyrArgs a) {
     s_tot[l] = ex + tot;
   }
   __syncthreads();
-  // phase 2: ranks and writes.  s_run[w][l] is the wave's running row at
-  // scale l; it is uniform over the wave, read by every lane and advanced by
-  // lane 0 after the read (LDS operations of one wave complete in order).
-  if (lane < nl) s_run[w][lane] = s_gb[lane] + s_wc[w][lane];
+  // phase 2: ranks and writes; row at scale l = tile base + wave offset +
+  // earlier slots of the wave + lanes below in this slot
 #pragma unroll
   for (int j = 0; j < PYR_KPT; ++j) {
     const int lv = lvj[j];
@@ -264,8 +299,7 @@ __global__ void __launch_bounds__(PYR_THREADS) k_pyramid(PyrArgs a) {
     for (int l = 0; l < nl; ++l) {
       const bool here = lv <= l;
       const uint64_t m = __ballot(here);
-      const uint32_t pos = s_run[w][l] + rank_below(m);
-      if (lane == 0) s_run[w][l] += (uint32_t)__popcll(m);
+      const uint32_t pos = s_gb[l] + s_wc[w][l] + s_jex[w][j][l] + rank_below(m);
       if (here) {
         const int b = a.b0 + l;
         const int64_t r = (int64_t)l * a.cap_pts + pos;
@@ -275,7 +309,6 @@ __global__ void __launch_bounds__(PYR_THREADS) k_pyramid(PyrArgs a) {
         // parent run precedes it (exclusive count - 1); above, it is itself
         a.parent[r] = (l == 0) ? -1 : (l == lv ? prev_pos - 1 : prev_pos);
         if (l > lv) a.fc[(int64_t)(l - 1) * a.cap_pts + prev_pos] = (int32_t)pos;
-        if (b > a.b0 && b < a.B) hash_insert(a.hash, a.hash_lg, tag_key(kb, b), (int32_t)pos, a.err);
       }
       prev_pos = (int32_t)pos;
     }
@@ -299,13 +332,15 @@ __global__ void __launch_bounds__(PYR_THREADS) k_pyramid(PyrArgs a) {
 // FOG codes for every scale b0 <= b < B: the children of parent p are the
 // rows [fc[p], fc[p+1]) of V_{b+1}; the code ORs 1 << (child key & 7)
 // (Sec. 3.1: weights 1..128 over the octants).  Also writes each child's
-// layer-1 input bits: delta | code << 3.
+// layer-1 input bits (delta | code << 3) and inserts every parent of a model
+// scale (b0 <= b <= B-2) into the coordinate hash with its code and first child.
 __global__ void __launch_bounds__(256) k_codes(const uint64_t* __restrict__ key,
                                                const int32_t* __restrict__ fc,
                                                uint8_t* __restrict__ code,
                                                uint16_t* __restrict__ feat,
                                                const int32_t* __restrict__ count, int b0, int B,
-                                               int64_t cap_pts, uint32_t* err) {
+                                               int64_t cap_pts, HashSlot* hash, int hash_lg,
+                                               uint32_t* err) {
   __shared__ int64_t s_pre[NLEV + 1];
   if (threadIdx.x == 0) {
     int64_t acc = 0;
@@ -327,17 +362,28 @@ __global__ void __launch_bounds__(256) k_codes(const uint64_t* __restrict__ key,
     const int64_t np = count[b];
     const int64_t rb = (int64_t)l * cap_pts, rc = (int64_t)(l + 1) * cap_pts;
     const int32_t nn = count[b + 1];
-    int32_t lo = fc[rb + p];
-    int32_t hi = (p + 1 < np) ? fc[rb + p + 1] : nn;
+    const int32_t lo = fc[rb + p];
+    const int32_t hi = (p + 1 < np) ? fc[rb + p + 1] : nn;
     if (lo < 0 || hi > nn || hi <= lo || hi - lo > 8) {  // never expected: children runs are 1..8
       latch(err, ERR_INTERNAL);
-      lo = 0;
-      hi = 0;
+      continue;
     }
+    const int nk = hi - lo;
+    // all child keys are loaded at once (clamped rows), then used from registers
+    uint64_t kc[8];
+#pragma unroll
+    for (int i = 0; i < 8; ++i) kc[i] = key[rc + lo + (i < nk ? i : nk - 1)];
     uint32_t c = 0;
-    for (int32_t j = lo; j < hi; ++j) c |= 1u << (uint32_t)(key[rc + j] & 7ull);
+#pragma unroll
+    for (int i = 0; i < 8; ++i)
+      if (i < nk) c |= 1u << (uint32_t)(kc[i] & 7ull);
     code[rb + p] = (uint8_t)c;
-    for (int32_t j = lo; j < hi; ++j) feat[rc + j] = (uint16_t)((key[rc + j] & 7ull) | (c << 3));
+#pragma unroll
+    for (int i = 0; i < 8; ++i)
+      if (i < nk) feat[rc + lo + i] = (uint16_t)((kc[i] & 7ull) | (c << 3));
+    // parents of model scales go into the coordinate hash with their code
+    // and first child
+    if (b <= B - 2) hash_insert(hash, hash_lg, tag_key(key[rb + p], b), lo, c, err);
   }
 }
 
@@ -412,7 +458,8 @@ hipError_t launch_codes(Ctx& c, int B) {
   if (blocks > 2048) blocks = 2048;
   if (blocks < 1) blocks = 1;
   hipLaunchKernelGGL(k_codes, dim3((unsigned)blocks), dim3(256), 0, c.stream, c.lv_key, c.lv_fc,
-                     c.lv_code, c.lv_feat, c.d_count, c.b0(), B, c.cap_pts, c.d_err);
+                     c.lv_code, c.lv_feat, c.d_count, c.b0(), B, c.cap_pts, c.d_hash, c.hash_lg,
+                     c.d_err);
   return hipGetLastError();
 }
 
