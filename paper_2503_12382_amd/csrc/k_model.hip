@@ -26,7 +26,7 @@ typedef float f4 __attribute__((ext_vector_type(4)));
 
 constexpr int CONV_THREADS = 1024;
 constexpr int CONV_WAVES = CONV_THREADS / 64;
-constexpr int KCH = 8;  // offsets whose gathers are in flight together
+constexpr int NXCD = 8;  // MI355X: 8 accelerator complex dies, each with its own L2
 
 __device__ __forceinline__ f4 mfma4(float a, float b, f4 c) {
   return __builtin_amdgcn_mfma_f32_16x16x4f32(a, b, c, 0, 0, 0);
@@ -135,6 +135,11 @@ __global__ void __launch_bounds__(CONV_THREADS) k_conv(ConvArgs a) {
   constexpr int KT = C / 4;
   constexpr int WSZ = 27 * NCB * 64 * KSP;
   constexpr int HSZ = LAST ? 16 * 64 * KT : 4;
+  constexpr int PCH = FIRST ? 8 : 4;  // offsets per pipeline stage
+  struct Gath {                        // one gathered neighbour slice
+    uint32_t word;                     // first layer: 11 input bits
+    f4 v[FIRST ? 1 : KSP / 4];         // later layers: KS channels
+  };
   __shared__ __attribute__((aligned(16))) float s_w[WSZ];
   __shared__ __attribute__((aligned(16))) float s_h[HSZ];
   __shared__ uint64_t s_par[FIRST ? CONV_WAVES : 1][16][8];  // per wave: parent cells (code<<32|first)
@@ -155,9 +160,12 @@ __global__ void __launch_bounds__(CONV_THREADS) k_conv(ConvArgs a) {
     if (mo + nb > a.cap_model) nb = 0;  // overflow was latched where the size was made
     total_tiles += (nb + 15) / 16;
   }
-  // tile t runs on block t % grid, so a small scale spreads over many CUs
-  // instead of queueing its tiles on one CU's matrix pipes
-  if ((int64_t)blockIdx.x >= total_tiles) return;  // whole block idle: skip the weight staging
+  {  // whole block idle (see the tile order below): skip the weight staging
+    const int64_t per = (total_tiles + NXCD - 1) / NXCD;
+    const int64_t lo = (blockIdx.x % NXCD) * per;
+    const int64_t cnt = (lo + per < total_tiles ? lo + per : total_tiles) - lo;
+    if ((int64_t)(blockIdx.x / NXCD) >= cnt) return;
+  }
   if (tid == 0) {
     int64_t acc = 0;
     for (int i = 0; i < nsc; ++i) {
@@ -177,8 +185,16 @@ __global__ void __launch_bounds__(CONV_THREADS) k_conv(ConvArgs a) {
                                      tid);
   __syncthreads();
 
-  const int64_t wave_stride = (int64_t)gridDim.x * CONV_WAVES;
-  for (int64_t tile = (int64_t)w * gridDim.x + blockIdx.x; tile < total_tiles; tile += wave_stride) {
+  // XCD-aware tile order: blocks are dispatched round-robin over the 8 XCDs,
+  // so block x runs on XCD x % 8.  Each XCD takes a contiguous range of
+  // tiles (Morton order: the neighbour rows of a tile sit in nearby tiles and
+  // stay in that XCD's L2); inside the range, tiles go round-robin over the
+  // XCD's blocks first so that a short range still spreads over CUs.
+  const int64_t xcd = blockIdx.x % NXCD, xb = blockIdx.x / NXCD, nxb = gridDim.x / NXCD;
+  const int64_t per_xcd = (total_tiles + NXCD - 1) / NXCD;
+  const int64_t t_lo = xcd * per_xcd;
+  const int64_t t_hi = t_lo + per_xcd < total_tiles ? t_lo + per_xcd : total_tiles;
+  for (int64_t tile = t_lo + (int64_t)w * nxb + xb; tile < t_hi; tile += nxb * CONV_WAVES) {
     int si = 0;
     while (si + 1 < nsc && s_tpre[si + 1] <= tile) ++si;
     const int b = a.b_lo + si;
@@ -256,46 +272,52 @@ __global__ void __launch_bounds__(CONV_THREADS) k_conv(ConvArgs a) {
     }
     uint32_t offs = (uint32_t)__builtin_amdgcn_readfirstlane((int)wave_or(present));
 
-    // ---- accumulate over the occupied offsets, KCH gathers in flight
+    // ---- accumulate over the occupied offsets, software-pipelined: the
+    // gathers of the next PCH offsets are issued before the MFMAs of the
+    // current ones (double buffer; loads are never skipped, an unused slot
+    // reads the zero row, so the wait counts stay exact).
     f4 acc[NCB];
 #pragma unroll
     for (int cb = 0; cb < NCB; ++cb) acc[cb] = *reinterpret_cast<const f4*>(a.bias + 16 * cb + 4 * g);
-    while (offs) {
-      int ks[KCH];
+    auto take = [&](int (&ks)[PCH]) {
 #pragma unroll
-      for (int c = 0; c < KCH; ++c) {
+      for (int c = 0; c < PCH; ++c) {
         ks[c] = offs ? __builtin_ctz(offs) : -1;
         offs &= offs ? offs - 1u : 0u;
       }
-      float bsrc[KCH][KSP];
+    };
+    auto gather = [&](const int (&ks)[PCH], Gath (&gb)[PCH]) {
 #pragma unroll
-      for (int c = 0; c < KCH; ++c) {
-        if (ks[c] < 0) break;
-        int32_t n = __shfl(pick8(nlo, nhi, ks[c] & 7), r + 16 * (ks[c] >> 3));
-        if (!valid) n = -1;
-        if (FIRST) {
+      for (int c = 0; c < PCH; ++c) {
+        int32_t n = __shfl(pick8(nlo, nhi, ks[c] & 7), r + 16 * ((ks[c] & 31) >> 3));
+        if (!valid || ks[c] < 0) n = -1;
+        if constexpr (FIRST) {
           // absent neighbours read the reserved zero entry: no select on loaded data
-          const uint32_t word = n >= 0 ? a.lv_feat[lvb + n] : a.lv_feat[a.zero_feat];
-#pragma unroll
-          for (int s = 0; s < KSP; ++s) bsrc[c][s] = (float)((word >> (g * KS + s)) & 1u);
-          // slot s = KS (padding) meets zero weights
+          gb[c].word = n >= 0 ? a.lv_feat[lvb + n] : a.lv_feat[a.zero_feat];
         } else {
           // absent neighbours read the reserved all-zero row cap_model
           const int64_t srow = n >= 0 ? mo + n : a.cap_model;
           const f4* src = reinterpret_cast<const f4*>(a.h_in + srow * C + g * KS);
 #pragma unroll
-          for (int q = 0; q < KSP / 4; ++q) {
-            const f4 v = src[q];
-            bsrc[c][4 * q + 0] = v[0];
-            bsrc[c][4 * q + 1] = v[1];
-            bsrc[c][4 * q + 2] = v[2];
-            bsrc[c][4 * q + 3] = v[3];
-          }
+          for (int q = 0; q < KSP / 4; ++q) gb[c].v[q] = src[q];
         }
       }
+    };
+    auto mma = [&](const int (&ks)[PCH], const Gath (&gb)[PCH]) {
 #pragma unroll
-      for (int c = 0; c < KCH; ++c) {
+      for (int c = 0; c < PCH; ++c) {
         if (ks[c] < 0) break;
+        float bsrc[KSP];
+        if constexpr (FIRST) {
+#pragma unroll
+          for (int s = 0; s < KSP; ++s) bsrc[s] = (float)((gb[c].word >> (g * KS + s)) & 1u);
+          // slot s = KS (padding) meets zero weights
+        } else {
+#pragma unroll
+          for (int q = 0; q < KSP / 4; ++q)
+#pragma unroll
+            for (int e = 0; e < 4; ++e) bsrc[4 * q + e] = gb[c].v[q][e];
+        }
 #pragma unroll
         for (int cb = 0; cb < NCB; ++cb) {
           const f4* wp = reinterpret_cast<const f4*>(s_w + ((ks[c] * NCB + cb) * 64 + lane) * KSP);
@@ -304,9 +326,25 @@ __global__ void __launch_bounds__(CONV_THREADS) k_conv(ConvArgs a) {
             const f4 wv = wp[q];
 #pragma unroll
             for (int e = 0; e < 4; ++e)
-              if (4 * q + e < KS) acc[cb] = mfma4(wv[e], bsrc[c][4 * q + e], acc[cb]);
+              if (4 * q + e < KS) acc[cb] = mfma4(wv[e], bsrc[4 * q + e], acc[cb]);
           }
         }
+      }
+    };
+    {
+      int ksA[PCH], ksB[PCH];
+      Gath gA[PCH], gB[PCH];
+      take(ksA);
+      gather(ksA, gA);
+      while (true) {
+        take(ksB);
+        gather(ksB, gB);
+        mma(ksA, gA);
+        if (ksB[0] < 0) break;
+        take(ksA);
+        gather(ksA, gA);
+        mma(ksB, gB);
+        if (ksA[0] < 0) break;
       }
     }
 #pragma unroll
