@@ -26,7 +26,6 @@ typedef float f4 __attribute__((ext_vector_type(4)));
 
 constexpr int CONV_THREADS = 1024;
 constexpr int CONV_WAVES = CONV_THREADS / 64;
-constexpr int NXCD = 8;  // MI355X: 8 accelerator complex dies, each with its own L2
 
 __device__ __forceinline__ f4 mfma4(float a, float b, f4 c) {
   return __builtin_amdgcn_mfma_f32_16x16x4f32(a, b, c, 0, 0, 0);
@@ -146,6 +145,7 @@ __global__ void __launch_bounds__(CONV_THREADS) k_conv(ConvArgs a) {
   __shared__ int64_t s_tpre[NLEV + 1];
   __shared__ int64_t s_nv[NLEV];   // N_b of the launch's scales
   __shared__ int64_t s_mo[NLEV];   // first packed row of each scale
+  __shared__ int s_next;           // next dynamically handed-out tile slot of this block
 
   const int tid = threadIdx.x, w = tid >> 6, lane = tid & 63;
   const int r = lane & 15, g = lane >> 4;
@@ -160,13 +160,9 @@ __global__ void __launch_bounds__(CONV_THREADS) k_conv(ConvArgs a) {
     if (mo + nb > a.cap_model) nb = 0;  // overflow was latched where the size was made
     total_tiles += (nb + 15) / 16;
   }
-  {  // whole block idle (see the tile order below): skip the weight staging
-    const int64_t per = (total_tiles + NXCD - 1) / NXCD;
-    const int64_t lo = (blockIdx.x % NXCD) * per;
-    const int64_t cnt = (lo + per < total_tiles ? lo + per : total_tiles) - lo;
-    if ((int64_t)(blockIdx.x / NXCD) >= cnt) return;
-  }
+  if ((int64_t)blockIdx.x >= total_tiles) return;  // whole block idle: skip the weight staging
   if (tid == 0) {
+    s_next = 0;
     int64_t acc = 0;
     for (int i = 0; i < nsc; ++i) {
       const int b = a.b_lo + i;
@@ -177,7 +173,7 @@ __global__ void __launch_bounds__(CONV_THREADS) k_conv(ConvArgs a) {
       s_mo[i] = a.moff[b];
       acc += (nb + 15) / 16;
     }
-    s_tpre[nsc] = acc;
+    for (int i = nsc; i <= NLEV; ++i) s_tpre[i] = acc;  // padding: never below a valid tile
   }
   stage_lds<WSZ / 4, CONV_THREADS>(reinterpret_cast<const f4*>(a.w), reinterpret_cast<f4*>(s_w), tid);
   if (LAST)
@@ -185,18 +181,18 @@ __global__ void __launch_bounds__(CONV_THREADS) k_conv(ConvArgs a) {
                                      tid);
   __syncthreads();
 
-  // XCD-aware tile order: blocks are dispatched round-robin over the 8 XCDs,
-  // so block x runs on XCD x % 8.  Each XCD takes a contiguous range of
-  // tiles (Morton order: the neighbour rows of a tile sit in nearby tiles and
-  // stay in that XCD's L2); inside the range, tiles go round-robin over the
-  // XCD's blocks first so that a short range still spreads over CUs.
-  const int64_t xcd = blockIdx.x % NXCD, xb = blockIdx.x / NXCD, nxb = gridDim.x / NXCD;
-  const int64_t per_xcd = (total_tiles + NXCD - 1) / NXCD;
-  const int64_t t_lo = xcd * per_xcd;
-  const int64_t t_hi = t_lo + per_xcd < total_tiles ? t_lo + per_xcd : total_tiles;
-  for (int64_t tile = t_lo + (int64_t)w * nxb + xb; tile < t_hi; tile += nxb * CONV_WAVES) {
-    int si = 0;
-    while (si + 1 < nsc && s_tpre[si + 1] <= tile) ++si;
+  // Tile order: block x owns tiles x, x + G, x + 2G, ... (G = grid size), a
+  // sample of every scale of the launch, so all blocks carry about the same
+  // mix of cheap and expensive tiles (coarse scales have far more occupied
+  // offsets per tile).  Inside a block the waves take the block's tiles
+  // dynamically from an LDS counter: the first CONV_WAVES slots statically,
+  // the rest first come, first served.
+  for (int64_t slot = w;;) {
+    const int64_t tile = (int64_t)blockIdx.x + slot * gridDim.x;
+    if (tile >= total_tiles) break;
+    int si = 0;  // scale of the tile: all prefix loads issued together
+#pragma unroll
+    for (int i = 1; i < NLEV; ++i) si += (s_tpre[i] <= tile) ? 1 : 0;
     const int b = a.b_lo + si;
     const int64_t nvox = s_nv[si];
     const int64_t mo = s_mo[si];
@@ -262,15 +258,20 @@ __global__ void __launch_bounds__(CONV_THREADS) k_conv(ConvArgs a) {
       nlo = src[0];
       nhi = src[1];
     }
-    uint32_t present = 0;
-    if (valid) {
-      present = (uint32_t)(nlo.x >= 0) | ((uint32_t)(nlo.y >= 0) << 1) |
-                ((uint32_t)(nlo.z >= 0) << 2) | ((uint32_t)(nlo.w >= 0) << 3) |
-                ((uint32_t)(nhi.x >= 0) << 4) | ((uint32_t)(nhi.y >= 0) << 5) |
-                ((uint32_t)(nhi.z >= 0) << 6) | ((uint32_t)(nhi.w >= 0) << 7);
-      present = (present << (8 * g)) & 0x7FFFFFFu;  // the 5 padding entries are -1 anyway
+    // occupied offsets of the tile: one ballot per entry slot j, lanes of
+    // group g covering offsets 8g + j (the 5 padding entries are -1)
+    uint32_t offs = 0;
+    {
+      const int32_t e8[8] = {nlo.x, nlo.y, nlo.z, nlo.w, nhi.x, nhi.y, nhi.z, nhi.w};
+#pragma unroll
+      for (int j = 0; j < 8; ++j) {
+        const uint64_t bal = __ballot(valid && e8[j] >= 0);
+#pragma unroll
+        for (int gg = 0; gg < 4; ++gg)
+          offs |= ((bal >> (16 * gg)) & 0xFFFFull) ? (1u << (8 * gg + j)) : 0u;
+      }
+      offs &= 0x7FFFFFFu;
     }
-    uint32_t offs = (uint32_t)__builtin_amdgcn_readfirstlane((int)wave_or(present));
 
     // ---- accumulate over the occupied offsets, software-pipelined: the
     // gathers of the next PCH offsets are issued before the MFMAs of the
@@ -287,10 +288,13 @@ __global__ void __launch_bounds__(CONV_THREADS) k_conv(ConvArgs a) {
       }
     };
     auto gather = [&](const int (&ks)[PCH], Gath (&gb)[PCH]) {
+      int32_t nn[PCH];
+#pragma unroll
+      for (int c = 0; c < PCH; ++c) nn[c] = __shfl(pick8(nlo, nhi, ks[c] & 7), r + 16 * ((ks[c] & 31) >> 3));
+      __builtin_amdgcn_sched_barrier(0);  // keep the exchanges back to back (one wait for all)
 #pragma unroll
       for (int c = 0; c < PCH; ++c) {
-        int32_t n = __shfl(pick8(nlo, nhi, ks[c] & 7), r + 16 * ((ks[c] & 31) >> 3));
-        if (!valid || ks[c] < 0) n = -1;
+        const int32_t n = (valid && ks[c] >= 0) ? nn[c] : -1;
         if constexpr (FIRST) {
           // absent neighbours read the reserved zero entry: no select on loaded data
           gb[c].word = n >= 0 ? a.lv_feat[lvb + n] : a.lv_feat[a.zero_feat];
@@ -303,10 +307,20 @@ __global__ void __launch_bounds__(CONV_THREADS) k_conv(ConvArgs a) {
         }
       }
     };
+    auto load_w = [&](int k, f4 (&wv)[NCB][KSP / 4]) {
+#pragma unroll
+      for (int cb = 0; cb < NCB; ++cb) {
+        const f4* wp = reinterpret_cast<const f4*>(s_w + ((k * NCB + cb) * 64 + lane) * KSP);
+#pragma unroll
+        for (int q = 0; q < KSP / 4; ++q) wv[cb][q] = wp[q];
+      }
+    };
     auto mma = [&](const int (&ks)[PCH], const Gath (&gb)[PCH]) {
 #pragma unroll
       for (int c = 0; c < PCH; ++c) {
         if (ks[c] < 0) break;
+        f4 wv[NCB][KSP / 4];
+        load_w(ks[c], wv);
         float bsrc[KSP];
         if constexpr (FIRST) {
 #pragma unroll
@@ -318,17 +332,11 @@ __global__ void __launch_bounds__(CONV_THREADS) k_conv(ConvArgs a) {
 #pragma unroll
             for (int e = 0; e < 4; ++e) bsrc[4 * q + e] = gb[c].v[q][e];
         }
+        // column blocks interleaved: NCB independent accumulator chains
 #pragma unroll
-        for (int cb = 0; cb < NCB; ++cb) {
-          const f4* wp = reinterpret_cast<const f4*>(s_w + ((ks[c] * NCB + cb) * 64 + lane) * KSP);
+        for (int s = 0; s < KS; ++s)
 #pragma unroll
-          for (int q = 0; q < KSP / 4; ++q) {
-            const f4 wv = wp[q];
-#pragma unroll
-            for (int e = 0; e < 4; ++e)
-              if (4 * q + e < KS) acc[cb] = mfma4(wv[e], bsrc[4 * q + e], acc[cb]);
-          }
-        }
+          for (int cb = 0; cb < NCB; ++cb) acc[cb] = mfma4(wv[cb][s / 4][s % 4], bsrc[s], acc[cb]);
       }
     };
     {
@@ -405,6 +413,9 @@ __global__ void __launch_bounds__(CONV_THREADS) k_conv(ConvArgs a) {
       }
       if (valid && g == 0) a.lse[prow] = m + __logf(ssum);
     }
+    int nxt = 0;
+    if (lane == 0) nxt = atomicAdd(&s_next, 1);
+    slot = CONV_WAVES + __builtin_amdgcn_readfirstlane(__shfl(nxt, 0));
   }
 }
 
