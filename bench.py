@@ -29,6 +29,80 @@ sys.path.insert(0, ROOT)
 
 PEAK_FP32_MFMA_TFLOPS = 157.3
 PEAK_HBM_GBS = 8000.0
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "conv_last_traffic_hdl64_b14.txt")
+MODEL_SRC = os.path.join(ROOT, "paper_2503_12382_amd", "csrc", "k_model.hip")
+
+
+def alg_bytes_per_frame(counts, b0, B, M, C, hash_slots, status_words):
+    """Minimum HBM bytes per frame (encoder + decoder) of each kernel kind:
+    every input read once, every output written once.  Gathers of
+    neighbour rows and hash probes that hit cached lines are not counted, so
+    these are lower bounds on the traffic."""
+    N = {b0 + i: n for i, n in enumerate(counts)}
+    model = [b for b in range(b0 + 1, B)]
+    nm = sum(N[b] for b in model)
+    parents_hashed = sum(N[b] for b in range(b0, B - 1))
+    passes = (3 * B + 7) // 8
+    row = 4 * C
+    out = {}
+    out["zero"] = 2 * (16 * hash_slots + 4 * status_words)
+    out["quantize"] = M * (12 + 8)
+    out["sort"] = passes * M * 16
+    out["pyramid"] = M * 8 + sum(N[b] * 12 for b in range(b0, B + 1)) + sum(N[b] * 4 for b in range(b0, B))
+    # codes: child keys read, codes + child feature words written, parents hashed
+    out["codes"] = sum(N[b + 1] * (8 + 2) + N[b] for b in range(b0, B)) + 16 * parents_hashed
+    out["set_base"] = N[b0] * (12 + 1 + 8)
+    # expand: parent key + code read; child key, parent row, feature word and the
+    # parent's first-child row written; parents hashed
+    out["expand"] = sum(N[b] * (8 + 1 + 4) + N[b + 1] * (8 + 4 + 2) for b in range(b0, B)) + \
+        16 * parents_hashed
+    # conv layers (encoder + decoder): first reads keys, parent slots and feature
+    # words, writes the neighbour map and h; later layers read map + h, write h
+    first = sum(N[b] * (8 + 2 + 4 * 32 + row) + 16 * N[b - 1] for b in model)
+    mid = nm * (4 * 32 + 2 * row)
+    out["conv_first"] = 2 * first
+    out["conv_mid"] = 2 * mid
+    out["conv_last"] = 2 * (mid + nm * 4)
+    out["code_length"] = 2 * nm * (1 + 4 + row)
+    return out
+
+
+def read_traffic():
+    """HBM traffic of conv_last per launch from the committed rocprofv3 PMC
+    summary, or None when the kernel source changed since it was taken."""
+    import hashlib
+    if not os.path.exists(TRAFFIC_FILE):
+        return None
+    kv = {}
+    for line in open(TRAFFIC_FILE):
+        if "=" in line and not line.startswith("#"):
+            k, v = line.split("=", 1)
+            kv[k.strip()] = v.strip()
+    src = hashlib.sha256(open(MODEL_SRC, "rb").read()).hexdigest()[:16]
+    if kv.get("k_model_sha256_16") != src:
+        return None
+    return float(kv["bytes_per_launch"])
+
+
+def oracle_frame(args):
+    """One frame through the oracle (encode: pyramid, codes, model, bits;
+    decode: FCG expansion, model, bits); returns (T, t_enc, t_dec)."""
+    cfg_name, seed_shift = args
+    import oracle
+    from synth import BY_NAME, gen_scan, gen_weights
+    cfg = BY_NAME[cfg_name]
+    pts = gen_scan(cfg)
+    w = gen_weights(cfg.channels, cfg.layers, seed=cfg.weight_seed)
+    B, b0 = cfg.bit_depth, cfg.min_bit_depth
+    t = time.perf_counter()
+    P = oracle.Pyramid.from_points(pts, B, b0, cfg.range_m)
+    T_enc, _ = P.totals(w)
+    t_enc = time.perf_counter() - t
+    t = time.perf_counter()
+    D = oracle.Pyramid.from_codes(P.xyz(b0), b0, B, [P.codes(b) for b in range(b0, B)])
+    T_dec, _ = D.totals(w)
+    t_dec = time.perf_counter() - t
+    return T_enc, T_dec, t_enc, t_dec
 
 
 def log(*a):
@@ -43,6 +117,10 @@ def main():
     ap.add_argument("--config", default="hdl64_b14")
     ap.add_argument("--mode", choices=["graph", "eager"], default="graph")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-workers", type=int, default=0,
+                    help="processes for the all-cores oracle baseline (0: the CPUs this process may use, at most 16)")
+    ap.add_argument("--calib-copy", action="store_true",
+                    help="run one 256 MiB device-to-device copy first (counter calibration for PMC runs)")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py runs on one GPU only (got --gpus {args.gpus}): frames are independent, "
@@ -65,6 +143,15 @@ def main():
     stream = torch.cuda.Stream(device=dev)
     pts = torch.from_numpy(pts_np).to(dev)
     wd = reno.weights_to_device(w_np, dev)
+    if args.calib_copy:
+        # plain kernels of known traffic: a fill (256 MiB written), then an
+        # elementwise copy (256 MiB read, 256 MiB written)
+        src = torch.ones(64 << 20, dtype=torch.float32, device=dev)
+        dst = torch.empty_like(src)
+        torch.mul(src, 1.0, out=dst)
+        torch.cuda.synchronize()
+        log("calibration: fill writes 268435456 bytes; copy reads and writes 268435456 bytes")
+        del src, dst
 
     # probe pass with the always-sufficient capacity to learn this sensor's
     # model-voxel count; the timed contexts are sized to it (+12.5 %)
@@ -167,12 +254,19 @@ def main():
         be, bd = enc.profile_read(), dec.profile_read()
         enc.profile([])
         dec.profile([])
+    mem = enc.memory_info()
+    alg = alg_bytes_per_frame(counts, b0, B, M, C, mem["hash_slots"], mem["status_words"])
     breakdown = {}
     for k in kinds:
         ms = be.get(k, (0.0, 0))[0] + bd.get(k, (0.0, 0))[0]
         n = be.get(k, (0.0, 0))[1] + bd.get(k, (0.0, 0))[1]
         if n:
-            breakdown[k] = {"us_per_frame": round(1000.0 * ms / nb, 2), "launches_per_frame": n // nb}
+            us = 1000.0 * ms / nb
+            breakdown[k] = {"us_per_frame": round(us, 2), "launches_per_frame": n // nb}
+            if k in alg:
+                gbs = alg[k] / (us * 1e-6) / 1e9
+                breakdown[k].update({"alg_bytes_per_frame": alg[k], "alg_GBs": round(gbs, 1),
+                                     "hbm_frac": round(gbs / PEAK_HBM_GBS, 4)})
     cl_ms = pe["conv_last"][0] + pd["conv_last"][0]
     cl_launches = pe["conv_last"][1] + pd["conv_last"][1]
     # algorithmic flops of the last conv layer + head: per voxel, 2*C*C per
@@ -182,28 +276,34 @@ def main():
     log(f"conv_last: {cl_launches} launches, {1000 * cl_ms / cl_launches:.1f} us avg, "
         f"{achieved_tflops:.2f} TFLOP/s algorithmic")
 
-    # ---- CPU baseline: the oracle, single-threaded, one frame encode + decode ----
+    # ---- CPU baseline: the oracle (single-threaded C++, fp64), one frame per
+    # process, first alone, then one process per available core at once ----
     cpu = None
     oracle_bpp = None
     if not args.no_cpu_baseline:
-        import oracle
-        t = time.perf_counter()
-        P = oracle.Pyramid.from_points(pts_np, B, b0, cfg.range_m)
-        T_enc, _ = P.totals(w_np)
-        t_enc = time.perf_counter() - t
-        t = time.perf_counter()
-        D = oracle.Pyramid.from_codes(P.xyz(b0), b0, B, [P.codes(b) for b in range(b0, B)])
-        T_dec, _ = D.totals(w_np)
-        t_dec = time.perf_counter() - t
+        import multiprocessing as mp
+        T_enc, T_dec, t_enc, t_dec = oracle_frame((cfg.name, 0))
         oracle_bpp = T_enc / M
-        cpu = {"value": round(1.0 / (t_enc + t_dec), 4), "unit": "frames/s", "cores": 1,
+        single = 1.0 / (t_enc + t_dec)
+        workers = args.cpu_workers or min(16, len(os.sched_getaffinity(0)))
+        t = time.perf_counter()
+        with mp.get_context("spawn").Pool(workers) as pool:
+            res = pool.map(oracle_frame, [(cfg.name, i) for i in range(workers)])
+        wall = time.perf_counter() - t
+        if any(r[0] != T_enc for r in res):
+            log("oracle runs disagree")
+            sys.exit(1)
+        cpu = {"value": round(workers / wall, 4), "unit": "frames/s", "cores": workers,
                "kind": "oracle",
-               "sample": f"one {cfg.name} frame ({M} points): oracle encode {t_enc:.1f} s "
-                         f"(pyramid, codes, model, bits) + decode {t_dec:.1f} s "
-                         f"(FCG expansion, model, bits), single-threaded C++ in fp64"}
+               "sample": f"{workers} copies of one {cfg.name} frame ({M} points), one process per core, "
+                         f"{wall:.1f} s wall; each: oracle encode (pyramid, codes, model, bits) + decode "
+                         f"(FCG expansion, model, bits) in single-threaded C++ fp64",
+               "single_thread_value": round(single, 4),
+               "single_thread_sample": f"one frame alone: encode {t_enc:.1f} s + decode {t_dec:.1f} s"}
         log("cpu baseline", cpu)
 
     voxels_frame = sum(counts)
+    traffic = read_traffic()
     out = {
         "metric": "frames/s + Mvoxels/s, encode+decode model path, 14-bit 64-beam scan; bits/pt",
         "value": round(fps, 2),
@@ -225,11 +325,12 @@ def main():
                                f"random-init predictor C={C} L={L}, one frame encoded + decoded "
                                "per step",
                    "points": M, "voxels_per_frame": voxels_frame, "model_voxels": model_vox,
+                   "device_bytes_per_context": mem["device_bytes"],
                    "mode": args.mode},
         "roofline": {"bound": "mfma", "kernel": "conv_last (last sparse conv + 256-way head)",
                      "achieved": round(achieved_tflops, 3), "peak": PEAK_FP32_MFMA_TFLOPS,
                      "unit": "TFLOP/s", "frac": round(achieved_tflops / PEAK_FP32_MFMA_TFLOPS, 4),
-                     "traffic": None,
+                     "traffic": traffic,
                      "avg_launch_us": round(1000 * cl_ms / cl_launches, 2),
                      "launches": cl_launches},
         "cpu_baseline": cpu,

@@ -104,6 +104,11 @@ reno_status reno_destroy(reno_ctx* ctx);
 const char* reno_last_error(const reno_ctx* ctx);
 /* Waits for the context stream and reports latched device errors. */
 reno_status reno_sync(reno_ctx* ctx);
+/* Sizes fixed at create time, into info_host[4] (host memory): [0] coordinate
+ * hash slots (16 bytes each), [1] look-back status words (4 bytes each), [2]
+ * model-row capacity (max_model_voxels as resolved), [3] device bytes the
+ * context allocated.  No device work. */
+reno_status reno_memory_info(const reno_ctx* ctx, int64_t* info_host);
 
 /* Copies the model weights into the context's operand layout (Sec. 3.2:
  * one parameter set shared by all scales).  Must precede predict_probs. */

@@ -57,6 +57,7 @@ _SIGS = {
     "reno_destroy": (_int, [_vp]),
     "reno_last_error": (ctypes.c_char_p, [_vp]),
     "reno_sync": (_int, [_vp]),
+    "reno_memory_info": (_int, [_vp, _vp]),
     "reno_set_weights": (_int, [_vp, ctypes.POINTER(reno_weights)]),
     "reno_build_pyramid": (_int, [_vp, _vp, _i64, _int]),
     "reno_set_base": (_int, [_vp, _int, _vp, _vp, _i64]),
@@ -248,6 +249,14 @@ class Context:
         out = self._empty((max(n, 1), 27), self.torch.int32)
         self._check(lib().reno_neighbor_map(self._h, scale, _ptr(out)))
         return out[:n]
+
+    def memory_info(self) -> dict:
+        """Sizes fixed at create time: hash slots, look-back status words,
+        model-row capacity and the device bytes the context allocated."""
+        info = np.zeros(4, np.int64)
+        self._check(lib().reno_memory_info(self._h, info.ctypes.data_as(_vp)))
+        return {"hash_slots": int(info[0]), "status_words": int(info[1]),
+                "model_rows": int(info[2]), "device_bytes": int(info[3])}
 
     def profile(self, kinds=()):
         """Time the launches of the named kernel kinds (see KERNELS) with HIP events."""

@@ -32,9 +32,12 @@ reno_status fail(Ctx* c, reno_status s, const std::string& msg) {
 
 size_t round256(size_t n) { return (n + 255) & ~size_t(255); }
 
+// device allocation, tallied into *total (bytes actually requested)
 template <typename T>
-hipError_t dalloc(T** p, size_t count) {
-  return hipMalloc(reinterpret_cast<void**>(p), round256(count * sizeof(T) + 16));
+hipError_t dalloc(T** p, size_t count, int64_t* total) {
+  const size_t bytes = round256(count * sizeof(T) + 16);
+  *total += (int64_t)bytes;
+  return hipMalloc(reinterpret_cast<void**>(p), bytes);
 }
 
 bool has(uint32_t mask, int b) { return b >= 0 && b < 32 && ((mask >> b) & 1u); }
@@ -156,36 +159,36 @@ reno_status reno_create(const reno_params* p, void* hip_stream, reno_ctx** out) 
   auto A = [&](hipError_t r) {
     if (e == hipSuccess) e = r;
   };
-  A(dalloc(&c->keys_a, c->cap_pts));
-  A(dalloc(&c->keys_b, c->cap_pts));
-  A(dalloc(&c->lv_key, lvn));
-  A(dalloc(&c->lv_code, lvn));
-  A(dalloc(&c->lv_parent, lvn));
-  A(dalloc(&c->lv_fc, lvn));
-  A(dalloc(&c->lv_feat, lvn + 8));  // entry lvn stays zero: absent-neighbour input
-  A(dalloc(&c->d_count, reno::NLEV));
-  A(dalloc(&c->d_moff, reno::NLEV + 1));
-  A(dalloc(&c->d_err, 4));
-  A(dalloc(&c->d_hist, reno::MAX_PASSES * reno::RADIX));
-  A(dalloc(&c->d_ticket, reno::TICKETS));
-  A(dalloc(&c->d_status, (size_t)c->status_words));
-  A(dalloc(&c->d_hash, size_t(1) << c->hash_lg));
-  A(dalloc(&c->h_a, (size_t)(cap_model + 1) * C));  // row cap_model stays zero
-  A(dalloc(&c->h_b, (size_t)(cap_model + 1) * C));
-  A(dalloc(&c->d_nbr, (size_t)cap_model * reno::NBR_STRIDE));
-  A(dalloc(&c->d_lse, (size_t)cap_model));
-  A(dalloc(&c->d_partial, (size_t)reno::NLEV * ((c->cap_pts + 1023) / 1024)));
-  A(dalloc(&c->d_total, reno::NLEV));
+  A(dalloc(&c->keys_a, c->cap_pts, &c->device_bytes));
+  A(dalloc(&c->keys_b, c->cap_pts, &c->device_bytes));
+  A(dalloc(&c->lv_key, lvn, &c->device_bytes));
+  A(dalloc(&c->lv_code, lvn, &c->device_bytes));
+  A(dalloc(&c->lv_parent, lvn, &c->device_bytes));
+  A(dalloc(&c->lv_fc, lvn, &c->device_bytes));
+  A(dalloc(&c->lv_feat, lvn + 8, &c->device_bytes));  // entry lvn stays zero: absent-neighbour input
+  A(dalloc(&c->d_count, reno::NLEV, &c->device_bytes));
+  A(dalloc(&c->d_moff, reno::NLEV + 1, &c->device_bytes));
+  A(dalloc(&c->d_err, 4, &c->device_bytes));
+  A(dalloc(&c->d_hist, reno::MAX_PASSES * reno::RADIX, &c->device_bytes));
+  A(dalloc(&c->d_ticket, reno::TICKETS, &c->device_bytes));
+  A(dalloc(&c->d_status, (size_t)c->status_words, &c->device_bytes));
+  A(dalloc(&c->d_hash, size_t(1) << c->hash_lg, &c->device_bytes));
+  A(dalloc(&c->h_a, (size_t)(cap_model + 1) * C, &c->device_bytes));  // row cap_model stays zero
+  A(dalloc(&c->h_b, (size_t)(cap_model + 1) * C, &c->device_bytes));
+  A(dalloc(&c->d_nbr, (size_t)cap_model * reno::NBR_STRIDE, &c->device_bytes));
+  A(dalloc(&c->d_lse, (size_t)cap_model, &c->device_bytes));
+  A(dalloc(&c->d_partial, (size_t)reno::NLEV * ((c->cap_pts + 1023) / 1024), &c->device_bytes));
+  A(dalloc(&c->d_total, reno::NLEV, &c->device_bytes));
   int c_in = RENO_IN_FEATURES;
   for (int l = 0; l < p->layers; ++l) {
     const int KS = (c_in + 3) / 4, KSP = (KS + 3) & ~3;
-    A(dalloc(&c->w_conv[l], (size_t)27 * (C / 16) * 64 * KSP));
-    A(dalloc(&c->w_bias[l], (size_t)C));
+    A(dalloc(&c->w_conv[l], (size_t)27 * (C / 16) * 64 * KSP, &c->device_bytes));
+    A(dalloc(&c->w_bias[l], (size_t)C, &c->device_bytes));
     c_in = C;
   }
-  A(dalloc(&c->w_head, (size_t)16 * 64 * (C / 4)));
-  A(dalloc(&c->w_hbias, 256));
-  A(dalloc(&c->w_head_plain, (size_t)C * 256));
+  A(dalloc(&c->w_head, (size_t)16 * 64 * (C / 4), &c->device_bytes));
+  A(dalloc(&c->w_hbias, 256, &c->device_bytes));
+  A(dalloc(&c->w_head_plain, (size_t)C * 256, &c->device_bytes));
   A(hipHostMalloc(reinterpret_cast<void**>(&c->h_total), sizeof(double) * reno::NLEV, 0));
   A(hipHostMalloc(reinterpret_cast<void**>(&c->h_count), sizeof(int32_t) * reno::NLEV, 0));
   A(hipHostMalloc(reinterpret_cast<void**>(&c->h_err), 64, 0));
@@ -220,6 +223,15 @@ reno_status reno_destroy(reno_ctx* c) {
   (void)hipStreamSynchronize(c->stream);
   free_all(c);
   delete c;
+  return RENO_OK;
+}
+
+reno_status reno_memory_info(const reno_ctx* c, int64_t* info_host) {
+  if (!c || !info_host) return RENO_E_INVALID;
+  info_host[0] = int64_t(1) << c->hash_lg;
+  info_host[1] = c->status_words;
+  info_host[2] = c->cap_model;
+  info_host[3] = c->device_bytes;
   return RENO_OK;
 }
 

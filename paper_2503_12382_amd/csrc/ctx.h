@@ -54,6 +54,7 @@ struct Ctx {
   int hash_lg = 0;
   int64_t sort_tiles = 0;   // max tiles of one sort pass
   int64_t status_words = 0; // look-back status capacity (uint32)
+  int64_t device_bytes = 0; // device memory allocated by reno_create
 
   // per-scale regions: scale b lives at (b - b0) * cap_pts
   uint64_t* keys_a = nullptr;   // sort ping-pong [cap_pts]
