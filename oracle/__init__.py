@@ -35,7 +35,11 @@ class OrcWeights(ctypes.Structure):
     _fields_ = [("c_in", ctypes.c_int), ("channels", ctypes.c_int), ("layers", ctypes.c_int),
                 ("pad", ctypes.c_int),
                 ("conv_w", ctypes.c_void_p * 8), ("conv_b", ctypes.c_void_p * 8),
-                ("head_w", ctypes.c_void_p), ("head_b", ctypes.c_void_p)]
+                ("head_w", ctypes.c_void_p), ("head_b", ctypes.c_void_p),
+                ("head_mode", ctypes.c_int), ("pad2", ctypes.c_int),
+                ("head1_w", ctypes.c_void_p), ("head1_b", ctypes.c_void_p),
+                ("emb_s1", ctypes.c_void_p), ("head2_w", ctypes.c_void_p),
+                ("head2_b", ctypes.c_void_p)]
 
 
 def lib():
@@ -63,6 +67,8 @@ def lib():
             "orc_features": (None, [vp, c_int, vp]),
             "orc_sparse_conv": (c_int, [vp, i64, c_int, vp, c_int, vp, vp, c_int, c_int, vp]),
             "orc_model": (c_int, [vp, c_int, ctypes.POINTER(OrcWeights), vp, i64, vp, vp, vp]),
+            "orc_model2": (c_int, [vp, c_int, ctypes.POINTER(OrcWeights), vp, i64, vp, vp, vp, vp,
+                                   vp, vp]),
             "orc_totals": (dbl, [vp, ctypes.POINTER(OrcWeights), vp]),
             "orc_freqs_from_probs": (None, [vp, vp]),
             "orc_rans_encode": (i64, [vp, vp, i64, vp, i64]),
@@ -95,7 +101,7 @@ def quantize(points: np.ndarray, B: int, R: float) -> np.ndarray:
 class _W:
     """Keeps the fp32 weight arrays alive while the oracle holds pointers."""
 
-    def __init__(self, w: dict):
+    def __init__(self, w: dict, two_stage=None):
         self.arrays = []
         s = OrcWeights()
         s.c_in = w["c_in"]
@@ -112,6 +118,14 @@ class _W:
         self.arrays += [hw, hb]
         s.head_w = hw.ctypes.data
         s.head_b = hb.ctypes.data
+        if two_stage is None:
+            two_stage = "head1_w" in w
+        s.head_mode = 1 if two_stage else 0
+        if two_stage:
+            for name in ("head1_w", "head1_b", "emb_s1", "head2_w", "head2_b"):
+                a = np.ascontiguousarray(w[name], dtype=np.float32)
+                self.arrays.append(a)
+                setattr(s, name, a.ctypes.data)
         self.s = s
 
 
@@ -211,10 +225,34 @@ class Pyramid:
             raise ValueError("oracle model rejected the arguments")
         return lg, lse, bt
 
-    def totals(self, weights: dict):
-        """(T, per_scale[B+1]): total ideal bits and its split per scale."""
+    def model2(self, b: int, weights: dict, rows=None, s1=None, logits=True, bits=True):
+        """Bitwise two-stage head: (logits1 [n][16], logits2 [n][16], lse1 [n],
+        lse2 [n], bits [n]) for the requested rows.  S1 (the low nibble) comes
+        from ``s1`` when given, else from the codes of scale b (then bits are
+        returned for b < B)."""
+        if rows is None:
+            rows = np.arange(self.num(b), dtype=np.int64)
+        rows = np.ascontiguousarray(rows, dtype=np.int64)
+        n = rows.size
+        s1a = None if s1 is None else np.ascontiguousarray(s1, dtype=np.uint8)
+        l1 = np.empty((n, 16)) if logits else None
+        l2 = np.empty((n, 16)) if logits else None
+        lse1, lse2 = np.empty(n), np.empty(n)
+        bt = np.empty(n) if (bits and s1 is None and b < self.B) else None
+        W = _W(weights, two_stage=True)
+        rc = lib().orc_model2(self._h, b, ctypes.byref(W.s), _p(rows), n,
+                              _p(s1a) if s1a is not None else None,
+                              _p(l1) if l1 is not None else None, _p(l2) if l2 is not None else None,
+                              _p(lse1), _p(lse2), _p(bt) if bt is not None else None)
+        if rc != 0:
+            raise ValueError("oracle two-stage model rejected the arguments")
+        return l1, l2, lse1, lse2, bt
+
+    def totals(self, weights: dict, two_stage=None):
+        """(T, per_scale[B+1]): total ideal bits and its split per scale
+        (two-stage head when the weights carry one, unless told otherwise)."""
         per = np.zeros(self.B + 1, dtype=np.float64)
-        W = _W(weights)
+        W = _W(weights, two_stage)
         T = lib().orc_totals(self._h, ctypes.byref(W.s), _p(per))
         if T < 0:
             raise ValueError("oracle totals failed")

@@ -202,6 +202,13 @@ struct OrcWeights {
   const float* conv_b[8];   // [C_out]
   const float* head_w;      // [C][256]
   const float* head_b;      // [256]
+  // bitwise two-stage head (Sec. 3.2, Eqs. 11-13), used when head_mode == 1
+  int head_mode, pad2;
+  const float* head1_w;     // [C][16]  stage 1 over S1 = O & 15
+  const float* head1_b;     // [16]
+  const float* emb_s1;      // [16][C]  Emb(S1), added to the features before stage 2
+  const float* head2_w;     // [C][16]  stage 2 over S2 = O >> 4
+  const float* head2_b;     // [16]
 };
 
 uint64_t orc_morton(int64_t x, int64_t y, int64_t z, int bits) {
@@ -398,11 +405,13 @@ int orc_sparse_conv(const int64_t* xyz, int64_t n, int bits, const double* feats
 // each layer is computed on the receptive field those rows need.
 //   logits [nrows][256] (or NULL), lse [nrows] natural-log normaliser (or
 //   NULL), bits [nrows] (or NULL; needs b < B).
-int orc_model(void* h, int b, const OrcWeights* w, const int64_t* rows, int64_t nrows,
-              double* logits, double* lse, double* bits) {
+// Features h_L of the last conv layer for the requested rows, stored densely
+// over all N rows of the scale in `cur` ([N][C]; rows outside the requested
+// set are zero).  Returns -1 on bad arguments.
+static int final_features(void* h, int b, const OrcWeights* w, const int64_t* rows, int64_t nrows,
+                   std::vector<double>& cur) {
   Pyramid* P = static_cast<Pyramid*>(h);
   if (b <= P->b0 || b > P->B || w->layers < 1 || w->layers > 8) return -1;
-  if (bits && b >= P->B) return -1;
   const Level& L = P->lv[b];
   const int C = w->channels;
   const int64_t N = (int64_t)L.v.size();
@@ -434,7 +443,8 @@ int orc_model(void* h, int b, const OrcWeights* w, const int64_t* rows, int64_t 
   orc_features(h, b, feat_all.data());
   for (int64_t r : need[0])
     for (int j = 0; j < 11; ++j) x[r * 11 + j] = feat_all[r * 11 + j];
-  std::vector<double> cur = x, y;
+  cur = x;
+  std::vector<double> y;
   int c_in = 11;
   for (int l = 1; l <= w->layers; ++l) {
     std::vector<int64_t> out_rows = need[l];
@@ -448,6 +458,26 @@ int orc_model(void* h, int b, const OrcWeights* w, const int64_t* rows, int64_t 
     cur.swap(nxt);
     c_in = C;
   }
+  return 0;
+}
+
+// Natural-log normaliser of a logit vector (max subtracted first).
+static double log_sum_exp(const double* z, int n) {
+  double m = z[0];
+  for (int s = 1; s < n; ++s) m = std::max(m, z[s]);
+  double sum = 0.0;
+  for (int s = 0; s < n; ++s) sum += std::exp(z[s] - m);
+  return m + std::log(sum);
+}
+
+int orc_model(void* h, int b, const OrcWeights* w, const int64_t* rows, int64_t nrows,
+              double* logits, double* lse, double* bits) {
+  Pyramid* P = static_cast<Pyramid*>(h);
+  if (bits && b >= P->B) return -1;
+  std::vector<double> cur;
+  if (final_features(h, b, w, rows, nrows, cur) != 0) return -1;
+  const Level& L = P->lv[b];
+  const int C = w->channels;
   for (int64_t i = 0; i < nrows; ++i) {
     const int64_t r = rows[i];
     double z[256];
@@ -456,14 +486,56 @@ int orc_model(void* h, int b, const OrcWeights* w, const int64_t* rows, int64_t 
       for (int c = 0; c < C; ++c) acc += (double)w->head_w[c * 256 + s] * cur[r * C + c];
       z[s] = acc;
     }
-    double m = z[0];
-    for (int s = 1; s < 256; ++s) m = std::max(m, z[s]);
-    double sum = 0.0;
-    for (int s = 0; s < 256; ++s) sum += std::exp(z[s] - m);
-    double l = m + std::log(sum);
+    const double l = log_sum_exp(z, 256);
     if (logits) for (int s = 0; s < 256; ++s) logits[i * 256 + s] = z[s];
     if (lse) lse[i] = l;
     if (bits) bits[i] = (l - z[L.code[r]]) / std::log(2.0);
+  }
+  return 0;
+}
+
+// Bitwise two-stage head (Sec. 3.2, Eqs. 11-13; linear MLPs in this model):
+// the code O splits into S1 = O & 15 (children delta = 0..3, coded first) and
+// S2 = O >> 4 (delta = 4..7), and P(O) = P(S1) P(S2 | S1) with
+//   z1 = head1_w^T h + head1_b,                 P(S1)      = softmax(z1)
+//   z2 = head2_w^T (h + emb_s1[S1]) + head2_b,  P(S2 | S1) = softmax(z2).
+// S1 is taken from `s1` ([nrows], values 0..15) when given, else from O_b.
+//   logits1 / logits2 [nrows][16], lse1 / lse2 [nrows] (each may be NULL),
+//   bits [nrows] = -log2 P(S1) - log2 P(S2 | S1) (or NULL; needs b < B and
+//   S1 from O_b).
+int orc_model2(void* h, int b, const OrcWeights* w, const int64_t* rows, int64_t nrows,
+               const uint8_t* s1, double* logits1, double* logits2, double* lse1, double* lse2,
+               double* bits) {
+  Pyramid* P = static_cast<Pyramid*>(h);
+  if (w->head_mode != 1) return -1;
+  if ((bits || !s1) && b >= P->B) return -1;
+  if (bits && s1) return -1;
+  std::vector<double> cur;
+  if (final_features(h, b, w, rows, nrows, cur) != 0) return -1;
+  const Level& L = P->lv[b];
+  const int C = w->channels;
+  for (int64_t i = 0; i < nrows; ++i) {
+    const int64_t r = rows[i];
+    const int a = s1 ? s1[i] : (L.code[r] & 15);
+    if (a < 0 || a > 15) return -1;
+    double z1[16], z2[16];
+    for (int s = 0; s < 16; ++s) {
+      double acc = (double)w->head1_b[s];
+      for (int c = 0; c < C; ++c) acc += (double)w->head1_w[c * 16 + s] * cur[r * C + c];
+      z1[s] = acc;
+    }
+    for (int s = 0; s < 16; ++s) {
+      double acc = (double)w->head2_b[s];
+      for (int c = 0; c < C; ++c)
+        acc += (double)w->head2_w[c * 16 + s] * (cur[r * C + c] + (double)w->emb_s1[a * C + c]);
+      z2[s] = acc;
+    }
+    const double l1 = log_sum_exp(z1, 16), l2 = log_sum_exp(z2, 16);
+    if (logits1) for (int s = 0; s < 16; ++s) logits1[i * 16 + s] = z1[s];
+    if (logits2) for (int s = 0; s < 16; ++s) logits2[i * 16 + s] = z2[s];
+    if (lse1) lse1[i] = l1;
+    if (lse2) lse2[i] = l2;
+    if (bits) bits[i] = ((l1 - z1[a]) + (l2 - z2[L.code[r] >> 4])) / std::log(2.0);
   }
   return 0;
 }
@@ -484,7 +556,11 @@ double orc_totals(void* h, const OrcWeights* w, double* per_scale /*[B+1] or NUL
     std::vector<int64_t> rows(N);
     for (int64_t i = 0; i < N; ++i) rows[i] = i;
     std::vector<double> bits(N);
-    if (orc_model(h, b, w, rows.data(), N, nullptr, nullptr, bits.data()) != 0) return -1.0;
+    const int rc = w->head_mode == 1
+                       ? orc_model2(h, b, w, rows.data(), N, nullptr, nullptr, nullptr, nullptr,
+                                    nullptr, bits.data())
+                       : orc_model(h, b, w, rows.data(), N, nullptr, nullptr, bits.data());
+    if (rc != 0) return -1.0;
     double s = 0.0;
     for (double v : bits) s += v;
     if (per_scale) per_scale[b] = s;

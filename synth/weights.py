@@ -5,6 +5,11 @@ Layout (fp32, row-major, shared by every consumer):
   conv_b[l]  [C_out]
   head_w     [C][256]
   head_b     [256]
+and, with ``two_stage=True``, the bitwise two-stage head (Sec. 3.2,
+Eqs. 11-13): S1 = O & 15 first, then S2 = O >> 4 given S1:
+  head1_w    [C][16]    head1_b [16]     stage 1: z1 = head1_w^T h + head1_b
+  emb_s1     [16][C]                     Emb(S1), added to h before stage 2
+  head2_w    [C][16]    head2_b [16]     stage 2: z2 = head2_w^T (h + emb_s1[S1]) + head2_b
 with C_in = 11 for the first layer and C for the rest.  Kaiming-normal:
 std = sqrt(2 / fan_in), fan_in = 27 * C_in for a conv and C for the head.
 Biases are zero unless ``bias_std`` is given (tests use non-zero biases so
@@ -23,7 +28,8 @@ _W_STREAM = 21
 
 
 def gen_weights(channels: int, layers: int, seed: int = 2, bias_std: float = 0.0,
-                head_scale: float = 1.0, in_features: int = IN_FEATURES) -> dict:
+                head_scale: float = 1.0, in_features: int = IN_FEATURES,
+                two_stage: bool = False, emb_std: float = 1.0) -> dict:
     draw = [0]
 
     def normals(n):
@@ -42,9 +48,17 @@ def gen_weights(channels: int, layers: int, seed: int = 2, bias_std: float = 0.0
         c_in = channels
     hw = normals(channels * SYMBOLS) * np.sqrt(2.0 / channels) * head_scale
     hb = normals(SYMBOLS) * bias_std * head_scale
-    return {
+    out = {
         "c_in": in_features, "channels": channels, "layers": layers,
         "conv_w": conv_w, "conv_b": conv_b,
         "head_w": hw.reshape(channels, SYMBOLS).astype(np.float32),
         "head_b": hb.astype(np.float32),
     }
+    if two_stage:  # drawn after the one-stage weights, which stay unchanged
+        std = np.sqrt(2.0 / channels) * head_scale
+        out["head1_w"] = (normals(channels * 16) * std).reshape(channels, 16).astype(np.float32)
+        out["head1_b"] = (normals(16) * bias_std * head_scale).astype(np.float32)
+        out["emb_s1"] = (normals(16 * channels) * emb_std).reshape(16, channels).astype(np.float32)
+        out["head2_w"] = (normals(channels * 16) * std).reshape(channels, 16).astype(np.float32)
+        out["head2_b"] = (normals(16) * bias_std * head_scale).astype(np.float32)
+    return out

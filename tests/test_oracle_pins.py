@@ -374,3 +374,121 @@ def test_rans_rejects_corruption():
     words = oracle.rans_encode(sym, freq)
     with pytest.raises(ValueError):
         oracle.rans_decode(words[:-1], freq, n)
+
+
+# ---- bitwise two-stage head (Sec. 3.2, Eqs. 11-13) -------------------------------------
+
+def _two_stage_weights(C, L, seed=9):
+    return gen_weights(C, L, seed=seed, bias_std=0.2, two_stage=True)
+
+
+def _factorised_one_stage(w, shift=None):
+    """One-stage head whose logits split as z(O) = u(O & 15) + v(O >> 4): with no
+    S1 dependence in stage 2, P(O) = softmax(u)[S1] * softmax(v)[S2] exactly."""
+    o = np.arange(256)
+    f = dict(w)
+    f["head_w"] = (w["head1_w"][:, o & 15].astype(np.float64) + w["head2_w"][:, o >> 4]).astype(np.float32)
+    hb = w["head1_b"][o & 15].astype(np.float64) + w["head2_b"][o >> 4]
+    if shift is not None:
+        hb = hb + shift[o >> 4]
+    f["head_b"] = hb.astype(np.float32)
+    return f
+
+
+def _fp32_exact(w):
+    """Weights whose fp32 sums used above are exact (values on a 2^-10 grid)."""
+    out = dict(w)
+    for k in ("head1_w", "head2_w", "head1_b", "head2_b", "emb_s1"):
+        out[k] = (np.round(np.asarray(w[k], np.float64) * 1024) / 1024).astype(np.float32)
+    return out
+
+
+def test_two_stage_without_embedding_equals_factorised_one_stage(scan_cache):
+    c = CONFIGS[0]
+    P = oracle.Pyramid.from_points(scan_cache(0), c.bit_depth, c.min_bit_depth, c.range_m)
+    w = _fp32_exact(_two_stage_weights(c.channels, c.layers))
+    w["emb_s1"] = np.zeros_like(w["emb_s1"])
+    one = _factorised_one_stage(w)
+    for b in range(c.min_bit_depth + 1, c.bit_depth):
+        _, _, _, _, bits2 = P.model2(b, w)
+        _, _, bits1 = P.model(b, one)
+        np.testing.assert_allclose(bits2, bits1, rtol=0, atol=1e-9)
+    # the same with one embedding vector for every S1: it only moves stage-2 logits by head2_w^T e
+    e = (np.arange(c.channels) % 7 - 3).astype(np.float32) / 8
+    w["emb_s1"] = np.tile(e, (16, 1))
+    one = _factorised_one_stage(w, shift=w["head2_w"].astype(np.float64).T @ e)
+    b = c.bit_depth - 1
+    np.testing.assert_allclose(P.model2(b, w)[4], P.model(b, one)[2], rtol=0, atol=1e-9)
+    T2, _ = P.totals(w)
+    T1, _ = P.totals(one)
+    assert T2 == pytest.approx(T1, rel=1e-12)
+
+
+def test_two_stage_embedding_limit_selects_s2():
+    """Stage 2 reads the first 16 channels (head2_w = [I; 0]) and Emb(S1) puts a
+    large logit on symbol g(S1): S2 costs ~0 bits where S2 = g(S1) and about
+    gamma / ln 2 elsewhere, which fixes S1 = low nibble, S2 = high nibble and the
+    row of the embedding that is used."""
+    rs = np.random.default_rng(4)
+    B, b0 = 7, 3
+    xyz = rs.integers(0, 1 << B, size=(1500, 3)) // 2 + 20
+    P = oracle.Pyramid.from_voxels(xyz, B, b0)
+    C, L, gamma = 16, 2, 60.0
+    w = _two_stage_weights(C, L, seed=5)
+    w["head2_w"] = np.eye(C, 16, dtype=np.float32)
+    w["head2_b"] = np.zeros(16, np.float32)
+    g = (5 * np.arange(16) + 3) % 16
+    emb = np.zeros((16, C), np.float32)
+    emb[np.arange(16), g] = gamma
+    w["emb_s1"] = emb
+    hits = misses = 0
+    for b in range(b0 + 1, B):
+        l1, l2, lse1, lse2, bits = P.model2(b, w)
+        code = P.codes(b).astype(np.int64)
+        s1, s2 = code & 15, code >> 4
+        stage1 = (lse1 - l1[np.arange(len(code)), s1]) / math.log(2)
+        stage2 = bits - stage1
+        hit = s2 == g[s1]
+        hits += hit.sum()
+        misses += (~hit).sum()
+        assert np.all(stage2[hit] < 1e-12 + 1e-9)
+        assert np.all(stage2[~hit] > 40.0)
+        # the winning stage-2 logit is symbol g(S1) for every voxel
+        assert np.array_equal(l2.argmax(1), g[s1])
+    assert hits > 0 and misses > 0
+
+
+def test_two_stage_zero_heads_give_8_bits(scan_cache):
+    c = CONFIGS[0]
+    P = oracle.Pyramid.from_points(scan_cache(0), c.bit_depth, c.min_bit_depth, c.range_m)
+    w = _two_stage_weights(c.channels, c.layers)
+    for k in ("head1_w", "head1_b", "head2_w", "head2_b"):
+        w[k] = np.zeros_like(w[k])
+    for b in range(c.min_bit_depth + 1, c.bit_depth):
+        _, _, lse1, lse2, bits = P.model2(b, w)
+        np.testing.assert_allclose(bits, 8.0, rtol=0, atol=1e-12)
+        np.testing.assert_allclose(lse1, math.log(16.0), atol=1e-12)
+
+
+def test_two_stage_rows_normalised_and_s1_input_path(scan_cache):
+    c = CONFIGS[0]
+    P = oracle.Pyramid.from_points(scan_cache(0), c.bit_depth, c.min_bit_depth, c.range_m)
+    w = _two_stage_weights(c.channels, c.layers, seed=12)
+    b = c.bit_depth - 2
+    l1, l2, lse1, lse2, bits = P.model2(b, w)
+    np.testing.assert_allclose(np.exp(l1 - lse1[:, None]).sum(1), 1.0, atol=1e-12)
+    np.testing.assert_allclose(np.exp(l2 - lse2[:, None]).sum(1), 1.0, atol=1e-12)
+    code = P.codes(b).astype(np.int64)
+    ref = -(l1[np.arange(len(code)), code & 15] - lse1 + l2[np.arange(len(code)), code >> 4] - lse2) / math.log(2)
+    np.testing.assert_allclose(bits, ref, atol=1e-12)
+    # S1 handed in (as a decoder would after decoding it) gives the same stage 2
+    rows = np.arange(0, P.num(b), 3)
+    s1 = (code[rows] & 15).astype(np.uint8)
+    m1, m2, _, _, none = P.model2(b, w, rows=rows, s1=s1)
+    assert none is None
+    np.testing.assert_allclose(m2, l2[rows], atol=1e-12)
+    np.testing.assert_allclose(m1, l1[rows], atol=1e-12)
+    # and a different S1 changes stage 2 only
+    m1b, m2b, _, _, _ = P.model2(b, w, rows=rows, s1=(s1 + 1) % 16)
+    np.testing.assert_allclose(m1b, m1, atol=0)
+    assert np.abs(m2b - m2).max() > 1e-3
