@@ -65,6 +65,8 @@ typedef enum {
 #define RENO_IN_FEATURES 11
 #define RENO_MAX_BIT_DEPTH 21
 #define RENO_ALL_SCALES (-1)
+#define RENO_HEAD_ONE_STAGE 0   /* one 256-way softmax over the code (Eq. 10) */
+#define RENO_HEAD_TWO_STAGE 1   /* bitwise two-stage head (Eqs. 11-13) */
 
 /* Capacities and model shape, fixed for the life of a context. */
 typedef struct {
@@ -79,19 +81,31 @@ typedef struct {
   int in_features;           /* must be RENO_IN_FEATURES */
   int channels;              /* C: 16 or 32 */
   int layers;                /* L: 1 .. RENO_MAX_LAYERS sparse conv layers */
+  int head_mode;             /* RENO_HEAD_ONE_STAGE (0) or RENO_HEAD_TWO_STAGE */
 } reno_params;
 
 /* Model weights (fp32, device memory, row-major).  Layout:
  *   conv_w[l]  [27][C_in][C]   C_in = 11 for l = 0, C otherwise;
  *              offset k = (dx+1) + 3(dy+1) + 9(dz+1)
  *   conv_b[l]  [C]
- *   head_w     [C][256]
- *   head_b     [256]                                                        */
+ *   head_w     [C][256]      one-stage head
+ *   head_b     [256]
+ * Two-stage head (Sec. 3.2, Eqs. 11-13; the code O splits into the first
+ * sub-code S1 = O & 15, children delta 0..3, coded first, and S2 = O >> 4):
+ *   head1_w    [C][16]   head1_b [16]   z1 = head1_w^T h + head1_b
+ *   emb_s1     [16][C]                  Emb(S1), added to h before stage 2
+ *   head2_w    [C][16]   head2_b [16]   z2 = head2_w^T (h + emb_s1[S1]) + head2_b
+ * Only the pointers of the context's head mode are read.                    */
 typedef struct {
   const float* conv_w[RENO_MAX_LAYERS];
   const float* conv_b[RENO_MAX_LAYERS];
   const float* head_w;
   const float* head_b;
+  const float* head1_w;
+  const float* head1_b;
+  const float* emb_s1;
+  const float* head2_w;
+  const float* head2_b;
 } reno_weights;
 
 /* Creates a context on the current HIP device that enqueues on `hip_stream`
@@ -157,11 +171,24 @@ reno_status reno_parent_rows(reno_ctx* ctx, int scale, int32_t* parent);
  * scale in one batch (all scales must exist).  logits: optional fp32
  * [N_scale][256] (for RENO_ALL_SCALES, the scales concatenated in increasing
  * order).  weights: NULL uses the weights of the last reno_set_weights;
- * otherwise they are set first. */
+ * otherwise they are set first.
+ * Two-stage head: stage 1 (16 logits over S1) always; stage 2 as well when
+ * O_scale is known (an encoder context), with S1 = O_scale & 15.  logits is
+ * then [N_scale][32]: the 16 stage-1 logits, then the 16 stage-2 logits
+ * (left untouched when stage 2 does not run). */
 reno_status reno_predict_probs(reno_ctx* ctx, int scale, const reno_weights* weights, float* logits);
 
+/* Stage 2 of the two-stage head (Eq. 13) for a decoder that has decoded S1:
+ * s1 uint8 [N_scale] (values 0..15; device memory) or NULL to take
+ * S1 = O_scale & 15 when O_scale is known.  Needs predict_probs of the scale
+ * (it reuses the features of the last conv layer).  logits2: optional fp32
+ * [N_scale][16].  Values of s1 above 15 latch RENO_E_INPUT.  RENO_E_STATE in
+ * a one-stage context. */
+reno_status reno_predict_second(reno_ctx* ctx, int scale, const uint8_t* s1, float* logits2);
+
 /* Ideal code length (Eq. 4): for a model scale, bits_v = -log2 p(O_scale[v])
- * under the distribution of the last predict_probs of that scale; for
+ * under the distribution of the last predict_probs of that scale (two-stage
+ * head: -log2 P(S1) - log2 P(S2 | S1), which needs stage 2 of the scale); for
  * scale == b0 the raw cost of the initial state, 32 + N_b0 * (3*b0 + 8) bits.
  * bits_per_voxel: optional fp32 [N_scale] (NULL for b0).  total_host:
  * optional, synchronises; the sum in double.  RENO_ALL_SCALES: the whole

@@ -25,6 +25,8 @@ RENO_E_CAPACITY = -5
 RENO_E_INPUT = -6
 RENO_MAX_LAYERS = 8
 RENO_ALL_SCALES = -1
+RENO_HEAD_ONE_STAGE = 0
+RENO_HEAD_TWO_STAGE = 1
 SYMBOLS = 256
 
 _STATUS = {0: "RENO_OK", -1: "RENO_E_INVALID", -2: "RENO_E_STATE", -3: "RENO_E_NOMEM",
@@ -41,13 +43,17 @@ class reno_params(ctypes.Structure):
     _fields_ = [("max_points", ctypes.c_int64), ("max_model_voxels", ctypes.c_int64),
                 ("max_bit_depth", ctypes.c_int), ("min_bit_depth", ctypes.c_int),
                 ("range_m", ctypes.c_double), ("in_features", ctypes.c_int),
-                ("channels", ctypes.c_int), ("layers", ctypes.c_int)]
+                ("channels", ctypes.c_int), ("layers", ctypes.c_int),
+                ("head_mode", ctypes.c_int)]
 
 
 class reno_weights(ctypes.Structure):
     _fields_ = [("conv_w", ctypes.c_void_p * RENO_MAX_LAYERS),
                 ("conv_b", ctypes.c_void_p * RENO_MAX_LAYERS),
-                ("head_w", ctypes.c_void_p), ("head_b", ctypes.c_void_p)]
+                ("head_w", ctypes.c_void_p), ("head_b", ctypes.c_void_p),
+                ("head1_w", ctypes.c_void_p), ("head1_b", ctypes.c_void_p),
+                ("emb_s1", ctypes.c_void_p), ("head2_w", ctypes.c_void_p),
+                ("head2_b", ctypes.c_void_p)]
 
 
 # exported symbol -> (restype, argtypes); exactly the functions of include/reno.h
@@ -67,6 +73,7 @@ _SIGS = {
     "reno_occupancy_codes": (_int, [_vp, _int, _vp]),
     "reno_parent_rows": (_int, [_vp, _int, _vp]),
     "reno_predict_probs": (_int, [_vp, _int, ctypes.POINTER(reno_weights), _vp]),
+    "reno_predict_second": (_int, [_vp, _int, _vp, _vp]),
     "reno_code_length": (_int, [_vp, _int, _vp, ctypes.POINTER(ctypes.c_double)]),
     "reno_neighbor_map": (_int, [_vp, _int, _vp]),
     "reno_symbol_freqs": (_int, [_vp, _int, _vp]),
@@ -110,13 +117,14 @@ class Context:
     """One codec context (reno_ctx) bound to a torch device and stream."""
 
     def __init__(self, max_points: int, max_bit_depth: int, min_bit_depth: int, range_m: float,
-                 channels: int, layers: int, max_model_voxels: int = 0, stream=None):
+                 channels: int, layers: int, max_model_voxels: int = 0, stream=None,
+                 two_stage: bool = False):
         import torch
         self.torch = torch
         self.device = torch.device("cuda", torch.cuda.current_device())
         self.stream = stream if stream is not None else torch.cuda.current_stream()
         p = reno_params(max_points, max_model_voxels, max_bit_depth, min_bit_depth, range_m, 11,
-                        channels, layers)
+                        channels, layers, RENO_HEAD_TWO_STAGE if two_stage else RENO_HEAD_ONE_STAGE)
         h = ctypes.c_void_p()
         rc = lib().reno_create(ctypes.byref(p), ctypes.c_void_p(self.stream.cuda_stream),
                                ctypes.byref(h))
@@ -127,6 +135,7 @@ class Context:
         self.b0 = min_bit_depth
         self.channels = channels
         self.layers = layers
+        self.two_stage = two_stage
         self.B = 0
         self._keep = []
 
@@ -162,11 +171,12 @@ class Context:
             keep += [cw, cb]
             w.conv_w[l] = cw.data_ptr()
             w.conv_b[l] = cb.data_ptr()
-        hw = weights["head_w"].contiguous()
-        hb = weights["head_b"].contiguous()
-        keep += [hw, hb]
-        w.head_w = hw.data_ptr()
-        w.head_b = hb.data_ptr()
+        names = (("head1_w", "head1_b", "emb_s1", "head2_w", "head2_b") if self.two_stage
+                 else ("head_w", "head_b"))
+        for name in names:
+            t = weights[name].contiguous()
+            keep.append(t)
+            setattr(w, name, t.data_ptr())
         self._check(lib().reno_set_weights(self._h, ctypes.byref(w)))
         self._keep = keep        # alive until the next set_weights (stream-ordered)
 
@@ -225,11 +235,24 @@ class Context:
                 n = sum(self.num_voxels(b) for b in range(self.b0 + 1, self.B))
             else:
                 n = self.num_voxels(scale)
-            out = self._empty((max(n, 1), SYMBOLS), self.torch.float32)
+            out = self._empty((max(n, 1), 32 if self.two_stage else SYMBOLS), self.torch.float32)
         self._check(lib().reno_predict_probs(self._h, scale, None, _ptr(out)))
         if logits:
             return out[:n]
         return None
+
+    def predict_second(self, scale: int, s1=None, logits: bool = False):
+        """Stage 2 of the two-stage head given the first sub-codes S1 (uint8
+        device tensor [N_scale]); None takes S1 from the known codes."""
+        out = None
+        n = self.num_voxels(scale) if logits else 0
+        if logits:
+            out = self._empty((max(n, 1), 16), self.torch.float32)
+        s1c = None if s1 is None else s1.contiguous()
+        self._check(lib().reno_predict_second(self._h, scale, _ptr(s1c) if s1c is not None else None,
+                                              _ptr(out)))
+        self._s1 = s1c
+        return out[:n] if logits else None
 
     def code_length(self, scale: int, per_voxel: bool = True, total: bool = True):
         out = None
@@ -306,7 +329,9 @@ def rans_decode(words: np.ndarray, freq: np.ndarray, n: int) -> np.ndarray:
 def weights_to_device(w: dict, device="cuda") -> dict:
     """numpy weight dict (synth layout) -> fp32 device tensors."""
     import torch
-    return {"conv_w": [torch.from_numpy(np.ascontiguousarray(x)).to(device) for x in w["conv_w"]],
-            "conv_b": [torch.from_numpy(np.ascontiguousarray(x)).to(device) for x in w["conv_b"]],
-            "head_w": torch.from_numpy(np.ascontiguousarray(w["head_w"])).to(device),
-            "head_b": torch.from_numpy(np.ascontiguousarray(w["head_b"])).to(device)}
+    out = {"conv_w": [torch.from_numpy(np.ascontiguousarray(x)).to(device) for x in w["conv_w"]],
+           "conv_b": [torch.from_numpy(np.ascontiguousarray(x)).to(device) for x in w["conv_b"]]}
+    for name in ("head_w", "head_b", "head1_w", "head1_b", "emb_s1", "head2_w", "head2_b"):
+        if name in w:
+            out[name] = torch.from_numpy(np.ascontiguousarray(w[name], dtype=np.float32)).to(device)
+    return out

@@ -51,7 +51,8 @@ void free_all(Ctx* c) {
   void* ptrs[] = {c->keys_a,  c->keys_b,    c->lv_key,   c->lv_code,  c->lv_parent, c->lv_fc,
                   c->lv_feat, c->d_count,   c->d_moff,   c->d_err,    c->d_hist,    c->d_ticket,
                   c->d_status, c->d_hash,   c->h_a,      c->h_b,      c->d_nbr,     c->d_lse,
-                  c->d_partial, c->d_total, c->w_head,   c->w_hbias,  c->w_head_plain};
+                  c->d_partial, c->d_total, c->w_head,   c->w_hbias,  c->w_head_plain,
+                  c->d_lse2,    c->w_emb};
   for (void* p : ptrs)
     if (p) (void)hipFree(p);
   for (int l = 0; l < RENO_MAX_LAYERS; ++l) {
@@ -81,6 +82,7 @@ reno_status sync_check(Ctx* c) {
   if (e & reno::ERR_SPIN) msg += " internal: look-back wait bound exceeded;";
   if (e & reno::ERR_DUP_KEY) msg += " internal: duplicate hash key;";
   if (e & reno::ERR_INTERNAL) msg += " internal: consistency check failed;";
+  if (e & reno::ERR_SYMBOL) msg += " first sub-code outside 0..15;";
   if (e & (reno::ERR_CAPACITY | reno::ERR_HASH_FULL)) return fail(c, RENO_E_CAPACITY, msg);
   if (e & (reno::ERR_SPIN | reno::ERR_DUP_KEY | reno::ERR_INTERNAL)) return fail(c, RENO_E_HIP, msg);
   return fail(c, RENO_E_INPUT, msg);
@@ -101,6 +103,10 @@ reno_status frame_init(Ctx* c) {
 }
 
 bool model_scale(const Ctx* c, int b) { return c->B > 0 && b > c->b0() && b < c->B; }
+// the two-stage head needs stage 2 of a scale before its code lengths
+bool stage2_ok(const Ctx* c, int b) {
+  return c->p.head_mode != RENO_HEAD_TWO_STAGE || has(c->have_pred2, b);
+}
 
 }  // namespace
 
@@ -127,6 +133,8 @@ reno_status reno_create(const reno_params* p, void* hip_stream, reno_ctx** out) 
     return fail(nullptr, RENO_E_INVALID, "channels must be 16 or 32");
   if (p->layers < 1 || p->layers > RENO_MAX_LAYERS)
     return fail(nullptr, RENO_E_INVALID, "layers must be in [1, 8]");
+  if (p->head_mode != RENO_HEAD_ONE_STAGE && p->head_mode != RENO_HEAD_TWO_STAGE)
+    return fail(nullptr, RENO_E_INVALID, "head_mode must be RENO_HEAD_ONE_STAGE or RENO_HEAD_TWO_STAGE");
   // N_b <= N_{b+1} <= max_points, so (model scales) x max_points always suffices
   const int64_t nmodel = p->max_bit_depth - p->min_bit_depth - 1 > 0
                              ? p->max_bit_depth - p->min_bit_depth - 1 : 1;
@@ -177,6 +185,7 @@ reno_status reno_create(const reno_params* p, void* hip_stream, reno_ctx** out) 
   A(dalloc(&c->h_b, (size_t)(cap_model + 1) * C, &c->device_bytes));
   A(dalloc(&c->d_nbr, (size_t)cap_model * reno::NBR_STRIDE, &c->device_bytes));
   A(dalloc(&c->d_lse, (size_t)cap_model, &c->device_bytes));
+  A(dalloc(&c->d_lse2, (size_t)cap_model, &c->device_bytes));
   A(dalloc(&c->d_partial, (size_t)reno::NLEV * ((c->cap_pts + 1023) / 1024), &c->device_bytes));
   A(dalloc(&c->d_total, reno::NLEV, &c->device_bytes));
   int c_in = RENO_IN_FEATURES;
@@ -189,6 +198,7 @@ reno_status reno_create(const reno_params* p, void* hip_stream, reno_ctx** out) 
   A(dalloc(&c->w_head, (size_t)16 * 64 * (C / 4), &c->device_bytes));
   A(dalloc(&c->w_hbias, 256, &c->device_bytes));
   A(dalloc(&c->w_head_plain, (size_t)C * 256, &c->device_bytes));
+  A(dalloc(&c->w_emb, (size_t)16 * C, &c->device_bytes));
   A(hipHostMalloc(reinterpret_cast<void**>(&c->h_total), sizeof(double) * reno::NLEV, 0));
   A(hipHostMalloc(reinterpret_cast<void**>(&c->h_count), sizeof(int32_t) * reno::NLEV, 0));
   A(hipHostMalloc(reinterpret_cast<void**>(&c->h_err), 64, 0));
@@ -244,7 +254,12 @@ reno_status reno_set_weights(reno_ctx* c, const reno_weights* w) {
   if (!c || !w) return fail(c, RENO_E_INVALID, "null argument");
   for (int l = 0; l < c->p.layers; ++l)
     if (!w->conv_w[l] || !w->conv_b[l]) return fail(c, RENO_E_INVALID, "missing conv weights");
-  if (!w->head_w || !w->head_b) return fail(c, RENO_E_INVALID, "missing head weights");
+  if (c->p.head_mode == RENO_HEAD_TWO_STAGE) {
+    if (!w->head1_w || !w->head1_b || !w->emb_s1 || !w->head2_w || !w->head2_b)
+      return fail(c, RENO_E_INVALID, "missing two-stage head weights");
+  } else if (!w->head_w || !w->head_b) {
+    return fail(c, RENO_E_INVALID, "missing head weights");
+  }
   RENO_HIP(c, reno::launch_pack_weights(*c, *w));
   c->have_weights = true;
   return RENO_OK;
@@ -263,6 +278,7 @@ reno_status reno_build_pyramid(reno_ctx* c, const float* points, int64_t n, int 
   c->have_level = bits_range(c->b0(), B);
   c->have_codes = bits_range(c->b0(), B - 1);
   c->have_pred = 0;
+  c->have_pred2 = 0;
   reno_status s = frame_init(c);
   if (s != RENO_OK) return s;
   if (n == 0) return RENO_OK;
@@ -295,6 +311,7 @@ reno_status reno_set_base(reno_ctx* c, int bit_depth, const int32_t* xyz, const 
   c->have_level = 1u << c->b0();
   c->have_codes = 1u << c->b0();
   c->have_pred = 0;
+  c->have_pred2 = 0;
   reno_status s = frame_init(c);
   if (s != RENO_OK) return s;
   RENO_HIP(c, reno::launch_set_base(*c, xyz, codes, n, bit_depth));
@@ -370,8 +387,25 @@ reno_status reno_predict_probs(reno_ctx* c, int scale, const reno_weights* weigh
       return fail(c, RENO_E_STATE, "scale or the codes of its parent scale unknown");
     lo = hi = scale;
   }
-  RENO_HIP(c, reno::launch_model(*c, lo, hi, logits));
+  const bool two = c->p.head_mode == RENO_HEAD_TWO_STAGE;
+  const bool second = two && (c->have_codes & bits_range(lo, hi)) == bits_range(lo, hi);
+  RENO_HIP(c, reno::launch_model(*c, lo, hi, logits, second));
   c->have_pred |= bits_range(lo, hi);
+  c->have_pred2 &= ~bits_range(lo, hi);
+  if (second) c->have_pred2 |= bits_range(lo, hi);
+  return RENO_OK;
+}
+
+reno_status reno_predict_second(reno_ctx* c, int scale, const uint8_t* s1, float* logits2) {
+  if (!c) return RENO_E_INVALID;
+  if (c->p.head_mode != RENO_HEAD_TWO_STAGE) return fail(c, RENO_E_STATE, "one-stage context");
+  if (c->B == 0) return fail(c, RENO_E_STATE, "no frame");
+  if (!model_scale(c, scale)) return fail(c, RENO_E_INVALID, "not a model scale");
+  if (!has(c->have_pred, scale)) return fail(c, RENO_E_STATE, "predict_probs of the scale not run");
+  if (!s1 && !has(c->have_codes, scale))
+    return fail(c, RENO_E_STATE, "no first sub-codes given and the codes of the scale unknown");
+  RENO_HIP(c, reno::launch_head2(*c, scale, s1, logits2));
+  c->have_pred2 |= 1u << scale;
   return RENO_OK;
 }
 
@@ -387,14 +421,14 @@ reno_status reno_code_length(reno_ctx* c, int scale, float* bits_per_voxel, doub
     lo = b0 + 1;
     hi = c->B - 1;
     for (int b = lo; b <= hi; ++b)
-      if (!has(c->have_pred, b) || !has(c->have_codes, b))
+      if (!has(c->have_pred, b) || !has(c->have_codes, b) || !stage2_ok(c, b))
         return fail(c, RENO_E_STATE, "every model scale needs predict_probs and its codes");
   } else if (scale == b0) {
     if (bits_per_voxel) return fail(c, RENO_E_INVALID, "the base scale has no per-voxel bits");
     with_base = true;
   } else {
     if (!model_scale(c, scale)) return fail(c, RENO_E_INVALID, "not a model scale");
-    if (!has(c->have_pred, scale) || !has(c->have_codes, scale))
+    if (!has(c->have_pred, scale) || !has(c->have_codes, scale) || !stage2_ok(c, scale))
       return fail(c, RENO_E_STATE, "scale needs predict_probs and its codes");
     lo = hi = scale;
   }
@@ -422,6 +456,8 @@ reno_status reno_neighbor_map(reno_ctx* c, int scale, int32_t* map) {
 
 reno_status reno_symbol_freqs(reno_ctx* c, int scale, uint16_t* freq) {
   if (!c || !freq) return fail(c, RENO_E_INVALID, "null argument");
+  if (c->p.head_mode != RENO_HEAD_ONE_STAGE)
+    return fail(c, RENO_E_STATE, "symbol tables are built for the one-stage head only");
   if (!has(c->have_pred, scale)) return fail(c, RENO_E_STATE, "predict_probs of the scale not run");
   RENO_HIP(c, reno::launch_symbol_freqs(*c, scale, freq));
   return RENO_OK;

@@ -78,7 +78,8 @@ struct Ctx {
   float* h_a = nullptr;         // [cap_model][C]
   float* h_b = nullptr;
   int32_t* d_nbr = nullptr;     // [cap_model][NBR_STRIDE]
-  float* d_lse = nullptr;       // [cap_model]
+  float* d_lse = nullptr;       // [cap_model] (two-stage head: stage 1)
+  float* d_lse2 = nullptr;      // [cap_model] stage 2 of the two-stage head
   double* d_partial = nullptr;  // [NLEV][ceil(cap_pts / 1024)] per-chunk bit sums
   double* d_total = nullptr;    // [NLEV]
   double* h_total = nullptr;    // pinned host mirror [NLEV]
@@ -90,7 +91,8 @@ struct Ctx {
   float* w_bias[RENO_MAX_LAYERS] = {};
   float* w_head = nullptr;
   float* w_hbias = nullptr;
-  float* w_head_plain = nullptr;  // [C][256] as given, for code lengths and symbol tables
+  float* w_head_plain = nullptr;  // [C][256] as given (two-stage: [C][H1 | H2]), for code lengths
+  float* w_emb = nullptr;         // [16][C] Emb(S1) of the two-stage head
   bool have_weights = false;
 
   // frame state
@@ -98,7 +100,8 @@ struct Ctx {
   bool encoder = false;
   uint32_t have_level = 0;      // bit b: V_b built
   uint32_t have_codes = 0;      // bit b: O_b known
-  uint32_t have_pred = 0;       // bit b: TOP evaluated on V_b
+  uint32_t have_pred = 0;       // bit b: TOP evaluated on V_b (two-stage: stage 1)
+  uint32_t have_pred2 = 0;      // bit b: stage 2 of the two-stage head evaluated
   int64_t npoints = 0;
 
   // kernel timing (reno_profile)
@@ -150,7 +153,8 @@ hipError_t launch_codes(Ctx& c, int B);
 hipError_t launch_set_base(Ctx& c, const int32_t* xyz, const uint8_t* codes, int64_t n, int B);
 hipError_t launch_expand(Ctx& c, int b, const uint8_t* codes, int B);
 hipError_t launch_pack_weights(Ctx& c, const reno_weights& w);
-hipError_t launch_model(Ctx& c, int b_lo, int b_hi, float* logits);
+hipError_t launch_model(Ctx& c, int b_lo, int b_hi, float* logits, bool second);
+hipError_t launch_head2(Ctx& c, int b, const uint8_t* s1, float* logits2);
 hipError_t launch_code_length(Ctx& c, int b_lo, int b_hi, float* bits);
 hipError_t launch_symbol_freqs(Ctx& c, int b, uint16_t* freq);
 hipError_t launch_coords(Ctx& c, int b, int32_t* xyz, uint64_t* keys);

@@ -20,6 +20,7 @@ enum : uint32_t {
   ERR_SPIN = 64u,        // a look-back wait exceeded its bound (never expected)
   ERR_DUP_KEY = 128u,    // the same key inserted twice (never expected: keys are a set)
   ERR_INTERNAL = 256u,   // an internal consistency check failed (never expected)
+  ERR_SYMBOL = 512u,     // a decoded sub-code outside its alphabet (S1 above 15)
 };
 
 __device__ __forceinline__ void latch(uint32_t* err, uint32_t bit) { atomicOr(err, bit); }

@@ -51,18 +51,69 @@ __global__ void k_pack_conv(const float* __restrict__ W, int c_in, int C, int KS
   }
 }
 
-// Head: step t = 4*cb + r carries channel c = 16*cb + 4*g + r (the conv
-// accumulator register r of column block cb); lane l carries symbol
-// 16*sb + l%16.  Packed [16][64][C/4].
-__global__ void k_pack_head(const float* __restrict__ H, int C, float* __restrict__ out) {
+// Head H [C][NS] (NS = 256, or 16 per stage of the two-stage head): step
+// t = 4*cb + r carries channel c = 16*cb + 4*g + r (the conv accumulator
+// register r of column block cb); lane l carries symbol 16*sb + l%16.
+// Packed [NS/16][64][C/4].
+__global__ void k_pack_head(const float* __restrict__ H, int C, int NS, float* __restrict__ out) {
   const int KT = C / 4;
-  const int total = 16 * 64 * KT;
+  const int total = NS / 16 * 64 * KT;
   for (int i = blockIdx.x * blockDim.x + threadIdx.x; i < total; i += gridDim.x * blockDim.x) {
     const int t = i % KT;
     const int lane = (i / KT) % 64;
     const int sb = i / (KT * 64);
     const int c = 16 * (t >> 2) + 4 * (lane >> 4) + (t & 3);
-    out[i] = H[(size_t)c * 256 + sb * 16 + (lane & 15)];
+    out[i] = H[(size_t)c * NS + sb * 16 + (lane & 15)];
+  }
+}
+
+// Copies H [C][16] into columns col0 .. col0+15 of a [C][32] table.
+__global__ void k_put_cols16(const float* __restrict__ H, int C, int col0, float* __restrict__ out) {
+  for (int i = blockIdx.x * blockDim.x + threadIdx.x; i < C * 16; i += gridDim.x * blockDim.x)
+    out[(i / 16) * 32 + col0 + (i % 16)] = H[i];
+}
+
+// ---------------------------------------------------------------------------
+// Two-stage head pieces, shared by the last conv layer (encoder: S1 known)
+// and the decoder's stage-2 kernel, so both produce identical bits.
+//
+// 16 logits of one packed symbol block for a tile: lane (r, g) ends with the
+// logits of symbols 4g .. 4g+3 of voxel r.  h is the tile's feature block in
+// the accumulator layout (lane (r, g), register e of block q: channel
+// 16q + 4g + e of voxel r).
+template <int C>
+__device__ __forceinline__ f4 head16(const f4* __restrict__ hp, const float* __restrict__ hb, const f4 (&h)[C / 16],
+                                     int g) {
+  f4 zz = *reinterpret_cast<const f4*>(hb + 4 * g);
+#pragma unroll
+  for (int q = 0; q < C / 16; ++q) {
+    const f4 hv = hp[q];
+#pragma unroll
+    for (int e = 0; e < 4; ++e) zz = mfma4(hv[e], h[q][e], zz);
+  }
+  return zz;
+}
+
+// Natural-log normaliser of the 16 logits spread over lanes r, r+16, r+32, r+48.
+__device__ __forceinline__ float lse16(const f4& z) {
+  float m = fmaxf(fmaxf(z[0], z[1]), fmaxf(z[2], z[3]));
+  m = fmaxf(m, __shfl_xor(m, 16));
+  m = fmaxf(m, __shfl_xor(m, 32));
+  float s = (__expf(z[0] - m) + __expf(z[1] - m)) + (__expf(z[2] - m) + __expf(z[3] - m));
+  s += __shfl_xor(s, 16);
+  s += __shfl_xor(s, 32);
+  return m + __logf(s);
+}
+
+// h + Emb(S1) in the accumulator layout (emb_row = emb_s1 + S1 * C).
+template <int C>
+__device__ __forceinline__ void add_emb(const f4 (&h)[C / 16], const float* __restrict__ emb_row, int g,
+                                        f4 (&out)[C / 16]) {
+#pragma unroll
+  for (int q = 0; q < C / 16; ++q) {
+    const f4 e = *reinterpret_cast<const f4*>(emb_row + 16 * q + 4 * g);
+#pragma unroll
+    for (int i = 0; i < 4; ++i) out[q][i] = h[q][i] + e[i];
   }
 }
 
@@ -90,8 +141,12 @@ struct ConvArgs {
   const float* hw;        // packed head weights (last layer)
   const float* hb;        // [256]
   float* lse;             // [cap_model]
-  float* logits;          // optional [rows][256], row = packed row - moff[b_lo]
+  float* logits;          // optional [rows][256] (two-stage: [rows][32]), row = packed row - moff[b_lo]
   uint32_t* err;
+  // two-stage head
+  const float* emb;       // [16][C]
+  const uint8_t* s1_code; // codes of the per-scale regions (S1 = O & 15), or NULL: stage 1 only
+  float* lse2;            // [cap_model]
 };
 
 // Entry j (wave-uniform) of the 8 neighbour rows a lane holds in two int4,
@@ -126,14 +181,14 @@ __device__ __forceinline__ void stage_lds(const f4* __restrict__ src, f4* dst, i
   }
 }
 
-template <int C, bool FIRST, bool LAST>
+template <int C, bool FIRST, bool LAST, bool TWO>
 __global__ void __launch_bounds__(CONV_THREADS) k_conv(ConvArgs a) {
   constexpr int NCB = C / 16;
   constexpr int KS = FIRST ? 3 : C / 4;
   constexpr int KSP = (KS + 3) & ~3;
   constexpr int KT = C / 4;
   constexpr int WSZ = 27 * NCB * 64 * KSP;
-  constexpr int HSZ = LAST ? 16 * 64 * KT : 4;
+  constexpr int HSZ = LAST ? (TWO ? 2 : 16) * 64 * KT : 4;
   constexpr int PCH = FIRST ? 8 : 4;  // offsets per pipeline stage
   struct Gath {                        // one gathered neighbour slice
     uint32_t word;                     // first layer: 11 input bits
@@ -365,7 +420,26 @@ __global__ void __launch_bounds__(CONV_THREADS) k_conv(ConvArgs a) {
         *reinterpret_cast<f4*>(a.h_out + prow * C + 16 * cb + 4 * g) = acc[cb];
     }
 
-    if (LAST) {
+    if constexpr (LAST && TWO) {
+      // ---- two-stage head (Eqs. 11-13): stage 1 over S1; stage 2 over S2
+      // with h + Emb(S1) when the codes of the scale are known
+      const f4* hp = reinterpret_cast<const f4*>(s_h) + lane * (KT / 4);
+      const f4 z1 = head16<C>(hp, a.hb, acc, g);
+      const float l1 = lse16(z1);
+      if (valid && g == 0) a.lse[prow] = l1;
+      float* lo = (a.logits && valid) ? a.logits + (prow - s_mo[0]) * 32 + 4 * g : nullptr;
+      if (lo) *reinterpret_cast<f4*>(lo) = z1;
+      if (a.s1_code) {
+        const int s1 = a.s1_code[lvb + (prow - mo)] & 15;
+        f4 h2[NCB];
+        add_emb<C>(acc, a.emb + s1 * C, g, h2);
+        const f4 z2 = head16<C>(hp + 64 * (KT / 4), a.hb + 16, h2, g);
+        const float l2 = lse16(z2);
+        if (valid && g == 0) a.lse2[prow] = l2;
+        if (lo) *reinterpret_cast<f4*>(lo + 16) = z2;
+      }
+    }
+    if constexpr (LAST && !TWO) {
       // ---- head: z^T[256][16] = H^T h^T with the conv accumulators as the B
       // operand; 64 symbols at a time with a running (max, sum of exp)
       float m = -INFINITY, ssum = 0.0f;
@@ -419,19 +493,61 @@ __global__ void __launch_bounds__(CONV_THREADS) k_conv(ConvArgs a) {
   }
 }
 
-template <int C, bool FIRST, bool LAST>
+template <int C, bool FIRST, bool LAST, bool TWO>
 hipError_t run_conv(Ctx& c, const ConvArgs& a) {
-  // one block per CU is enough to stage the weights once and keep 8 waves busy
-  hipLaunchKernelGGL((k_conv<C, FIRST, LAST>), dim3(256), dim3(CONV_THREADS), 0, c.stream, a);
+  // one block per CU stages the weights once for its 16 waves
+  hipLaunchKernelGGL((k_conv<C, FIRST, LAST, TWO>), dim3(256), dim3(CONV_THREADS), 0, c.stream, a);
   return hipGetLastError();
 }
 
 template <int C>
-hipError_t run_layer(Ctx& c, bool first, bool last, const ConvArgs& a) {
-  if (first && last) return run_conv<C, true, true>(c, a);
-  if (first) return run_conv<C, true, false>(c, a);
-  if (last) return run_conv<C, false, true>(c, a);
-  return run_conv<C, false, false>(c, a);
+hipError_t run_layer(Ctx& c, bool first, bool last, bool two, const ConvArgs& a) {
+  if (first && last) return two ? run_conv<C, true, true, true>(c, a) : run_conv<C, true, true, false>(c, a);
+  if (first) return run_conv<C, true, false, false>(c, a);
+  if (last) return two ? run_conv<C, false, true, true>(c, a) : run_conv<C, false, true, false>(c, a);
+  return run_conv<C, false, false, false>(c, a);
+}
+
+// Stage 2 of the two-stage head for one scale from the stored features of the
+// last conv layer and a given S1 per voxel (decoder).  One wave per tile of
+// 16 voxels, the same tile split and arithmetic as the fused path.
+template <int C>
+__global__ void __launch_bounds__(256) k_head2(int b, const int32_t* __restrict__ count,
+                                               const int32_t* __restrict__ moff, int64_t cap_model,
+                                               const float* __restrict__ hL, const uint8_t* __restrict__ s1,
+                                               const uint8_t* __restrict__ code, const float* __restrict__ hw2,
+                                               const float* __restrict__ hb2, const float* __restrict__ emb,
+                                               float* __restrict__ lse2, float* __restrict__ logits2,
+                                               uint32_t* err) {
+  constexpr int NCB = C / 16;
+  const int lane = threadIdx.x & 63, r = lane & 15, g = lane >> 4;
+  const int64_t mo = moff[b];
+  int64_t n = count[b];
+  if (mo + n > cap_model) n = 0;  // overflow was latched where the size was made
+  const int64_t ntiles = (n + 15) / 16;
+  const int wpb = blockDim.x / 64;
+  const f4* hp = reinterpret_cast<const f4*>(hw2) + lane * (C / 16);
+  for (int64_t tile = (int64_t)blockIdx.x * wpb + (threadIdx.x >> 6); tile < ntiles;
+       tile += (int64_t)gridDim.x * wpb) {
+    const int64_t row = tile * 16 + r;
+    const bool valid = row < n;
+    const int64_t vr = valid ? row : n - 1;
+    const int64_t prow = mo + vr;
+    f4 h[NCB];
+#pragma unroll
+    for (int q = 0; q < NCB; ++q) h[q] = *reinterpret_cast<const f4*>(hL + prow * C + 16 * q + 4 * g);
+    int a1 = s1 ? s1[vr] : (code[vr] & 15);
+    if (a1 > 15) {
+      if (valid) latch(err, ERR_SYMBOL);
+      a1 = 0;
+    }
+    f4 h2[NCB];
+    add_emb<C>(h, emb + a1 * C, g, h2);
+    const f4 z2 = head16<C>(hp, hb2, h2, g);
+    const float l2 = lse16(z2);
+    if (valid && g == 0) lse2[prow] = l2;
+    if (valid && logits2) *reinterpret_cast<f4*>(logits2 + row * 16 + 4 * g) = z2;
+  }
 }
 
 }  // namespace
@@ -448,14 +564,26 @@ hipError_t launch_pack_weights(Ctx& c, const reno_weights& w) {
     hipLaunchKernelGGL(k_copy_f32, dim3(1), dim3(256), 0, c.stream, w.conv_b[l], c.w_bias[l], C);
     c_in = C;
   }
-  hipLaunchKernelGGL(k_pack_head, dim3(32), dim3(256), 0, c.stream, w.head_w, C, c.w_head);
-  hipLaunchKernelGGL(k_copy_f32, dim3(1), dim3(256), 0, c.stream, w.head_b, c.w_hbias, 256);
-  hipLaunchKernelGGL(k_copy_f32, dim3(32), dim3(256), 0, c.stream, w.head_w, c.w_head_plain,
-                     C * 256);
+  if (c.p.head_mode == RENO_HEAD_TWO_STAGE) {
+    // packed blocks [stage 1][stage 2], biases [b1 | b2], plain [C][H1 | H2]
+    const int blk = 64 * (C / 4);
+    hipLaunchKernelGGL(k_pack_head, dim3(4), dim3(256), 0, c.stream, w.head1_w, C, 16, c.w_head);
+    hipLaunchKernelGGL(k_pack_head, dim3(4), dim3(256), 0, c.stream, w.head2_w, C, 16, c.w_head + blk);
+    hipLaunchKernelGGL(k_copy_f32, dim3(1), dim3(64), 0, c.stream, w.head1_b, c.w_hbias, 16);
+    hipLaunchKernelGGL(k_copy_f32, dim3(1), dim3(64), 0, c.stream, w.head2_b, c.w_hbias + 16, 16);
+    hipLaunchKernelGGL(k_put_cols16, dim3(2), dim3(256), 0, c.stream, w.head1_w, C, 0, c.w_head_plain);
+    hipLaunchKernelGGL(k_put_cols16, dim3(2), dim3(256), 0, c.stream, w.head2_w, C, 16, c.w_head_plain);
+    hipLaunchKernelGGL(k_copy_f32, dim3(2), dim3(256), 0, c.stream, w.emb_s1, c.w_emb, 16 * C);
+  } else {
+    hipLaunchKernelGGL(k_pack_head, dim3(32), dim3(256), 0, c.stream, w.head_w, C, 256, c.w_head);
+    hipLaunchKernelGGL(k_copy_f32, dim3(1), dim3(256), 0, c.stream, w.head_b, c.w_hbias, 256);
+    hipLaunchKernelGGL(k_copy_f32, dim3(32), dim3(256), 0, c.stream, w.head_w, c.w_head_plain,
+                       C * 256);
+  }
   return hipGetLastError();
 }
 
-hipError_t launch_model(Ctx& c, int b_lo, int b_hi, float* logits) {
+hipError_t launch_model(Ctx& c, int b_lo, int b_hi, float* logits, bool second) {
   ConvArgs a{};
   a.b_lo = b_lo;
   a.b_hi = b_hi;
@@ -474,6 +602,10 @@ hipError_t launch_model(Ctx& c, int b_lo, int b_hi, float* logits) {
   a.hw = c.w_head;
   a.lse = c.d_lse;
   a.err = c.d_err;
+  a.emb = c.w_emb;
+  a.s1_code = second ? c.lv_code : nullptr;
+  a.lse2 = c.d_lse2;
+  const bool two = c.p.head_mode == RENO_HEAD_TWO_STAGE;
   const int L = c.p.layers;
   hipError_t e = hipSuccess;
   for (int l = 0; l < L && e == hipSuccess; ++l) {
@@ -484,9 +616,25 @@ hipError_t launch_model(Ctx& c, int b_lo, int b_hi, float* logits) {
     a.logits = (l == L - 1) ? logits : nullptr;
     const bool first = l == 0, last = l == L - 1;
     ProfScope ps_(c, last ? RENO_K_CONV_LAST : (first ? RENO_K_CONV_FIRST : RENO_K_CONV_MID));
-    e = (c.p.channels == 32) ? run_layer<32>(c, first, last, a) : run_layer<16>(c, first, last, a);
+    e = (c.p.channels == 32) ? run_layer<32>(c, first, last, two, a) : run_layer<16>(c, first, last, two, a);
   }
   return e;
+}
+
+hipError_t launch_head2(Ctx& c, int b, const uint8_t* s1, float* logits2) {
+  ProfScope ps_(c, RENO_K_CONV_LAST);
+  const float* hw2 = c.w_head + 64 * (c.p.channels / 4);
+  const uint8_t* code = c.lv_code + c.lv(b);
+  const int blocks = (int)std::min<int64_t>(1024, (c.cap_pts + 63) / 64);
+  if (c.p.channels == 32)
+    hipLaunchKernelGGL(k_head2<32>, dim3(blocks), dim3(256), 0, c.stream, b, c.d_count, c.d_moff,
+                       (int64_t)c.cap_model, c.hlast(), s1, code, hw2, c.w_hbias + 16, c.w_emb, c.d_lse2,
+                       logits2, c.d_err);
+  else
+    hipLaunchKernelGGL(k_head2<16>, dim3(blocks), dim3(256), 0, c.stream, b, c.d_count, c.d_moff,
+                       (int64_t)c.cap_model, c.hlast(), s1, code, hw2, c.w_hbias + 16, c.w_emb, c.d_lse2,
+                       logits2, c.d_err);
+  return hipGetLastError();
 }
 
 }  // namespace reno

@@ -10,21 +10,26 @@ namespace {
 constexpr float INV_LN2 = 1.4426950408889634f;
 
 // bits_v = (lse_v - z_{O_b[v]}) / ln 2 with z_o = hb[o] + sum_c H[c][o] h_L[v][c]
-// (fp32, channel order).  Block (chunk, scale) handles 1024 voxels of one
-// scale with H staged in LDS; per-chunk sums in double are reduced in chunk
-// order by the last block of the scale to finish (deterministic).
+// (fp32, channel order).  Two-stage head (TWO): with a = O & 15, s = O >> 4,
+// bits_v = ((lse1_v - z1_a) + (lse2_v - z2_s)) / ln 2, z1_a = hb1[a] +
+// sum_c H1[c][a] h[c], z2_s = hb2[s] + sum_c H2[c][s] (h[c] + E[a][c]).
+// Block (chunk, scale) handles 1024 voxels of one scale with the head staged
+// in LDS; per-chunk sums in double are reduced in chunk order by the last
+// block of the scale to finish (deterministic).
 constexpr int CL_THREADS = 256;
 constexpr int CL_CHUNK = 1024;
 
-template <int C>
+template <int C, bool TWO>
 __global__ void __launch_bounds__(CL_THREADS) k_code_length(
     int b_lo, int b0, const int32_t* __restrict__ count, const int32_t* __restrict__ moff,
     int64_t cap_pts, int64_t cap_model, const uint8_t* __restrict__ lv_code,
     const float* __restrict__ hL, const float* __restrict__ H, const float* __restrict__ hb,
-    const float* __restrict__ lse, float* __restrict__ bits_out, double* partial, int max_chunks,
-    double* total, uint32_t* done) {
-  __shared__ float s_H[C * 256];
-  __shared__ float s_hb[256];
+    const float* __restrict__ lse, const float* __restrict__ lse2, const float* __restrict__ emb,
+    float* __restrict__ bits_out, double* partial, int max_chunks, double* total, uint32_t* done) {
+  constexpr int NS = TWO ? 32 : 256;  // columns of the plain head table
+  __shared__ float s_H[C * NS];
+  __shared__ float s_hb[NS];
+  __shared__ float s_emb[TWO ? 16 * C : 1];
   __shared__ double s_red[CL_THREADS / 64];
   __shared__ bool s_last;
   const int b = b_lo + blockIdx.y;
@@ -37,7 +42,11 @@ __global__ void __launch_bounds__(CL_THREADS) k_code_length(
     return;
   }
   if ((int64_t)blockIdx.x >= nchunks) return;
-  {  // stage the head in LDS, every load of a thread issued before its stores
+  if constexpr (TWO) {  // small tables: plain strided copies
+    for (int i = threadIdx.x; i < C * NS; i += CL_THREADS) s_H[i] = H[i];
+    for (int i = threadIdx.x; i < 16 * C; i += CL_THREADS) s_emb[i] = emb[i];
+    if (threadIdx.x < NS) s_hb[threadIdx.x] = hb[threadIdx.x];
+  } else {  // stage the head in LDS, every load of a thread issued before its stores
     constexpr int PER = C * 256 / 4 / CL_THREADS;
     float4 v[PER];
     const float4* src = reinterpret_cast<const float4*>(H);
@@ -55,29 +64,48 @@ __global__ void __launch_bounds__(CL_THREADS) k_code_length(
   constexpr int PV = CL_CHUNK / CL_THREADS;  // voxels per thread
   int64_t vv[PV];
   int oo[PV];
-  float ll[PV];
+  float ll[PV], ll2[PV];
 #pragma unroll
   for (int i = 0; i < PV; ++i) {  // clamped rows: every load is issued up front
     const int64_t v = (int64_t)blockIdx.x * CL_CHUNK + i * CL_THREADS + threadIdx.x;
     vv[i] = v < n ? v : n - 1;
     oo[i] = code[vv[i]];
     ll[i] = lse[mo + vv[i]];
+    ll2[i] = TWO ? lse2[mo + vv[i]] : 0.0f;
   }
 #pragma unroll
   for (int i = 0; i < PV; ++i) {
     const int64_t v = (int64_t)blockIdx.x * CL_CHUNK + i * CL_THREADS + threadIdx.x;
     const int o = oo[i];
     const float4* h = reinterpret_cast<const float4*>(hL + (mo + vv[i]) * C);
-    float z = s_hb[o];
+    float bt;
+    if constexpr (TWO) {
+      const int a1 = o & 15, a2 = 16 + (o >> 4);
+      float z1 = s_hb[a1], z2 = s_hb[a2];
 #pragma unroll
-    for (int c4 = 0; c4 < C / 4; ++c4) {
-      const float4 hv = h[c4];
-      z = fmaf(s_H[(4 * c4 + 0) * 256 + o], hv.x, z);
-      z = fmaf(s_H[(4 * c4 + 1) * 256 + o], hv.y, z);
-      z = fmaf(s_H[(4 * c4 + 2) * 256 + o], hv.z, z);
-      z = fmaf(s_H[(4 * c4 + 3) * 256 + o], hv.w, z);
+      for (int c4 = 0; c4 < C / 4; ++c4) {
+        const float4 hv = h[c4];
+        const float hc[4] = {hv.x, hv.y, hv.z, hv.w};
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+          const int ch = 4 * c4 + j;
+          z1 = fmaf(s_H[ch * NS + a1], hc[j], z1);
+          z2 = fmaf(s_H[ch * NS + a2], hc[j] + s_emb[a1 * C + ch], z2);
+        }
+      }
+      bt = ((ll[i] - z1) + (ll2[i] - z2)) * INV_LN2;
+    } else {
+      float z = s_hb[o];
+#pragma unroll
+      for (int c4 = 0; c4 < C / 4; ++c4) {
+        const float4 hv = h[c4];
+        z = fmaf(s_H[(4 * c4 + 0) * 256 + o], hv.x, z);
+        z = fmaf(s_H[(4 * c4 + 1) * 256 + o], hv.y, z);
+        z = fmaf(s_H[(4 * c4 + 2) * 256 + o], hv.z, z);
+        z = fmaf(s_H[(4 * c4 + 3) * 256 + o], hv.w, z);
+      }
+      bt = (ll[i] - z) * INV_LN2;
     }
-    const float bt = (ll[i] - z) * INV_LN2;
     if (v < n) {
       if (bits_out) bits_out[out0 + v] = bt;
       acc += (double)bt;
@@ -217,20 +245,23 @@ unsigned grid_for(int64_t cap, int per_block) {
 
 }  // namespace
 
-hipError_t launch_code_length(Ctx& c, int b_lo, int b_hi, float* bits) {
-  ProfScope ps_(c, RENO_K_CODE_LENGTH);
+template <int C, bool TWO>
+void run_code_length(Ctx& c, int b_lo, int b_hi, float* bits) {
   const int max_chunks = (int)((c.cap_pts + CL_CHUNK - 1) / CL_CHUNK);
   const dim3 grid(max_chunks, b_hi - b_lo + 1);
+  hipLaunchKernelGGL((k_code_length<C, TWO>), grid, dim3(CL_THREADS), 0, c.stream, b_lo, c.b0(),
+                     c.d_count, c.d_moff, c.cap_pts, c.cap_model, c.lv_code, c.hlast(),
+                     c.w_head_plain, c.w_hbias, c.d_lse, c.d_lse2, c.w_emb, bits, c.d_partial,
+                     max_chunks, c.d_total, c.d_ticket + TK_RED);
+}
+
+hipError_t launch_code_length(Ctx& c, int b_lo, int b_hi, float* bits) {
+  ProfScope ps_(c, RENO_K_CODE_LENGTH);
+  const bool two = c.p.head_mode == RENO_HEAD_TWO_STAGE;
   if (c.p.channels == 32)
-    hipLaunchKernelGGL(k_code_length<32>, grid, dim3(CL_THREADS), 0, c.stream, b_lo, c.b0(),
-                       c.d_count, c.d_moff, c.cap_pts, c.cap_model, c.lv_code, c.hlast(),
-                       c.w_head_plain, c.w_hbias, c.d_lse, bits, c.d_partial, max_chunks,
-                       c.d_total, c.d_ticket + TK_RED);
+    two ? run_code_length<32, true>(c, b_lo, b_hi, bits) : run_code_length<32, false>(c, b_lo, b_hi, bits);
   else
-    hipLaunchKernelGGL(k_code_length<16>, grid, dim3(CL_THREADS), 0, c.stream, b_lo, c.b0(),
-                       c.d_count, c.d_moff, c.cap_pts, c.cap_model, c.lv_code, c.hlast(),
-                       c.w_head_plain, c.w_hbias, c.d_lse, bits, c.d_partial, max_chunks,
-                       c.d_total, c.d_ticket + TK_RED);
+    two ? run_code_length<16, true>(c, b_lo, b_hi, bits) : run_code_length<16, false>(c, b_lo, b_hi, bits);
   return hipGetLastError();
 }
 

@@ -25,7 +25,19 @@ def declared_functions():
 def test_header_and_binding_agree():
     decl = declared_functions()
     assert decl == set(reno._SIGS), decl ^ set(reno._SIGS)
-    assert len(decl) == 21
+    assert len(decl) == 22
+
+
+def _struct_fields(name):
+    src = re.sub(r"/\*.*?\*/", "", open(HEADER).read(), flags=re.S)
+    body = re.search(r"typedef struct \{([^{}]*)\}\s*" + name + r"\s*;", src).group(1)
+    return [m.group(1) for m in re.finditer(r"(\w+)\s*(?:\[[^\]]*\])?\s*;", body)]
+
+
+@pytest.mark.parametrize("name,cls", [("reno_params", reno.reno_params), ("reno_weights", reno.reno_weights)])
+def test_struct_layouts_agree(name, cls):
+    """The ctypes structures list the header's fields in the header's order."""
+    assert _struct_fields(name) == [f[0] for f in cls._fields_]
 
 
 def test_every_symbol_exported():
