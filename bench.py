@@ -109,6 +109,115 @@ def log(*a):
     print("[bench]", *a, file=sys.stderr, flush=True)
 
 
+class Codec:
+    """An encoder and a decoder context on one stream and one encode + decode
+    step over a resident frame.  The decoder's symbols come from the encoder
+    (a stand-in for an instant entropy decoder)."""
+
+    def __init__(self, reno, torch, cfg, pts, M, cap_model, stream, w_np, two_stage):
+        self.reno, self.torch, self.stream = reno, torch, stream
+        B, b0, C, L = cfg.bit_depth, cfg.min_bit_depth, cfg.channels, cfg.layers
+        self.B, self.b0, self.C, self.two_stage = B, b0, C, two_stage
+        wd = reno.weights_to_device(w_np)
+        with torch.cuda.stream(stream):
+            mk = lambda: reno.Context(M, B, b0, cfg.range_m, C, L, max_model_voxels=cap_model,
+                                      stream=stream, two_stage=two_stage)
+            self.enc, self.dec = mk(), mk()
+            self.enc.set_weights(wd)
+            self.dec.set_weights(wd)
+            # decoder inputs (resident before timing): initial state and every scale's codes
+            self.enc.build_pyramid(pts, B)
+            base, _ = self.enc.coords(b0)
+            self.base = base.clone()
+            self.codes = {b: self.enc.occupancy_codes(b).clone() for b in range(b0, B)}
+            self.s1 = {b: (self.codes[b] & 15).contiguous() for b in range(b0, B)}
+            self.enc.predict_probs(reno.RENO_ALL_SCALES)
+            _, self.enc_total = self.enc.code_length(reno.RENO_ALL_SCALES, per_voxel=False)
+            self.pairs = {b: int((self.enc.neighbor_map(b) >= 0).sum().item()) for b in range(b0 + 1, B)}
+            stream.synchronize()
+        self.pts = pts
+        self.graph = None
+
+    def step(self):
+        reno, enc, dec, B, b0 = self.reno, self.enc, self.dec, self.B, self.b0
+        enc.build_pyramid(self.pts, B)
+        enc.predict_probs(reno.RENO_ALL_SCALES)
+        enc.code_length(reno.RENO_ALL_SCALES, per_voxel=False, total=False)
+        dec.set_base(B, self.base, self.codes[b0])
+        for b in range(b0 + 1, B):
+            dec.expand(b - 1, None if b - 1 == b0 else self.codes[b - 1])
+            dec.predict_probs(b)
+            if self.two_stage:
+                dec.predict_second(b, self.s1[b])
+        dec.expand(B - 1, self.codes[B - 1])
+        dec.code_length(reno.RENO_ALL_SCALES, per_voxel=False, total=False)
+
+    def check(self, what):
+        reno = self.reno
+        with self.torch.cuda.stream(self.stream):
+            _, d = self.dec.code_length(reno.RENO_ALL_SCALES, per_voxel=False)
+            _, e = self.enc.code_length(reno.RENO_ALL_SCALES, per_voxel=False)
+        if not (d == e == self.enc_total):
+            log(what, "decoder/encoder bit totals differ", d, e, self.enc_total)
+            sys.exit(1)
+
+    def time(self, steps, warmup, mode):
+        """Milliseconds per step over `steps` steps (HIP events on the stream)."""
+        torch, stream = self.torch, self.stream
+        with torch.cuda.stream(stream):
+            for _ in range(warmup):
+                self.step()
+            stream.synchronize()
+        self.check("after warm-up:")
+        if mode == "graph" and self.graph is None:
+            self.graph = torch.cuda.CUDAGraph()
+            with torch.cuda.graph(self.graph, stream=stream):
+                self.step()
+            with torch.cuda.stream(stream):
+                for _ in range(warmup):
+                    self.graph.replay()
+            stream.synchronize()
+        t0 = torch.cuda.Event(enable_timing=True)
+        t1 = torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        with torch.cuda.stream(stream):
+            t0.record(stream)
+            for _ in range(steps):
+                if mode == "graph":
+                    self.graph.replay()
+                else:
+                    self.step()
+            t1.record(stream)
+        torch.cuda.synchronize()
+        self.check("after the timed steps:")  # the last replayed frame is consistent
+        return t0.elapsed_time(t1) / steps
+
+    def profile_conv_last(self, steps):
+        """(total ms, launches) of conv_last over `steps` eager steps, each launch
+        bracketed by HIP events on the context stream."""
+        with self.torch.cuda.stream(self.stream):
+            self.enc.profile(["conv_last"])
+            self.dec.profile(["conv_last"])
+            for _ in range(steps):
+                self.step()
+            pe, pd = self.enc.profile_read(), self.dec.profile_read()
+            self.enc.profile([])
+            self.dec.profile([])
+        return pe["conv_last"][0] + pd["conv_last"][0], pe["conv_last"][1] + pd["conv_last"][1]
+
+    def conv_last_flops(self, counts):
+        """Algorithmic flops of the last conv layer + head per frame (encoder +
+        decoder): 2*C*C per occupied neighbour and, per voxel, 2*C*256 (one-stage
+        head) or 2*C*16*2 (two stages of 16)."""
+        C = self.C
+        head = 2 * C * 32 if self.two_stage else 2 * C * 256
+        return 2 * sum(2 * C * C * self.pairs[b] + head * counts[b - self.b0] for b in self.pairs)
+
+    def close(self):
+        self.enc.close()
+        self.dec.close()
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawTextHelpFormatter)
     ap.add_argument("--gpus", type=int, default=1)
@@ -117,6 +226,7 @@ def main():
     ap.add_argument("--config", default="hdl64_b14")
     ap.add_argument("--mode", choices=["graph", "eager"], default="graph")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-two-stage", action="store_true", help="skip the two-stage head measurement")
     ap.add_argument("--cpu-workers", type=int, default=0,
                     help="processes for the all-cores oracle baseline (0: the CPUs this process may use, at most 16)")
     ap.add_argument("--calib-copy", action="store_true",
@@ -142,7 +252,6 @@ def main():
     torch.cuda.set_device(dev)
     stream = torch.cuda.Stream(device=dev)
     pts = torch.from_numpy(pts_np).to(dev)
-    wd = reno.weights_to_device(w_np, dev)
     if args.calib_copy:
         # plain kernels of known traffic: a fill (256 MiB written), then an
         # elementwise copy (256 MiB read, 256 MiB written)
@@ -164,91 +273,23 @@ def main():
     cap_model = (model_vox + model_vox // 8 + 4095) // 4096 * 4096
     log("N_b", counts, "model voxels", model_vox, "capacity", cap_model)
 
-    with torch.cuda.stream(stream):
-        enc = reno.Context(M, B, b0, cfg.range_m, C, L, max_model_voxels=cap_model, stream=stream)
-        dec = reno.Context(M, B, b0, cfg.range_m, C, L, max_model_voxels=cap_model, stream=stream)
-        enc.set_weights(wd)
-        dec.set_weights(wd)
-        # decoder inputs (resident before timing): initial state and every scale's codes
-        enc.build_pyramid(pts, B)
-        base_xyz, _ = enc.coords(b0)
-        base_xyz = base_xyz.clone()
-        codes = {b: enc.occupancy_codes(b).clone() for b in range(b0, B)}
-        enc.predict_probs(reno.RENO_ALL_SCALES)
-        _, enc_total = enc.code_length(reno.RENO_ALL_SCALES, per_voxel=False)
-        pairs = {b: int((enc.neighbor_map(b) >= 0).sum().item()) for b in range(b0 + 1, B)}
-        stream.synchronize()
-
-    def step():
-        enc.build_pyramid(pts, B)
-        enc.predict_probs(reno.RENO_ALL_SCALES)
-        enc.code_length(reno.RENO_ALL_SCALES, per_voxel=False, total=False)
-        dec.set_base(B, base_xyz, codes[b0])
-        for b in range(b0 + 1, B):
-            dec.expand(b - 1, None if b - 1 == b0 else codes[b - 1])
-            dec.predict_probs(b)
-        dec.expand(B - 1, codes[B - 1])
-        dec.code_length(reno.RENO_ALL_SCALES, per_voxel=False, total=False)
-
-    with torch.cuda.stream(stream):
-        for _ in range(args.warmup):
-            step()
-        stream.synchronize()
-        _, dec_total = dec.code_length(reno.RENO_ALL_SCALES, per_voxel=False)
-        _, enc_total2 = enc.code_length(reno.RENO_ALL_SCALES, per_voxel=False)
-    if not (dec_total == enc_total == enc_total2):
-        log("decoder/encoder bit totals differ", dec_total, enc_total, enc_total2)
-        sys.exit(1)
-
-    graph = None
-    if args.mode == "graph":
-        graph = torch.cuda.CUDAGraph()
-        with torch.cuda.graph(graph, stream=stream):
-            step()
-        with torch.cuda.stream(stream):
-            for _ in range(args.warmup):
-                graph.replay()
-        stream.synchronize()
-
-    # ---- timed region ----
-    t0 = torch.cuda.Event(enable_timing=True)
-    t1 = torch.cuda.Event(enable_timing=True)
-    torch.cuda.synchronize()
-    wall0 = time.perf_counter()
-    with torch.cuda.stream(stream):
-        t0.record(stream)
-        for _ in range(args.steps):
-            if graph is not None:
-                graph.replay()
-            else:
-                step()
-        t1.record(stream)
-    torch.cuda.synchronize()
-    wall = time.perf_counter() - wall0
-    ms_total = t0.elapsed_time(t1)
-    ms_step = ms_total / args.steps
+    one = Codec(reno, torch, cfg, pts, M, cap_model, stream, w_np, two_stage=False)
+    enc, dec, step = one.enc, one.dec, one.step
+    pairs, enc_total = one.pairs, one.enc_total
+    ms_step = one.time(args.steps, args.warmup, args.mode)
     fps = 1000.0 / ms_step
-    log(f"{args.mode}: {ms_step * 1000:.1f} us/frame, {fps:.1f} frames/s (wall {wall:.3f} s)")
-    # results of the last replayed frame are still consistent
-    with torch.cuda.stream(stream):
-        _, chk = dec.code_length(reno.RENO_ALL_SCALES, per_voxel=False)
-    if chk != enc_total:
-        log("post-timing check failed", chk, enc_total)
-        sys.exit(1)
+    log(f"{args.mode}: {ms_step * 1000:.1f} us/frame, {fps:.1f} frames/s")
+    cl_ms, cl_launches = one.profile_conv_last(args.steps)
+    achieved_tflops = one.conv_last_flops(counts) * args.steps / (cl_ms * 1e-3) / 1e12
+    log(f"conv_last: {cl_launches} launches, {1000 * cl_ms / cl_launches:.1f} us avg, "
+        f"{achieved_tflops:.2f} TFLOP/s algorithmic")
 
-    # ---- live kernel timing of the dominant kernel (HIP events on the same stream) ----
+    # per-kind breakdown over 20 eager frames (all kernels bracketed)
+    kinds = reno.KERNELS
+    nb = 20
     with torch.cuda.stream(stream):
-        enc.profile(["conv_last"])
-        dec.profile(["conv_last"])
-        for _ in range(args.steps):
-            step()
-        pe = enc.profile_read()
-        pd = dec.profile_read()
-        # per-kind breakdown of one eager frame (all kernels bracketed)
-        kinds = reno.KERNELS
         enc.profile(kinds)
         dec.profile(kinds)
-        nb = 20
         for _ in range(nb):
             step()
         be, bd = enc.profile_read(), dec.profile_read()
@@ -267,14 +308,23 @@ def main():
                 gbs = alg[k] / (us * 1e-6) / 1e9
                 breakdown[k].update({"alg_bytes_per_frame": alg[k], "alg_GBs": round(gbs, 1),
                                      "hbm_frac": round(gbs / PEAK_HBM_GBS, 4)})
-    cl_ms = pe["conv_last"][0] + pd["conv_last"][0]
-    cl_launches = pe["conv_last"][1] + pd["conv_last"][1]
-    # algorithmic flops of the last conv layer + head: per voxel, 2*C*C per
-    # occupied neighbour (the conv) and 2*C*256 (the head); encoder + decoder
-    flops_frame = 2 * sum(2 * C * C * pairs[b] + 2 * C * 256 * counts[b - b0] for b in pairs)
-    achieved_tflops = flops_frame * args.steps / (cl_ms * 1e-3) / 1e12
-    log(f"conv_last: {cl_launches} launches, {1000 * cl_ms / cl_launches:.1f} us avg, "
-        f"{achieved_tflops:.2f} TFLOP/s algorithmic")
+
+    # ---- the bitwise two-stage head (the paper's default head), same frame ----
+    two = None
+    if not args.no_two_stage:
+        w2_np = gen_weights(C, L, seed=cfg.weight_seed, two_stage=True)
+        ts = Codec(reno, torch, cfg, pts, M, cap_model, stream, w2_np, two_stage=True)
+        st = max(args.steps // 2, 1)
+        ms2 = ts.time(st, args.warmup, args.mode)
+        cl2_ms, cl2_n = ts.profile_conv_last(st)
+        tf2 = ts.conv_last_flops(counts) * st / (cl2_ms * 1e-3) / 1e12
+        two = {"value": round(1000.0 / ms2, 2), "unit": "frames/s", "ms_per_step": round(ms2, 5),
+               "steps": st, "bits_per_point": round(ts.enc_total / M, 4),
+               "conv_last_avg_launch_us": round(1000 * cl2_ms / cl2_n, 2),
+               "conv_last_achieved_tflops": round(tf2, 3),
+               "conv_last_frac": round(tf2 / PEAK_FP32_MFMA_TFLOPS, 4)}
+        log("two-stage head", two)
+        ts.close()
 
     # ---- CPU baseline: the oracle (single-threaded C++, fp64), one frame per
     # process, first alone, then one process per available core at once ----
@@ -335,10 +385,10 @@ def main():
                      "launches": cl_launches},
         "cpu_baseline": cpu,
         "kernels": breakdown,
+        "two_stage_head": two,
     }
     print(json.dumps(out), flush=True)
-    enc.close()
-    dec.close()
+    one.close()
 
 
 if __name__ == "__main__":
