@@ -227,6 +227,10 @@ def main():
     ap.add_argument("--mode", choices=["graph", "eager"], default="graph")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-two-stage", action="store_true", help="skip the two-stage head measurement")
+    ap.add_argument("--stream-config", default="stream10_hdl64_b14",
+                    help="multi-frame workload measured with frames in flight on several streams")
+    ap.add_argument("--streams", default="1,2,4",
+                    help="stream counts for the multi-frame measurement ('' to skip)")
     ap.add_argument("--cpu-workers", type=int, default=0,
                     help="processes for the all-cores oracle baseline (0: the CPUs this process may use, at most 16)")
     ap.add_argument("--calib-copy", action="store_true",
@@ -326,6 +330,56 @@ def main():
         log("two-stage head", two)
         ts.close()
 
+    # ---- multi-frame throughput: F different frames, each with its own encoder
+    # and decoder context and captured step, replayed round-robin over S
+    # streams so that frames are in flight together ----
+    multi = None
+    if args.streams and args.mode == "graph":
+        mcfg = BY_NAME[args.stream_config]
+        frames = [gen_scan(mcfg, f) for f in range(mcfg.frames)]
+        mw = gen_weights(mcfg.channels, mcfg.layers, seed=mcfg.weight_seed)
+        ns = [int(x) for x in args.streams.split(",")]
+        streams = [torch.cuda.Stream(device=dev) for _ in range(max(ns))]
+        mM = max(f.shape[0] for f in frames)
+        codecs = []
+        for i, f in enumerate(frames):
+            fp = torch.from_numpy(f).to(dev)
+            with torch.cuda.stream(streams[0]):
+                pr = reno.Context(mM, mcfg.bit_depth, mcfg.min_bit_depth, mcfg.range_m, mcfg.channels,
+                                  mcfg.layers, stream=streams[0])
+                pr.build_pyramid(fp, mcfg.bit_depth)
+                mv = sum(pr.num_voxels(b) for b in range(mcfg.min_bit_depth + 1, mcfg.bit_depth))
+                pr.close()
+            cap = (mv + mv // 8 + 4095) // 4096 * 4096
+            codecs.append((fp, cap))
+        cap_all = max(c[1] for c in codecs)
+        vox = 0
+        multi = {"workload": f"{mcfg.name}: {mcfg.frames} consecutive synthetic {mcfg.beams}-beam scans "
+                             f"(sensor moving {mcfg.frame_step_m} m per frame), {mcfg.bit_depth}-bit, "
+                             "each frame encoded + decoded", "frames": mcfg.frames, "runs": []}
+        for S in ns:
+            cs = [Codec(reno, torch, mcfg, fp, mM, cap_all, streams[i % S], mw, two_stage=False)
+                  for i, (fp, _) in enumerate(codecs)]
+            for c in cs:
+                c.time(1, 2, "graph")              # warm-up, capture, self-check
+            reps = max(args.steps // 10, 2)
+            torch.cuda.synchronize()
+            t = time.perf_counter()
+            for _ in range(reps):
+                for c in cs:
+                    with torch.cuda.stream(c.stream):
+                        c.graph.replay()
+            torch.cuda.synchronize()
+            ms = (time.perf_counter() - t) * 1000.0 / reps
+            for c in cs:
+                c.check("multi-frame:")
+            multi["runs"].append({"streams": S, "frames_per_s": round(len(cs) * 1000.0 / ms, 2),
+                                  "ms_per_batch": round(ms, 4)})
+            log(f"multi-frame {len(cs)} frames on {S} streams: {ms:.3f} ms, {len(cs) * 1000.0 / ms:.1f} frames/s")
+            for c in cs:
+                c.close()
+        del codecs
+
     # ---- CPU baseline: the oracle (single-threaded C++, fp64), one frame per
     # process, first alone, then one process per available core at once ----
     cpu = None
@@ -386,6 +440,7 @@ def main():
         "cpu_baseline": cpu,
         "kernels": breakdown,
         "two_stage_head": two,
+        "multi_frame": multi,
     }
     print(json.dumps(out), flush=True)
     one.close()
