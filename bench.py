@@ -28,6 +28,7 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
 PEAK_FP32_MFMA_TFLOPS = 157.3
+PEAK_BF16_MFMA_TFLOPS = 2500.0
 PEAK_HBM_GBS = 8000.0
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "conv_last_traffic_hdl64_b14.txt")
 MODEL_SRC = os.path.join(ROOT, "paper_2503_12382_amd", "csrc", "k_model.hip")
@@ -114,14 +115,14 @@ class Codec:
     step over a resident frame.  The decoder's symbols come from the encoder
     (a stand-in for an instant entropy decoder)."""
 
-    def __init__(self, reno, torch, cfg, pts, M, cap_model, stream, w_np, two_stage):
+    def __init__(self, reno, torch, cfg, pts, M, cap_model, stream, w_np, two_stage, precision=0):
         self.reno, self.torch, self.stream = reno, torch, stream
         B, b0, C, L = cfg.bit_depth, cfg.min_bit_depth, cfg.channels, cfg.layers
         self.B, self.b0, self.C, self.two_stage = B, b0, C, two_stage
         wd = reno.weights_to_device(w_np)
         with torch.cuda.stream(stream):
             mk = lambda: reno.Context(M, B, b0, cfg.range_m, C, L, max_model_voxels=cap_model,
-                                      stream=stream, two_stage=two_stage)
+                                      stream=stream, two_stage=two_stage, precision=precision)
             self.enc, self.dec = mk(), mk()
             self.enc.set_weights(wd)
             self.dec.set_weights(wd)
@@ -227,6 +228,7 @@ def main():
     ap.add_argument("--mode", choices=["graph", "eager"], default="graph")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-two-stage", action="store_true", help="skip the two-stage head measurement")
+    ap.add_argument("--no-bf16x3", action="store_true", help="skip the split-bf16 precision measurement")
     ap.add_argument("--stream-config", default="stream10_hdl64_b14",
                     help="multi-frame workload measured with frames in flight on several streams")
     ap.add_argument("--streams", default="1,2,4",
@@ -329,6 +331,26 @@ def main():
                "conv_last_frac": round(tf2 / PEAK_FP32_MFMA_TFLOPS, 4)}
         log("two-stage head", two)
         ts.close()
+
+    # ---- split-bf16 precision (bf16 hi + lo operands, three bf16 MFMA products
+    # per fp32 product), same frame and weights ----
+    bfx = None
+    if not args.no_bf16x3:
+        bc = Codec(reno, torch, cfg, pts, M, cap_model, stream, w_np, two_stage=False,
+                   precision=reno.RENO_PREC_BF16X3)
+        st = max(args.steps // 2, 1)
+        msb = bc.time(st, args.warmup, args.mode)
+        clb_ms, clb_n = bc.profile_conv_last(st)
+        tfb = bc.conv_last_flops(counts) * st / (clb_ms * 1e-3) / 1e12
+        bfx = {"value": round(1000.0 / msb, 2), "unit": "frames/s", "ms_per_step": round(msb, 5),
+               "steps": st, "dtype": "bf16x3 (fp32 accumulate)",
+               "bits_per_point": round(bc.enc_total / M, 4),
+               "bits_rel_diff_vs_fp32": abs(bc.enc_total - enc_total) / enc_total,
+               "conv_last_avg_launch_us": round(1000 * clb_ms / clb_n, 2),
+               "conv_last_achieved_tflops": round(tfb, 3),
+               "conv_last_frac_of_bf16_peak": round(tfb / PEAK_BF16_MFMA_TFLOPS, 4)}
+        log("bf16x3", bfx)
+        bc.close()
 
     # ---- multi-frame throughput: F different frames, each with its own encoder
     # and decoder context and captured step, replayed round-robin over S
@@ -440,6 +462,7 @@ def main():
         "cpu_baseline": cpu,
         "kernels": breakdown,
         "two_stage_head": two,
+        "precision_bf16x3": bfx,
         "multi_frame": multi,
     }
     print(json.dumps(out), flush=True)

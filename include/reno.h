@@ -67,6 +67,10 @@ typedef enum {
 #define RENO_ALL_SCALES (-1)
 #define RENO_HEAD_ONE_STAGE 0   /* one 256-way softmax over the code (Eq. 10) */
 #define RENO_HEAD_TWO_STAGE 1   /* bitwise two-stage head (Eqs. 11-13) */
+#define RENO_PREC_FP32 0        /* conv layers and heads on fp32 MFMA */
+#define RENO_PREC_BF16X3 1      /* each fp32 operand split into bf16 hi + lo, products
+                                   hi*hi + hi*lo + lo*hi on bf16 MFMA with fp32
+                                   accumulation (~2^-16 relative per product) */
 
 /* Capacities and model shape, fixed for the life of a context. */
 typedef struct {
@@ -82,6 +86,7 @@ typedef struct {
   int channels;              /* C: 16 or 32 */
   int layers;                /* L: 1 .. RENO_MAX_LAYERS sparse conv layers */
   int head_mode;             /* RENO_HEAD_ONE_STAGE (0) or RENO_HEAD_TWO_STAGE */
+  int precision;             /* RENO_PREC_FP32 (0) or RENO_PREC_BF16X3 */
 } reno_params;
 
 /* Model weights (fp32, device memory, row-major).  Layout:

@@ -27,6 +27,8 @@ RENO_MAX_LAYERS = 8
 RENO_ALL_SCALES = -1
 RENO_HEAD_ONE_STAGE = 0
 RENO_HEAD_TWO_STAGE = 1
+RENO_PREC_FP32 = 0
+RENO_PREC_BF16X3 = 1
 SYMBOLS = 256
 
 _STATUS = {0: "RENO_OK", -1: "RENO_E_INVALID", -2: "RENO_E_STATE", -3: "RENO_E_NOMEM",
@@ -44,7 +46,7 @@ class reno_params(ctypes.Structure):
                 ("max_bit_depth", ctypes.c_int), ("min_bit_depth", ctypes.c_int),
                 ("range_m", ctypes.c_double), ("in_features", ctypes.c_int),
                 ("channels", ctypes.c_int), ("layers", ctypes.c_int),
-                ("head_mode", ctypes.c_int)]
+                ("head_mode", ctypes.c_int), ("precision", ctypes.c_int)]
 
 
 class reno_weights(ctypes.Structure):
@@ -118,13 +120,14 @@ class Context:
 
     def __init__(self, max_points: int, max_bit_depth: int, min_bit_depth: int, range_m: float,
                  channels: int, layers: int, max_model_voxels: int = 0, stream=None,
-                 two_stage: bool = False):
+                 two_stage: bool = False, precision: int = RENO_PREC_FP32):
         import torch
         self.torch = torch
         self.device = torch.device("cuda", torch.cuda.current_device())
         self.stream = stream if stream is not None else torch.cuda.current_stream()
         p = reno_params(max_points, max_model_voxels, max_bit_depth, min_bit_depth, range_m, 11,
-                        channels, layers, RENO_HEAD_TWO_STAGE if two_stage else RENO_HEAD_ONE_STAGE)
+                        channels, layers, RENO_HEAD_TWO_STAGE if two_stage else RENO_HEAD_ONE_STAGE,
+                        precision)
         h = ctypes.c_void_p()
         rc = lib().reno_create(ctypes.byref(p), ctypes.c_void_p(self.stream.cuda_stream),
                                ctypes.byref(h))

@@ -2,6 +2,7 @@
 // ownership and device-error reporting.  Every compute step is a HIP kernel
 // enqueued on the context stream (see the k_*.hip files).
 
+#include <algorithm>
 #include <cmath>
 #include <cstring>
 #include <string>
@@ -135,6 +136,8 @@ reno_status reno_create(const reno_params* p, void* hip_stream, reno_ctx** out) 
     return fail(nullptr, RENO_E_INVALID, "layers must be in [1, 8]");
   if (p->head_mode != RENO_HEAD_ONE_STAGE && p->head_mode != RENO_HEAD_TWO_STAGE)
     return fail(nullptr, RENO_E_INVALID, "head_mode must be RENO_HEAD_ONE_STAGE or RENO_HEAD_TWO_STAGE");
+  if (p->precision != RENO_PREC_FP32 && p->precision != RENO_PREC_BF16X3)
+    return fail(nullptr, RENO_E_INVALID, "precision must be RENO_PREC_FP32 or RENO_PREC_BF16X3");
   // N_b <= N_{b+1} <= max_points, so (model scales) x max_points always suffices
   const int64_t nmodel = p->max_bit_depth - p->min_bit_depth - 1 > 0
                              ? p->max_bit_depth - p->min_bit_depth - 1 : 1;
@@ -191,11 +194,12 @@ reno_status reno_create(const reno_params* p, void* hip_stream, reno_ctx** out) 
   int c_in = RENO_IN_FEATURES;
   for (int l = 0; l < p->layers; ++l) {
     const int KS = (c_in + 3) / 4, KSP = (KS + 3) & ~3;
-    A(dalloc(&c->w_conv[l], (size_t)27 * (C / 16) * 64 * KSP, &c->device_bytes));
+    // fp32: KSP floats per (offset, column block, lane); bf16x3: 8 words
+    A(dalloc(&c->w_conv[l], (size_t)27 * (C / 16) * 64 * std::max(KSP, 8), &c->device_bytes));
     A(dalloc(&c->w_bias[l], (size_t)C, &c->device_bytes));
     c_in = C;
   }
-  A(dalloc(&c->w_head, (size_t)16 * 64 * (C / 4), &c->device_bytes));
+  A(dalloc(&c->w_head, (size_t)16 * 64 * std::max(C / 4, 8), &c->device_bytes));
   A(dalloc(&c->w_hbias, 256, &c->device_bytes));
   A(dalloc(&c->w_head_plain, (size_t)C * 256, &c->device_bytes));
   A(dalloc(&c->w_emb, (size_t)16 * C, &c->device_bytes));

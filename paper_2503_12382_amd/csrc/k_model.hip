@@ -17,18 +17,54 @@
 // Output-stationary: no atomics, a fixed summation order per voxel, so an
 // encoder and a decoder evaluating the same scale get bit-identical results.
 
+#include <type_traits>
+
 #include "ctx.h"
 
 namespace reno {
 namespace {
 
 typedef float f4 __attribute__((ext_vector_type(4)));
+typedef __bf16 bf8 __attribute__((ext_vector_type(8)));
 
 constexpr int CONV_THREADS = 1024;
 constexpr int CONV_WAVES = CONV_THREADS / 64;
 
 __device__ __forceinline__ f4 mfma4(float a, float b, f4 c) {
   return __builtin_amdgcn_mfma_f32_16x16x4f32(a, b, c, 0, 0, 0);
+}
+
+// ---- split-bf16 arithmetic (precision RENO_PREC_BF16X3) ----
+// An fp32 operand x is carried as hi = bf16(x) and lo = bf16(x - hi) (both
+// round to nearest even), so x = hi + lo to about 2^-16 relative; a product
+// is taken as hi*hi + hi*lo + lo*hi (the lo*lo term, ~2^-16 relative, is
+// dropped) on v_mfma_f32_16x16x32_bf16 with fp32 accumulation.  Operands
+// travel as 8 bf16 packed in a uint4 (lane l: row/column l % 16, K slots
+// 8 (l / 16) .. 8 (l / 16) + 7).
+__device__ __forceinline__ f4 mfma_bf(const uint4& a, const uint4& b, f4 c) {
+  return __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf8, a), __builtin_bit_cast(bf8, b),
+                                                 c, 0, 0, 0);
+}
+__device__ __forceinline__ uint32_t bf_bits(__bf16 h) { return __builtin_bit_cast(uint16_t, h); }
+// hi and lo words of two floats (x0 in the low half)
+__device__ __forceinline__ void split2(float x0, float x1, uint32_t& hi, uint32_t& lo) {
+  const __bf16 h0 = (__bf16)x0, h1 = (__bf16)x1;
+  const __bf16 l0 = (__bf16)(x0 - (float)h0), l1 = (__bf16)(x1 - (float)h1);
+  hi = bf_bits(h0) | (bf_bits(h1) << 16);
+  lo = bf_bits(l0) | (bf_bits(l1) << 16);
+}
+// split of 8 floats into packed hi / lo operands
+__device__ __forceinline__ void split8(const float (&x)[8], uint4& hi, uint4& lo) {
+  split2(x[0], x[1], hi.x, lo.x);
+  split2(x[2], x[3], hi.y, lo.y);
+  split2(x[4], x[5], hi.z, lo.z);
+  split2(x[6], x[7], hi.w, lo.w);
+}
+// hi*hi + hi*lo + lo*hi accumulated into c
+__device__ __forceinline__ f4 mfma_bf3(const uint4& ah, const uint4& al, const uint4& bh, const uint4& bl, f4 c) {
+  c = mfma_bf(ah, bh, c);
+  c = mfma_bf(ah, bl, c);
+  return mfma_bf(al, bh, c);
 }
 
 // ---------------------------------------------------------------------------
@@ -64,6 +100,57 @@ __global__ void k_pack_head(const float* __restrict__ H, int C, int NS, float* _
     const int sb = i / (KT * 64);
     const int c = 16 * (t >> 2) + 4 * (lane >> 4) + (t & 3);
     out[i] = H[(size_t)c * NS + sb * 16 + (lane & 15)];
+  }
+}
+
+// bf16x3 conv weights: per (offset k, column block cb, lane (r, g)) the A
+// operand W^T[co = 16cb + r][ci = 8g + j], j = 0..7 (zero for ci >= c_in),
+// as 4 words of hi then 4 words of lo.  Packed [27][C/16][64][8] uint32.
+__global__ void k_pack_conv_bf(const float* __restrict__ W, int c_in, int C, uint32_t* __restrict__ out) {
+  const int ncb = C / 16;
+  const int total = 27 * ncb * 64 * 4;
+  for (int i = blockIdx.x * blockDim.x + threadIdx.x; i < total; i += gridDim.x * blockDim.x) {
+    const int pr = i % 4;                 // pair of K slots
+    const int lane = (i / 4) % 64;
+    const int cb = (i / 256) % ncb;
+    const int k = i / (256 * ncb);
+    const int co = cb * 16 + (lane & 15);
+    float x[2];
+    for (int h = 0; h < 2; ++h) {
+      const int ci = 8 * (lane >> 4) + 2 * pr + h;
+      x[h] = ci < c_in ? W[((size_t)k * c_in + ci) * C + co] : 0.0f;
+    }
+    uint32_t hi, lo;
+    split2(x[0], x[1], hi, lo);
+    uint32_t* o = out + ((size_t)(k * ncb + cb) * 64 + lane) * 8;
+    o[pr] = hi;
+    o[4 + pr] = lo;
+  }
+}
+
+// bf16x3 head H [C][NS]: per symbol block sb and lane (r, g) the A operand
+// H[c(g, j)][16 sb + r] with the K slot -> channel map c(g, j) = 16 (j / 4) +
+// 4g + (j % 4), which is the channel that register j % 4 of accumulator block
+// j / 4 holds in lane (r, g) of the last conv layer (zero beyond C).  Packed
+// [NS/16][64][8] uint32 (hi words, then lo words).
+__global__ void k_pack_head_bf(const float* __restrict__ H, int C, int NS, uint32_t* __restrict__ out) {
+  const int total = NS / 16 * 64 * 4;
+  for (int i = blockIdx.x * blockDim.x + threadIdx.x; i < total; i += gridDim.x * blockDim.x) {
+    const int pr = i % 4;
+    const int lane = (i / 4) % 64;
+    const int sb = i / 256;
+    const int sym = sb * 16 + (lane & 15);
+    float x[2];
+    for (int h = 0; h < 2; ++h) {
+      const int j = 2 * pr + h;
+      const int c = 16 * (j >> 2) + 4 * (lane >> 4) + (j & 3);
+      x[h] = c < C ? H[(size_t)c * NS + sym] : 0.0f;
+    }
+    uint32_t hi, lo;
+    split2(x[0], x[1], hi, lo);
+    uint32_t* o = out + ((size_t)sb * 64 + lane) * 8;
+    o[pr] = hi;
+    o[4 + pr] = lo;
   }
 }
 
@@ -103,6 +190,24 @@ __device__ __forceinline__ float lse16(const f4& z) {
   s += __shfl_xor(s, 16);
   s += __shfl_xor(s, 32);
   return m + __logf(s);
+}
+
+// B operand of the bf16x3 head from the accumulator layout (K slot j of lane
+// (r, g) = register j % 4 of block j / 4; zero beyond C).
+template <int C>
+__device__ __forceinline__ void head_operand_bf(const f4 (&h)[C / 16], uint4& hi, uint4& lo) {
+  float x[8];
+#pragma unroll
+  for (int j = 0; j < 8; ++j) x[j] = (j / 4 < C / 16) ? h[j / 4 < C / 16 ? j / 4 : 0][j % 4] : 0.0f;
+  split8(x, hi, lo);
+}
+
+// bf16x3 version of head16: hp points at this lane's packed words of the block.
+template <int C>
+__device__ __forceinline__ f4 head16_bf(const uint4* __restrict__ hp, const float* __restrict__ hb,
+                                        const uint4& bh, const uint4& bl, int g) {
+  f4 zz = *reinterpret_cast<const f4*>(hb + 4 * g);
+  return mfma_bf3(hp[0], hp[1], bh, bl, zz);
 }
 
 // h + Emb(S1) in the accumulator layout (emb_row = emb_s1 + S1 * C).
@@ -181,19 +286,25 @@ __device__ __forceinline__ void stage_lds(const f4* __restrict__ src, f4* dst, i
   }
 }
 
-template <int C, bool FIRST, bool LAST, bool TWO>
+template <int C, bool FIRST, bool LAST, bool TWO, bool BF>
 __global__ void __launch_bounds__(CONV_THREADS) k_conv(ConvArgs a) {
   constexpr int NCB = C / 16;
   constexpr int KS = FIRST ? 3 : C / 4;
   constexpr int KSP = (KS + 3) & ~3;
   constexpr int KT = C / 4;
-  constexpr int WSZ = 27 * NCB * 64 * KSP;
-  constexpr int HSZ = LAST ? (TWO ? 2 : 16) * 64 * KT : 4;
+  // packed weights per (offset, column block, lane): fp32 KSP floats, bf16x3 8 words
+  constexpr int WSZ = 27 * NCB * 64 * (BF ? 8 : KSP);
+  constexpr int HSZ = LAST ? (TWO ? 2 : 16) * 64 * (BF ? 8 : KT) : 4;
   constexpr int PCH = FIRST ? 8 : 4;  // offsets per pipeline stage
   struct Gath {                        // one gathered neighbour slice
     uint32_t word;                     // first layer: 11 input bits
-    f4 v[FIRST ? 1 : KSP / 4];         // later layers: KS channels
+    f4 v[FIRST ? 1 : KSP / 4];         // later layers, fp32: KS channels
   };
+  struct GathB {                       // later layers, bf16x3: channels 8g .. 8g+7
+    uint32_t word;
+    uint4 hi, lo;
+  };
+  using G = typename std::conditional<BF, GathB, Gath>::type;
   __shared__ __attribute__((aligned(16))) float s_w[WSZ];
   __shared__ __attribute__((aligned(16))) float s_h[HSZ];
   __shared__ uint64_t s_par[FIRST ? CONV_WAVES : 1][16][8];  // per wave: parent cells (code<<32|first)
@@ -342,7 +453,7 @@ __global__ void __launch_bounds__(CONV_THREADS) k_conv(ConvArgs a) {
         offs &= offs ? offs - 1u : 0u;
       }
     };
-    auto gather = [&](const int (&ks)[PCH], Gath (&gb)[PCH]) {
+    auto gather = [&](const int (&ks)[PCH], G (&gb)[PCH]) {
       int32_t nn[PCH];
 #pragma unroll
       for (int c = 0; c < PCH; ++c) nn[c] = __shfl(pick8(nlo, nhi, ks[c] & 7), r + 16 * ((ks[c] & 31) >> 3));
@@ -353,6 +464,14 @@ __global__ void __launch_bounds__(CONV_THREADS) k_conv(ConvArgs a) {
         if constexpr (FIRST) {
           // absent neighbours read the reserved zero entry: no select on loaded data
           gb[c].word = n >= 0 ? a.lv_feat[lvb + n] : a.lv_feat[a.zero_feat];
+        } else if constexpr (BF) {
+          // rows hold [hi plane: C bf16][lo plane: C bf16]; lanes beyond C/8 feed zeros
+          const int64_t srow = n >= 0 ? mo + n : a.cap_model;
+          const uint4* src = reinterpret_cast<const uint4*>(a.h_in + srow * C);
+          const int gq = g < C / 8 ? g : 0;
+          gb[c].hi = src[gq];
+          gb[c].lo = src[C / 8 + gq];
+          if (g >= C / 8) gb[c].hi = gb[c].lo = make_uint4(0, 0, 0, 0);
         } else {
           // absent neighbours read the reserved all-zero row cap_model
           const int64_t srow = n >= 0 ? mo + n : a.cap_model;
@@ -370,7 +489,48 @@ __global__ void __launch_bounds__(CONV_THREADS) k_conv(ConvArgs a) {
         for (int q = 0; q < KSP / 4; ++q) wv[cb][q] = wp[q];
       }
     };
-    auto mma = [&](const int (&ks)[PCH], const Gath (&gb)[PCH]) {
+    auto mma_bf = [&](const int (&ks)[PCH], const G (&gb)[PCH]) {
+      if constexpr (BF) {
+#pragma unroll
+      for (int c = 0; c < PCH; ++c) {
+        if (ks[c] < 0) break;
+        uint4 wa[NCB][2];
+#pragma unroll
+        for (int cb = 0; cb < NCB; ++cb) {
+          const uint4* wp = reinterpret_cast<const uint4*>(s_w) + ((ks[c] * NCB + cb) * 64 + lane) * 2;
+          wa[cb][0] = wp[0];
+          wa[cb][1] = wp[1];
+        }
+        uint4 bh, bl;
+        if constexpr (FIRST) {
+          // 11 input bits: lane group 0 carries bits 0..7, group 1 bits 8..10
+          // (exact in bf16), groups 2-3 zeros; products hi*x + lo*x
+          const uint32_t bits = g < 2 ? (gb[c].word >> (8 * g)) & (g == 0 ? 0xFFu : 0x7u) : 0u;
+          uint32_t wd[4];
+#pragma unroll
+          for (int pr = 0; pr < 4; ++pr)
+            wd[pr] = (((bits >> (2 * pr)) & 1u) ? 0x3F80u : 0u) | (((bits >> (2 * pr + 1)) & 1u) ? 0x3F800000u : 0u);
+          bh = make_uint4(wd[0], wd[1], wd[2], wd[3]);
+#pragma unroll
+          for (int cb = 0; cb < NCB; ++cb) acc[cb] = mfma_bf(wa[cb][0], bh, acc[cb]);
+#pragma unroll
+          for (int cb = 0; cb < NCB; ++cb) acc[cb] = mfma_bf(wa[cb][1], bh, acc[cb]);
+        } else {
+          bh = gb[c].hi;
+          bl = gb[c].lo;
+          // the three products, column blocks interleaved
+#pragma unroll
+          for (int cb = 0; cb < NCB; ++cb) acc[cb] = mfma_bf(wa[cb][0], bh, acc[cb]);
+#pragma unroll
+          for (int cb = 0; cb < NCB; ++cb) acc[cb] = mfma_bf(wa[cb][0], bl, acc[cb]);
+#pragma unroll
+          for (int cb = 0; cb < NCB; ++cb) acc[cb] = mfma_bf(wa[cb][1], bh, acc[cb]);
+        }
+      }
+      }
+    };
+    auto mma_f32 = [&](const int (&ks)[PCH], const G (&gb)[PCH]) {
+      if constexpr (!BF) {
 #pragma unroll
       for (int c = 0; c < PCH; ++c) {
         if (ks[c] < 0) break;
@@ -381,7 +541,7 @@ __global__ void __launch_bounds__(CONV_THREADS) k_conv(ConvArgs a) {
 #pragma unroll
           for (int s = 0; s < KSP; ++s) bsrc[s] = (float)((gb[c].word >> (g * KS + s)) & 1u);
           // slot s = KS (padding) meets zero weights
-        } else {
+        } else if constexpr (!BF) {
 #pragma unroll
           for (int q = 0; q < KSP / 4; ++q)
 #pragma unroll
@@ -393,10 +553,15 @@ __global__ void __launch_bounds__(CONV_THREADS) k_conv(ConvArgs a) {
 #pragma unroll
           for (int cb = 0; cb < NCB; ++cb) acc[cb] = mfma4(wv[cb][s / 4][s % 4], bsrc[s], acc[cb]);
       }
+      }
+    };
+    auto mma = [&](const int (&ks)[PCH], const G (&gb)[PCH]) {
+      if constexpr (BF) mma_bf(ks, gb);
+      else mma_f32(ks, gb);
     };
     {
       int ksA[PCH], ksB[PCH];
-      Gath gA[PCH], gB[PCH];
+      G gA[PCH], gB[PCH];
       take(ksA);
       gather(ksA, gA);
       while (true) {
@@ -415,16 +580,37 @@ __global__ void __launch_bounds__(CONV_THREADS) k_conv(ConvArgs a) {
 #pragma unroll
       for (int e = 0; e < 4; ++e) acc[cb][e] = fmaxf(acc[cb][e], 0.0f);
     if (valid) {
+      if constexpr (BF && !LAST) {
+        // next layer's input as [hi plane | lo plane] of bf16 (split once per voxel)
+        uint16_t* row = reinterpret_cast<uint16_t*>(a.h_out + prow * C);
 #pragma unroll
-      for (int cb = 0; cb < NCB; ++cb)
-        *reinterpret_cast<f4*>(a.h_out + prow * C + 16 * cb + 4 * g) = acc[cb];
+        for (int cb = 0; cb < NCB; ++cb) {
+          uint32_t h0, l0, h1, l1;
+          split2(acc[cb][0], acc[cb][1], h0, l0);
+          split2(acc[cb][2], acc[cb][3], h1, l1);
+          *reinterpret_cast<uint2*>(row + 16 * cb + 4 * g) = make_uint2(h0, h1);
+          *reinterpret_cast<uint2*>(row + C + 16 * cb + 4 * g) = make_uint2(l0, l1);
+        }
+      } else {
+#pragma unroll
+        for (int cb = 0; cb < NCB; ++cb)
+          *reinterpret_cast<f4*>(a.h_out + prow * C + 16 * cb + 4 * g) = acc[cb];
+      }
     }
 
     if constexpr (LAST && TWO) {
       // ---- two-stage head (Eqs. 11-13): stage 1 over S1; stage 2 over S2
       // with h + Emb(S1) when the codes of the scale are known
       const f4* hp = reinterpret_cast<const f4*>(s_h) + lane * (KT / 4);
-      const f4 z1 = head16<C>(hp, a.hb, acc, g);
+      const uint4* hpb = reinterpret_cast<const uint4*>(s_h) + lane * 2;
+      f4 z1;
+      if constexpr (BF) {
+        uint4 bh, bl;
+        head_operand_bf<C>(acc, bh, bl);
+        z1 = head16_bf<C>(hpb, a.hb, bh, bl, g);
+      } else {
+        z1 = head16<C>(hp, a.hb, acc, g);
+      }
       const float l1 = lse16(z1);
       if (valid && g == 0) a.lse[prow] = l1;
       float* lo = (a.logits && valid) ? a.logits + (prow - s_mo[0]) * 32 + 4 * g : nullptr;
@@ -433,7 +619,14 @@ __global__ void __launch_bounds__(CONV_THREADS) k_conv(ConvArgs a) {
         const int s1 = a.s1_code[lvb + (prow - mo)] & 15;
         f4 h2[NCB];
         add_emb<C>(acc, a.emb + s1 * C, g, h2);
-        const f4 z2 = head16<C>(hp + 64 * (KT / 4), a.hb + 16, h2, g);
+        f4 z2;
+        if constexpr (BF) {
+          uint4 bh, bl;
+          head_operand_bf<C>(h2, bh, bl);
+          z2 = head16_bf<C>(hpb + 64 * 2, a.hb + 16, bh, bl, g);
+        } else {
+          z2 = head16<C>(hp + 64 * (KT / 4), a.hb + 16, h2, g);
+        }
         const float l2 = lse16(z2);
         if (valid && g == 0) a.lse2[prow] = l2;
         if (lo) *reinterpret_cast<f4*>(lo + 16) = z2;
@@ -444,19 +637,26 @@ __global__ void __launch_bounds__(CONV_THREADS) k_conv(ConvArgs a) {
       // operand; 64 symbols at a time with a running (max, sum of exp)
       float m = -INFINITY, ssum = 0.0f;
       float* lo = (a.logits && valid) ? a.logits + (prow - s_mo[0]) * 256 + 4 * g : nullptr;
+      uint4 bh = make_uint4(0, 0, 0, 0), bl = bh;
+      if constexpr (BF) head_operand_bf<C>(acc, bh, bl);
 #pragma unroll 1
       for (int grp = 0; grp < 4; ++grp) {
         f4 zz[4];
 #pragma unroll
         for (int q4 = 0; q4 < 4; ++q4) {
           const int sb = grp * 4 + q4;
-          zz[q4] = *reinterpret_cast<const f4*>(a.hb + 16 * sb + 4 * g);
-          const f4* hp = reinterpret_cast<const f4*>(s_h + (sb * 64 + lane) * KT);
+          if constexpr (BF) {
+            zz[q4] = head16_bf<C>(reinterpret_cast<const uint4*>(s_h) + (sb * 64 + lane) * 2, a.hb + 16 * sb,
+                                  bh, bl, g);
+          } else {
+            zz[q4] = *reinterpret_cast<const f4*>(a.hb + 16 * sb + 4 * g);
+            const f4* hp = reinterpret_cast<const f4*>(s_h + (sb * 64 + lane) * KT);
 #pragma unroll
-          for (int q = 0; q < KT / 4; ++q) {
-            const f4 hv = hp[q];
+            for (int q = 0; q < KT / 4; ++q) {
+              const f4 hv = hp[q];
 #pragma unroll
-            for (int e = 0; e < 4; ++e) zz[q4] = mfma4(hv[e], acc[q][e], zz[q4]);
+              for (int e = 0; e < 4; ++e) zz[q4] = mfma4(hv[e], acc[q][e], zz[q4]);
+            }
           }
         }
         float gm = zz[0][0];
@@ -493,25 +693,26 @@ __global__ void __launch_bounds__(CONV_THREADS) k_conv(ConvArgs a) {
   }
 }
 
-template <int C, bool FIRST, bool LAST, bool TWO>
+template <int C, bool FIRST, bool LAST, bool TWO, bool BF>
 hipError_t run_conv(Ctx& c, const ConvArgs& a) {
   // one block per CU stages the weights once for its 16 waves
-  hipLaunchKernelGGL((k_conv<C, FIRST, LAST, TWO>), dim3(256), dim3(CONV_THREADS), 0, c.stream, a);
+  hipLaunchKernelGGL((k_conv<C, FIRST, LAST, TWO, BF>), dim3(256), dim3(CONV_THREADS), 0, c.stream, a);
   return hipGetLastError();
 }
 
-template <int C>
+template <int C, bool BF>
 hipError_t run_layer(Ctx& c, bool first, bool last, bool two, const ConvArgs& a) {
-  if (first && last) return two ? run_conv<C, true, true, true>(c, a) : run_conv<C, true, true, false>(c, a);
-  if (first) return run_conv<C, true, false, false>(c, a);
-  if (last) return two ? run_conv<C, false, true, true>(c, a) : run_conv<C, false, true, false>(c, a);
-  return run_conv<C, false, false, false>(c, a);
+  if (first && last)
+    return two ? run_conv<C, true, true, true, BF>(c, a) : run_conv<C, true, true, false, BF>(c, a);
+  if (first) return run_conv<C, true, false, false, BF>(c, a);
+  if (last) return two ? run_conv<C, false, true, true, BF>(c, a) : run_conv<C, false, true, false, BF>(c, a);
+  return run_conv<C, false, false, false, BF>(c, a);
 }
 
 // Stage 2 of the two-stage head for one scale from the stored features of the
 // last conv layer and a given S1 per voxel (decoder).  One wave per tile of
 // 16 voxels, the same tile split and arithmetic as the fused path.
-template <int C>
+template <int C, bool BF>
 __global__ void __launch_bounds__(256) k_head2(int b, const int32_t* __restrict__ count,
                                                const int32_t* __restrict__ moff, int64_t cap_model,
                                                const float* __restrict__ hL, const uint8_t* __restrict__ s1,
@@ -543,7 +744,14 @@ __global__ void __launch_bounds__(256) k_head2(int b, const int32_t* __restrict_
     }
     f4 h2[NCB];
     add_emb<C>(h, emb + a1 * C, g, h2);
-    const f4 z2 = head16<C>(hp, hb2, h2, g);
+    f4 z2;
+    if constexpr (BF) {
+      uint4 bh, bl;
+      head_operand_bf<C>(h2, bh, bl);
+      z2 = head16_bf<C>(reinterpret_cast<const uint4*>(hw2) + lane * 2, hb2, bh, bl, g);
+    } else {
+      z2 = head16<C>(hp, hb2, h2, g);
+    }
     const float l2 = lse16(z2);
     if (valid && g == 0) lse2[prow] = l2;
     if (valid && logits2) *reinterpret_cast<f4*>(logits2 + row * 16 + 4 * g) = z2;
@@ -556,26 +764,41 @@ hipError_t launch_pack_weights(Ctx& c, const reno_weights& w) {
   ProfScope ps_(c, RENO_K_OTHER);
   const int C = c.p.channels;
   int c_in = RENO_IN_FEATURES;
+  const bool bf = c.p.precision == RENO_PREC_BF16X3;
   for (int l = 0; l < c.p.layers; ++l) {
     const int KS = (c_in + 3) / 4;
     const int KSP = (KS + 3) & ~3;
-    hipLaunchKernelGGL(k_pack_conv, dim3(64), dim3(256), 0, c.stream, w.conv_w[l], c_in, C, KS, KSP,
-                       c.w_conv[l]);
+    if (bf)
+      hipLaunchKernelGGL(k_pack_conv_bf, dim3(64), dim3(256), 0, c.stream, w.conv_w[l], c_in, C,
+                         reinterpret_cast<uint32_t*>(c.w_conv[l]));
+    else
+      hipLaunchKernelGGL(k_pack_conv, dim3(64), dim3(256), 0, c.stream, w.conv_w[l], c_in, C, KS, KSP,
+                         c.w_conv[l]);
     hipLaunchKernelGGL(k_copy_f32, dim3(1), dim3(256), 0, c.stream, w.conv_b[l], c.w_bias[l], C);
     c_in = C;
   }
   if (c.p.head_mode == RENO_HEAD_TWO_STAGE) {
     // packed blocks [stage 1][stage 2], biases [b1 | b2], plain [C][H1 | H2]
-    const int blk = 64 * (C / 4);
-    hipLaunchKernelGGL(k_pack_head, dim3(4), dim3(256), 0, c.stream, w.head1_w, C, 16, c.w_head);
-    hipLaunchKernelGGL(k_pack_head, dim3(4), dim3(256), 0, c.stream, w.head2_w, C, 16, c.w_head + blk);
+    const int blk = bf ? 64 * 8 : 64 * (C / 4);
+    if (bf) {
+      uint32_t* hw = reinterpret_cast<uint32_t*>(c.w_head);
+      hipLaunchKernelGGL(k_pack_head_bf, dim3(1), dim3(256), 0, c.stream, w.head1_w, C, 16, hw);
+      hipLaunchKernelGGL(k_pack_head_bf, dim3(1), dim3(256), 0, c.stream, w.head2_w, C, 16, hw + blk);
+    } else {
+      hipLaunchKernelGGL(k_pack_head, dim3(4), dim3(256), 0, c.stream, w.head1_w, C, 16, c.w_head);
+      hipLaunchKernelGGL(k_pack_head, dim3(4), dim3(256), 0, c.stream, w.head2_w, C, 16, c.w_head + blk);
+    }
     hipLaunchKernelGGL(k_copy_f32, dim3(1), dim3(64), 0, c.stream, w.head1_b, c.w_hbias, 16);
     hipLaunchKernelGGL(k_copy_f32, dim3(1), dim3(64), 0, c.stream, w.head2_b, c.w_hbias + 16, 16);
     hipLaunchKernelGGL(k_put_cols16, dim3(2), dim3(256), 0, c.stream, w.head1_w, C, 0, c.w_head_plain);
     hipLaunchKernelGGL(k_put_cols16, dim3(2), dim3(256), 0, c.stream, w.head2_w, C, 16, c.w_head_plain);
     hipLaunchKernelGGL(k_copy_f32, dim3(2), dim3(256), 0, c.stream, w.emb_s1, c.w_emb, 16 * C);
   } else {
-    hipLaunchKernelGGL(k_pack_head, dim3(32), dim3(256), 0, c.stream, w.head_w, C, 256, c.w_head);
+    if (bf)
+      hipLaunchKernelGGL(k_pack_head_bf, dim3(16), dim3(256), 0, c.stream, w.head_w, C, 256,
+                         reinterpret_cast<uint32_t*>(c.w_head));
+    else
+      hipLaunchKernelGGL(k_pack_head, dim3(32), dim3(256), 0, c.stream, w.head_w, C, 256, c.w_head);
     hipLaunchKernelGGL(k_copy_f32, dim3(1), dim3(256), 0, c.stream, w.head_b, c.w_hbias, 256);
     hipLaunchKernelGGL(k_copy_f32, dim3(32), dim3(256), 0, c.stream, w.head_w, c.w_head_plain,
                        C * 256);
@@ -616,24 +839,32 @@ hipError_t launch_model(Ctx& c, int b_lo, int b_hi, float* logits, bool second) 
     a.logits = (l == L - 1) ? logits : nullptr;
     const bool first = l == 0, last = l == L - 1;
     ProfScope ps_(c, last ? RENO_K_CONV_LAST : (first ? RENO_K_CONV_FIRST : RENO_K_CONV_MID));
-    e = (c.p.channels == 32) ? run_layer<32>(c, first, last, two, a) : run_layer<16>(c, first, last, two, a);
+    if (c.p.precision == RENO_PREC_BF16X3)
+      e = (c.p.channels == 32) ? run_layer<32, true>(c, first, last, two, a)
+                               : run_layer<16, true>(c, first, last, two, a);
+    else
+      e = (c.p.channels == 32) ? run_layer<32, false>(c, first, last, two, a)
+                               : run_layer<16, false>(c, first, last, two, a);
   }
   return e;
 }
 
 hipError_t launch_head2(Ctx& c, int b, const uint8_t* s1, float* logits2) {
   ProfScope ps_(c, RENO_K_CONV_LAST);
-  const float* hw2 = c.w_head + 64 * (c.p.channels / 4);
+  const bool bf = c.p.precision == RENO_PREC_BF16X3;
+  const float* hw2 = c.w_head + (bf ? 64 * 8 : 64 * (c.p.channels / 4));
   const uint8_t* code = c.lv_code + c.lv(b);
   const int blocks = (int)std::min<int64_t>(1024, (c.cap_pts + 63) / 64);
-  if (c.p.channels == 32)
-    hipLaunchKernelGGL(k_head2<32>, dim3(blocks), dim3(256), 0, c.stream, b, c.d_count, c.d_moff,
-                       (int64_t)c.cap_model, c.hlast(), s1, code, hw2, c.w_hbias + 16, c.w_emb, c.d_lse2,
-                       logits2, c.d_err);
-  else
-    hipLaunchKernelGGL(k_head2<16>, dim3(blocks), dim3(256), 0, c.stream, b, c.d_count, c.d_moff,
-                       (int64_t)c.cap_model, c.hlast(), s1, code, hw2, c.w_hbias + 16, c.w_emb, c.d_lse2,
-                       logits2, c.d_err);
+#define RENO_HEAD2(CC, BFV)                                                                       \
+  hipLaunchKernelGGL((k_head2<CC, BFV>), dim3(blocks), dim3(256), 0, c.stream, b, c.d_count, c.d_moff, \
+                     (int64_t)c.cap_model, c.hlast(), s1, code, hw2, c.w_hbias + 16, c.w_emb, c.d_lse2, \
+                     logits2, c.d_err)
+  if (c.p.channels == 32) {
+    if (bf) RENO_HEAD2(32, true); else RENO_HEAD2(32, false);
+  } else {
+    if (bf) RENO_HEAD2(16, true); else RENO_HEAD2(16, false);
+  }
+#undef RENO_HEAD2
   return hipGetLastError();
 }
 
