@@ -212,6 +212,17 @@ reno_status reno_neighbor_map(reno_ctx* ctx, int scale, int32_t* map);
  * Deterministic: an encoder and a decoder context that computed the same
  * distribution produce identical tables. */
 reno_status reno_symbol_freqs(reno_ctx* ctx, int scale, uint16_t* freq);
+/* Two-stage head: the same rule over 16 symbols, f_s = 1 + floor(p_s * 65504)
+ * (2^16 - 2*16), uint16 [N_scale][16]; stage 1 after predict_probs, stage 2
+ * (given the S1 of the last stage-2 evaluation) after predict_second.  In
+ * general for K symbols: f_s = 1 + floor(p_s * (2^16 - 2K)). */
+reno_status reno_symbol_freqs16(reno_ctx* ctx, int scale, int stage, uint16_t* freq);
+/* Encoder side of the same tables without shipping them: for each voxel the
+ * interval (start = sum of f below the symbol, f) of its code in its table,
+ * uint16 [N][2] (one-stage) or [N][4] (two-stage: S1 in the stage-1 table,
+ * then S2 in the stage-2 table).  Needs the codes and predict_probs (and
+ * stage 2).  RENO_ALL_SCALES: every model scale, concatenated in order. */
+reno_status reno_symbol_intervals(reno_ctx* ctx, int scale, uint16_t* iv);
 
 /* Host rANS coder (Duda, arXiv:1311.2540) for one scale's stream; HOST
  * pointers.  64-bit state in [2^31, 2^63), 32-bit renormalisation words.
@@ -220,6 +231,14 @@ reno_status reno_symbol_freqs(reno_ctx* ctx, int scale, uint16_t* freq);
  * inverse; fails with RENO_E_INPUT on a corrupt or truncated stream. */
 reno_status reno_rans_encode(const uint8_t* sym, const uint16_t* freq, int64_t n, uint32_t* out,
                              int64_t cap, int64_t* nwords_host);
+/* rANS encode from intervals (host memory): iv[i * stride] = start,
+ * iv[i * stride + 1] = frequency of symbol i (start + f <= 2^16); same
+ * stream format as reno_rans_encode. */
+reno_status reno_rans_encode_intervals(const uint16_t* iv, int64_t n, int64_t stride, uint32_t* out,
+                                       int64_t cap, int64_t* nwords_host);
+/* Decoding with 16-symbol tables freq [n][16] (the two-stage head). */
+reno_status reno_rans_decode16(const uint32_t* in, int64_t nwords, const uint16_t* freq, int64_t n,
+                               uint8_t* sym);
 reno_status reno_rans_decode(const uint32_t* in, int64_t nwords, const uint16_t* freq, int64_t n,
                              uint8_t* sym);
 

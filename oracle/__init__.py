@@ -71,6 +71,7 @@ def lib():
                                    vp, vp]),
             "orc_totals": (dbl, [vp, ctypes.POINTER(OrcWeights), vp]),
             "orc_freqs_from_probs": (None, [vp, vp]),
+            "orc_freqs_from_probs_k": (None, [vp, c_int, vp]),
             "orc_rans_encode": (i64, [vp, vp, i64, vp, i64]),
             "orc_rans_decode": (c_int, [vp, i64, vp, i64, vp]),
         }
@@ -273,11 +274,12 @@ def sparse_conv(xyz: np.ndarray, bits: int, feats: np.ndarray, W: np.ndarray, bi
     return out
 
 
-def freqs_from_probs(p: np.ndarray) -> np.ndarray:
-    p = np.ascontiguousarray(p, dtype=np.float64).reshape(-1, SYMBOLS)
+def freqs_from_probs(p: np.ndarray, k: int = SYMBOLS) -> np.ndarray:
+    """Quantised tables [n][k] from probabilities [n][k] (k = 256 or 16)."""
+    p = np.ascontiguousarray(p, dtype=np.float64).reshape(-1, k)
     out = np.empty(p.shape, dtype=np.uint32)
     for i in range(p.shape[0]):
-        lib().orc_freqs_from_probs(_p(p[i]), _p(out[i]))
+        lib().orc_freqs_from_probs_k(_p(p[i]), k, _p(out[i]))
     return out
 
 

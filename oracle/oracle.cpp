@@ -576,21 +576,26 @@ double orc_totals(void* h, const OrcWeights* w, double* per_scale /*[B+1] or NUL
 // precision: a symbol with start s and frequency f (sum of f <= 2^16) maps
 //   x -> floor(x / f) * 2^16 + (x mod f) + s.
 // Symbols are encoded in reverse so that the decoder emits them forward.
-// Frequencies from probabilities: f = 1 + floor(p * 65024) in fp32, and the
-// 2^16 - sum(f) leftover slots go to the lowest-index most frequent symbol.
+// Frequencies from probabilities over K symbols: f = 1 + floor(p * (2^16 - 2K))
+// in fp32 (65024 for K = 256, 65504 for the 16-way stages of the two-stage
+// head), and the 2^16 - sum(f) leftover slots go to the lowest-index most
+// frequent symbol.
 
-void orc_freqs_from_probs(const double* p, uint32_t* f) {
+void orc_freqs_from_probs_k(const double* p, int k, uint32_t* f) {
+  const float scale = (float)(65536 - 2 * k);
   uint32_t sum = 0;
-  for (int s = 0; s < 256; ++s) {
+  for (int s = 0; s < k; ++s) {
     float pf = (float)p[s];
-    f[s] = 1u + (uint32_t)std::floor(pf * 65024.0f);
+    f[s] = 1u + (uint32_t)std::floor(pf * scale);
     sum += f[s];
   }
   int best = 0;
-  for (int s = 1; s < 256; ++s)
+  for (int s = 1; s < k; ++s)
     if (f[s] > f[best]) best = s;
   f[best] += 65536u - sum;
 }
+
+void orc_freqs_from_probs(const double* p, uint32_t* f) { orc_freqs_from_probs_k(p, 256, f); }
 
 // Encodes n symbols; freq [n][256]; writes 32-bit words to out (capacity
 // `cap`), returns the number of words or -1.

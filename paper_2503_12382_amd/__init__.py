@@ -79,6 +79,10 @@ _SIGS = {
     "reno_code_length": (_int, [_vp, _int, _vp, ctypes.POINTER(ctypes.c_double)]),
     "reno_neighbor_map": (_int, [_vp, _int, _vp]),
     "reno_symbol_freqs": (_int, [_vp, _int, _vp]),
+    "reno_symbol_freqs16": (_int, [_vp, _int, _int, _vp]),
+    "reno_symbol_intervals": (_int, [_vp, _int, _vp]),
+    "reno_rans_encode_intervals": (_int, [_vp, _i64, _i64, _vp, _i64, ctypes.POINTER(_i64)]),
+    "reno_rans_decode16": (_int, [_vp, _i64, _vp, _i64, _vp]),
     "reno_rans_encode": (_int, [_vp, _vp, _i64, _vp, _i64, ctypes.POINTER(_i64)]),
     "reno_rans_decode": (_int, [_vp, _i64, _vp, _i64, _vp]),
     "reno_profile": (_int, [_vp, ctypes.c_uint32]),
@@ -297,6 +301,27 @@ class Context:
         self._check(lib().reno_profile_read(self._h, ms.ctypes.data_as(_vp), n.ctypes.data_as(_vp)))
         return {k: (float(ms[i]), int(n[i])) for i, k in enumerate(KERNELS) if n[i]}
 
+    def symbol_freqs16(self, scale: int, stage: int):
+        """Two-stage head: uint16 [N][16] table of stage 1 or 2 per voxel."""
+        n = self.num_voxels(scale)
+        out = self._empty((max(n, 1), 16), self.torch.int16)
+        self._check(lib().reno_symbol_freqs16(self._h, scale, stage, _ptr(out)))
+        return out[:n]
+
+    def symbol_intervals(self, scale: int, out=None):
+        """(start, freq) of each voxel's code in its table: int16-typed uint16
+        [N][2] (one-stage) or [N][4] (two-stage); RENO_ALL_SCALES concatenates
+        the model scales.  ``out`` may be a preallocated device tensor."""
+        if scale == RENO_ALL_SCALES:
+            n = sum(self.num_voxels(b) for b in range(self.b0 + 1, self.B))
+        else:
+            n = self.num_voxels(scale)
+        per = 4 if self.two_stage else 2
+        if out is None:
+            out = self._empty((max(n, 1), per), self.torch.int16)
+        self._check(lib().reno_symbol_intervals(self._h, scale, _ptr(out)))
+        return out[:n]
+
     def symbol_freqs(self, scale: int):
         n = self.num_voxels(scale)
         out = self._empty((max(n, 1), SYMBOLS), self.torch.int16)
@@ -319,14 +344,32 @@ def rans_encode(sym: np.ndarray, freq: np.ndarray) -> np.ndarray:
 
 
 def rans_decode(words: np.ndarray, freq: np.ndarray, n: int) -> np.ndarray:
+    """Host rANS decode with per-symbol tables of 256 (or, [n][16], 16) entries."""
     w = np.ascontiguousarray(words, dtype=np.uint32)
-    f = np.ascontiguousarray(freq, dtype=np.uint16).reshape(-1, SYMBOLS)
+    k = 16 if (np.asarray(freq).ndim == 2 and np.asarray(freq).shape[1] == 16) else SYMBOLS
+    f = np.ascontiguousarray(freq, dtype=np.uint16).reshape(-1, k)
     out = np.empty(n, dtype=np.uint8)
-    rc = lib().reno_rans_decode(w.ctypes.data_as(_vp), w.size, f.ctypes.data_as(_vp), n,
-                                out.ctypes.data_as(_vp))
+    fn = lib().reno_rans_decode16 if k == 16 else lib().reno_rans_decode
+    rc = fn(w.ctypes.data_as(_vp), w.size, f.ctypes.data_as(_vp), n, out.ctypes.data_as(_vp))
     if rc != RENO_OK:
         raise RenoError(rc, "rANS decode failed")
     return out
+
+
+def rans_encode_intervals(iv: np.ndarray, stride: int = 2, offset: int = 0) -> np.ndarray:
+    """Host rANS encode from (start, freq) intervals: symbol i uses
+    iv.flat[offset + i * stride] and the entry after it (a contiguous uint16
+    array, e.g. [n][2], or [n][4] with offset 0 / 2 for the two stages)."""
+    a = np.ascontiguousarray(iv, dtype=np.uint16).reshape(-1)
+    n = (a.size - offset - 2) // stride + 1 if a.size >= offset + 2 else 0
+    cap = n + 16
+    out = np.empty(cap, dtype=np.uint32)
+    nw = ctypes.c_int64()
+    rc = lib().reno_rans_encode_intervals(a[offset:].ctypes.data_as(_vp), n, stride,
+                                          out.ctypes.data_as(_vp), cap, ctypes.byref(nw))
+    if rc != RENO_OK:
+        raise RenoError(rc, "rANS encode failed")
+    return out[:nw.value].copy()
 
 
 def weights_to_device(w: dict, device="cuda") -> dict:

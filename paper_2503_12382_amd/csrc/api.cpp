@@ -53,7 +53,7 @@ void free_all(Ctx* c) {
                   c->lv_feat, c->d_count,   c->d_moff,   c->d_err,    c->d_hist,    c->d_ticket,
                   c->d_status, c->d_hash,   c->h_a,      c->h_b,      c->d_nbr,     c->d_lse,
                   c->d_partial, c->d_total, c->w_head,   c->w_hbias,  c->w_head_plain,
-                  c->d_lse2,    c->w_emb};
+                  c->d_lse2,    c->w_emb,   c->d_s1};
   for (void* p : ptrs)
     if (p) (void)hipFree(p);
   for (int l = 0; l < RENO_MAX_LAYERS; ++l) {
@@ -189,6 +189,7 @@ reno_status reno_create(const reno_params* p, void* hip_stream, reno_ctx** out) 
   A(dalloc(&c->d_nbr, (size_t)cap_model * reno::NBR_STRIDE, &c->device_bytes));
   A(dalloc(&c->d_lse, (size_t)cap_model, &c->device_bytes));
   A(dalloc(&c->d_lse2, (size_t)cap_model, &c->device_bytes));
+  A(dalloc(&c->d_s1, (size_t)cap_model, &c->device_bytes));
   A(dalloc(&c->d_partial, (size_t)reno::NLEV * ((c->cap_pts + 1023) / 1024), &c->device_bytes));
   A(dalloc(&c->d_total, reno::NLEV, &c->device_bytes));
   int c_in = RENO_IN_FEATURES;
@@ -464,6 +465,37 @@ reno_status reno_symbol_freqs(reno_ctx* c, int scale, uint16_t* freq) {
     return fail(c, RENO_E_STATE, "symbol tables are built for the one-stage head only");
   if (!has(c->have_pred, scale)) return fail(c, RENO_E_STATE, "predict_probs of the scale not run");
   RENO_HIP(c, reno::launch_symbol_freqs(*c, scale, freq));
+  return RENO_OK;
+}
+
+reno_status reno_symbol_freqs16(reno_ctx* c, int scale, int stage, uint16_t* freq) {
+  if (!c || !freq) return fail(c, RENO_E_INVALID, "null argument");
+  if (c->p.head_mode != RENO_HEAD_TWO_STAGE) return fail(c, RENO_E_STATE, "one-stage context");
+  if (stage != 1 && stage != 2) return fail(c, RENO_E_INVALID, "stage must be 1 or 2");
+  if (!model_scale(c, scale)) return fail(c, RENO_E_INVALID, "not a model scale");
+  if (!has(stage == 1 ? c->have_pred : c->have_pred2, scale))
+    return fail(c, RENO_E_STATE, stage == 1 ? "predict_probs of the scale not run"
+                                            : "stage 2 of the scale not run");
+  RENO_HIP(c, reno::launch_symbol_freqs16(*c, scale, stage, freq));
+  return RENO_OK;
+}
+
+reno_status reno_symbol_intervals(reno_ctx* c, int scale, uint16_t* iv) {
+  if (!c || !iv) return fail(c, RENO_E_INVALID, "null argument");
+  if (c->B == 0) return fail(c, RENO_E_STATE, "no frame");
+  int lo, hi;
+  if (scale == RENO_ALL_SCALES) {
+    lo = c->b0() + 1;
+    hi = c->B - 1;
+    if (lo > hi) return RENO_OK;
+  } else {
+    if (!model_scale(c, scale)) return fail(c, RENO_E_INVALID, "not a model scale");
+    lo = hi = scale;
+  }
+  for (int b = lo; b <= hi; ++b)
+    if (!has(c->have_pred, b) || !has(c->have_codes, b) || !stage2_ok(c, b))
+      return fail(c, RENO_E_STATE, "intervals need predict_probs (both stages) and the codes");
+  RENO_HIP(c, reno::launch_symbol_intervals(*c, lo, hi, iv));
   return RENO_OK;
 }
 

@@ -80,6 +80,7 @@ struct Ctx {
   int32_t* d_nbr = nullptr;     // [cap_model][NBR_STRIDE]
   float* d_lse = nullptr;       // [cap_model] (two-stage head: stage 1)
   float* d_lse2 = nullptr;      // [cap_model] stage 2 of the two-stage head
+  uint8_t* d_s1 = nullptr;      // [cap_model] S1 that stage 2 was evaluated with
   double* d_partial = nullptr;  // [NLEV][ceil(cap_pts / 1024)] per-chunk bit sums
   double* d_total = nullptr;    // [NLEV]
   double* h_total = nullptr;    // pinned host mirror [NLEV]
@@ -157,6 +158,8 @@ hipError_t launch_model(Ctx& c, int b_lo, int b_hi, float* logits, bool second);
 hipError_t launch_head2(Ctx& c, int b, const uint8_t* s1, float* logits2);
 hipError_t launch_code_length(Ctx& c, int b_lo, int b_hi, float* bits);
 hipError_t launch_symbol_freqs(Ctx& c, int b, uint16_t* freq);
+hipError_t launch_symbol_freqs16(Ctx& c, int b, int stage, uint16_t* freq);
+hipError_t launch_symbol_intervals(Ctx& c, int b_lo, int b_hi, uint16_t* iv);
 hipError_t launch_coords(Ctx& c, int b, int32_t* xyz, uint64_t* keys);
 hipError_t launch_copy_level_u8(Ctx& c, int b, uint8_t* out);
 hipError_t launch_copy_level_i32(Ctx& c, int b, const int32_t* src, int32_t* out);

@@ -252,6 +252,7 @@ struct ConvArgs {
   const float* emb;       // [16][C]
   const uint8_t* s1_code; // codes of the per-scale regions (S1 = O & 15), or NULL: stage 1 only
   float* lse2;            // [cap_model]
+  uint8_t* s1_out;        // [cap_model] the S1 stage 2 used
 };
 
 // Entry j (wave-uniform) of the 8 neighbour rows a lane holds in two int4,
@@ -628,7 +629,10 @@ __global__ void __launch_bounds__(CONV_THREADS) k_conv(ConvArgs a) {
           z2 = head16<C>(hp + 64 * (KT / 4), a.hb + 16, h2, g);
         }
         const float l2 = lse16(z2);
-        if (valid && g == 0) a.lse2[prow] = l2;
+        if (valid && g == 0) {
+          a.lse2[prow] = l2;
+          a.s1_out[prow] = (uint8_t)s1;
+        }
         if (lo) *reinterpret_cast<f4*>(lo + 16) = z2;
       }
     }
@@ -719,7 +723,7 @@ __global__ void __launch_bounds__(256) k_head2(int b, const int32_t* __restrict_
                                                const uint8_t* __restrict__ code, const float* __restrict__ hw2,
                                                const float* __restrict__ hb2, const float* __restrict__ emb,
                                                float* __restrict__ lse2, float* __restrict__ logits2,
-                                               uint32_t* err) {
+                                               uint8_t* __restrict__ s1_out, uint32_t* err) {
   constexpr int NCB = C / 16;
   const int lane = threadIdx.x & 63, r = lane & 15, g = lane >> 4;
   const int64_t mo = moff[b];
@@ -753,7 +757,10 @@ __global__ void __launch_bounds__(256) k_head2(int b, const int32_t* __restrict_
       z2 = head16<C>(hp, hb2, h2, g);
     }
     const float l2 = lse16(z2);
-    if (valid && g == 0) lse2[prow] = l2;
+    if (valid && g == 0) {
+      lse2[prow] = l2;
+      s1_out[prow] = (uint8_t)a1;
+    }
     if (valid && logits2) *reinterpret_cast<f4*>(logits2 + row * 16 + 4 * g) = z2;
   }
 }
@@ -828,6 +835,7 @@ hipError_t launch_model(Ctx& c, int b_lo, int b_hi, float* logits, bool second) 
   a.emb = c.w_emb;
   a.s1_code = second ? c.lv_code : nullptr;
   a.lse2 = c.d_lse2;
+  a.s1_out = c.d_s1;
   const bool two = c.p.head_mode == RENO_HEAD_TWO_STAGE;
   const int L = c.p.layers;
   hipError_t e = hipSuccess;
@@ -858,7 +866,7 @@ hipError_t launch_head2(Ctx& c, int b, const uint8_t* s1, float* logits2) {
 #define RENO_HEAD2(CC, BFV)                                                                       \
   hipLaunchKernelGGL((k_head2<CC, BFV>), dim3(blocks), dim3(256), 0, c.stream, b, c.d_count, c.d_moff, \
                      (int64_t)c.cap_model, c.hlast(), s1, code, hw2, c.w_hbias + 16, c.w_emb, c.d_lse2, \
-                     logits2, c.d_err)
+                     logits2, c.d_s1, c.d_err)
   if (c.p.channels == 32) {
     if (bf) RENO_HEAD2(32, true); else RENO_HEAD2(32, false);
   } else {

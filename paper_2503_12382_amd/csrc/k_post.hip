@@ -140,9 +140,80 @@ __global__ void __launch_bounds__(CL_THREADS) k_code_length(
   }
 }
 
-// One wavefront per voxel: logits recomputed from h_L, p = exp(z - lse),
-// f = 1 + floor(p * 65024) in fp32, the leftover of 65536 - sum f added to the
-// lowest-index largest f.
+// Quantised distributions for the host coder (Sec. 3, Eq. 4 made concrete):
+// over K symbols, f_s = 1 + floor(p_s * (2^16 - 2K)) in fp32 with p_s =
+// exp(z_s - lse) and z_s recomputed from h_L in channel order; the leftover
+// 2^16 - sum f goes to the lowest-index largest f_s, so sum f = 2^16 and every
+// f_s >= 1.  Encoder intervals and decoder tables come from the same code and
+// inputs, so they agree bit for bit.
+
+// 256-symbol table of one voxel in one wavefront: lane l ends with the final
+// frequencies of symbols 4l .. 4l+3.
+__device__ __forceinline__ void table256(const float* __restrict__ h, float l, const float* __restrict__ H,
+                                         const float* __restrict__ hb, int C, int lane, uint32_t (&f)[4]) {
+  uint32_t sum = 0, best = 0;
+  int besti = 0;
+  for (int e = 0; e < 4; ++e) {
+    const int s = lane * 4 + e;
+    float z = hb[s];
+    for (int c = 0; c < C; ++c) z = fmaf(H[c * 256 + s], h[c], z);
+    const float p = __expf(z - l);
+    f[e] = 1u + (uint32_t)floorf(p * 65024.0f);
+    sum += f[e];
+    if (f[e] > best) {
+      best = f[e];
+      besti = s;
+    }
+  }
+  for (int o = 32; o > 0; o >>= 1) {
+    sum += (uint32_t)__shfl_xor((int)sum, o);
+    const uint32_t ob = (uint32_t)__shfl_xor((int)best, o);
+    const int oi = __shfl_xor(besti, o);
+    if (ob > best || (ob == best && oi < besti)) {
+      best = ob;
+      besti = oi;
+    }
+  }
+  const uint32_t left = 65536u - sum;
+  for (int e = 0; e < 4; ++e) f[e] += (lane * 4 + e == besti) ? left : 0u;
+}
+
+// 16-symbol table of one voxel over 16 consecutive lanes (s = lane % 16): the
+// stage-1 or stage-2 distribution of the two-stage head.  Hp is the plain
+// [C][32] table of both stages (column col0 + s), emb_row the Emb(S1) row added
+// to h for stage 2 (NULL for stage 1).  Returns f_s.
+__device__ __forceinline__ uint32_t table16(const float* __restrict__ h, const float* __restrict__ emb_row,
+                                            float l, const float* __restrict__ Hp, int col0,
+                                            const float* __restrict__ hb, int C, int s) {
+  float z = hb[col0 + s];
+  for (int c = 0; c < C; ++c) z = fmaf(Hp[c * 32 + col0 + s], emb_row ? h[c] + emb_row[c] : h[c], z);
+  const float p = __expf(z - l);
+  uint32_t f = 1u + (uint32_t)floorf(p * 65504.0f);
+  uint32_t sum = f, best = f;
+  int besti = s;
+  for (int o = 1; o < 16; o <<= 1) {
+    sum += (uint32_t)__shfl_xor((int)sum, o);
+    const uint32_t ob = (uint32_t)__shfl_xor((int)best, o);
+    const int oi = __shfl_xor(besti, o);
+    if (ob > best || (ob == best && oi < besti)) {
+      best = ob;
+      besti = oi;
+    }
+  }
+  return f + (s == besti ? 65536u - sum : 0u);
+}
+
+// exclusive prefix of v over the 16-lane group of this lane
+__device__ __forceinline__ uint32_t excl16(uint32_t v, int s) {
+  uint32_t inc = v;
+  for (int o = 1; o < 16; o <<= 1) {
+    const uint32_t t = (uint32_t)__shfl_up((int)inc, o, 16);
+    if (s >= o) inc += t;
+  }
+  return inc - v;
+}
+
+// One-stage tables [N][256] of one scale: one wavefront per voxel.
 __global__ void __launch_bounds__(256) k_symbol_freqs(const int32_t* __restrict__ count,
                                                       const int32_t* __restrict__ moff, int b,
                                                       int64_t cap_model,
@@ -157,37 +228,102 @@ __global__ void __launch_bounds__(256) k_symbol_freqs(const int32_t* __restrict_
   if (mo + n > cap_model) n = 0;
   const int64_t wstride = (int64_t)gridDim.x * (blockDim.x / 64);
   for (int64_t v = (int64_t)blockIdx.x * (blockDim.x / 64) + (threadIdx.x >> 6); v < n; v += wstride) {
-    const float* h = hL + (mo + v) * C;
-    const float l = lse[mo + v];
     uint32_t f[4];
-    uint32_t sum = 0, best = 0;
-    int besti = 0;
-    for (int e = 0; e < 4; ++e) {
-      const int s = lane * 4 + e;
-      float z = hb[s];
-      for (int c = 0; c < C; ++c) z = fmaf(H[c * 256 + s], h[c], z);
-      const float p = __expf(z - l);
-      f[e] = 1u + (uint32_t)floorf(p * 65024.0f);
-      sum += f[e];
-      if (f[e] > best) {
-        best = f[e];
-        besti = s;
-      }
-    }
-    for (int o = 32; o > 0; o >>= 1) {
-      sum += (uint32_t)__shfl_xor((int)sum, o);
-      const uint32_t ob = (uint32_t)__shfl_xor((int)best, o);
-      const int oi = __shfl_xor(besti, o);
-      if (ob > best || (ob == best && oi < besti)) {
-        best = ob;
-        besti = oi;
-      }
-    }
-    const uint32_t left = 65536u - sum;
+    table256(hL + (mo + v) * C, lse[mo + v], H, hb, C, lane, f);
     uint16_t* dst = out + v * 256 + lane * 4;
-    for (int e = 0; e < 4; ++e) {
-      const int s = lane * 4 + e;
-      dst[e] = (uint16_t)(f[e] + (s == besti ? left : 0u));
+    for (int e = 0; e < 4; ++e) dst[e] = (uint16_t)f[e];
+  }
+}
+
+// One-stage encoder intervals [N][2] = (start, freq) of O_b[v] in its table.
+__global__ void __launch_bounds__(256) k_symbol_intervals(const int32_t* __restrict__ count,
+                                                          const int32_t* __restrict__ moff, int b, int b_lo,
+                                                          int64_t cap_model, const uint8_t* __restrict__ code,
+                                                          const float* __restrict__ hL, int C,
+                                                          const float* __restrict__ H,
+                                                          const float* __restrict__ hb,
+                                                          const float* __restrict__ lse,
+                                                          uint16_t* __restrict__ out) {
+  const int lane = threadIdx.x & 63;
+  const int64_t mo = moff[b];
+  int64_t n = count[b];
+  if (mo + n > cap_model) n = 0;
+  const int64_t wstride = (int64_t)gridDim.x * (blockDim.x / 64);
+  for (int64_t v = (int64_t)blockIdx.x * (blockDim.x / 64) + (threadIdx.x >> 6); v < n; v += wstride) {
+    uint32_t f[4];
+    table256(hL + (mo + v) * C, lse[mo + v], H, hb, C, lane, f);
+    const int o = code[v];
+    const uint32_t mine = f[0] + f[1] + f[2] + f[3];
+    uint32_t inc = mine;  // inclusive prefix over lanes
+    for (int d = 1; d < 64; d <<= 1) {
+      const uint32_t t = (uint32_t)__shfl_up((int)inc, d);
+      if (lane >= d) inc += t;
+    }
+    if (lane == (o >> 2)) {
+      uint32_t st = inc - mine;
+      for (int e = 0; e < (o & 3); ++e) st += f[e];
+      const int64_t ro = mo - moff[b_lo] + v;  // row in the concatenated output
+      out[ro * 2] = (uint16_t)st;
+      out[ro * 2 + 1] = (uint16_t)f[o & 3];
+    }
+  }
+}
+
+// Two-stage tables [N][16] of one scale and stage: 4 voxels per wavefront.
+__global__ void __launch_bounds__(256) k_symbol_freqs16(const int32_t* __restrict__ count,
+                                                        const int32_t* __restrict__ moff, int b, int stage,
+                                                        int64_t cap_model, const float* __restrict__ hL, int C,
+                                                        const float* __restrict__ Hp, const float* __restrict__ hb,
+                                                        const float* __restrict__ emb, const uint8_t* __restrict__ s1,
+                                                        const float* __restrict__ lse, const float* __restrict__ lse2,
+                                                        uint16_t* __restrict__ out) {
+  const int s = threadIdx.x & 15;
+  const int64_t mo = moff[b];
+  int64_t n = count[b];
+  if (mo + n > cap_model) n = 0;
+  const int64_t gstride = (int64_t)gridDim.x * (blockDim.x / 16);
+  for (int64_t v = (int64_t)blockIdx.x * (blockDim.x / 16) + (threadIdx.x >> 4); v < n; v += gstride) {
+    const int64_t pr = mo + v;
+    const float* h = hL + pr * C;
+    const uint32_t f = stage == 1 ? table16(h, nullptr, lse[pr], Hp, 0, hb, C, s)
+                                  : table16(h, emb + (int)s1[pr] * C, lse2[pr], Hp, 16, hb, C, s);
+    out[v * 16 + s] = (uint16_t)f;
+  }
+}
+
+// Two-stage encoder intervals [N][4]: (start, freq) of S1 = O & 15 in the
+// stage-1 table, then of S2 = O >> 4 in the stage-2 table given that S1.
+__global__ void __launch_bounds__(256) k_symbol_intervals16(const int32_t* __restrict__ count,
+                                                            const int32_t* __restrict__ moff, int b, int b_lo,
+                                                            int64_t cap_model, const uint8_t* __restrict__ code,
+                                                            const float* __restrict__ hL, int C,
+                                                            const float* __restrict__ Hp,
+                                                            const float* __restrict__ hb,
+                                                            const float* __restrict__ emb,
+                                                            const float* __restrict__ lse,
+                                                            const float* __restrict__ lse2,
+                                                            uint16_t* __restrict__ out) {
+  const int s = threadIdx.x & 15;
+  const int64_t mo = moff[b];
+  int64_t n = count[b];
+  if (mo + n > cap_model) n = 0;
+  const int64_t gstride = (int64_t)gridDim.x * (blockDim.x / 16);
+  for (int64_t v = (int64_t)blockIdx.x * (blockDim.x / 16) + (threadIdx.x >> 4); v < n; v += gstride) {
+    const int64_t pr = mo + v;
+    const float* h = hL + pr * C;
+    const int o = code[v], a1 = o & 15, a2 = o >> 4;
+    const uint32_t f1 = table16(h, nullptr, lse[pr], Hp, 0, hb, C, s);
+    const uint32_t st1 = excl16(f1, s);
+    const uint32_t f2 = table16(h, emb + a1 * C, lse2[pr], Hp, 16, hb, C, s);
+    const uint32_t st2 = excl16(f2, s);
+    const int64_t ro = mo - moff[b_lo] + v;  // row in the concatenated output
+    if (s == a1) {
+      out[ro * 4] = (uint16_t)st1;
+      out[ro * 4 + 1] = (uint16_t)f1;
+    }
+    if (s == a2) {
+      out[ro * 4 + 2] = (uint16_t)st2;
+      out[ro * 4 + 3] = (uint16_t)f2;
     }
   }
 }
@@ -269,8 +405,33 @@ hipError_t launch_symbol_freqs(Ctx& c, int b, uint16_t* freq) {
   ProfScope ps_(c, RENO_K_OTHER);
   hipLaunchKernelGGL(k_symbol_freqs, dim3(grid_for(c.cap_pts, 4)), dim3(256), 0, c.stream,
                      c.d_count, c.d_moff, b, c.cap_model, c.hlast(), c.p.channels, c.w_head_plain,
-                     c.w_hbias,
-                     c.d_lse, freq);
+                     c.w_hbias, c.d_lse, freq);
+  return hipGetLastError();
+}
+
+hipError_t launch_symbol_freqs16(Ctx& c, int b, int stage, uint16_t* freq) {
+  ProfScope ps_(c, RENO_K_OTHER);
+  hipLaunchKernelGGL(k_symbol_freqs16, dim3(grid_for(c.cap_pts, 16)), dim3(256), 0, c.stream,
+                     c.d_count, c.d_moff, b, stage, c.cap_model, c.hlast(), c.p.channels, c.w_head_plain,
+                     c.w_hbias, c.w_emb, c.d_s1, c.d_lse, c.d_lse2, freq);
+  return hipGetLastError();
+}
+
+hipError_t launch_symbol_intervals(Ctx& c, int b_lo, int b_hi, uint16_t* iv) {
+  ProfScope ps_(c, RENO_K_OTHER);
+  const bool two = c.p.head_mode == RENO_HEAD_TWO_STAGE;
+  // model rows of consecutive scales are consecutive, so each scale's output
+  // starts at its model-row offset relative to b_lo (read on the device)
+  for (int b = b_lo; b <= b_hi; ++b) {
+    if (two)
+      hipLaunchKernelGGL(k_symbol_intervals16, dim3(grid_for(c.cap_pts, 16)), dim3(256), 0, c.stream,
+                         c.d_count, c.d_moff, b, b_lo, c.cap_model, c.lv_code + c.lv(b), c.hlast(),
+                         c.p.channels, c.w_head_plain, c.w_hbias, c.w_emb, c.d_lse, c.d_lse2, iv);
+    else
+      hipLaunchKernelGGL(k_symbol_intervals, dim3(grid_for(c.cap_pts, 4)), dim3(256), 0, c.stream,
+                         c.d_count, c.d_moff, b, b_lo, c.cap_model, c.lv_code + c.lv(b), c.hlast(),
+                         c.p.channels, c.w_head_plain, c.w_hbias, c.d_lse, iv);
+  }
   return hipGetLastError();
 }
 

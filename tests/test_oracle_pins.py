@@ -492,3 +492,18 @@ def test_two_stage_rows_normalised_and_s1_input_path(scan_cache):
     m1b, m2b, _, _, _ = P.model2(b, w, rows=rows, s1=(s1 + 1) % 16)
     np.testing.assert_allclose(m1b, m1, atol=0)
     assert np.abs(m2b - m2).max() > 1e-3
+
+
+def test_freqs_rule_16_symbols_worked_values():
+    """f_s = 1 + floor(p_s * (2^16 - 2K)) in fp32, leftover to the lowest-index
+    largest: hand-computed for K = 16."""
+    p = np.zeros(16)
+    p[:3] = [0.5, 0.25, 0.25]
+    f = oracle.freqs_from_probs(p, 16)[0]
+    # 1 + floor(0.5 * 65504) = 32753, 1 + floor(0.25 * 65504) = 16377, 13 ones: sum 65520
+    assert list(f[:3]) == [32753 + 16, 16377, 16377] and list(f[3:]) == [1] * 13
+    u = oracle.freqs_from_probs(np.full(16, 1 / 16), 16)[0]
+    assert list(u) == [4095 + 16] + [4095] * 15          # 16 * 4095 = 65520
+    # ties for the largest go to the lowest index; the total is always 2^16
+    t = oracle.freqs_from_probs(np.array([0.1] * 2 + [0.4, 0.4] + [0.0] * 12), 16)[0]
+    assert t[2] > t[3] and t.sum() == 65536 and t.min() >= 1
