@@ -219,6 +219,125 @@ class Codec:
         self.dec.close()
 
 
+class EndToEnd:
+    """True end-to-end coding of one frame: GPU pyramid + model, the symbol
+    intervals (encoder) or tables (decoder) copied to pinned host memory, and
+    host rANS with one stream per scale (and per stage with the two-stage
+    head); the decoder decodes each scale's symbols before it expands them."""
+
+    def __init__(self, reno, torch, cfg, pts, M, cap_model, stream, w_np, two_stage, threads=8):
+        from concurrent.futures import ThreadPoolExecutor
+        self.reno, self.torch, self.stream, self.two = reno, torch, stream, two_stage
+        self.B, self.b0 = cfg.bit_depth, cfg.min_bit_depth
+        wd = reno.weights_to_device(w_np)
+        mk = lambda: reno.Context(M, self.B, self.b0, cfg.range_m, cfg.channels, cfg.layers,
+                                  max_model_voxels=cap_model, stream=stream, two_stage=two_stage)
+        with torch.cuda.stream(stream):
+            self.enc, self.dec = mk(), mk()
+            self.enc.set_weights(wd)
+            self.dec.set_weights(wd)
+        self.pts = pts
+        per = 4 if two_stage else 2
+        self.iv_host = torch.empty((cap_model, per), dtype=torch.int16, pin_memory=True)
+        k = 16 if two_stage else 256
+        self.tab_host = torch.empty((M, k), dtype=torch.int16, pin_memory=True)
+        self.code_host = torch.empty(M, dtype=torch.uint8, pin_memory=True)
+        # decoded codes of consecutive scales alternate between two buffers; S1 has its own
+        self.code_dev = [torch.empty(M, dtype=torch.uint8, device=pts.device) for _ in range(3)]
+        self.pool = ThreadPoolExecutor(threads)
+
+    def encode(self):
+        """-> (bitstream dict, N_b per scale, base xyz, base codes)."""
+        reno, torch, enc, B, b0 = self.reno, self.torch, self.enc, self.B, self.b0
+        with torch.cuda.stream(self.stream):
+            enc.build_pyramid(self.pts, B)
+            enc.predict_probs(reno.RENO_ALL_SCALES)
+            counts = enc.scale_counts()                       # synchronises once
+            nm = int(counts[b0 + 1:B].sum())
+            iv = enc.symbol_intervals(reno.RENO_ALL_SCALES)
+            self.iv_host[:nm].copy_(iv, non_blocking=True)
+            base_xyz, _ = enc.coords(b0)
+            base_codes = enc.occupancy_codes(b0)
+            self.stream.synchronize()
+        ivh = self.iv_host.numpy().view(np.uint16)
+        jobs, off = [], 0
+        for b in range(b0 + 1, B):
+            rows = ivh[off:off + counts[b]]
+            if self.two:
+                jobs += [(b, 0, rows, 4, 0), (b, 1, rows, 4, 2)]
+            else:
+                jobs.append((b, 0, rows, 2, 0))
+            off += counts[b]
+        words = dict(zip([(j[0], j[1]) for j in jobs],
+                         self.pool.map(lambda j: reno.rans_encode_intervals(j[2], j[3], j[4]), jobs)))
+        return words, counts, base_xyz, base_codes
+
+    def decode(self, words, counts, base_xyz, base_codes):
+        reno, torch, dec, B, b0 = self.reno, self.torch, self.dec, self.B, self.b0
+        with torch.cuda.stream(self.stream):
+            dec.set_base(B, base_xyz, base_codes)
+            prev = None
+            for b in range(b0 + 1, B):
+                n = int(counts[b])
+                dec.expand(b - 1, prev)
+                dec.predict_probs(b)
+                if self.two:
+                    t1 = dec.symbol_freqs16(b, 1)
+                    self.tab_host[:n].copy_(t1, non_blocking=True)
+                    self.stream.synchronize()
+                    s1 = reno.rans_decode(words[(b, 0)], self.tab_host[:n].numpy().view(np.uint16), n)
+                    self.code_host[:n].copy_(torch.from_numpy(s1))
+                    s1_dev = self.code_dev[2][:n]
+                    s1_dev.copy_(self.code_host[:n], non_blocking=True)
+                    dec.predict_second(b, s1_dev)
+                    t2 = dec.symbol_freqs16(b, 2)
+                    self.tab_host[:n].copy_(t2, non_blocking=True)
+                    self.stream.synchronize()
+                    s2 = reno.rans_decode(words[(b, 1)], self.tab_host[:n].numpy().view(np.uint16), n)
+                    codes = s1 | (s2 << 4)
+                else:
+                    t = dec.symbol_freqs(b)
+                    self.tab_host[:n].copy_(t, non_blocking=True)
+                    self.stream.synchronize()
+                    codes = reno.rans_decode(words[(b, 0)], self.tab_host[:n].numpy().view(np.uint16), n)
+                self.code_host[:n].copy_(torch.from_numpy(codes))
+                cd = self.code_dev[b & 1][:n]
+                cd.copy_(self.code_host[:n], non_blocking=True)
+                prev = cd
+            dec.expand(B - 1, prev)
+            self.stream.synchronize()
+
+    def run(self, frames, check=True):
+        """Mean seconds per frame of encode and of decode, coded bits."""
+        reno, torch = self.reno, self.torch
+        te = td = 0.0
+        bits = None
+        for i in range(frames + 1):                        # first pass: warm-up
+            t = time.perf_counter()
+            words, counts, bx, bc = self.encode()
+            t1 = time.perf_counter()
+            self.decode(words, counts, bx, bc)
+            t2 = time.perf_counter()
+            if i:
+                te += t1 - t
+                td += t2 - t1
+            if check and i in (0, frames):
+                with torch.cuda.stream(self.stream):
+                    a, _ = self.dec.coords(self.B)
+                    e, _ = self.enc.coords(self.B)
+                    same = bool(torch.equal(a, e))
+                if not same:
+                    log("end-to-end: decoded frame differs from the input")
+                    sys.exit(1)
+            bits = 32 + int(counts[self.b0]) * (3 * self.b0 + 8) + sum(32 * w.size for w in words.values())
+        return te / frames, td / frames, bits
+
+    def close(self):
+        self.pool.shutdown()
+        self.enc.close()
+        self.dec.close()
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawTextHelpFormatter)
     ap.add_argument("--gpus", type=int, default=1)
@@ -229,6 +348,8 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-two-stage", action="store_true", help="skip the two-stage head measurement")
     ap.add_argument("--no-bf16x3", action="store_true", help="skip the split-bf16 precision measurement")
+    ap.add_argument("--e2e-frames", type=int, default=20,
+                    help="frames for the end-to-end (GPU + host rANS) measurement (0 to skip)")
     ap.add_argument("--stream-config", default="stream10_hdl64_b14",
                     help="multi-frame workload measured with frames in flight on several streams")
     ap.add_argument("--streams", default="1,2,4",
@@ -352,6 +473,23 @@ def main():
         log("bf16x3", bfx)
         bc.close()
 
+    # ---- end to end: GPU model + host rANS per scale, both heads ----
+    e2e = None
+    if args.e2e_frames > 0:
+        e2e = {}
+        for name, two, wts in (("one_stage", False, w_np),
+                               ("two_stage", True, gen_weights(C, L, seed=cfg.weight_seed, two_stage=True))):
+            ee = EndToEnd(reno, torch, cfg, pts, M, cap_model, stream, wts, two)
+            te, td, bits = ee.run(args.e2e_frames)
+            e2e[name] = {"encode_frames_per_s": round(1.0 / te, 2), "decode_frames_per_s": round(1.0 / td, 2),
+                         "encode_ms": round(1000 * te, 3), "decode_ms": round(1000 * td, 3),
+                         "coded_bits_per_point": round(bits / M, 4)}
+            log("end-to-end", name, e2e[name])
+            ee.close()
+        e2e["note"] = ("wall-clock per frame: GPU pyramid + model + symbol intervals (encoder) or tables "
+                       "(decoder), pinned copies, host rANS with one stream per scale (and stage); the decoder "
+                       "decodes each scale before expanding it; encoder streams coded on 8 host threads")
+
     # ---- multi-frame throughput: F different frames, each with its own encoder
     # and decoder context and captured step, replayed round-robin over S
     # streams so that frames are in flight together ----
@@ -463,6 +601,7 @@ def main():
         "kernels": breakdown,
         "two_stage_head": two,
         "precision_bf16x3": bfx,
+        "end_to_end": e2e,
         "multi_frame": multi,
     }
     print(json.dumps(out), flush=True)

@@ -159,6 +159,9 @@ reno_status reno_expand(reno_ctx* ctx, int scale, const uint8_t* codes);
 
 /* Number of voxels of a scale (synchronises). */
 reno_status reno_num_voxels(reno_ctx* ctx, int scale, int64_t* n_host);
+/* N_b of every scale in one copy: counts_host[b] for b = 0 .. RENO_MAX_BIT_DEPTH
+ * (0 for scales not built); synchronises. */
+reno_status reno_scale_counts(reno_ctx* ctx, int64_t* counts_host);
 /* Voxels of a scale: xyz int32 [N][3] and/or Morton keys uint64 [N] (either may be NULL). */
 reno_status reno_coords(reno_ctx* ctx, int scale, int32_t* xyz, uint64_t* keys);
 /* Occupancy codes O_scale uint8 [N_scale], b0 <= scale < B (Eq. 1). */

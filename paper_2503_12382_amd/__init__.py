@@ -24,6 +24,7 @@ RENO_E_HIP = -4
 RENO_E_CAPACITY = -5
 RENO_E_INPUT = -6
 RENO_MAX_LAYERS = 8
+RENO_MAX_BIT_DEPTH = 21
 RENO_ALL_SCALES = -1
 RENO_HEAD_ONE_STAGE = 0
 RENO_HEAD_TWO_STAGE = 1
@@ -71,6 +72,7 @@ _SIGS = {
     "reno_set_base": (_int, [_vp, _int, _vp, _vp, _i64]),
     "reno_expand": (_int, [_vp, _int, _vp]),
     "reno_num_voxels": (_int, [_vp, _int, ctypes.POINTER(_i64)]),
+    "reno_scale_counts": (_int, [_vp, _vp]),
     "reno_coords": (_int, [_vp, _int, _vp, _vp]),
     "reno_occupancy_codes": (_int, [_vp, _int, _vp]),
     "reno_parent_rows": (_int, [_vp, _int, _vp]),
@@ -279,6 +281,12 @@ class Context:
         out = self._empty((max(n, 1), 27), self.torch.int32)
         self._check(lib().reno_neighbor_map(self._h, scale, _ptr(out)))
         return out[:n]
+
+    def scale_counts(self) -> np.ndarray:
+        """N_b of every scale (index b), one synchronising copy."""
+        out = np.zeros(RENO_MAX_BIT_DEPTH + 1, np.int64)
+        self._check(lib().reno_scale_counts(self._h, out.ctypes.data_as(_vp)))
+        return out
 
     def memory_info(self) -> dict:
         """Sizes fixed at create time: hash slots, look-back status words,

@@ -337,6 +337,17 @@ reno_status reno_expand(reno_ctx* c, int scale, const uint8_t* codes) {
   return RENO_OK;
 }
 
+reno_status reno_scale_counts(reno_ctx* c, int64_t* counts_host) {
+  if (!c || !counts_host) return fail(c, RENO_E_INVALID, "null argument");
+  RENO_HIP(c, hipMemcpyAsync(c->h_count, c->d_count, sizeof(int32_t) * reno::NLEV,
+                             hipMemcpyDeviceToHost, c->stream));
+  reno_status s = sync_check(c);
+  if (s != RENO_OK) return s;
+  for (int b = 0; b < reno::NLEV; ++b)
+    counts_host[b] = (c->B > 0 && has(c->have_level, b)) ? (int64_t)c->h_count[b] : 0;
+  return RENO_OK;
+}
+
 reno_status reno_num_voxels(reno_ctx* c, int scale, int64_t* n_host) {
   if (!c || !n_host) return fail(c, RENO_E_INVALID, "null argument");
   if (!has(c->have_level, scale)) return fail(c, RENO_E_STATE, "scale not built");
