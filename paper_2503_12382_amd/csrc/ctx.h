@@ -81,7 +81,7 @@ struct Ctx {
   float* d_lse = nullptr;       // [cap_model] (two-stage head: stage 1)
   float* d_lse2 = nullptr;      // [cap_model] stage 2 of the two-stage head
   uint8_t* d_s1 = nullptr;      // [cap_model] S1 that stage 2 was evaluated with
-  double* d_partial = nullptr;  // [NLEV][ceil(cap_pts / 1024)] per-chunk bit sums
+  double* d_partial = nullptr;  // [NLEV][ceil(cap_pts / 64)] per-chunk bit sums
   double* d_total = nullptr;    // [NLEV]
   double* h_total = nullptr;    // pinned host mirror [NLEV]
   int32_t* h_count = nullptr;   // pinned host mirror [NLEV]
@@ -94,6 +94,7 @@ struct Ctx {
   float* w_hbias = nullptr;
   float* w_head_plain = nullptr;  // [C][256] as given (two-stage: [C][H1 | H2]), for code lengths
   float* w_emb = nullptr;         // [16][C] Emb(S1) of the two-stage head
+  float* w_head_t = nullptr;      // head transposed, one row per symbol: [256][C] (two-stage: [H1^T; H2^T])
   bool have_weights = false;
 
   // frame state

@@ -154,6 +154,14 @@ __global__ void k_pack_head_bf(const float* __restrict__ H, int C, int NS, uint3
   }
 }
 
+// Transposes H [C][NS] into rows row0 .. row0+NS-1 of a [*][C] table.
+__global__ void k_transpose_head(const float* __restrict__ H, int C, int NS, int row0, float* __restrict__ out) {
+  for (int i = blockIdx.x * blockDim.x + threadIdx.x; i < C * NS; i += gridDim.x * blockDim.x) {
+    const int c = i / NS, s = i % NS;
+    out[(size_t)(row0 + s) * C + c] = H[i];
+  }
+}
+
 // Copies H [C][16] into columns col0 .. col0+15 of a [C][32] table.
 __global__ void k_put_cols16(const float* __restrict__ H, int C, int col0, float* __restrict__ out) {
   for (int i = blockIdx.x * blockDim.x + threadIdx.x; i < C * 16; i += gridDim.x * blockDim.x)
@@ -800,6 +808,8 @@ hipError_t launch_pack_weights(Ctx& c, const reno_weights& w) {
     hipLaunchKernelGGL(k_put_cols16, dim3(2), dim3(256), 0, c.stream, w.head1_w, C, 0, c.w_head_plain);
     hipLaunchKernelGGL(k_put_cols16, dim3(2), dim3(256), 0, c.stream, w.head2_w, C, 16, c.w_head_plain);
     hipLaunchKernelGGL(k_copy_f32, dim3(2), dim3(256), 0, c.stream, w.emb_s1, c.w_emb, 16 * C);
+    hipLaunchKernelGGL(k_transpose_head, dim3(2), dim3(256), 0, c.stream, w.head1_w, C, 16, 0, c.w_head_t);
+    hipLaunchKernelGGL(k_transpose_head, dim3(2), dim3(256), 0, c.stream, w.head2_w, C, 16, 16, c.w_head_t);
   } else {
     if (bf)
       hipLaunchKernelGGL(k_pack_head_bf, dim3(16), dim3(256), 0, c.stream, w.head_w, C, 256,
@@ -809,6 +819,7 @@ hipError_t launch_pack_weights(Ctx& c, const reno_weights& w) {
     hipLaunchKernelGGL(k_copy_f32, dim3(1), dim3(256), 0, c.stream, w.head_b, c.w_hbias, 256);
     hipLaunchKernelGGL(k_copy_f32, dim3(32), dim3(256), 0, c.stream, w.head_w, c.w_head_plain,
                        C * 256);
+    hipLaunchKernelGGL(k_transpose_head, dim3(32), dim3(256), 0, c.stream, w.head_w, C, 256, 0, c.w_head_t);
   }
   return hipGetLastError();
 }

@@ -13,131 +13,140 @@ constexpr float INV_LN2 = 1.4426950408889634f;
 // (fp32, channel order).  Two-stage head (TWO): with a = O & 15, s = O >> 4,
 // bits_v = ((lse1_v - z1_a) + (lse2_v - z2_s)) / ln 2, z1_a = hb1[a] +
 // sum_c H1[c][a] h[c], z2_s = hb2[s] + sum_c H2[c][s] (h[c] + E[a][c]).
-// Block (chunk, scale) handles 1024 voxels of one scale with the head staged
-// in LDS; per-chunk sums in double are reduced in chunk order by the last
-// block of the scale to finish (deterministic).
-constexpr int CL_THREADS = 256;
-constexpr int CL_CHUNK = 1024;
+// Blocks stage the transposed head HT [NS][C] in LDS once (rows padded by one
+// word so that lanes reading different symbols hit different banks), then
+// waves take chunks of 64 voxels (one per lane) over all scales of the
+// launch.  Each chunk's sum in double goes to partial[b][chunk], and a second
+// one-wave-per-scale kernel sums them in chunk order (lane-strided, then a
+// fixed xor tree): deterministic.  The kernel boundary publishes the partials;
+// a device-scope fence inside the kernel would write back the whole L2 of the
+// XCD and costs more than the second launch.
+constexpr int CL_THREADS = 1024;
+constexpr int CL_CHUNK = 64;
 
 template <int C, bool TWO>
 __global__ void __launch_bounds__(CL_THREADS) k_code_length(
-    int b_lo, int b0, const int32_t* __restrict__ count, const int32_t* __restrict__ moff,
+    int b_lo, int nsc, int b0, const int32_t* __restrict__ count, const int32_t* __restrict__ moff,
     int64_t cap_pts, int64_t cap_model, const uint8_t* __restrict__ lv_code,
-    const float* __restrict__ hL, const float* __restrict__ H, const float* __restrict__ hb,
+    const float* __restrict__ hL, const float* __restrict__ HT, const float* __restrict__ hb,
     const float* __restrict__ lse, const float* __restrict__ lse2, const float* __restrict__ emb,
-    float* __restrict__ bits_out, double* partial, int max_chunks, double* total, uint32_t* done) {
-  constexpr int NS = TWO ? 32 : 256;  // columns of the plain head table
-  __shared__ float s_H[C * NS];
+    float* __restrict__ bits_out, double* partial, int max_chunks) {
+  constexpr int NS = TWO ? 32 : 256;
+  constexpr int RS = C + 1;  // padded LDS row
+  __shared__ float s_HT[NS * RS];
   __shared__ float s_hb[NS];
   __shared__ float s_emb[TWO ? 16 * C : 1];
-  __shared__ double s_red[CL_THREADS / 64];
-  __shared__ bool s_last;
-  const int b = b_lo + blockIdx.y;
-  const int64_t mo = moff[b];
-  int64_t n = count[b];
-  if (mo + n > cap_model) n = 0;  // capacity overflow, latched where the size was made
-  const int64_t nchunks = (n + CL_CHUNK - 1) / CL_CHUNK;
-  if (nchunks == 0) {
-    if (blockIdx.x == 0 && threadIdx.x == 0) total[b] = 0.0;
-    return;
+  __shared__ int64_t s_cpre[NLEV + 1];  // chunk prefix over the launch's scales
+  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+  if (tid == 0) {
+    int64_t acc = 0;
+    for (int i = 0; i < nsc; ++i) {
+      const int b = b_lo + i;
+      int64_t n = count[b];
+      if (moff[b] + n > cap_model) n = 0;  // capacity overflow, latched where the size was made
+      s_cpre[i] = acc;
+      acc += (n + CL_CHUNK - 1) / CL_CHUNK;
+    }
+    s_cpre[nsc] = acc;
   }
-  if ((int64_t)blockIdx.x >= nchunks) return;
-  if constexpr (TWO) {  // small tables: plain strided copies
-    for (int i = threadIdx.x; i < C * NS; i += CL_THREADS) s_H[i] = H[i];
-    for (int i = threadIdx.x; i < 16 * C; i += CL_THREADS) s_emb[i] = emb[i];
-    if (threadIdx.x < NS) s_hb[threadIdx.x] = hb[threadIdx.x];
-  } else {  // stage the head in LDS, every load of a thread issued before its stores
-    constexpr int PER = C * 256 / 4 / CL_THREADS;
-    float4 v[PER];
-    const float4* src = reinterpret_cast<const float4*>(H);
+  {  // staging: every load of a thread issued before its stores
+    constexpr int PER = (NS * C + CL_THREADS - 1) / CL_THREADS;
+    float t[PER];
 #pragma unroll
-    for (int i = 0; i < PER; ++i) v[i] = src[i * CL_THREADS + threadIdx.x];
-    const float hbv = hb[threadIdx.x];
+    for (int k = 0; k < PER; ++k) {
+      const int i = k * CL_THREADS + tid;
+      t[k] = i < NS * C ? HT[i] : 0.0f;
+    }
 #pragma unroll
-    for (int i = 0; i < PER; ++i) reinterpret_cast<float4*>(s_H)[i * CL_THREADS + threadIdx.x] = v[i];
-    s_hb[threadIdx.x] = hbv;
+    for (int k = 0; k < PER; ++k) {
+      const int i = k * CL_THREADS + tid;
+      if (i < NS * C) s_HT[(i / C) * RS + (i % C)] = t[k];
+    }
   }
+  for (int i = tid; i < NS; i += CL_THREADS) s_hb[i] = hb[i];
+  if constexpr (TWO)
+    for (int i = tid; i < 16 * C; i += CL_THREADS) s_emb[i] = emb[i];
   __syncthreads();
-  const int64_t out0 = mo - moff[b_lo];
-  const uint8_t* code = lv_code + (int64_t)(b - b0) * cap_pts;
-  double acc = 0.0;
-  constexpr int PV = CL_CHUNK / CL_THREADS;  // voxels per thread
-  int64_t vv[PV];
-  int oo[PV];
-  float ll[PV], ll2[PV];
+  const int64_t nchunks_all = s_cpre[nsc];
+  const int64_t waves = (int64_t)gridDim.x * (CL_THREADS / 64);
+  for (int64_t ch = (int64_t)blockIdx.x * (CL_THREADS / 64) + w; ch < nchunks_all; ch += waves) {
+    int si = 0;
+    while (si + 1 < nsc && s_cpre[si + 1] <= ch) ++si;
+    const int b = b_lo + si;
+    const int64_t mo = moff[b];
+    const int64_t n = count[b];
+    const int64_t cib = ch - s_cpre[si];  // chunk index inside the scale
+    const int64_t nch = s_cpre[si + 1] - s_cpre[si];
+    const int64_t v = cib * CL_CHUNK + lane;
+    const int64_t vv = v < n ? v : n - 1;  // clamped: every load is issued
+    const int o = lv_code[(int64_t)(b - b0) * cap_pts + vv];
+    const float l1 = lse[mo + vv];
+    const float l2 = TWO ? lse2[mo + vv] : 0.0f;
+    float h[C];
+    const float4* hr = reinterpret_cast<const float4*>(hL + (mo + vv) * C);
 #pragma unroll
-  for (int i = 0; i < PV; ++i) {  // clamped rows: every load is issued up front
-    const int64_t v = (int64_t)blockIdx.x * CL_CHUNK + i * CL_THREADS + threadIdx.x;
-    vv[i] = v < n ? v : n - 1;
-    oo[i] = code[vv[i]];
-    ll[i] = lse[mo + vv[i]];
-    ll2[i] = TWO ? lse2[mo + vv[i]] : 0.0f;
-  }
-#pragma unroll
-  for (int i = 0; i < PV; ++i) {
-    const int64_t v = (int64_t)blockIdx.x * CL_CHUNK + i * CL_THREADS + threadIdx.x;
-    const int o = oo[i];
-    const float4* h = reinterpret_cast<const float4*>(hL + (mo + vv[i]) * C);
+    for (int c4 = 0; c4 < C / 4; ++c4) {
+      const float4 t = hr[c4];
+      h[4 * c4] = t.x;
+      h[4 * c4 + 1] = t.y;
+      h[4 * c4 + 2] = t.z;
+      h[4 * c4 + 3] = t.w;
+    }
     float bt;
     if constexpr (TWO) {
       const int a1 = o & 15, a2 = 16 + (o >> 4);
       float z1 = s_hb[a1], z2 = s_hb[a2];
 #pragma unroll
-      for (int c4 = 0; c4 < C / 4; ++c4) {
-        const float4 hv = h[c4];
-        const float hc[4] = {hv.x, hv.y, hv.z, hv.w};
-#pragma unroll
-        for (int j = 0; j < 4; ++j) {
-          const int ch = 4 * c4 + j;
-          z1 = fmaf(s_H[ch * NS + a1], hc[j], z1);
-          z2 = fmaf(s_H[ch * NS + a2], hc[j] + s_emb[a1 * C + ch], z2);
-        }
+      for (int c = 0; c < C; ++c) {
+        z1 = fmaf(s_HT[a1 * RS + c], h[c], z1);
+        z2 = fmaf(s_HT[a2 * RS + c], h[c] + s_emb[a1 * C + c], z2);
       }
-      bt = ((ll[i] - z1) + (ll2[i] - z2)) * INV_LN2;
+      bt = ((l1 - z1) + (l2 - z2)) * INV_LN2;
     } else {
       float z = s_hb[o];
 #pragma unroll
-      for (int c4 = 0; c4 < C / 4; ++c4) {
-        const float4 hv = h[c4];
-        z = fmaf(s_H[(4 * c4 + 0) * 256 + o], hv.x, z);
-        z = fmaf(s_H[(4 * c4 + 1) * 256 + o], hv.y, z);
-        z = fmaf(s_H[(4 * c4 + 2) * 256 + o], hv.z, z);
-        z = fmaf(s_H[(4 * c4 + 3) * 256 + o], hv.w, z);
-      }
-      bt = (ll[i] - z) * INV_LN2;
+      for (int c = 0; c < C; ++c) z = fmaf(s_HT[o * RS + c], h[c], z);
+      bt = (l1 - z) * INV_LN2;
     }
+    double acc = 0.0;
     if (v < n) {
-      if (bits_out) bits_out[out0 + v] = bt;
-      acc += (double)bt;
+      if (bits_out) bits_out[mo - moff[b_lo] + v] = bt;
+      acc = (double)bt;
     }
+    for (int d = 32; d > 0; d >>= 1) acc += __shfl_xor(acc, d);
+    if (lane == 0) partial[(int64_t)b * max_chunks + cib] = acc;
   }
-  for (int o = 32; o > 0; o >>= 1) acc += __shfl_xor(acc, o);
-  if ((threadIdx.x & 63) == 0) s_red[threadIdx.x >> 6] = acc;
-  __syncthreads();
-  if (threadIdx.x == 0) {
-    double t = 0.0;
-    for (int i = 0; i < CL_THREADS / 64; ++i) t += s_red[i];
-    partial[(int64_t)b * max_chunks + blockIdx.x] = t;
-    __threadfence();
-    const uint32_t prev = atomicAdd(&done[b], 1u);
-    s_last = prev == (uint32_t)(nchunks - 1);
-  }
-  __syncthreads();
-  if (s_last && threadIdx.x < 64) {
-    // the first wave sums the chunk partials: lane i takes chunks i, i+64, ...
-    // in order, then a fixed xor tree; the same result whatever the arrival order
-    __threadfence();
-    const int lane = threadIdx.x;
-    double t = 0.0;
-    for (int64_t i = lane; i < nchunks; i += 64)
-      t += __hip_atomic_load(&partial[(int64_t)b * max_chunks + i], __ATOMIC_RELAXED,
-                             __HIP_MEMORY_SCOPE_AGENT);
-    for (int o = 32; o > 0; o >>= 1) t += __shfl_xor(t, o);
-    if (lane == 0) {
-      total[b] = t;
-      done[b] = 0u;  // ready for the next call
+}
+
+// Per-scale totals from the chunk partials: one block of 256 threads per
+// scale; thread t adds chunks t, t+256, ... in order (loads issued in batches
+// before the adds), then a fixed tree: xor within each wave, waves in order.
+__global__ void __launch_bounds__(256) k_bits_total(int b_lo, const int32_t* __restrict__ count,
+                                                    const int32_t* __restrict__ moff, int64_t cap_model,
+                                                    const double* __restrict__ partial, int max_chunks,
+                                                    double* __restrict__ total) {
+  __shared__ double s_w[4];
+  const int b = b_lo + blockIdx.x, tid = threadIdx.x;
+  int64_t n = count[b];
+  if (moff[b] + n > cap_model) n = 0;
+  const int64_t nch = (n + CL_CHUNK - 1) / CL_CHUNK;
+  const double* p = partial + (int64_t)b * max_chunks;
+  double t = 0.0;
+  constexpr int BATCH = 8;
+  for (int64_t i0 = tid; i0 < nch; i0 += 256 * BATCH) {
+    double x[BATCH];
+#pragma unroll
+    for (int k = 0; k < BATCH; ++k) {
+      const int64_t i = i0 + (int64_t)k * 256;
+      x[k] = i < nch ? p[i] : 0.0;
     }
+#pragma unroll
+    for (int k = 0; k < BATCH; ++k) t += x[k];
   }
+  for (int d = 32; d > 0; d >>= 1) t += __shfl_xor(t, d);
+  if ((tid & 63) == 0) s_w[tid >> 6] = t;
+  __syncthreads();
+  if (tid == 0) total[b] = (s_w[0] + s_w[1]) + (s_w[2] + s_w[3]);
 }
 
 // Quantised distributions for the host coder (Sec. 3, Eq. 4 made concrete):
@@ -384,11 +393,15 @@ unsigned grid_for(int64_t cap, int per_block) {
 template <int C, bool TWO>
 void run_code_length(Ctx& c, int b_lo, int b_hi, float* bits) {
   const int max_chunks = (int)((c.cap_pts + CL_CHUNK - 1) / CL_CHUNK);
-  const dim3 grid(max_chunks, b_hi - b_lo + 1);
-  hipLaunchKernelGGL((k_code_length<C, TWO>), grid, dim3(CL_THREADS), 0, c.stream, b_lo, c.b0(),
-                     c.d_count, c.d_moff, c.cap_pts, c.cap_model, c.lv_code, c.hlast(),
-                     c.w_head_plain, c.w_hbias, c.d_lse, c.d_lse2, c.w_emb, bits, c.d_partial,
-                     max_chunks, c.d_total, c.d_ticket + TK_RED);
+  // one block per CU at most; small batches need fewer
+  const int64_t chunks = (int64_t)(b_hi - b_lo + 1) * max_chunks;
+  const int blocks = (int)std::min<int64_t>(256, (chunks + CL_THREADS / 64 - 1) / (CL_THREADS / 64));
+  hipLaunchKernelGGL((k_code_length<C, TWO>), dim3(blocks), dim3(CL_THREADS), 0, c.stream, b_lo,
+                     b_hi - b_lo + 1, c.b0(), c.d_count, c.d_moff, c.cap_pts, c.cap_model, c.lv_code,
+                     c.hlast(), c.w_head_t, c.w_hbias, c.d_lse, c.d_lse2, c.w_emb, bits, c.d_partial,
+                     max_chunks);
+  hipLaunchKernelGGL(k_bits_total, dim3(b_hi - b_lo + 1), dim3(256), 0, c.stream, b_lo, c.d_count, c.d_moff,
+                     (int64_t)c.cap_model, c.d_partial, max_chunks, c.d_total);
 }
 
 hipError_t launch_code_length(Ctx& c, int b_lo, int b_hi, float* bits) {
