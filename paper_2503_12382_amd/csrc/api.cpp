@@ -53,7 +53,7 @@ void free_all(Ctx* c) {
                   c->lv_feat, c->d_count,   c->d_moff,   c->d_err,    c->d_hist,    c->d_ticket,
                   c->d_status, c->d_hash,   c->h_a,      c->h_b,      c->d_nbr,     c->d_lse,
                   c->d_partial, c->d_total, c->w_head,   c->w_hbias,  c->w_head_plain,
-                  c->d_lse2,    c->w_emb,   c->d_s1,     c->w_head_t};
+                  c->d_lse2,    c->w_emb,   c->d_s1,     c->w_head_t, c->d_perm};
   for (void* p : ptrs)
     if (p) (void)hipFree(p);
   for (int l = 0; l < RENO_MAX_LAYERS; ++l) {
@@ -189,6 +189,7 @@ reno_status reno_create(const reno_params* p, void* hip_stream, reno_ctx** out) 
   A(dalloc(&c->d_nbr, (size_t)cap_model * reno::NBR_STRIDE, &c->device_bytes));
   A(dalloc(&c->d_lse, (size_t)cap_model, &c->device_bytes));
   A(dalloc(&c->d_lse2, (size_t)cap_model, &c->device_bytes));
+  A(dalloc(&c->d_perm, (size_t)cap_model, &c->device_bytes));
   A(dalloc(&c->d_s1, (size_t)cap_model, &c->device_bytes));
   A(dalloc(&c->d_partial, (size_t)reno::NLEV * ((c->cap_pts + 63) / 64), &c->device_bytes));
   A(dalloc(&c->d_total, reno::NLEV, &c->device_bytes));

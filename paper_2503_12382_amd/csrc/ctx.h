@@ -78,6 +78,7 @@ struct Ctx {
   float* h_a = nullptr;         // [cap_model][C]
   float* h_b = nullptr;
   int32_t* d_nbr = nullptr;     // [cap_model][NBR_STRIDE]
+  int32_t* d_perm = nullptr;    // [cap_model] tile order of the conv layers after the first
   float* d_lse = nullptr;       // [cap_model] (two-stage head: stage 1)
   float* d_lse2 = nullptr;      // [cap_model] stage 2 of the two-stage head
   uint8_t* d_s1 = nullptr;      // [cap_model] S1 that stage 2 was evaluated with
