@@ -477,9 +477,9 @@ def main():
     e2e = None
     if args.e2e_frames > 0:
         e2e = {}
-        for name, two, wts in (("one_stage", False, w_np),
-                               ("two_stage", True, gen_weights(C, L, seed=cfg.weight_seed, two_stage=True))):
-            ee = EndToEnd(reno, torch, cfg, pts, M, cap_model, stream, wts, two)
+        for name, is_two, wts in (("one_stage", False, w_np),
+                                  ("two_stage", True, gen_weights(C, L, seed=cfg.weight_seed, two_stage=True))):
+            ee = EndToEnd(reno, torch, cfg, pts, M, cap_model, stream, wts, is_two)
             te, td, bits = ee.run(args.e2e_frames)
             e2e[name] = {"encode_frames_per_s": round(1.0 / te, 2), "decode_frames_per_s": round(1.0 / td, 2),
                          "encode_ms": round(1000 * te, 3), "decode_ms": round(1000 * td, 3),
