@@ -39,7 +39,10 @@ class OrcWeights(ctypes.Structure):
                 ("head_mode", ctypes.c_int), ("pad2", ctypes.c_int),
                 ("head1_w", ctypes.c_void_p), ("head1_b", ctypes.c_void_p),
                 ("emb_s1", ctypes.c_void_p), ("head2_w", ctypes.c_void_p),
-                ("head2_b", ctypes.c_void_p)]
+                ("head2_b", ctypes.c_void_p),
+                ("model_mode", ctypes.c_int), ("pad3", ctypes.c_int),
+                ("emb_o", ctypes.c_void_p), ("emb_d", ctypes.c_void_p),
+                ("top_w", ctypes.c_void_p * 4), ("top_b", ctypes.c_void_p * 4)]
 
 
 def lib():
@@ -127,6 +130,18 @@ class _W:
                 a = np.ascontiguousarray(w[name], dtype=np.float32)
                 self.arrays.append(a)
                 setattr(s, name, a.ctypes.data)
+        if "top_w" in w:  # the full predictor
+            s.model_mode = 1
+            for name in ("emb_o", "emb_d"):
+                a = np.ascontiguousarray(w[name], dtype=np.float32)
+                self.arrays.append(a)
+                setattr(s, name, a.ctypes.data)
+            for i in range(4):
+                tw = np.ascontiguousarray(w["top_w"][i], dtype=np.float32)
+                tb = np.ascontiguousarray(w["top_b"][i], dtype=np.float32)
+                self.arrays += [tw, tb]
+                s.top_w[i] = tw.ctypes.data
+                s.top_b[i] = tb.ctypes.data
         self.s = s
 
 

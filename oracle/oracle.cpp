@@ -209,6 +209,12 @@ struct OrcWeights {
   const float* emb_s1;      // [16][C]  Emb(S1), added to the features before stage 2
   const float* head2_w;     // [C][16]  stage 2 over S2 = O >> 4
   const float* head2_b;     // [16]
+  // full target occupancy predictor (Sec. 3.2, Eqs. 6-9), used when model_mode == 1
+  int model_mode, pad3;
+  const float* emb_o;       // [256][C]  Emb(O^{d-1})
+  const float* emb_d;       // [8][C]    Emb(delta)
+  const float* top_w[4];    // [27][C][C] residual blocks: A1, A2 (scale d-1), B1, B2 (scale d)
+  const float* top_b[4];    // [C]
 };
 
 uint64_t orc_morton(int64_t x, int64_t y, int64_t z, int bits) {
@@ -405,13 +411,61 @@ int orc_sparse_conv(const int64_t* xyz, int64_t n, int bits, const double* feats
 // each layer is computed on the receptive field those rows need.
 //   logits [nrows][256] (or NULL), lse [nrows] natural-log normaliser (or
 //   NULL), bits [nrows] (or NULL; needs b < B).
+// Residual block of the full predictor: x + conv2(ReLU(conv1(x))), then ReLU
+// (3x3x3 submanifold convs C -> C with bias, on the neighbour lists nb).
+static void res_block(const std::vector<std::array<int64_t, 27>>& nb, const std::vector<double>& x, int C,
+                      const float* w1, const float* b1, const float* w2, const float* b2,
+                      std::vector<double>& out) {
+  std::vector<double> t, y;
+  sparse_conv(nb, x, C, w1, b1, C, true, t);
+  sparse_conv(nb, t, C, w2, b2, C, false, y);
+  out.resize(x.size());
+  for (size_t i = 0; i < x.size(); ++i) out[i] = std::max(x[i] + y[i], 0.0);
+}
+
+// Full target occupancy predictor (Sec. 3.2), in this reading of Eqs. 6-9:
+//   F^{d-1} = RB_A(C^{d-1}, Emb_O[O^{d-1}])                 occupancy features (Eq. 6)
+//   X^d(v)  = F^{d-1}(parent(v)) + Emb_D[delta(v)]           replication + octant (Eqs. 7-9)
+//   F^d     = RB_B(C^d, X^d)                                  (Eq. 9)
+// evaluated on every voxel of scales b-1 and b; cur = F^b [N_b][C].
+static int top_features(Pyramid* P, int b, const OrcWeights* w, std::vector<double>& cur) {
+  const Level& L = P->lv[b];
+  const Level& Pl = P->lv[b - 1];
+  const int C = w->channels;
+  const int64_t Np = (int64_t)Pl.v.size(), N = (int64_t)L.v.size();
+  std::vector<std::array<int64_t, 27>> nbA(Np), nbB(N);
+  for (int64_t u = 0; u < Np; ++u) nbA[u] = neighbours_of(Pl.row, b - 1, Pl.v[u]);
+  for (int64_t v = 0; v < N; ++v) nbB[v] = neighbours_of(L.row, b, L.v[v]);
+  std::vector<double> xa(Np * C), fa, xb(N * C);
+  for (int64_t u = 0; u < Np; ++u)
+    for (int c = 0; c < C; ++c) xa[u * C + c] = (double)w->emb_o[(size_t)Pl.code[u] * C + c];
+  res_block(nbA, xa, C, w->top_w[0], w->top_b[0], w->top_w[1], w->top_b[1], fa);
+  for (int64_t v = 0; v < N; ++v) {
+    const Vox& c0 = L.v[v];
+    const int64_t p = L.parent[v];
+    const Vox& pv = Pl.v[p];
+    int delta = 0;
+    for (int a = 0; a < 3; ++a) delta += (int)(c0[a] - 2 * pv[a]) << a;
+    for (int c = 0; c < C; ++c) xb[v * C + c] = fa[p * C + c] + (double)w->emb_d[delta * C + c];
+  }
+  res_block(nbB, xb, C, w->top_w[2], w->top_b[2], w->top_w[3], w->top_b[3], cur);
+  return 0;
+}
+
 // Features h_L of the last conv layer for the requested rows, stored densely
 // over all N rows of the scale in `cur` ([N][C]; rows outside the requested
-// set are zero).  Returns -1 on bad arguments.
+// set are zero, except for the full predictor, which evaluates every row).
+// Returns -1 on bad arguments.
 static int final_features(void* h, int b, const OrcWeights* w, const int64_t* rows, int64_t nrows,
                    std::vector<double>& cur) {
   Pyramid* P = static_cast<Pyramid*>(h);
-  if (b <= P->b0 || b > P->B || w->layers < 1 || w->layers > 8) return -1;
+  if (b <= P->b0 || b > P->B) return -1;
+  if (w->model_mode == 1) {
+    for (int64_t i = 0; i < nrows; ++i)
+      if (rows[i] < 0 || rows[i] >= (int64_t)P->lv[b].v.size()) return -1;
+    return top_features(P, b, w, cur);
+  }
+  if (w->layers < 1 || w->layers > 8) return -1;
   const Level& L = P->lv[b];
   const int C = w->channels;
   const int64_t N = (int64_t)L.v.size();

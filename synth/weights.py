@@ -10,6 +10,12 @@ Eqs. 11-13): S1 = O & 15 first, then S2 = O >> 4 given S1:
   head1_w    [C][16]    head1_b [16]     stage 1: z1 = head1_w^T h + head1_b
   emb_s1     [16][C]                     Emb(S1), added to h before stage 2
   head2_w    [C][16]    head2_b [16]     stage 2: z2 = head2_w^T (h + emb_s1[S1]) + head2_b
+and, with ``top=True``, the full target occupancy predictor (Sec. 3.2,
+Eqs. 6-9), which replaces the L plain layers:
+  emb_o      [256][C]   Emb(O^{d-1}) of the parent-scale codes
+  emb_d      [8][C]     Emb(delta) of the octant
+  top_w[i]   [27][C][C], top_b[i] [C], i = A1, A2 (residual block at scale
+             d-1), B1, B2 (residual block at scale d)
 with C_in = 11 for the first layer and C for the rest.  Kaiming-normal:
 std = sqrt(2 / fan_in), fan_in = 27 * C_in for a conv and C for the head.
 Biases are zero unless ``bias_std`` is given (tests use non-zero biases so
@@ -29,7 +35,7 @@ _W_STREAM = 21
 
 def gen_weights(channels: int, layers: int, seed: int = 2, bias_std: float = 0.0,
                 head_scale: float = 1.0, in_features: int = IN_FEATURES,
-                two_stage: bool = False, emb_std: float = 1.0) -> dict:
+                two_stage: bool = False, emb_std: float = 1.0, top: bool = False) -> dict:
     draw = [0]
 
     def normals(n):
@@ -61,4 +67,12 @@ def gen_weights(channels: int, layers: int, seed: int = 2, bias_std: float = 0.0
         out["emb_s1"] = (normals(16 * channels) * emb_std).reshape(16, channels).astype(np.float32)
         out["head2_w"] = (normals(channels * 16) * std).reshape(channels, 16).astype(np.float32)
         out["head2_b"] = (normals(16) * bias_std * head_scale).astype(np.float32)
+    if top:  # drawn after everything above, which stays unchanged
+        out["emb_o"] = (normals(256 * channels) * emb_std).reshape(256, channels).astype(np.float32)
+        out["emb_d"] = (normals(8 * channels) * emb_std).reshape(8, channels).astype(np.float32)
+        out["top_w"], out["top_b"] = [], []
+        for _ in range(4):
+            w_ = normals(KVOL * channels * channels) * np.sqrt(2.0 / (KVOL * channels))
+            out["top_w"].append(w_.reshape(KVOL, channels, channels).astype(np.float32))
+            out["top_b"].append((normals(channels) * bias_std).astype(np.float32))
     return out

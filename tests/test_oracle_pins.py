@@ -507,3 +507,74 @@ def test_freqs_rule_16_symbols_worked_values():
     # ties for the largest go to the lowest index; the total is always 2^16
     t = oracle.freqs_from_probs(np.array([0.1] * 2 + [0.4, 0.4] + [0.0] * 12), 16)[0]
     assert t[2] > t[3] and t.sum() == 65536 and t.min() >= 1
+
+
+# ---- full target occupancy predictor (Sec. 3.2, Eqs. 6-9) ------------------------------
+
+def _top_weights(C, seed=21, **kw):
+    return gen_weights(C, 2, seed=seed, bias_std=0.1, top=True, **kw)
+
+
+def _top_by_composition(P, b, w):
+    """The predictor rebuilt from pinned pieces: residual blocks from the
+    sparse conv pinned against a dense conv3d, the target embedding and the
+    head written out with numpy."""
+    def block(xyz, bits, x, i1, i2):
+        t = oracle.sparse_conv(xyz, bits, x, w["top_w"][i1], w["top_b"][i1], True)
+        y = oracle.sparse_conv(xyz, bits, t, w["top_w"][i2], w["top_b"][i2], False)
+        return np.maximum(x + y, 0.0)
+    xp = P.xyz(b - 1)
+    fa = block(xp, b - 1, w["emb_o"].astype(np.float64)[P.codes(b - 1)], 0, 1)
+    xyz = P.xyz(b)
+    par = P.parent(b).astype(np.int64)
+    delta = (xyz[:, 0] & 1) + 2 * (xyz[:, 1] & 1) + 4 * (xyz[:, 2] & 1)
+    fb = block(xyz, b, fa[par] + w["emb_d"].astype(np.float64)[delta], 2, 3)
+    return fb @ w["head_w"].astype(np.float64) + w["head_b"].astype(np.float64)
+
+
+def test_top_equals_composition_of_pinned_pieces():
+    rs = np.random.default_rng(8)
+    B, b0 = 7, 3
+    xyz = rs.integers(0, 1 << B, size=(900, 3)) // 2 + 16
+    P = oracle.Pyramid.from_voxels(xyz, B, b0)
+    w = _top_weights(16)
+    for b in (b0 + 1, B - 1):
+        lg, lse, bits = P.model(b, w)
+        ref = _top_by_composition(P, b, w)
+        np.testing.assert_allclose(lg, ref, rtol=0, atol=1e-9)
+        code = P.codes(b).astype(np.int64)
+        np.testing.assert_allclose(bits, (lse - ref[np.arange(len(code)), code]) / math.log(2), atol=1e-9)
+
+
+def test_top_zero_convs_reduce_to_embeddings(scan_cache):
+    """With every conv weight and bias zero each residual block is a ReLU, so a
+    voxel's logits depend only on its parent's code and its octant."""
+    c = CONFIGS[0]
+    P = oracle.Pyramid.from_points(scan_cache(0), c.bit_depth, c.min_bit_depth, c.range_m)
+    w = _top_weights(c.channels)
+    w["top_w"] = [np.zeros_like(x) for x in w["top_w"]]
+    w["top_b"] = [np.zeros_like(x) for x in w["top_b"]]
+    b = c.bit_depth - 1
+    lg, _, _ = P.model(b, w)
+    xyz = P.xyz(b)
+    delta = (xyz[:, 0] & 1) + 2 * (xyz[:, 1] & 1) + 4 * (xyz[:, 2] & 1)
+    pcode = P.codes(b - 1)[P.parent(b)]
+    eo, ed = w["emb_o"].astype(np.float64), w["emb_d"].astype(np.float64)
+    f = np.maximum(np.maximum(eo[pcode], 0.0) + ed[delta], 0.0)
+    np.testing.assert_allclose(lg, f @ w["head_w"].astype(np.float64) + w["head_b"], rtol=0, atol=1e-9)
+    # the same (parent code, octant) gives the same row
+    key = pcode.astype(np.int64) * 8 + delta
+    _, first = np.unique(key, return_index=True)
+    np.testing.assert_array_equal(lg, lg[first[np.searchsorted(np.unique(key), key)]])
+
+
+def test_top_two_stage_head_and_totals(scan_cache):
+    c = CONFIGS[0]
+    P = oracle.Pyramid.from_points(scan_cache(0), c.bit_depth, c.min_bit_depth, c.range_m)
+    w = _top_weights(c.channels, two_stage=True)
+    b = c.bit_depth - 2
+    l1, l2, lse1, lse2, bits = P.model2(b, w)
+    np.testing.assert_allclose(np.exp(l1 - lse1[:, None]).sum(1), 1.0, atol=1e-12)
+    T, per = P.totals(w)
+    assert per[b] == pytest.approx(bits.sum(), rel=1e-12)
+    assert T == pytest.approx(per.sum(), rel=1e-12)
