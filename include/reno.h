@@ -71,6 +71,12 @@ typedef enum {
 #define RENO_PREC_BF16X3 1      /* each fp32 operand split into bf16 hi + lo, products
                                    hi*hi + hi*lo + lo*hi on bf16 MFMA with fp32
                                    accumulation (~2^-16 relative per product) */
+#define RENO_MODEL_PLAIN 0      /* 11 input bits [delta, parent code] (Eqs. 7-8), L sparse
+                                   conv + ReLU layers (Eq. 9) */
+#define RENO_MODEL_TOP 1        /* full target occupancy predictor (Sec. 3.2, Eqs. 6-9):
+                                   Emb_O of the parent scale's codes and a residual block
+                                   on the parent scale, replication + Emb_D of the octant
+                                   and a residual block on the target scale; fp32 only */
 
 /* Capacities and model shape, fixed for the life of a context. */
 typedef struct {
@@ -87,6 +93,9 @@ typedef struct {
   int layers;                /* L: 1 .. RENO_MAX_LAYERS sparse conv layers */
   int head_mode;             /* RENO_HEAD_ONE_STAGE (0) or RENO_HEAD_TWO_STAGE */
   int precision;             /* RENO_PREC_FP32 (0) or RENO_PREC_BF16X3 */
+  int model_mode;            /* RENO_MODEL_PLAIN (0) or RENO_MODEL_TOP (layers is then
+                                unused: the full predictor has its four convs) */
+  int pad0;
 } reno_params;
 
 /* Model weights (fp32, device memory, row-major).  Layout:
@@ -100,7 +109,13 @@ typedef struct {
  *   head1_w    [C][16]   head1_b [16]   z1 = head1_w^T h + head1_b
  *   emb_s1     [16][C]                  Emb(S1), added to h before stage 2
  *   head2_w    [C][16]   head2_b [16]   z2 = head2_w^T (h + emb_s1[S1]) + head2_b
- * Only the pointers of the context's head mode are read.                    */
+ * Full predictor (RENO_MODEL_TOP; conv_w / conv_b are then not read):
+ *   emb_o      [256][C]  Emb_O, indexed by the code of a voxel of scale d-1
+ *   emb_d      [8][C]    Emb_D, indexed by the octant delta of a voxel of scale d
+ *   top_w[i]   [27][C][C], top_b[i] [C]: convs A1, A2 (residual block on scale
+ *              d-1) and B1, B2 (residual block on scale d); a block computes
+ *              ReLU(x + conv2(ReLU(conv1(x)))) with biases inside both convs
+ * Only the pointers of the context's model and head modes are read.        */
 typedef struct {
   const float* conv_w[RENO_MAX_LAYERS];
   const float* conv_b[RENO_MAX_LAYERS];
@@ -111,6 +126,10 @@ typedef struct {
   const float* emb_s1;
   const float* head2_w;
   const float* head2_b;
+  const float* emb_o;
+  const float* emb_d;
+  const float* top_w[4];
+  const float* top_b[4];
 } reno_weights;
 
 /* Creates a context on the current HIP device that enqueues on `hip_stream`
@@ -265,6 +284,7 @@ typedef enum {
   RENO_K_CONV_LAST,     /* last conv layer fused with the 256-way head and softmax normaliser */
   RENO_K_CODE_LENGTH,   /* ideal bits and per-scale sums */
   RENO_K_OTHER,         /* weight packing, getters, symbol tables */
+  RENO_K_TOP_INPUT,     /* full predictor: neighbour maps and embedding inputs */
   RENO_K_COUNT
 } reno_kernel;
 

@@ -30,6 +30,8 @@ RENO_HEAD_ONE_STAGE = 0
 RENO_HEAD_TWO_STAGE = 1
 RENO_PREC_FP32 = 0
 RENO_PREC_BF16X3 = 1
+RENO_MODEL_PLAIN = 0
+RENO_MODEL_TOP = 1
 SYMBOLS = 256
 
 _STATUS = {0: "RENO_OK", -1: "RENO_E_INVALID", -2: "RENO_E_STATE", -3: "RENO_E_NOMEM",
@@ -47,7 +49,8 @@ class reno_params(ctypes.Structure):
                 ("max_bit_depth", ctypes.c_int), ("min_bit_depth", ctypes.c_int),
                 ("range_m", ctypes.c_double), ("in_features", ctypes.c_int),
                 ("channels", ctypes.c_int), ("layers", ctypes.c_int),
-                ("head_mode", ctypes.c_int), ("precision", ctypes.c_int)]
+                ("head_mode", ctypes.c_int), ("precision", ctypes.c_int),
+                ("model_mode", ctypes.c_int), ("pad0", ctypes.c_int)]
 
 
 class reno_weights(ctypes.Structure):
@@ -56,7 +59,9 @@ class reno_weights(ctypes.Structure):
                 ("head_w", ctypes.c_void_p), ("head_b", ctypes.c_void_p),
                 ("head1_w", ctypes.c_void_p), ("head1_b", ctypes.c_void_p),
                 ("emb_s1", ctypes.c_void_p), ("head2_w", ctypes.c_void_p),
-                ("head2_b", ctypes.c_void_p)]
+                ("head2_b", ctypes.c_void_p), ("emb_o", ctypes.c_void_p),
+                ("emb_d", ctypes.c_void_p), ("top_w", ctypes.c_void_p * 4),
+                ("top_b", ctypes.c_void_p * 4)]
 
 
 # exported symbol -> (restype, argtypes); exactly the functions of include/reno.h
@@ -92,7 +97,7 @@ _SIGS = {
 }
 
 KERNELS = ["zero", "quantize", "sort", "pyramid", "codes", "set_base", "expand", "conv_first",
-           "conv_mid", "conv_last", "code_length", "other"]
+           "conv_mid", "conv_last", "code_length", "other", "top_input"]
 
 _lib = None
 
@@ -126,14 +131,14 @@ class Context:
 
     def __init__(self, max_points: int, max_bit_depth: int, min_bit_depth: int, range_m: float,
                  channels: int, layers: int, max_model_voxels: int = 0, stream=None,
-                 two_stage: bool = False, precision: int = RENO_PREC_FP32):
+                 two_stage: bool = False, precision: int = RENO_PREC_FP32, top: bool = False):
         import torch
         self.torch = torch
         self.device = torch.device("cuda", torch.cuda.current_device())
         self.stream = stream if stream is not None else torch.cuda.current_stream()
         p = reno_params(max_points, max_model_voxels, max_bit_depth, min_bit_depth, range_m, 11,
                         channels, layers, RENO_HEAD_TWO_STAGE if two_stage else RENO_HEAD_ONE_STAGE,
-                        precision)
+                        precision, RENO_MODEL_TOP if top else RENO_MODEL_PLAIN, 0)
         h = ctypes.c_void_p()
         rc = lib().reno_create(ctypes.byref(p), ctypes.c_void_p(self.stream.cuda_stream),
                                ctypes.byref(h))
@@ -145,6 +150,7 @@ class Context:
         self.channels = channels
         self.layers = layers
         self.two_stage = two_stage
+        self.top = top
         self.B = 0
         self._keep = []
 
@@ -171,17 +177,28 @@ class Context:
         self._check(lib().reno_sync(self._h))
 
     def set_weights(self, weights: dict):
-        """weights: dict of fp32 device tensors conv_w[l], conv_b[l], head_w, head_b."""
+        """weights: dict of fp32 device tensors conv_w[l], conv_b[l] (full predictor:
+        emb_o, emb_d, top_w[4], top_b[4]) and the head of the context's head mode."""
         w = reno_weights()
         keep = []
-        for l in range(self.layers):
-            cw = weights["conv_w"][l].contiguous()
-            cb = weights["conv_b"][l].contiguous()
-            keep += [cw, cb]
-            w.conv_w[l] = cw.data_ptr()
-            w.conv_b[l] = cb.data_ptr()
+        if self.top:
+            for i in range(4):
+                tw = weights["top_w"][i].contiguous()
+                tb = weights["top_b"][i].contiguous()
+                keep += [tw, tb]
+                w.top_w[i] = tw.data_ptr()
+                w.top_b[i] = tb.data_ptr()
+        else:
+            for l in range(self.layers):
+                cw = weights["conv_w"][l].contiguous()
+                cb = weights["conv_b"][l].contiguous()
+                keep += [cw, cb]
+                w.conv_w[l] = cw.data_ptr()
+                w.conv_b[l] = cb.data_ptr()
         names = (("head1_w", "head1_b", "emb_s1", "head2_w", "head2_b") if self.two_stage
                  else ("head_w", "head_b"))
+        if self.top:
+            names = names + ("emb_o", "emb_d")
         for name in names:
             t = weights[name].contiguous()
             keep.append(t)
@@ -385,7 +402,12 @@ def weights_to_device(w: dict, device="cuda") -> dict:
     import torch
     out = {"conv_w": [torch.from_numpy(np.ascontiguousarray(x)).to(device) for x in w["conv_w"]],
            "conv_b": [torch.from_numpy(np.ascontiguousarray(x)).to(device) for x in w["conv_b"]]}
-    for name in ("head_w", "head_b", "head1_w", "head1_b", "emb_s1", "head2_w", "head2_b"):
+    for name in ("head_w", "head_b", "head1_w", "head1_b", "emb_s1", "head2_w", "head2_b",
+                 "emb_o", "emb_d"):
         if name in w:
             out[name] = torch.from_numpy(np.ascontiguousarray(w[name], dtype=np.float32)).to(device)
+    for name in ("top_w", "top_b"):
+        if name in w:
+            out[name] = [torch.from_numpy(np.ascontiguousarray(x, dtype=np.float32)).to(device)
+                         for x in w[name]]
     return out

@@ -53,7 +53,8 @@ void free_all(Ctx* c) {
                   c->lv_feat, c->d_count,   c->d_moff,   c->d_err,    c->d_hist,    c->d_ticket,
                   c->d_status, c->d_hash,   c->h_a,      c->h_b,      c->d_nbr,     c->d_lse,
                   c->d_partial, c->d_total, c->w_head,   c->w_hbias,  c->w_head_plain,
-                  c->d_lse2,    c->w_emb,   c->d_s1,     c->w_head_t, c->d_perm};
+                  c->d_lse2,    c->w_emb,   c->d_s1,     c->w_head_t, c->d_perm,
+                  c->h_c,       c->h_d,     c->w_embo,   c->w_embd};
   for (void* p : ptrs)
     if (p) (void)hipFree(p);
   for (int l = 0; l < RENO_MAX_LAYERS; ++l) {
@@ -138,6 +139,10 @@ reno_status reno_create(const reno_params* p, void* hip_stream, reno_ctx** out) 
     return fail(nullptr, RENO_E_INVALID, "head_mode must be RENO_HEAD_ONE_STAGE or RENO_HEAD_TWO_STAGE");
   if (p->precision != RENO_PREC_FP32 && p->precision != RENO_PREC_BF16X3)
     return fail(nullptr, RENO_E_INVALID, "precision must be RENO_PREC_FP32 or RENO_PREC_BF16X3");
+  if (p->model_mode != RENO_MODEL_PLAIN && p->model_mode != RENO_MODEL_TOP)
+    return fail(nullptr, RENO_E_INVALID, "model_mode must be RENO_MODEL_PLAIN or RENO_MODEL_TOP");
+  if (p->model_mode == RENO_MODEL_TOP && p->precision != RENO_PREC_FP32)
+    return fail(nullptr, RENO_E_INVALID, "the full predictor runs in RENO_PREC_FP32 only");
   // N_b <= N_{b+1} <= max_points, so (model scales) x max_points always suffices
   const int64_t nmodel = p->max_bit_depth - p->min_bit_depth - 1 > 0
                              ? p->max_bit_depth - p->min_bit_depth - 1 : 1;
@@ -184,17 +189,25 @@ reno_status reno_create(const reno_params* p, void* hip_stream, reno_ctx** out) 
   A(dalloc(&c->d_ticket, reno::TICKETS, &c->device_bytes));
   A(dalloc(&c->d_status, (size_t)c->status_words, &c->device_bytes));
   A(dalloc(&c->d_hash, size_t(1) << c->hash_lg, &c->device_bytes));
-  A(dalloc(&c->h_a, (size_t)(cap_model + 1) * C, &c->device_bytes));  // row cap_model stays zero
-  A(dalloc(&c->h_b, (size_t)(cap_model + 1) * C, &c->device_bytes));
-  A(dalloc(&c->d_nbr, (size_t)cap_model * reno::NBR_STRIDE, &c->device_bytes));
+  const bool top = c->top();
+  const size_t rows = (size_t)c->cap_rows();  // row cap_model stays zero
+  A(dalloc(&c->h_a, rows * C, &c->device_bytes));
+  A(dalloc(&c->h_b, rows * C, &c->device_bytes));
+  if (top) {
+    A(dalloc(&c->h_c, rows * C, &c->device_bytes));
+    A(dalloc(&c->h_d, rows * C, &c->device_bytes));
+    A(dalloc(&c->w_embo, (size_t)256 * C, &c->device_bytes));
+    A(dalloc(&c->w_embd, (size_t)8 * C, &c->device_bytes));
+  }
+  A(dalloc(&c->d_nbr, rows * reno::NBR_STRIDE, &c->device_bytes));
   A(dalloc(&c->d_lse, (size_t)cap_model, &c->device_bytes));
   A(dalloc(&c->d_lse2, (size_t)cap_model, &c->device_bytes));
-  A(dalloc(&c->d_perm, (size_t)cap_model, &c->device_bytes));
+  A(dalloc(&c->d_perm, rows, &c->device_bytes));
   A(dalloc(&c->d_s1, (size_t)cap_model, &c->device_bytes));
   A(dalloc(&c->d_partial, (size_t)reno::NLEV * ((c->cap_pts + 63) / 64), &c->device_bytes));
   A(dalloc(&c->d_total, reno::NLEV, &c->device_bytes));
-  int c_in = RENO_IN_FEATURES;
-  for (int l = 0; l < p->layers; ++l) {
+  int c_in = top ? C : RENO_IN_FEATURES;
+  for (int l = 0; l < (top ? 4 : p->layers); ++l) {
     const int KS = (c_in + 3) / 4, KSP = (KS + 3) & ~3;
     // fp32: KSP floats per (offset, column block, lane); bf16x3: 8 words
     A(dalloc(&c->w_conv[l], (size_t)27 * (C / 16) * 64 * std::max(KSP, 8), &c->device_bytes));
@@ -223,6 +236,8 @@ reno_status reno_create(const reno_params* p, void* hip_stream, reno_ctx** out) 
     e = hipMemsetAsync(c->h_a + (size_t)cap_model * C, 0, sizeof(float) * C, c->stream);
   if (e == hipSuccess)
     e = hipMemsetAsync(c->h_b + (size_t)cap_model * C, 0, sizeof(float) * C, c->stream);
+  if (e == hipSuccess && top)
+    e = hipMemsetAsync(c->h_c + (size_t)cap_model * C, 0, sizeof(float) * C, c->stream);
   if (e == hipSuccess) e = hipMemsetAsync(c->lv_feat + lvn, 0, 16, c->stream);
   if (e == hipSuccess) e = hipStreamSynchronize(c->stream);
   if (e != hipSuccess) {
@@ -259,8 +274,14 @@ reno_status reno_sync(reno_ctx* c) {
 
 reno_status reno_set_weights(reno_ctx* c, const reno_weights* w) {
   if (!c || !w) return fail(c, RENO_E_INVALID, "null argument");
-  for (int l = 0; l < c->p.layers; ++l)
-    if (!w->conv_w[l] || !w->conv_b[l]) return fail(c, RENO_E_INVALID, "missing conv weights");
+  if (c->top()) {
+    for (int l = 0; l < 4; ++l)
+      if (!w->top_w[l] || !w->top_b[l]) return fail(c, RENO_E_INVALID, "missing residual-block weights");
+    if (!w->emb_o || !w->emb_d) return fail(c, RENO_E_INVALID, "missing embedding weights");
+  } else {
+    for (int l = 0; l < c->p.layers; ++l)
+      if (!w->conv_w[l] || !w->conv_b[l]) return fail(c, RENO_E_INVALID, "missing conv weights");
+  }
   if (c->p.head_mode == RENO_HEAD_TWO_STAGE) {
     if (!w->head1_w || !w->head1_b || !w->emb_s1 || !w->head2_w || !w->head2_b)
       return fail(c, RENO_E_INVALID, "missing two-stage head weights");

@@ -75,10 +75,12 @@ struct Ctx {
   HashSlot* d_hash = nullptr;   // [1 << hash_lg]
 
   // model buffers (packed model rows: scale b at d_moff[b] ..)
-  float* h_a = nullptr;         // [cap_model][C]
+  float* h_a = nullptr;         // [cap_rows][C]
   float* h_b = nullptr;
-  int32_t* d_nbr = nullptr;     // [cap_model][NBR_STRIDE]
-  int32_t* d_perm = nullptr;    // [cap_model] tile order of the conv layers after the first
+  float* h_c = nullptr;         // full predictor: embedding inputs X (with a zero row)
+  float* h_d = nullptr;         // full predictor: F of the scale below
+  int32_t* d_nbr = nullptr;     // [cap_rows][NBR_STRIDE]
+  int32_t* d_perm = nullptr;    // [cap_rows] tile order of the conv layers after the first
   float* d_lse = nullptr;       // [cap_model] (two-stage head: stage 1)
   float* d_lse2 = nullptr;      // [cap_model] stage 2 of the two-stage head
   uint8_t* d_s1 = nullptr;      // [cap_model] S1 that stage 2 was evaluated with
@@ -96,6 +98,8 @@ struct Ctx {
   float* w_head_plain = nullptr;  // [C][256] as given (two-stage: [C][H1 | H2]), for code lengths
   float* w_emb = nullptr;         // [16][C] Emb(S1) of the two-stage head
   float* w_head_t = nullptr;      // head transposed, one row per symbol: [256][C] (two-stage: [H1^T; H2^T])
+  float* w_embo = nullptr;        // [256][C] Emb_O of the full predictor
+  float* w_embd = nullptr;        // [8][C]   Emb_D of the full predictor
   bool have_weights = false;
 
   // frame state
@@ -125,8 +129,12 @@ struct Ctx {
 
   int b0() const { return p.min_bit_depth; }
   int64_t lv(int b) const { return (int64_t)(b - p.min_bit_depth) * cap_pts; }
+  bool top() const { return p.model_mode == RENO_MODEL_TOP; }
+  // rows of the feature buffers: the model rows, the zero row cap_model and,
+  // for the full predictor, the base scale
+  int64_t cap_rows() const { return cap_model + 1 + (top() ? cap_pts : 0); }
   // buffer that holds the last conv layer's output (h_L), per the ping-pong
-  float* hlast() const { return (p.layers & 1) ? h_a : h_b; }
+  float* hlast() const { return top() ? h_a : ((p.layers & 1) ? h_a : h_b); }
 };
 
 // Brackets the launches made during its lifetime with a pair of events when

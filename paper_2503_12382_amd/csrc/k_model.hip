@@ -262,7 +262,36 @@ struct ConvArgs {
   float* lse2;            // [cap_model]
   uint8_t* s1_out;        // [cap_model] the S1 stage 2 used
   const int32_t* perm;    // optional tile order: tile slot -> packed row (layers after the first)
+  // full predictor
+  const float* res;       // residual input added before the ReLU (same rows as h_out), or NULL
+  int b_ext;              // scale whose rows live past the zero row (the base scale), or -1
+  int64_t ext_off;        // first packed row of that scale (cap_model + 1)
+  int64_t cap_rows;       // rows of the feature buffers
 };
+
+// Packed-row layout of the scales: scale b at moff[b] .. below the reserved
+// zero row cap_model; the full predictor also models the base scale, whose
+// rows sit past the zero row at ext_off.
+struct RowMap {
+  const int32_t* count;
+  const int32_t* moff;
+  int64_t cap_model;
+  int b_ext;
+  int64_t ext_off, cap_rows;
+};
+
+// First packed row and voxel count of scale b; a scale that would not fit
+// reads as empty (the overflow was latched where its size was made).
+__device__ __forceinline__ void scale_span(const RowMap& m, int b, int64_t& mo, int64_t& n) {
+  n = m.count[b];
+  if (b == m.b_ext) {
+    mo = m.ext_off;
+    if (mo + n > m.cap_rows) n = 0;
+  } else {
+    mo = m.moff[b];
+    if (mo + n > m.cap_model) n = 0;
+  }
+}
 
 // Entry j (wave-uniform) of the 8 neighbour rows a lane holds in two int4,
 // as a branch-free select tree.
@@ -292,6 +321,50 @@ __device__ __forceinline__ void stage_lds(const f4* __restrict__ src, f4* dst, i
     for (int i = 0; i < BATCH; ++i) {
       const int idx = (b0 + i) * THREADS + tid;
       if (b0 + i < PER && idx < N16) dst[idx] = v[i];
+    }
+  }
+}
+
+// Neighbour rows of a voxel from the parent scale.  The 27 cells around v lie
+// in at most 8 cells of the parent scale: the parent p and, per axis, the
+// neighbour of p on v's side.  Lane (r, g) probes cells e = 2g and 2g+1
+// (e = ex + 2ey + 4ez) of its voxel r; each hit gives the cell's code and
+// first-child row, from which every neighbour row follows by the FCG order.
+// par is the 8-entry LDS slot of voxel r (shared by the 4 lanes of r); the
+// lane ends with the rows of offsets 8g .. 8g+7 (-1: absent or off-grid).
+__device__ __forceinline__ void parent_cell_rows(uint64_t key, int b, int g, const HashSlot* __restrict__ hash,
+                                                 int hash_lg, volatile uint64_t* par, int32_t (&nb)[8]) {
+  const int x = (int)compact3(key), y = (int)compact3(key >> 1), z = (int)compact3(key >> 2);
+  const int px = x >> 1, py = y >> 1, pz = z >> 1;
+  const int sx = (x & 1) ? 1 : -1, sy = (y & 1) ? 1 : -1, sz = (z & 1) ? 1 : -1;
+  const int plim = 1 << (b - 1);
+  uint64_t tk[2];
+#pragma unroll
+  for (int i = 0; i < 2; ++i) {
+    const int e = 2 * g + i;
+    const int cx = px + ((e & 1) ? sx : 0), cy = py + ((e & 2) ? sy : 0), cz = pz + ((e & 4) ? sz : 0);
+    tk[i] = (cx >= 0 && cy >= 0 && cz >= 0 && cx < plim && cy < plim && cz < plim)
+                ? tag_key(morton3((uint32_t)cx, (uint32_t)cy, (uint32_t)cz), b - 1)
+                : 0ull;
+  }
+  uint2 hit[2];
+  hash_find_n<2>(hash, hash_lg, tk, hit);
+  // cross-lane exchange through LDS (volatile: every read goes to LDS)
+  par[2 * g] = ((uint64_t)hit[0].y << 32) | hit[0].x;
+  par[2 * g + 1] = ((uint64_t)hit[1].y << 32) | hit[1].x;
+  __builtin_amdgcn_wave_barrier();
+  const int lim = 1 << b;
+#pragma unroll
+  for (int j = 0; j < 8; ++j) {
+    const int k = 8 * g + j;
+    const int ux = x + (k % 3) - 1, uy = y + (k / 3) % 3 - 1, uz = z + (k / 9) % 3 - 1;
+    nb[j] = -1;
+    if (k < 27 && ux >= 0 && uy >= 0 && uz >= 0 && ux < lim && uy < lim && uz < lim) {
+      const int e = ((ux >> 1) != px ? 1 : 0) | ((uy >> 1) != py ? 2 : 0) | ((uz >> 1) != pz ? 4 : 0);
+      const uint64_t pc = par[e];
+      const uint32_t first = (uint32_t)pc, code = (uint32_t)(pc >> 32);
+      const uint32_t d = (uint32_t)((ux & 1) | ((uy & 1) << 1) | ((uz & 1) << 2));
+      if ((code >> d) & 1u) nb[j] = (int32_t)first + __popc(code & ((1u << d) - 1u));
     }
   }
 }
@@ -327,13 +400,12 @@ __global__ void __launch_bounds__(CONV_THREADS) k_conv(ConvArgs a) {
   const int r = lane & 15, g = lane >> 4;
   const int nsc = a.b_hi - a.b_lo + 1;
 
+  const RowMap rm{a.count, a.moff, a.cap_model, a.b_ext, a.ext_off, a.cap_rows};
   // tile prefix over the scales of this launch
   int64_t total_tiles = 0;
   for (int i = 0; i < nsc; ++i) {
-    const int b = a.b_lo + i;
-    int64_t nb = a.count[b];
-    const int64_t mo = a.moff[b];
-    if (mo + nb > a.cap_model) nb = 0;  // overflow was latched where the size was made
+    int64_t mo, nb;
+    scale_span(rm, a.b_lo + i, mo, nb);
     total_tiles += (nb + 15) / 16;
   }
   if ((int64_t)blockIdx.x >= total_tiles) return;  // whole block idle: skip the weight staging
@@ -341,12 +413,11 @@ __global__ void __launch_bounds__(CONV_THREADS) k_conv(ConvArgs a) {
     s_next = 0;
     int64_t acc = 0;
     for (int i = 0; i < nsc; ++i) {
-      const int b = a.b_lo + i;
-      int64_t nb = a.count[b];
-      if (a.moff[b] + nb > a.cap_model) nb = 0;
+      int64_t mo, nb;
+      scale_span(rm, a.b_lo + i, mo, nb);
       s_tpre[i] = acc;
       s_nv[i] = nb;
-      s_mo[i] = a.moff[b];
+      s_mo[i] = mo;
       acc += (nb + 15) / 16;
     }
     for (int i = nsc; i <= NLEV; ++i) s_tpre[i] = acc;  // padding: never below a valid tile
@@ -382,48 +453,8 @@ __global__ void __launch_bounds__(CONV_THREADS) k_conv(ConvArgs a) {
     // ---- neighbour rows: lane (r, g) holds offsets k = 8g .. 8g+7 of voxel r
     int4 nlo, nhi;
     if (FIRST) {
-      // The 27 cells around v lie in at most 8 cells of the parent scale: the
-      // parent p and, per axis, the neighbour of p on v's side.  Lane (r, g)
-      // probes cells e = 2g and 2g+1 (e = ex + 2ey + 4ez) of voxel r; each
-      // hit gives the cell's code and first-child row, from which every
-      // neighbour row follows by the FCG order.
-      const uint64_t key = a.lv_key[lvb + (prow - mo)];
-      const int x = (int)compact3(key), y = (int)compact3(key >> 1), z = (int)compact3(key >> 2);
-      const int px = x >> 1, py = y >> 1, pz = z >> 1;
-      const int sx = (x & 1) ? 1 : -1, sy = (y & 1) ? 1 : -1, sz = (z & 1) ? 1 : -1;
-      const int plim = 1 << (b - 1);
-      uint64_t tk[2];
-#pragma unroll
-      for (int i = 0; i < 2; ++i) {
-        const int e = 2 * g + i;
-        const int cx = px + ((e & 1) ? sx : 0), cy = py + ((e & 2) ? sy : 0),
-                  cz = pz + ((e & 4) ? sz : 0);
-        tk[i] = (cx >= 0 && cy >= 0 && cz >= 0 && cx < plim && cy < plim && cz < plim)
-                    ? tag_key(morton3((uint32_t)cx, (uint32_t)cy, (uint32_t)cz), b - 1)
-                    : 0ull;
-      }
-      uint2 hit[2];
-      hash_find_n<2>(a.hash, a.hash_lg, tk, hit);
-      // cross-lane exchange through LDS (volatile: every read goes to LDS)
-      volatile uint64_t* par = s_par[w][r];
-      par[2 * g] = ((uint64_t)hit[0].y << 32) | hit[0].x;
-      par[2 * g + 1] = ((uint64_t)hit[1].y << 32) | hit[1].x;
-      __builtin_amdgcn_wave_barrier();
-      const int lim = 1 << b;
       int32_t nb[8];
-#pragma unroll
-      for (int j = 0; j < 8; ++j) {
-        const int k = 8 * g + j;
-        const int ux = x + (k % 3) - 1, uy = y + (k / 3) % 3 - 1, uz = z + (k / 9) % 3 - 1;
-        nb[j] = -1;
-        if (k < 27 && ux >= 0 && uy >= 0 && uz >= 0 && ux < lim && uy < lim && uz < lim) {
-          const int e = ((ux >> 1) != px ? 1 : 0) | ((uy >> 1) != py ? 2 : 0) | ((uz >> 1) != pz ? 4 : 0);
-          const uint64_t pc = par[e];
-          const uint32_t first = (uint32_t)pc, code = (uint32_t)(pc >> 32);
-          const uint32_t d = (uint32_t)((ux & 1) | ((uy & 1) << 1) | ((uz & 1) << 2));
-          if ((code >> d) & 1u) nb[j] = (int32_t)first + __popc(code & ((1u << d) - 1u));
-        }
-      }
+      parent_cell_rows(a.lv_key[lvb + (prow - mo)], b, g, a.hash, a.hash_lg, s_par[w][r], nb);
       nlo = make_int4(nb[0], nb[1], nb[2], nb[3]);
       nhi = make_int4(nb[4], nb[5], nb[6], nb[7]);
       if (valid) {
@@ -587,6 +618,10 @@ __global__ void __launch_bounds__(CONV_THREADS) k_conv(ConvArgs a) {
         if (ksA[0] < 0) break;
       }
     }
+    if (a.res) {  // residual block: ReLU(x + conv(.)), x read at the voxel's own row
+#pragma unroll
+      for (int cb = 0; cb < NCB; ++cb) acc[cb] += *reinterpret_cast<const f4*>(a.res + prow * C + 16 * cb + 4 * g);
+    }
 #pragma unroll
     for (int cb = 0; cb < NCB; ++cb)
 #pragma unroll
@@ -721,8 +756,7 @@ constexpr int TO_W = 2048;
 constexpr int TO_THREADS = 1024;
 constexpr int TO_KEYS = 2048;
 
-__global__ void __launch_bounds__(TO_THREADS) k_tile_order(int b_lo, int nsc, const int32_t* __restrict__ count,
-                                                           const int32_t* __restrict__ moff, int64_t cap_model,
+__global__ void __launch_bounds__(TO_THREADS) k_tile_order(int b_lo, int nsc, RowMap rm,
                                                            const int32_t* __restrict__ nbr, int32_t* __restrict__ perm) {
   __shared__ uint32_t s_cnt[TO_KEYS];
   __shared__ uint32_t s_wsum[TO_THREADS / 64];
@@ -730,10 +764,8 @@ __global__ void __launch_bounds__(TO_THREADS) k_tile_order(int b_lo, int nsc, co
   __shared__ int64_t s_w0, s_wmo, s_wn;
   const int tid = threadIdx.x;
   if (tid < nsc) {  // sizes of the launch's scales, loaded in parallel
-    const int b = b_lo + tid;
-    int64_t n = count[b];
-    const int64_t mo = moff[b];
-    if (mo + n > cap_model) n = 0;
+    int64_t mo, n;
+    scale_span(rm, b_lo + tid, mo, n);
     s_n[tid] = n;
     s_mo[tid] = mo;
   }
@@ -805,6 +837,163 @@ __global__ void __launch_bounds__(TO_THREADS) k_tile_order(int b_lo, int nsc, co
   for (int e = 0; e < PER; ++e) {
     const int64_t i = w0 + e * TO_THREADS + tid;
     if (i < n) perm[mo + w0 + s_cnt[key[e]] + rank[e]] = (int32_t)(mo + i);
+  }
+}
+
+// ---------------------------------------------------------------------------
+// Inputs of the full predictor (Sec. 3.2): neighbour maps of the scales it
+// convolves on, occupancy embeddings Emb_O[O^{d-1}] (Eq. 6) and the target
+// embedding F^{d-1}[parent] + Emb_D[delta] (replication and octant
+// embedding, Eqs. 7-9).  Each launch covers the scales lo .. lo + nsc - 1;
+// elements map to their scale through a row prefix in LDS.
+
+// Prefix of rows over the launch's scales (padded with the total) and the
+// first packed row of each; thread 0 fills them.
+__device__ __forceinline__ void row_prefix(const RowMap& m, int lo, int nsc, int64_t* pre, int64_t* mo) {
+  int64_t acc = 0;
+  for (int i = 0; i < nsc; ++i) {
+    int64_t o, n;
+    scale_span(m, lo + i, o, n);
+    pre[i] = acc;
+    mo[i] = o;
+    acc += n;
+  }
+  for (int i = nsc; i < 32; ++i) pre[i] = acc;
+}
+
+// Last index si with pre[si] <= e (pre non-decreasing, 32 entries, pre[0] = 0
+// <= e): binary lifting, si + step never exceeds 31.
+__device__ __forceinline__ int scale_of(const int64_t* pre, int64_t e) {
+  int si = 0;
+#pragma unroll
+  for (int step = 16; step; step >>= 1)
+    if (pre[si + step] <= e) si += step;
+  return si;
+}
+
+// Neighbour maps of scales above the base: the parent-cell search of the
+// first conv layer, one wave per tile of 16 voxels.
+__global__ void __launch_bounds__(256) k_nbr_cells(int lo, int nsc, int b0, RowMap rm,
+                                                   const uint64_t* __restrict__ lv_key, int64_t cap_pts,
+                                                   const HashSlot* __restrict__ hash, int hash_lg,
+                                                   int32_t* __restrict__ nbr) {
+  __shared__ uint64_t s_par[4][16][8];
+  __shared__ int64_t s_pre[32], s_mo[32], s_tpre[32];
+  const int tid = threadIdx.x, w = tid >> 6, lane = tid & 63, r = lane & 15, g = lane >> 4;
+  if (tid == 0) {
+    int64_t acc = 0;
+    for (int i = 0; i < nsc; ++i) {
+      int64_t o, n;
+      scale_span(rm, lo + i, o, n);
+      s_tpre[i] = acc;
+      s_pre[i] = n;
+      s_mo[i] = o;
+      acc += (n + 15) / 16;
+    }
+    for (int i = nsc; i < 32; ++i) s_tpre[i] = acc;
+  }
+  __syncthreads();
+  const int64_t total = s_tpre[31];
+  for (int64_t tile = (int64_t)blockIdx.x * 4 + w; tile < total; tile += (int64_t)gridDim.x * 4) {
+    const int si = scale_of(s_tpre, tile);
+    const int b = lo + si;
+    const int64_t n = s_pre[si], mo = s_mo[si];
+    const int64_t row = (tile - s_tpre[si]) * 16 + r;
+    const bool valid = row < n;
+    const int64_t vr = valid ? row : n - 1;  // idle lanes search a real voxel
+    int32_t nb[8];
+    parent_cell_rows(lv_key[(int64_t)(b - b0) * cap_pts + vr], b, g, hash, hash_lg, s_par[w][r], nb);
+    if (valid) {
+      int4* dst = reinterpret_cast<int4*>(nbr + (mo + vr) * NBR_STRIDE + 8 * g);
+      dst[0] = make_int4(nb[0], nb[1], nb[2], nb[3]);
+      dst[1] = make_int4(nb[4], nb[5], nb[6], nb[7]);
+    }
+  }
+}
+
+// Neighbour map of the base scale (its parent scale is not stored): binary
+// search of each neighbour cell among the scale's sorted Morton keys, one
+// thread per (voxel, map entry); entries 27 .. are -1.
+__global__ void __launch_bounds__(256) k_nbr_base(int b0, RowMap rm, const uint64_t* __restrict__ key,
+                                                  int32_t* __restrict__ nbr) {
+  int64_t mo, n;
+  scale_span(rm, b0, mo, n);
+  const int lim = 1 << b0;
+  for (int64_t t = (int64_t)blockIdx.x * 256 + threadIdx.x; t < n * NBR_STRIDE; t += (int64_t)gridDim.x * 256) {
+    const int64_t i = t / NBR_STRIDE;
+    const int k = (int)(t % NBR_STRIDE);
+    int32_t out = -1;
+    if (k < 27) {
+      const uint64_t u = key[i];
+      const int x = (int)compact3(u) + k % 3 - 1, y = (int)compact3(u >> 1) + (k / 3) % 3 - 1,
+                z = (int)compact3(u >> 2) + k / 9 - 1;
+      if (x >= 0 && y >= 0 && z >= 0 && x < lim && y < lim && z < lim) {
+        const uint64_t want = morton3((uint32_t)x, (uint32_t)y, (uint32_t)z);
+        int64_t a = 0, e = n;
+        while (a < e) {
+          const int64_t mid = (a + e) >> 1;
+          if (key[mid] < want) a = mid + 1;
+          else e = mid;
+        }
+        if (a < n && key[a] == want) out = (int32_t)a;
+      }
+    }
+    nbr[(mo + i) * NBR_STRIDE + k] = out;
+  }
+}
+
+// X[row of u] = Emb_O[O_d[u]] for every voxel u of scales lo .. (Eq. 6 input),
+// one thread per 4 channels.
+template <int C>
+__global__ void __launch_bounds__(256) k_embed_codes(int lo, int nsc, int b0, RowMap rm,
+                                                     const uint8_t* __restrict__ lv_code, int64_t cap_pts,
+                                                     const float* __restrict__ emb, float* __restrict__ X) {
+  constexpr int Q = C / 4;
+  __shared__ int64_t s_pre[32], s_mo[32];
+  if (threadIdx.x == 0) row_prefix(rm, lo, nsc, s_pre, s_mo);
+  __syncthreads();
+  const int64_t total = s_pre[31] * Q;
+  for (int64_t t = (int64_t)blockIdx.x * 256 + threadIdx.x; t < total; t += (int64_t)gridDim.x * 256) {
+    const int64_t e = t / Q;
+    const int q = (int)(t % Q);
+    const int si = scale_of(s_pre, e);
+    const int64_t u = e - s_pre[si];
+    const int code = lv_code[(int64_t)(lo + si - b0) * cap_pts + u];
+    reinterpret_cast<f4*>(X + (s_mo[si] + u) * C)[q] = reinterpret_cast<const f4*>(emb + code * C)[q];
+  }
+}
+
+// X[row of v] = F[row of parent(v) in scale b-1] + Emb_D[delta(v)] for every
+// voxel v of scales lo .. (replication, Eq. 7, plus octant embedding, Eq. 8).
+template <int C>
+__global__ void __launch_bounds__(256) k_target_embed(int lo, int nsc, int b0, RowMap rm,
+                                                      const int32_t* __restrict__ lv_parent,
+                                                      const uint16_t* __restrict__ lv_feat, int64_t cap_pts,
+                                                      const float* __restrict__ F, const float* __restrict__ emb,
+                                                      float* __restrict__ X) {
+  constexpr int Q = C / 4;
+  __shared__ int64_t s_pre[32], s_mo[32], s_pmo[32];
+  if (threadIdx.x == 0) {
+    row_prefix(rm, lo, nsc, s_pre, s_mo);
+    for (int i = 0; i < nsc; ++i) {
+      int64_t o, n;
+      scale_span(rm, lo + i - 1, o, n);
+      s_pmo[i] = o;
+    }
+  }
+  __syncthreads();
+  const int64_t total = s_pre[31] * Q;
+  for (int64_t t = (int64_t)blockIdx.x * 256 + threadIdx.x; t < total; t += (int64_t)gridDim.x * 256) {
+    const int64_t e = t / Q;
+    const int q = (int)(t % Q);
+    const int si = scale_of(s_pre, e);
+    const int64_t v = e - s_pre[si];
+    const int64_t lvb = (int64_t)(lo + si - b0) * cap_pts;
+    const int64_t p = lv_parent[lvb + v];
+    const int delta = lv_feat[lvb + v] & 7;
+    const f4 f = reinterpret_cast<const f4*>(F + (s_pmo[si] + p) * C)[q];
+    const f4 d = reinterpret_cast<const f4*>(emb + delta * C)[q];
+    reinterpret_cast<f4*>(X + (s_mo[si] + v) * C)[q] = f + d;
   }
 }
 
@@ -883,7 +1072,16 @@ hipError_t launch_pack_weights(Ctx& c, const reno_weights& w) {
   const int C = c.p.channels;
   int c_in = RENO_IN_FEATURES;
   const bool bf = c.p.precision == RENO_PREC_BF16X3;
-  for (int l = 0; l < c.p.layers; ++l) {
+  if (c.p.model_mode == RENO_MODEL_TOP) {  // four C -> C convs (fp32) and the two embeddings
+    for (int l = 0; l < 4; ++l) {
+      hipLaunchKernelGGL(k_pack_conv, dim3(64), dim3(256), 0, c.stream, w.top_w[l], C, C, C / 4, C / 4,
+                         c.w_conv[l]);
+      hipLaunchKernelGGL(k_copy_f32, dim3(1), dim3(256), 0, c.stream, w.top_b[l], c.w_bias[l], C);
+    }
+    hipLaunchKernelGGL(k_copy_f32, dim3(32), dim3(256), 0, c.stream, w.emb_o, c.w_embo, 256 * C);
+    hipLaunchKernelGGL(k_copy_f32, dim3(1), dim3(256), 0, c.stream, w.emb_d, c.w_embd, 8 * C);
+  }
+  for (int l = 0; l < c.p.layers && c.p.model_mode != RENO_MODEL_TOP; ++l) {
     const int KS = (c_in + 3) / 4;
     const int KSP = (KS + 3) & ~3;
     if (bf)
@@ -927,7 +1125,104 @@ hipError_t launch_pack_weights(Ctx& c, const reno_weights& w) {
   return hipGetLastError();
 }
 
+// Full predictor on the scales b_lo .. b_hi (Sec. 3.2, Eqs. 6-9):
+//   X_A = Emb_O[O^{d-1}]                       on scales b_lo-1 .. b_hi-1  (h_c)
+//   F_A = ReLU(X_A + conv_A2(ReLU(conv_A1(X_A))))                           (T: h_b, F_A: h_d)
+//   X_B = F_A[parent] + Emb_D[delta]            on scales b_lo .. b_hi      (h_c)
+//   F_B = ReLU(X_B + conv_B2(ReLU(conv_B1(X_B)))), fused with the head      (T: h_b, F_B: h_a)
+// The base scale's rows live past the zero row; F_B of earlier calls is never
+// overwritten (code lengths of a scale stay valid after the next scale's call).
+hipError_t launch_top(Ctx& c, int b_lo, int b_hi, float* logits, bool second) {
+  const int b0 = c.b0();
+  const int64_t ext_off = c.cap_model + 1;
+  const RowMap rm{c.d_count, c.d_moff, (int64_t)c.cap_model, b0, ext_off, c.cap_rows()};
+  const int C = c.p.channels;
+  const int n_lo = b_lo - 1;  // stage A runs one scale below stage B
+  {
+    ProfScope ps_(c, RENO_K_TOP_INPUT);
+    const int blocks = (int)std::min<int64_t>(4096, (c.cap_rows() + 63) / 64);
+    if (n_lo == b0)
+      hipLaunchKernelGGL(k_nbr_base, dim3((unsigned)std::min<int64_t>(4096, (c.cap_pts * NBR_STRIDE + 255) / 256)),
+                         dim3(256), 0, c.stream, b0, rm, c.lv_key + c.lv(b0), c.d_nbr);
+    const int c_lo = std::max(n_lo, b0 + 1);
+    if (c_lo <= b_hi)
+      hipLaunchKernelGGL(k_nbr_cells, dim3(blocks), dim3(256), 0, c.stream, c_lo, b_hi - c_lo + 1, b0, rm, c.lv_key,
+                         (int64_t)c.cap_pts, c.d_hash, c.hash_lg, c.d_nbr);
+  }
+  ConvArgs a{};
+  a.b0 = b0;
+  a.count = c.d_count;
+  a.moff = c.d_moff;
+  a.cap_pts = c.cap_pts;
+  a.cap_model = c.cap_model;
+  a.lv_key = c.lv_key;
+  a.lv_feat = c.lv_feat;
+  a.hash = c.d_hash;
+  a.hash_lg = c.hash_lg;
+  a.nbr = c.d_nbr;
+  a.zero_feat = (int64_t)c.nlv * c.cap_pts;
+  a.hb = c.w_hbias;
+  a.hw = c.w_head;
+  a.lse = c.d_lse;
+  a.err = c.d_err;
+  a.emb = c.w_emb;
+  a.s1_code = second ? c.lv_code : nullptr;
+  a.lse2 = c.d_lse2;
+  a.s1_out = c.d_s1;
+  a.b_ext = b0;
+  a.ext_off = ext_off;
+  a.cap_rows = c.cap_rows();
+  const bool two = c.p.head_mode == RENO_HEAD_TWO_STAGE;
+  if (b_lo != b_hi || b_lo >= c.B - 3) {  // sorted tiles, as for the plain model
+    ProfScope pso_(c, RENO_K_OTHER);
+    const int nsc = b_hi - n_lo + 1;
+    const int64_t windows = (c.cap_model + c.cap_pts + TO_W - 1) / TO_W + nsc;
+    hipLaunchKernelGGL(k_tile_order, dim3((unsigned)windows), dim3(TO_THREADS), 0, c.stream, n_lo, nsc, rm, c.d_nbr,
+                       c.d_perm);
+    a.perm = c.d_perm;
+  }
+  const int eblocks = (int)std::min<int64_t>(8192, (c.cap_rows() * (C / 4) + 255) / 256);
+  hipError_t e = hipSuccess;
+  auto conv = [&](int lo, int hi, int wi, const float* in, float* out, const float* res, bool last) {
+    if (e != hipSuccess) return;
+    a.b_lo = lo;
+    a.b_hi = hi;
+    a.h_in = in;
+    a.h_out = out;
+    a.res = res;
+    a.w = c.w_conv[wi];
+    a.bias = c.w_bias[wi];
+    a.logits = last ? logits : nullptr;
+    ProfScope ps_(c, last ? RENO_K_CONV_LAST : RENO_K_CONV_MID);
+    e = (C == 32) ? run_layer<32, false>(c, false, last, two, a) : run_layer<16, false>(c, false, last, two, a);
+  };
+  {
+    ProfScope ps_(c, RENO_K_TOP_INPUT);
+    if (C == 32)
+      hipLaunchKernelGGL(k_embed_codes<32>, dim3(eblocks), dim3(256), 0, c.stream, n_lo, b_hi - n_lo, b0, rm,
+                         c.lv_code, (int64_t)c.cap_pts, c.w_embo, c.h_c);
+    else
+      hipLaunchKernelGGL(k_embed_codes<16>, dim3(eblocks), dim3(256), 0, c.stream, n_lo, b_hi - n_lo, b0, rm,
+                         c.lv_code, (int64_t)c.cap_pts, c.w_embo, c.h_c);
+  }
+  conv(n_lo, b_hi - 1, 0, c.h_c, c.h_b, nullptr, false);
+  conv(n_lo, b_hi - 1, 1, c.h_b, c.h_d, c.h_c, false);
+  if (e == hipSuccess) {
+    ProfScope ps_(c, RENO_K_TOP_INPUT);
+    if (C == 32)
+      hipLaunchKernelGGL(k_target_embed<32>, dim3(eblocks), dim3(256), 0, c.stream, b_lo, b_hi - b_lo + 1, b0, rm,
+                         c.lv_parent, c.lv_feat, (int64_t)c.cap_pts, c.h_d, c.w_embd, c.h_c);
+    else
+      hipLaunchKernelGGL(k_target_embed<16>, dim3(eblocks), dim3(256), 0, c.stream, b_lo, b_hi - b_lo + 1, b0, rm,
+                         c.lv_parent, c.lv_feat, (int64_t)c.cap_pts, c.h_d, c.w_embd, c.h_c);
+  }
+  conv(b_lo, b_hi, 2, c.h_c, c.h_b, nullptr, false);
+  conv(b_lo, b_hi, 3, c.h_b, c.h_a, c.h_c, true);
+  return e == hipSuccess ? hipGetLastError() : e;
+}
+
 hipError_t launch_model(Ctx& c, int b_lo, int b_hi, float* logits, bool second) {
+  if (c.p.model_mode == RENO_MODEL_TOP) return launch_top(c, b_lo, b_hi, logits, second);
   ConvArgs a{};
   a.b_lo = b_lo;
   a.b_hi = b_hi;
@@ -956,14 +1251,17 @@ hipError_t launch_model(Ctx& c, int b_lo, int b_hi, float* logits, bool second) 
   // or one of the three finest model scales (small scales are latency-bound
   // and would only pay for the extra launch)
   const bool order = L >= 2 && (b_lo != b_hi || b_lo >= c.B - 3);
+  a.b_ext = -1;
+  a.cap_rows = c.cap_model + 1;
+  const RowMap rm{c.d_count, c.d_moff, (int64_t)c.cap_model, -1, 0, (int64_t)c.cap_model + 1};
   hipError_t e = hipSuccess;
   for (int l = 0; l < L && e == hipSuccess; ++l) {
     if (l == 1 && order) {
       ProfScope pso_(c, RENO_K_OTHER);
       const int nsc = b_hi - b_lo + 1;
       const int64_t windows = (c.cap_model + TO_W - 1) / TO_W + nsc;
-      hipLaunchKernelGGL(k_tile_order, dim3((unsigned)windows), dim3(TO_THREADS), 0, c.stream, b_lo, nsc, c.d_count,
-                         c.d_moff, (int64_t)c.cap_model, c.d_nbr, c.d_perm);
+      hipLaunchKernelGGL(k_tile_order, dim3((unsigned)windows), dim3(TO_THREADS), 0, c.stream, b_lo, nsc, rm,
+                         c.d_nbr, c.d_perm);
       a.perm = c.d_perm;
     }
     a.h_in = (l & 1) ? c.h_a : c.h_b;   // layer l reads what layer l-1 wrote

@@ -76,7 +76,6 @@ __global__ void __launch_bounds__(CL_THREADS) k_code_length(
     const int64_t mo = moff[b];
     const int64_t n = count[b];
     const int64_t cib = ch - s_cpre[si];  // chunk index inside the scale
-    const int64_t nch = s_cpre[si + 1] - s_cpre[si];
     const int64_t v = cib * CL_CHUNK + lane;
     const int64_t vv = v < n ? v : n - 1;  // clamped: every load is issued
     const int o = lv_code[(int64_t)(b - b0) * cap_pts + vv];

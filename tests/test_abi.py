@@ -54,7 +54,8 @@ def test_create_rejects_bad_params_without_gpu():
                 range_m=131.0, in_features=11, channels=32, layers=3)
     bad_cases = [dict(max_points=0), dict(max_bit_depth=22), dict(min_bit_depth=12),
                  dict(range_m=-1.0), dict(range_m=float("inf")), dict(in_features=8),
-                 dict(channels=24), dict(layers=0), dict(layers=9), dict(max_points=1 << 30)]
+                 dict(channels=24), dict(layers=0), dict(layers=9), dict(max_points=1 << 30),
+                 dict(model_mode=2), dict(model_mode=reno.RENO_MODEL_TOP, precision=reno.RENO_PREC_BF16X3)]
     for bad in bad_cases:
         p = reno.reno_params(**{**good, **bad})
         rc = L.reno_create(ctypes.byref(p), None, ctypes.byref(h))
