@@ -115,14 +115,14 @@ class Codec:
     step over a resident frame.  The decoder's symbols come from the encoder
     (a stand-in for an instant entropy decoder)."""
 
-    def __init__(self, reno, torch, cfg, pts, M, cap_model, stream, w_np, two_stage, precision=0):
+    def __init__(self, reno, torch, cfg, pts, M, cap_model, stream, w_np, two_stage, precision=0, top=False):
         self.reno, self.torch, self.stream = reno, torch, stream
         B, b0, C, L = cfg.bit_depth, cfg.min_bit_depth, cfg.channels, cfg.layers
         self.B, self.b0, self.C, self.two_stage = B, b0, C, two_stage
         wd = reno.weights_to_device(w_np)
         with torch.cuda.stream(stream):
             mk = lambda: reno.Context(M, B, b0, cfg.range_m, C, L, max_model_voxels=cap_model,
-                                      stream=stream, two_stage=two_stage, precision=precision)
+                                      stream=stream, two_stage=two_stage, precision=precision, top=top)
             self.enc, self.dec = mk(), mk()
             self.enc.set_weights(wd)
             self.dec.set_weights(wd)
@@ -348,6 +348,7 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-two-stage", action="store_true", help="skip the two-stage head measurement")
     ap.add_argument("--no-bf16x3", action="store_true", help="skip the split-bf16 precision measurement")
+    ap.add_argument("--no-top", action="store_true", help="skip the full-predictor measurement")
     ap.add_argument("--e2e-frames", type=int, default=20,
                     help="frames for the end-to-end (GPU + host rANS) measurement (0 to skip)")
     ap.add_argument("--stream-config", default="stream10_hdl64_b14",
@@ -472,6 +473,38 @@ def main():
                "conv_last_frac_of_bf16_peak": round(tfb / PEAK_BF16_MFMA_TFLOPS, 4)}
         log("bf16x3", bfx)
         bc.close()
+
+    # ---- the full target occupancy predictor (occupancy embedding and a
+    # residual block on the parent scale, replication + octant embedding and a
+    # residual block on the target scale), both heads, same frame ----
+    topm = None
+    if not args.no_top:
+        topm = {}
+        for name, is_two in (("one_stage", False), ("two_stage", True)):
+            wt = gen_weights(C, L, seed=cfg.weight_seed, two_stage=is_two, top=True)
+            tc = Codec(reno, torch, cfg, pts, M, cap_model, stream, wt, two_stage=is_two, top=True)
+            st = max(args.steps // 2, 1)
+            mst = tc.time(st, args.warmup, args.mode)
+            clt_ms, clt_n = tc.profile_conv_last(st)
+            tft = tc.conv_last_flops(counts) * st / (clt_ms * 1e-3) / 1e12
+            with torch.cuda.stream(stream):
+                tc.enc.profile(kinds)
+                tc.dec.profile(kinds)
+                for _ in range(nb):
+                    tc.step()
+                pe, pd = tc.enc.profile_read(), tc.dec.profile_read()
+                tc.enc.profile([])
+                tc.dec.profile([])
+            kinds_us = {k: round(1000.0 * (pe.get(k, (0.0, 0))[0] + pd.get(k, (0.0, 0))[0]) / nb, 2)
+                        for k in kinds if k in pe or k in pd}
+            topm[name] = {"value": round(1000.0 / mst, 2), "unit": "frames/s", "ms_per_step": round(mst, 5),
+                          "steps": st, "bits_per_point": round(tc.enc_total / M, 4),
+                          "conv_last_avg_launch_us": round(1000 * clt_ms / clt_n, 2),
+                          "conv_last_achieved_tflops": round(tft, 3),
+                          "conv_last_frac": round(tft / PEAK_FP32_MFMA_TFLOPS, 4),
+                          "us_per_frame_by_kind": kinds_us}
+            log("full predictor", name, topm[name])
+            tc.close()
 
     # ---- end to end: GPU model + host rANS per scale, both heads ----
     e2e = None
@@ -601,6 +634,7 @@ def main():
         "kernels": breakdown,
         "two_stage_head": two,
         "precision_bf16x3": bfx,
+        "full_predictor": topm,
         "end_to_end": e2e,
         "multi_frame": multi,
     }

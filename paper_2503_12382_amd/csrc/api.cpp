@@ -238,6 +238,8 @@ reno_status reno_create(const reno_params* p, void* hip_stream, reno_ctx** out) 
     e = hipMemsetAsync(c->h_b + (size_t)cap_model * C, 0, sizeof(float) * C, c->stream);
   if (e == hipSuccess && top)
     e = hipMemsetAsync(c->h_c + (size_t)cap_model * C, 0, sizeof(float) * C, c->stream);
+  if (e == hipSuccess && top)
+    e = hipMemsetAsync(c->h_d + (size_t)cap_model * C, 0, sizeof(float) * C, c->stream);
   if (e == hipSuccess) e = hipMemsetAsync(c->lv_feat + lvn, 0, 16, c->stream);
   if (e == hipSuccess) e = hipStreamSynchronize(c->stream);
   if (e != hipSuccess) {

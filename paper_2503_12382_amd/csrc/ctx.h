@@ -77,8 +77,8 @@ struct Ctx {
   // model buffers (packed model rows: scale b at d_moff[b] ..)
   float* h_a = nullptr;         // [cap_rows][C]
   float* h_b = nullptr;
-  float* h_c = nullptr;         // full predictor: embedding inputs X (with a zero row)
-  float* h_d = nullptr;         // full predictor: F of the scale below
+  float* h_c = nullptr;         // full predictor: X_A = Emb_O[O] of the parent scales (with a zero row)
+  float* h_d = nullptr;         // full predictor: X_B of the target scales (with a zero row)
   int32_t* d_nbr = nullptr;     // [cap_rows][NBR_STRIDE]
   int32_t* d_perm = nullptr;    // [cap_rows] tile order of the conv layers after the first
   float* d_lse = nullptr;       // [cap_model] (two-stage head: stage 1)

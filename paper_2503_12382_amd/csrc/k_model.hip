@@ -267,6 +267,12 @@ struct ConvArgs {
   int b_ext;              // scale whose rows live past the zero row (the base scale), or -1
   int64_t ext_off;        // first packed row of that scale (cap_model + 1)
   int64_t cap_rows;       // rows of the feature buffers
+  // replication + octant embedding fused into the epilogue (Eqs. 7-8): each
+  // voxel's result F, plus Emb_D[delta], goes to the rows of its children
+  float* xb;              // child rows' input X_B (rows of scale b + 1), or NULL
+  const float* emb_d;     // [8][C]
+  const uint8_t* code;    // per-scale regions: O_b
+  const int32_t* fc;      // per-scale regions: first child row in V_{b+1}
 };
 
 // Packed-row layout of the scales: scale b at moff[b] .. below the reserved
@@ -626,7 +632,26 @@ __global__ void __launch_bounds__(CONV_THREADS) k_conv(ConvArgs a) {
     for (int cb = 0; cb < NCB; ++cb)
 #pragma unroll
       for (int e = 0; e < 4; ++e) acc[cb][e] = fmaxf(acc[cb][e], 0.0f);
-    if (valid) {
+    if (a.xb && valid) {  // children v of this voxel u: X_B[v] = F[u] + Emb_D[delta(v)]
+      int64_t cmo = a.moff[b + 1];
+      const int64_t cn = a.count[b + 1];
+      const uint32_t code = a.code[lvb + (prow - mo)];
+      const int64_t first = a.fc[lvb + (prow - mo)];
+      if (cmo + cn > a.cap_model) cmo = -1;  // overflow (latched where the size was made): no writes
+      int rank = 0;
+#pragma unroll
+      for (int d = 0; d < 8; ++d) {
+        if (cmo >= 0 && ((code >> d) & 1u)) {
+          float* dst = a.xb + (cmo + first + rank) * C;
+#pragma unroll
+          for (int cb = 0; cb < NCB; ++cb)
+            *reinterpret_cast<f4*>(dst + 16 * cb + 4 * g) =
+                acc[cb] + *reinterpret_cast<const f4*>(a.emb_d + d * C + 16 * cb + 4 * g);
+          ++rank;
+        }
+      }
+    }
+    if (valid && a.h_out) {
       if constexpr (BF && !LAST) {
         // next layer's input as [hi plane | lo plane] of bf16 (split once per voxel)
         uint16_t* row = reinterpret_cast<uint16_t*>(a.h_out + prow * C);
@@ -841,25 +866,10 @@ __global__ void __launch_bounds__(TO_THREADS) k_tile_order(int b_lo, int nsc, Ro
 }
 
 // ---------------------------------------------------------------------------
-// Inputs of the full predictor (Sec. 3.2): neighbour maps of the scales it
-// convolves on, occupancy embeddings Emb_O[O^{d-1}] (Eq. 6) and the target
-// embedding F^{d-1}[parent] + Emb_D[delta] (replication and octant
-// embedding, Eqs. 7-9).  Each launch covers the scales lo .. lo + nsc - 1;
-// elements map to their scale through a row prefix in LDS.
-
-// Prefix of rows over the launch's scales (padded with the total) and the
-// first packed row of each; thread 0 fills them.
-__device__ __forceinline__ void row_prefix(const RowMap& m, int lo, int nsc, int64_t* pre, int64_t* mo) {
-  int64_t acc = 0;
-  for (int i = 0; i < nsc; ++i) {
-    int64_t o, n;
-    scale_span(m, lo + i, o, n);
-    pre[i] = acc;
-    mo[i] = o;
-    acc += n;
-  }
-  for (int i = nsc; i < 32; ++i) pre[i] = acc;
-}
+// Inputs of the full predictor (Sec. 3.2): the neighbour maps of the scales
+// it convolves on and the occupancy embeddings X_A = Emb_O[O^{d-1}] (Eq. 6),
+// in one launch; one wave per tile of 16 voxels of the scales lo ..
+// lo + nsc - 1, the first n_embed of which also get X_A rows.
 
 // Last index si with pre[si] <= e (pre non-decreasing, 32 entries, pre[0] = 0
 // <= e): binary lifting, si + step never exceeds 31.
@@ -871,24 +881,58 @@ __device__ __forceinline__ int scale_of(const int64_t* pre, int64_t e) {
   return si;
 }
 
-// Neighbour maps of scales above the base: the parent-cell search of the
-// first conv layer, one wave per tile of 16 voxels.
-__global__ void __launch_bounds__(256) k_nbr_cells(int lo, int nsc, int b0, RowMap rm,
-                                                   const uint64_t* __restrict__ lv_key, int64_t cap_pts,
-                                                   const HashSlot* __restrict__ hash, int hash_lg,
-                                                   int32_t* __restrict__ nbr) {
+// Neighbour rows of a voxel of the base scale, whose parent scale is not
+// stored: the 8 cells of lane group g located among the scale's n sorted
+// Morton keys by 8 interleaved searches for the last key <= the cell
+// (wave-uniform trip count; every probe stays below n).
+__device__ __forceinline__ void base_cell_rows(uint64_t key, int b, int g, const uint64_t* __restrict__ keys,
+                                               int64_t n, int32_t (&nb)[8]) {
+  const int x = (int)compact3(key), y = (int)compact3(key >> 1), z = (int)compact3(key >> 2);
+  const int lim = 1 << b;
+  uint64_t want[8];
+  bool ok[8];
+  int64_t at[8];
+#pragma unroll
+  for (int j = 0; j < 8; ++j) {
+    const int k = 8 * g + j;
+    const int ux = x + (k % 3) - 1, uy = y + (k / 3) % 3 - 1, uz = z + (k / 9) % 3 - 1;
+    ok[j] = k < 27 && ux >= 0 && uy >= 0 && uz >= 0 && ux < lim && uy < lim && uz < lim;
+    want[j] = ok[j] ? morton3((uint32_t)ux, (uint32_t)uy, (uint32_t)uz) : 0ull;
+    at[j] = 0;
+  }
+  for (int64_t len = n; len > 1;) {
+    const int64_t half = len >> 1;
+#pragma unroll
+    for (int j = 0; j < 8; ++j) at[j] += (keys[at[j] + half] <= want[j]) ? half : 0;
+    len -= half;
+  }
+#pragma unroll
+  for (int j = 0; j < 8; ++j) nb[j] = (ok[j] && keys[at[j]] == want[j]) ? (int32_t)at[j] : -1;
+}
+
+template <int C>
+__global__ void __launch_bounds__(256) k_top_prep(int lo, int nsc, int n_embed, int b0, RowMap rm,
+                                                  const uint64_t* __restrict__ lv_key,
+                                                  const uint8_t* __restrict__ lv_code, int64_t cap_pts,
+                                                  const HashSlot* __restrict__ hash, int hash_lg,
+                                                  const float* __restrict__ emb_o, int32_t* __restrict__ nbr,
+                                                  float* __restrict__ X) {
+  constexpr int Q = C / 16;  // f4 per lane of a row
   __shared__ uint64_t s_par[4][16][8];
-  __shared__ int64_t s_pre[32], s_mo[32], s_tpre[32];
+  __shared__ int64_t s_n[32], s_mo[32], s_tpre[32];
   const int tid = threadIdx.x, w = tid >> 6, lane = tid & 63, r = lane & 15, g = lane >> 4;
+  if (tid < nsc) {  // sizes of the launch's scales, loaded in parallel
+    int64_t o, n;
+    scale_span(rm, lo + tid, o, n);
+    s_n[tid] = n;
+    s_mo[tid] = o;
+  }
+  __syncthreads();
   if (tid == 0) {
     int64_t acc = 0;
     for (int i = 0; i < nsc; ++i) {
-      int64_t o, n;
-      scale_span(rm, lo + i, o, n);
       s_tpre[i] = acc;
-      s_pre[i] = n;
-      s_mo[i] = o;
-      acc += (n + 15) / 16;
+      acc += (s_n[i] + 15) / 16;
     }
     for (int i = nsc; i < 32; ++i) s_tpre[i] = acc;
   }
@@ -897,103 +941,27 @@ __global__ void __launch_bounds__(256) k_nbr_cells(int lo, int nsc, int b0, RowM
   for (int64_t tile = (int64_t)blockIdx.x * 4 + w; tile < total; tile += (int64_t)gridDim.x * 4) {
     const int si = scale_of(s_tpre, tile);
     const int b = lo + si;
-    const int64_t n = s_pre[si], mo = s_mo[si];
+    const int64_t n = s_n[si], mo = s_mo[si];
     const int64_t row = (tile - s_tpre[si]) * 16 + r;
     const bool valid = row < n;
     const int64_t vr = valid ? row : n - 1;  // idle lanes search a real voxel
+    const int64_t lvb = (int64_t)(b - b0) * cap_pts;
     int32_t nb[8];
-    parent_cell_rows(lv_key[(int64_t)(b - b0) * cap_pts + vr], b, g, hash, hash_lg, s_par[w][r], nb);
+    if (b == rm.b_ext)
+      base_cell_rows(lv_key[lvb + vr], b, g, lv_key + lvb, n, nb);
+    else
+      parent_cell_rows(lv_key[lvb + vr], b, g, hash, hash_lg, s_par[w][r], nb);
     if (valid) {
       int4* dst = reinterpret_cast<int4*>(nbr + (mo + vr) * NBR_STRIDE + 8 * g);
       dst[0] = make_int4(nb[0], nb[1], nb[2], nb[3]);
       dst[1] = make_int4(nb[4], nb[5], nb[6], nb[7]);
-    }
-  }
-}
-
-// Neighbour map of the base scale (its parent scale is not stored): binary
-// search of each neighbour cell among the scale's sorted Morton keys, one
-// thread per (voxel, map entry); entries 27 .. are -1.
-__global__ void __launch_bounds__(256) k_nbr_base(int b0, RowMap rm, const uint64_t* __restrict__ key,
-                                                  int32_t* __restrict__ nbr) {
-  int64_t mo, n;
-  scale_span(rm, b0, mo, n);
-  const int lim = 1 << b0;
-  for (int64_t t = (int64_t)blockIdx.x * 256 + threadIdx.x; t < n * NBR_STRIDE; t += (int64_t)gridDim.x * 256) {
-    const int64_t i = t / NBR_STRIDE;
-    const int k = (int)(t % NBR_STRIDE);
-    int32_t out = -1;
-    if (k < 27) {
-      const uint64_t u = key[i];
-      const int x = (int)compact3(u) + k % 3 - 1, y = (int)compact3(u >> 1) + (k / 3) % 3 - 1,
-                z = (int)compact3(u >> 2) + k / 9 - 1;
-      if (x >= 0 && y >= 0 && z >= 0 && x < lim && y < lim && z < lim) {
-        const uint64_t want = morton3((uint32_t)x, (uint32_t)y, (uint32_t)z);
-        int64_t a = 0, e = n;
-        while (a < e) {
-          const int64_t mid = (a + e) >> 1;
-          if (key[mid] < want) a = mid + 1;
-          else e = mid;
-        }
-        if (a < n && key[a] == want) out = (int32_t)a;
+      if (si < n_embed) {
+        const f4* e = reinterpret_cast<const f4*>(emb_o + (int)lv_code[lvb + vr] * C) + g * Q;
+        f4* xr = reinterpret_cast<f4*>(X + (mo + vr) * C) + g * Q;
+#pragma unroll
+        for (int q = 0; q < Q; ++q) xr[q] = e[q];
       }
     }
-    nbr[(mo + i) * NBR_STRIDE + k] = out;
-  }
-}
-
-// X[row of u] = Emb_O[O_d[u]] for every voxel u of scales lo .. (Eq. 6 input),
-// one thread per 4 channels.
-template <int C>
-__global__ void __launch_bounds__(256) k_embed_codes(int lo, int nsc, int b0, RowMap rm,
-                                                     const uint8_t* __restrict__ lv_code, int64_t cap_pts,
-                                                     const float* __restrict__ emb, float* __restrict__ X) {
-  constexpr int Q = C / 4;
-  __shared__ int64_t s_pre[32], s_mo[32];
-  if (threadIdx.x == 0) row_prefix(rm, lo, nsc, s_pre, s_mo);
-  __syncthreads();
-  const int64_t total = s_pre[31] * Q;
-  for (int64_t t = (int64_t)blockIdx.x * 256 + threadIdx.x; t < total; t += (int64_t)gridDim.x * 256) {
-    const int64_t e = t / Q;
-    const int q = (int)(t % Q);
-    const int si = scale_of(s_pre, e);
-    const int64_t u = e - s_pre[si];
-    const int code = lv_code[(int64_t)(lo + si - b0) * cap_pts + u];
-    reinterpret_cast<f4*>(X + (s_mo[si] + u) * C)[q] = reinterpret_cast<const f4*>(emb + code * C)[q];
-  }
-}
-
-// X[row of v] = F[row of parent(v) in scale b-1] + Emb_D[delta(v)] for every
-// voxel v of scales lo .. (replication, Eq. 7, plus octant embedding, Eq. 8).
-template <int C>
-__global__ void __launch_bounds__(256) k_target_embed(int lo, int nsc, int b0, RowMap rm,
-                                                      const int32_t* __restrict__ lv_parent,
-                                                      const uint16_t* __restrict__ lv_feat, int64_t cap_pts,
-                                                      const float* __restrict__ F, const float* __restrict__ emb,
-                                                      float* __restrict__ X) {
-  constexpr int Q = C / 4;
-  __shared__ int64_t s_pre[32], s_mo[32], s_pmo[32];
-  if (threadIdx.x == 0) {
-    row_prefix(rm, lo, nsc, s_pre, s_mo);
-    for (int i = 0; i < nsc; ++i) {
-      int64_t o, n;
-      scale_span(rm, lo + i - 1, o, n);
-      s_pmo[i] = o;
-    }
-  }
-  __syncthreads();
-  const int64_t total = s_pre[31] * Q;
-  for (int64_t t = (int64_t)blockIdx.x * 256 + threadIdx.x; t < total; t += (int64_t)gridDim.x * 256) {
-    const int64_t e = t / Q;
-    const int q = (int)(t % Q);
-    const int si = scale_of(s_pre, e);
-    const int64_t v = e - s_pre[si];
-    const int64_t lvb = (int64_t)(lo + si - b0) * cap_pts;
-    const int64_t p = lv_parent[lvb + v];
-    const int delta = lv_feat[lvb + v] & 7;
-    const f4 f = reinterpret_cast<const f4*>(F + (s_pmo[si] + p) * C)[q];
-    const f4 d = reinterpret_cast<const f4*>(emb + delta * C)[q];
-    reinterpret_cast<f4*>(X + (s_mo[si] + v) * C)[q] = f + d;
   }
 }
 
@@ -1126,12 +1094,16 @@ hipError_t launch_pack_weights(Ctx& c, const reno_weights& w) {
 }
 
 // Full predictor on the scales b_lo .. b_hi (Sec. 3.2, Eqs. 6-9):
-//   X_A = Emb_O[O^{d-1}]                       on scales b_lo-1 .. b_hi-1  (h_c)
-//   F_A = ReLU(X_A + conv_A2(ReLU(conv_A1(X_A))))                           (T: h_b, F_A: h_d)
-//   X_B = F_A[parent] + Emb_D[delta]            on scales b_lo .. b_hi      (h_c)
-//   F_B = ReLU(X_B + conv_B2(ReLU(conv_B1(X_B)))), fused with the head      (T: h_b, F_B: h_a)
-// The base scale's rows live past the zero row; F_B of earlier calls is never
-// overwritten (code lengths of a scale stay valid after the next scale's call).
+//   neighbour maps of scales b_lo-1 .. b_hi, X_A = Emb_O[O^{d-1}] on scales
+//   b_lo-1 .. b_hi-1 (h_c)                                        one prep launch
+//   T = ReLU(conv_A1(X_A))                                        (h_b)
+//   F_A = ReLU(X_A + conv_A2(T)), scattered to the children as
+//   X_B = F_A[parent] + Emb_D[delta] on scales b_lo .. b_hi       (h_d; F_A itself is not stored)
+//   T = ReLU(conv_B1(X_B))                                        (h_b)
+//   F_B = ReLU(X_B + conv_B2(T)), fused with the head             (h_a)
+// The base scale's rows live past the zero row.  F_B of earlier calls is
+// never overwritten (code lengths of a scale stay valid after the next
+// scale's call).
 hipError_t launch_top(Ctx& c, int b_lo, int b_hi, float* logits, bool second) {
   const int b0 = c.b0();
   const int64_t ext_off = c.cap_model + 1;
@@ -1140,14 +1112,12 @@ hipError_t launch_top(Ctx& c, int b_lo, int b_hi, float* logits, bool second) {
   const int n_lo = b_lo - 1;  // stage A runs one scale below stage B
   {
     ProfScope ps_(c, RENO_K_TOP_INPUT);
-    const int blocks = (int)std::min<int64_t>(4096, (c.cap_rows() + 63) / 64);
-    if (n_lo == b0)
-      hipLaunchKernelGGL(k_nbr_base, dim3((unsigned)std::min<int64_t>(4096, (c.cap_pts * NBR_STRIDE + 255) / 256)),
-                         dim3(256), 0, c.stream, b0, rm, c.lv_key + c.lv(b0), c.d_nbr);
-    const int c_lo = std::max(n_lo, b0 + 1);
-    if (c_lo <= b_hi)
-      hipLaunchKernelGGL(k_nbr_cells, dim3(blocks), dim3(256), 0, c.stream, c_lo, b_hi - c_lo + 1, b0, rm, c.lv_key,
-                         (int64_t)c.cap_pts, c.d_hash, c.hash_lg, c.d_nbr);
+    const int blocks = (int)std::min<int64_t>(2048, (c.cap_rows() + 63) / 64);
+#define RENO_PREP(CC)                                                                                         \
+  hipLaunchKernelGGL(k_top_prep<CC>, dim3(blocks), dim3(256), 0, c.stream, n_lo, b_hi - n_lo + 1, b_hi - n_lo, b0, \
+                     rm, c.lv_key, c.lv_code, (int64_t)c.cap_pts, c.d_hash, c.hash_lg, c.w_embo, c.d_nbr, c.h_c)
+    if (C == 32) RENO_PREP(32); else RENO_PREP(16);
+#undef RENO_PREP
   }
   ConvArgs a{};
   a.b0 = b0;
@@ -1172,6 +1142,9 @@ hipError_t launch_top(Ctx& c, int b_lo, int b_hi, float* logits, bool second) {
   a.b_ext = b0;
   a.ext_off = ext_off;
   a.cap_rows = c.cap_rows();
+  a.emb_d = c.w_embd;
+  a.code = c.lv_code;
+  a.fc = c.lv_fc;
   const bool two = c.p.head_mode == RENO_HEAD_TWO_STAGE;
   if (b_lo != b_hi || b_lo >= c.B - 3) {  // sorted tiles, as for the plain model
     ProfScope pso_(c, RENO_K_OTHER);
@@ -1181,43 +1154,25 @@ hipError_t launch_top(Ctx& c, int b_lo, int b_hi, float* logits, bool second) {
                        c.d_perm);
     a.perm = c.d_perm;
   }
-  const int eblocks = (int)std::min<int64_t>(8192, (c.cap_rows() * (C / 4) + 255) / 256);
   hipError_t e = hipSuccess;
-  auto conv = [&](int lo, int hi, int wi, const float* in, float* out, const float* res, bool last) {
+  auto conv = [&](int lo, int hi, int wi, const float* in, float* out, const float* res, float* xb, bool last) {
     if (e != hipSuccess) return;
     a.b_lo = lo;
     a.b_hi = hi;
     a.h_in = in;
     a.h_out = out;
     a.res = res;
+    a.xb = xb;
     a.w = c.w_conv[wi];
     a.bias = c.w_bias[wi];
     a.logits = last ? logits : nullptr;
     ProfScope ps_(c, last ? RENO_K_CONV_LAST : RENO_K_CONV_MID);
     e = (C == 32) ? run_layer<32, false>(c, false, last, two, a) : run_layer<16, false>(c, false, last, two, a);
   };
-  {
-    ProfScope ps_(c, RENO_K_TOP_INPUT);
-    if (C == 32)
-      hipLaunchKernelGGL(k_embed_codes<32>, dim3(eblocks), dim3(256), 0, c.stream, n_lo, b_hi - n_lo, b0, rm,
-                         c.lv_code, (int64_t)c.cap_pts, c.w_embo, c.h_c);
-    else
-      hipLaunchKernelGGL(k_embed_codes<16>, dim3(eblocks), dim3(256), 0, c.stream, n_lo, b_hi - n_lo, b0, rm,
-                         c.lv_code, (int64_t)c.cap_pts, c.w_embo, c.h_c);
-  }
-  conv(n_lo, b_hi - 1, 0, c.h_c, c.h_b, nullptr, false);
-  conv(n_lo, b_hi - 1, 1, c.h_b, c.h_d, c.h_c, false);
-  if (e == hipSuccess) {
-    ProfScope ps_(c, RENO_K_TOP_INPUT);
-    if (C == 32)
-      hipLaunchKernelGGL(k_target_embed<32>, dim3(eblocks), dim3(256), 0, c.stream, b_lo, b_hi - b_lo + 1, b0, rm,
-                         c.lv_parent, c.lv_feat, (int64_t)c.cap_pts, c.h_d, c.w_embd, c.h_c);
-    else
-      hipLaunchKernelGGL(k_target_embed<16>, dim3(eblocks), dim3(256), 0, c.stream, b_lo, b_hi - b_lo + 1, b0, rm,
-                         c.lv_parent, c.lv_feat, (int64_t)c.cap_pts, c.h_d, c.w_embd, c.h_c);
-  }
-  conv(b_lo, b_hi, 2, c.h_c, c.h_b, nullptr, false);
-  conv(b_lo, b_hi, 3, c.h_b, c.h_a, c.h_c, true);
+  conv(n_lo, b_hi - 1, 0, c.h_c, c.h_b, nullptr, nullptr, false);
+  conv(n_lo, b_hi - 1, 1, c.h_b, nullptr, c.h_c, c.h_d, false);
+  conv(b_lo, b_hi, 2, c.h_d, c.h_b, nullptr, nullptr, false);
+  conv(b_lo, b_hi, 3, c.h_b, c.h_a, c.h_d, nullptr, true);
   return e == hipSuccess ? hipGetLastError() : e;
 }
 
