@@ -68,6 +68,29 @@ def alg_bytes_per_frame(counts, b0, B, M, C, hash_slots, status_words):
     return out
 
 
+def alg_bytes_encoder(counts, b0, B, M, C, hash_slots, status_words, fb):
+    """Minimum HBM bytes of one encoder pass over a frame batch (every input
+    read once, every output written once), per kernel kind; sort passes cover
+    the 3B Morton bits and the fb frame-id bits."""
+    N = {b0 + i: n for i, n in enumerate(counts)}
+    model = [b for b in range(b0 + 1, B)]
+    nm = sum(N[b] for b in model)
+    parents_hashed = sum(N[b] for b in range(b0, B - 1))
+    passes = (3 * B + fb + 7) // 8
+    row = 4 * C
+    return {
+        "zero": 16 * hash_slots + 4 * status_words,
+        "quantize": M * (12 + 8),
+        "sort": passes * M * 16,
+        "pyramid": M * 8 + sum(N[b] * 12 for b in range(b0, B + 1)) + sum(N[b] * 4 for b in range(b0, B)),
+        "codes": sum(N[b + 1] * (8 + 2) + N[b] for b in range(b0, B)) + 16 * parents_hashed,
+        "conv_first": sum(N[b] * (8 + 2 + 4 * 32 + row) + 16 * N[b - 1] for b in model),
+        "conv_mid": nm * (4 * 32 + 2 * row),
+        "conv_last": nm * (4 * 32 + 2 * row) + nm * 4,
+        "code_length": nm * (1 + 4 + row),
+    }
+
+
 def read_traffic():
     """HBM traffic of conv_last per launch from the committed rocprofv3 PMC
     summary, or None when the kernel source changed since it was taken."""
@@ -349,6 +372,9 @@ def main():
     ap.add_argument("--no-two-stage", action="store_true", help="skip the two-stage head measurement")
     ap.add_argument("--no-bf16x3", action="store_true", help="skip the split-bf16 precision measurement")
     ap.add_argument("--no-top", action="store_true", help="skip the full-predictor measurement")
+    ap.add_argument("--stress", default="1,8,64,512",
+                    help="frame-batch sizes K of the HBM stress pass (encoder stages on K frames in one key "
+                         "space); empty to skip")
     ap.add_argument("--e2e-frames", type=int, default=20,
                     help="frames for the end-to-end (GPU + host rANS) measurement (0 to skip)")
     ap.add_argument("--stream-config", default="stream10_hdl64_b14",
@@ -573,6 +599,91 @@ def main():
                 c.close()
         del codecs
 
+    # ---- HBM stress: K frames of the streaming generator (its 10 distinct
+    # frames, cycled) batched into one key space, frame id above the Morton
+    # bits; one encoder pass (pyramid, all model scales, code lengths) per
+    # batch, every launch bracketed with HIP events.  At K = 512 the keys,
+    # levels and feature rows far exceed the 256 MB Infinity Cache ----
+    stress = None
+    if args.stress:
+        scfg = BY_NAME[args.stream_config]
+        sframes = [gen_scan(scfg, f) for f in range(scfg.frames)]
+        sB, sb0, sC, sL = scfg.bit_depth, scfg.min_bit_depth, scfg.channels, scfg.layers
+        sw = reno.weights_to_device(gen_weights(sC, sL, seed=scfg.weight_seed))
+        mv = []
+        for f in sframes:
+            with torch.cuda.stream(stream):
+                pr = reno.Context(f.shape[0], sB, sb0, scfg.range_m, sC, sL, stream=stream)
+                pr.build_pyramid(torch.from_numpy(f).to(dev), sB)
+                mv.append(sum(pr.num_voxels(b) for b in range(sb0 + 1, sB)))
+                pr.close()
+        stress = {"workload": f"{scfg.name}: K frames (its {len(sframes)} distinct scans cycled) in one key "
+                              f"space, {sB}-bit, encoder pass (pyramid, codes + hash, {sL} conv layers + head "
+                              "on every model scale, code lengths)", "runs": []}
+        skinds = ["zero", "quantize", "sort", "pyramid", "codes", "conv_first", "conv_mid", "conv_last",
+                  "code_length", "other"]
+        for K in [int(x) for x in args.stress.split(",") if x]:
+            sel = [sframes[i % len(sframes)] for i in range(K)]
+            start = np.cumsum([0] + [f.shape[0] for f in sel]).astype(np.int64)
+            SM = int(start[-1])
+            cap = sum(mv[i % len(mv)] for i in range(K))
+            cap = (cap + cap // 8 + 4095) // 4096 * 4096
+            pts_d = torch.from_numpy(np.concatenate(sel)).to(dev)
+            st_d = torch.from_numpy(start).to(dev)
+            del sel
+            with torch.cuda.stream(stream):
+                sc = reno.Context(SM, sB, sb0, scfg.range_m, sC, sL, max_model_voxels=cap, stream=stream)
+                sc.set_weights(sw)
+
+                def enc():
+                    sc.build_pyramid_frames(pts_d, st_d, sB)
+                    sc.predict_probs(reno.RENO_ALL_SCALES)
+                    sc.code_length(reno.RENO_ALL_SCALES, per_voxel=False, total=False)
+
+                enc()
+                sc.sync()
+                reps = max(1, min(20, 64 // K))
+                t0 = torch.cuda.Event(enable_timing=True)
+                t1 = torch.cuda.Event(enable_timing=True)
+                t0.record(stream)
+                for _ in range(reps):
+                    enc()
+                t1.record(stream)
+                stream.synchronize()
+                ms = t0.elapsed_time(t1) / reps
+                sc.profile(skinds)
+                enc()
+                prof = sc.profile_read()
+                sc.profile([])
+                sc.sync()
+                cnt = sc.scale_counts()[sb0:sB + 1].tolist()
+                smem = sc.memory_info()
+            fb = max(0, (K - 1).bit_length())
+            alg = alg_bytes_encoder(cnt, sb0, sB, SM, sC, smem["hash_slots"], smem["status_words"], fb)
+            kinds_out = {}
+            for k in skinds:
+                if k not in prof:
+                    continue
+                us = 1000.0 * prof[k][0]
+                e = {"us": round(us, 1), "launches": prof[k][1]}
+                if k in alg:
+                    gbs = alg[k] / (us * 1e-6) / 1e9
+                    e.update({"alg_MB": round(alg[k] / 1e6, 2), "alg_GBs": round(gbs, 1),
+                              "hbm_frac": round(gbs / PEAK_HBM_GBS, 4)})
+                kinds_out[k] = e
+            run = {"K": K, "points": SM, "voxels": int(sum(cnt)), "model_rows_capacity": cap,
+                   "device_bytes": smem["device_bytes"], "encoder_ms_per_batch": round(ms, 4),
+                   "encoder_frames_per_s": round(K * 1000.0 / ms, 1), "kinds": kinds_out}
+            stress["runs"].append(run)
+            log("stress K", K, {k: (v["us"], v.get("hbm_frac")) for k, v in kinds_out.items()},
+                f"{ms:.3f} ms/batch")
+            sc.close()
+            del pts_d, st_d
+            torch.cuda.empty_cache()
+        stress["note"] = ("hbm_frac = algorithmic bytes (each input read once, each output written once) / "
+                          "kernel time / 8 TB/s; sort = all LSD passes, codes = code words + hash build, "
+                          "conv_first = hash probes + first-layer gather, conv_mid = neighbour-row gather")
+
     # ---- CPU baseline: the oracle (single-threaded C++, fp64), one frame per
     # process, first alone, then one process per available core at once ----
     cpu = None
@@ -635,6 +746,7 @@ def main():
         "two_stage_head": two,
         "precision_bf16x3": bfx,
         "full_predictor": topm,
+        "hbm_stress": stress,
         "end_to_end": e2e,
         "multi_frame": multi,
     }

@@ -65,6 +65,7 @@ typedef enum {
 #define RENO_IN_FEATURES 11
 #define RENO_MAX_BIT_DEPTH 21
 #define RENO_ALL_SCALES (-1)
+#define RENO_MAX_FRAMES 1024
 #define RENO_HEAD_ONE_STAGE 0   /* one 256-way softmax over the code (Eq. 10) */
 #define RENO_HEAD_TWO_STAGE 1   /* bitwise two-stage head (Eqs. 11-13) */
 #define RENO_PREC_FP32 0        /* conv layers and heads on fp32 MFMA */
@@ -166,6 +167,28 @@ reno_status reno_build_pyramid(reno_ctx* ctx, const float* points, int64_t n, in
  * ascending Morton order, coordinates in [0, 2^b0)) with codes [n] (1..255). */
 reno_status reno_set_base(reno_ctx* ctx, int bit_depth, const int32_t* xyz, const uint8_t* codes,
                           int64_t n);
+
+/* FRAME BATCH (several independent frames coded as one, for throughput; each
+ * frame is coded exactly as alone, Sec. 3 applied per frame).  The frames
+ * share one key space: a scale-b voxel of frame f has the key
+ * f << 3b | Morton(v), so frames never share a parent, a neighbour or a hash
+ * slot, and every scale's launch covers all frames.  fb = ceil(log2(frames))
+ * bits of frame id sit above the Morton bits; 3 * bit_depth + fb <= 63.
+ *
+ * Encoder: points of frame f are points[frame_start[f] .. frame_start[f+1])
+ * (frame_start: device int64 [frames + 1], 0 = first <= ... <= last = n;
+ * malformed ranges latch RENO_E_INPUT).  1 <= frames <= 1024.  Scale b then
+ * holds every frame's voxels in (frame, Morton) order; coords return the
+ * Morton part, the keys getter the full keys.  Code lengths add the raw
+ * initial state of every frame (32 bits each for the counts).
+ * Decoder: the base voxels carry their frame id (device int32 [n], in
+ * (frame, Morton) strictly ascending order together with xyz; an id outside
+ * [0, frames) latches RENO_E_INPUT); expand and predict then run on all
+ * frames at once.  Device arrays are read on the context stream. */
+reno_status reno_build_pyramid_frames(reno_ctx* ctx, const float* points, int64_t n,
+                                      const int64_t* frame_start, int frames, int bit_depth);
+reno_status reno_set_base_frames(reno_ctx* ctx, int bit_depth, const int32_t* xyz, const int32_t* frame_of,
+                                 const uint8_t* codes, int64_t n, int frames);
 
 /* DECODER step (Sec. 3.1 FCG).  Records O_scale := codes[N_scale] (codes may
  * be NULL when O_scale is already known, i.e. for the base scale after

@@ -26,6 +26,7 @@ RENO_E_INPUT = -6
 RENO_MAX_LAYERS = 8
 RENO_MAX_BIT_DEPTH = 21
 RENO_ALL_SCALES = -1
+RENO_MAX_FRAMES = 1024
 RENO_HEAD_ONE_STAGE = 0
 RENO_HEAD_TWO_STAGE = 1
 RENO_PREC_FP32 = 0
@@ -75,6 +76,8 @@ _SIGS = {
     "reno_set_weights": (_int, [_vp, ctypes.POINTER(reno_weights)]),
     "reno_build_pyramid": (_int, [_vp, _vp, _i64, _int]),
     "reno_set_base": (_int, [_vp, _int, _vp, _vp, _i64]),
+    "reno_build_pyramid_frames": (_int, [_vp, _vp, _i64, _vp, _int, _int]),
+    "reno_set_base_frames": (_int, [_vp, _int, _vp, _vp, _vp, _i64, _int]),
     "reno_expand": (_int, [_vp, _int, _vp]),
     "reno_num_voxels": (_int, [_vp, _int, ctypes.POINTER(_i64)]),
     "reno_scale_counts": (_int, [_vp, _vp]),
@@ -211,6 +214,28 @@ class Context:
         pts = points.contiguous()
         self._check(lib().reno_build_pyramid(self._h, _ptr(pts) if n else None, n, bit_depth))
         self._points = pts
+        self.B = bit_depth
+
+    def build_pyramid_frames(self, points, frame_start, bit_depth: int):
+        """Frame batch: points [n][3] of all frames back to back; frame_start int64
+        device tensor [frames + 1] (frame f = points[frame_start[f]:frame_start[f+1]])."""
+        n = int(points.shape[0])
+        pts = points.contiguous()
+        fs = frame_start.contiguous()
+        frames = int(fs.shape[0]) - 1
+        self._check(lib().reno_build_pyramid_frames(self._h, _ptr(pts) if n else None, n, _ptr(fs), frames,
+                                                    bit_depth))
+        self._points = (pts, fs)
+        self.B = bit_depth
+
+    def set_base_frames(self, bit_depth: int, xyz, frame_of, codes, frames: int):
+        """Frame batch decoder start: base voxels xyz [n][3] with their frame ids
+        (int32 [n]), strictly ascending in (frame, Morton) order."""
+        n = int(xyz.shape[0])
+        x, f, c = xyz.contiguous(), frame_of.contiguous(), codes.contiguous()
+        self._check(lib().reno_set_base_frames(self._h, bit_depth, _ptr(x) if n else None,
+                                               _ptr(f) if n else None, _ptr(c) if n else None, n, frames))
+        self._base = (x, f, c)
         self.B = bit_depth
 
     def set_base(self, bit_depth: int, xyz, codes):

@@ -85,6 +85,7 @@ reno_status sync_check(Ctx* c) {
   if (e & reno::ERR_DUP_KEY) msg += " internal: duplicate hash key;";
   if (e & reno::ERR_INTERNAL) msg += " internal: consistency check failed;";
   if (e & reno::ERR_SYMBOL) msg += " first sub-code outside 0..15;";
+  if (e & reno::ERR_FRAMES) msg += " frame ranges or frame ids of the batch malformed;";
   if (e & (reno::ERR_CAPACITY | reno::ERR_HASH_FULL)) return fail(c, RENO_E_CAPACITY, msg);
   if (e & (reno::ERR_SPIN | reno::ERR_DUP_KEY | reno::ERR_INTERNAL)) return fail(c, RENO_E_HIP, msg);
   return fail(c, RENO_E_INPUT, msg);
@@ -102,6 +103,13 @@ reno_status frame_init(Ctx* c) {
                  sizeof(reno::HashSlot) << c->hash_lg};
   RENO_HIP(c, reno::launch_zero(*c, p, n, 7));
   return RENO_OK;
+}
+
+// frame-id bits of a batch: ceil(log2(frames))
+int frame_bits(int frames) {
+  int fb = 0;
+  while ((1 << fb) < frames) ++fb;
+  return fb;
 }
 
 bool model_scale(const Ctx* c, int b) { return c->B > 0 && b > c->b0() && b < c->B; }
@@ -296,15 +304,26 @@ reno_status reno_set_weights(reno_ctx* c, const reno_weights* w) {
 }
 
 reno_status reno_build_pyramid(reno_ctx* c, const float* points, int64_t n, int bit_depth) {
+  return reno_build_pyramid_frames(c, points, n, nullptr, 1, bit_depth);
+}
+
+reno_status reno_build_pyramid_frames(reno_ctx* c, const float* points, int64_t n, const int64_t* frame_start,
+                                      int frames, int bit_depth) {
   if (!c) return RENO_E_INVALID;
   if (n < 0 || n > c->cap_pts) return fail(c, RENO_E_INVALID, "point count out of range");
   if (n > 0 && !points) return fail(c, RENO_E_INVALID, "null points");
   if (bit_depth <= c->b0() || bit_depth > c->p.max_bit_depth)
     return fail(c, RENO_E_INVALID, "bit_depth must be in (min_bit_depth, max_bit_depth]");
+  if (frames < 1 || frames > RENO_MAX_FRAMES) return fail(c, RENO_E_INVALID, "frames must be in [1, 1024]");
+  if (frames > 1 && !frame_start) return fail(c, RENO_E_INVALID, "null frame_start");
+  const int fb = frame_bits(frames);
+  if (3 * bit_depth + fb > 63) return fail(c, RENO_E_INVALID, "3 * bit_depth + frame-id bits exceed 63");
   const int B = bit_depth;
   c->B = B;
   c->encoder = true;
   c->npoints = n;
+  c->frames = frames;
+  c->fbits = fb;
   c->have_level = bits_range(c->b0(), B);
   c->have_codes = bits_range(c->b0(), B - 1);
   c->have_pred = 0;
@@ -312,8 +331,8 @@ reno_status reno_build_pyramid(reno_ctx* c, const float* points, int64_t n, int 
   reno_status s = frame_init(c);
   if (s != RENO_OK) return s;
   if (n == 0) return RENO_OK;
-  const int passes = (3 * B + reno::RADIX_BITS - 1) / reno::RADIX_BITS;
-  RENO_HIP(c, reno::launch_quantize(*c, points, n, B, passes));
+  const int passes = (3 * B + fb + reno::RADIX_BITS - 1) / reno::RADIX_BITS;
+  RENO_HIP(c, reno::launch_quantize(*c, points, n, B, passes, frames > 1 ? frame_start : nullptr, frames));
   uint64_t* src = c->keys_a;
   uint64_t* dst = c->keys_b;
   for (int ps = 0; ps < passes; ++ps) {
@@ -329,22 +348,33 @@ reno_status reno_build_pyramid(reno_ctx* c, const float* points, int64_t n, int 
 
 reno_status reno_set_base(reno_ctx* c, int bit_depth, const int32_t* xyz, const uint8_t* codes,
                           int64_t n) {
+  return reno_set_base_frames(c, bit_depth, xyz, nullptr, codes, n, 1);
+}
+
+reno_status reno_set_base_frames(reno_ctx* c, int bit_depth, const int32_t* xyz, const int32_t* frame_of,
+                                 const uint8_t* codes, int64_t n, int frames) {
   if (!c) return RENO_E_INVALID;
   if (bit_depth <= c->b0() || bit_depth > c->p.max_bit_depth)
     return fail(c, RENO_E_INVALID, "bit_depth must be in (min_bit_depth, max_bit_depth]");
+  if (frames < 1 || frames > RENO_MAX_FRAMES) return fail(c, RENO_E_INVALID, "frames must be in [1, 1024]");
+  if (frames > 1 && n > 0 && !frame_of) return fail(c, RENO_E_INVALID, "null frame ids");
+  const int fb = frame_bits(frames);
+  if (3 * bit_depth + fb > 63) return fail(c, RENO_E_INVALID, "3 * bit_depth + frame-id bits exceed 63");
   const int64_t grid = int64_t(1) << (3 * c->b0());
-  if (n < 0 || n > c->cap_pts || n > grid) return fail(c, RENO_E_INVALID, "base count out of range");
+  if (n < 0 || n > c->cap_pts || n > grid * frames) return fail(c, RENO_E_INVALID, "base count out of range");
   if (n > 0 && (!xyz || !codes)) return fail(c, RENO_E_INVALID, "null base arrays");
   c->B = bit_depth;
   c->encoder = false;
   c->npoints = 0;
+  c->frames = frames;
+  c->fbits = fb;
   c->have_level = 1u << c->b0();
   c->have_codes = 1u << c->b0();
   c->have_pred = 0;
   c->have_pred2 = 0;
   reno_status s = frame_init(c);
   if (s != RENO_OK) return s;
-  RENO_HIP(c, reno::launch_set_base(*c, xyz, codes, n, bit_depth));
+  RENO_HIP(c, reno::launch_set_base(*c, xyz, frames > 1 ? frame_of : nullptr, codes, n, bit_depth));
   return RENO_OK;
 }
 
@@ -481,7 +511,7 @@ reno_status reno_code_length(reno_ctx* c, int scale, float* bits_per_voxel, doub
                              hipMemcpyDeviceToHost, c->stream));
   reno_status s = sync_check(c);
   if (s != RENO_OK) return s;
-  if (with_base) base_bits = 32.0 + (double)c->h_count[b0] * (3.0 * b0 + 8.0);
+  if (with_base) base_bits = 32.0 * c->frames + (double)c->h_count[b0] * (3.0 * b0 + 8.0);
   double t = base_bits;
   for (int b = lo; b <= hi; ++b) t += c->h_total[b];
   *total_host = t;

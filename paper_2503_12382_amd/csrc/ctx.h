@@ -110,6 +110,8 @@ struct Ctx {
   uint32_t have_pred = 0;       // bit b: TOP evaluated on V_b (two-stage: stage 1)
   uint32_t have_pred2 = 0;      // bit b: stage 2 of the two-stage head evaluated
   int64_t npoints = 0;
+  int frames = 1;               // frames batched in this frame's keys
+  int fbits = 0;                // frame-id bits above the Morton bits (ceil(log2(frames)))
 
   // kernel timing (reno_profile)
   uint32_t prof_mask = 0;
@@ -157,11 +159,13 @@ struct ProfScope {
 
 // ---- kernel launchers (each enqueues on ctx.stream; return hipError_t) ----
 hipError_t launch_zero(Ctx& c, void* const* ptrs, const size_t* bytes, int n);
-hipError_t launch_quantize(Ctx& c, const float* pts, int64_t n, int B, int passes);
+hipError_t launch_quantize(Ctx& c, const float* pts, int64_t n, int B, int passes, const int64_t* frame_start,
+                           int frames);
 hipError_t launch_sort_pass(Ctx& c, const uint64_t* in, uint64_t* out, int64_t n, int pass);
 hipError_t launch_pyramid(Ctx& c, const uint64_t* sorted, int64_t n, int B);
 hipError_t launch_codes(Ctx& c, int B);
-hipError_t launch_set_base(Ctx& c, const int32_t* xyz, const uint8_t* codes, int64_t n, int B);
+hipError_t launch_set_base(Ctx& c, const int32_t* xyz, const int32_t* frame_of, const uint8_t* codes, int64_t n,
+                           int B);
 hipError_t launch_expand(Ctx& c, int b, const uint8_t* codes, int B);
 hipError_t launch_pack_weights(Ctx& c, const reno_weights& w);
 hipError_t launch_model(Ctx& c, int b_lo, int b_hi, float* logits, bool second);

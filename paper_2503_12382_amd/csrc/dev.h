@@ -21,6 +21,7 @@ enum : uint32_t {
   ERR_DUP_KEY = 128u,    // the same key inserted twice (never expected: keys are a set)
   ERR_INTERNAL = 256u,   // an internal consistency check failed (never expected)
   ERR_SYMBOL = 512u,     // a decoded sub-code outside its alphabet (S1 above 15)
+  ERR_FRAMES = 1024u,    // frame ranges or base frame ids of a frame batch malformed
 };
 
 __device__ __forceinline__ void latch(uint32_t* err, uint32_t bit) { atomicOr(err, bit); }
@@ -181,16 +182,25 @@ __device__ __forceinline__ uint32_t lookback_wave(uint32_t* status, int tile, ui
 // first child, so that any cell of the next scale can be resolved from one
 // probe: the child with octant d exists iff bit d of the code is set, and its
 // row is first + popcount(code & ((1 << d) - 1)) (the FCG order).  One table
-// serves every scale of a frame: a scale-b key is tagged with a sentinel bit
-// at position 3b (key < 2^{3b}), which makes tagged keys of different scales
-// distinct and never 0 (0 marks an empty slot).
+// serves every scale of a frame (or of a batch of frames): a scale-b key is
+// tagged with a sentinel bit at position 3b + fb, where fb is the number of
+// frame-id bits kept above the 3b Morton bits (0 for a single frame; key <
+// 2^{3b + fb}), which makes tagged keys of different scales distinct and
+// never 0 (0 marks an empty slot).
 struct alignas(16) HashSlot {
   unsigned long long key;
   int32_t first;   // row of the first child in the next scale
   uint32_t code;   // occupancy code of the voxel
 };
 
-__device__ __forceinline__ uint64_t tag_key(uint64_t key, int b) { return key | (1ull << (3 * b)); }
+__device__ __forceinline__ uint64_t tag_key(uint64_t key, int b, int fb) { return key | (1ull << (3 * b + fb)); }
+
+// A scale-b key of a frame batch: frame id above the 3b Morton bits, so the
+// parent of a key is key >> 3 and keys sort by (frame, Morton order).
+__device__ __forceinline__ uint64_t morton_part(uint64_t key, int b) {
+  return b >= 21 ? key : key & ((1ull << (3 * b)) - 1ull);
+}
+__device__ __forceinline__ uint64_t frame_part(uint64_t key, int b) { return b >= 21 ? 0ull : key >> (3 * b); }
 
 __device__ __forceinline__ uint32_t hash_home(uint64_t tk, int lg) {
   return (uint32_t)((tk * 0x9E3779B97F4A7C15ull) >> (64 - lg));

@@ -9,8 +9,10 @@
 namespace reno {
 namespace {
 
-// Scale b0 from int32 xyz (strictly ascending Morton order) and codes.
+// Scale b0 from int32 xyz and codes, strictly ascending in (frame, Morton)
+// order; a frame batch gives each voxel's frame id (key f << 3b0 | Morton).
 __global__ void __launch_bounds__(256) k_set_base(const int32_t* __restrict__ xyz,
+                                                  const int32_t* __restrict__ frame_of, int frames,
                                                   const uint8_t* __restrict__ codes, int64_t n,
                                                   int b0, uint64_t* __restrict__ key,
                                                   uint8_t* __restrict__ code,
@@ -31,10 +33,22 @@ __global__ void __launch_bounds__(256) k_set_base(const int32_t* __restrict__ xy
     q[a] = (uint32_t)v & (uint32_t)(lim - 1);
   }
   if (!range_ok) latch(err, ERR_BASE_RANGE);
-  const uint64_t k = morton3(q[0], q[1], q[2]);
+  int32_t f = 0, fp = 0;
+  if (frame_of) {
+    f = frame_of[i];
+    if (f < 0 || f >= frames) {
+      latch(err, ERR_FRAMES);
+      f = 0;
+    }
+    if (i > 0) {
+      fp = frame_of[i - 1];
+      fp = (fp < 0 || fp >= frames) ? 0 : fp;
+    }
+  }
+  const uint64_t k = morton3(q[0], q[1], q[2]) | ((uint64_t)f << (3 * b0));
   if (i > 0) {
     for (int a = 0; a < 3; ++a) qp[a] = (uint32_t)xyz[3 * (i - 1) + a] & (uint32_t)(lim - 1);
-    if (morton3(qp[0], qp[1], qp[2]) >= k) latch(err, ERR_BASE_ORDER);
+    if ((morton3(qp[0], qp[1], qp[2]) | ((uint64_t)fp << (3 * b0))) >= k) latch(err, ERR_BASE_ORDER);
   }
   const uint8_t c = codes[i];
   if (c == 0) latch(err, ERR_ZERO_CODE);
@@ -46,6 +60,7 @@ __global__ void __launch_bounds__(256) k_set_base(const int32_t* __restrict__ xy
 struct ExpArgs {
   const uint8_t* codes_in;  // caller codes for O_b, or null (already recorded)
   int b, B;
+  int fb;                   // frame-id bits above the Morton bits
   int64_t cap_pts;
   int64_t cap_model;
   const uint64_t* key_b;
@@ -166,19 +181,20 @@ __global__ void __launch_bounds__(EXP_THREADS) k_expand(ExpArgs a) {
     const int64_t p = base + (int64_t)w * 64 * EXP_KPT + j * 64 + lane;
     if (p >= np) continue;
     const int64_t q = wbase + incl[j] - (uint32_t)__popc(code[j]);
-    hash_insert(a.hash, a.hash_lg, tag_key(a.key_b[p], a.b), (int32_t)q, code[j], a.err);
+    hash_insert(a.hash, a.hash_lg, tag_key(a.key_b[p], a.b, a.fb), (int32_t)q, code[j], a.err);
   }
 }
 
 }  // namespace
 
-hipError_t launch_set_base(Ctx& c, const int32_t* xyz, const uint8_t* codes, int64_t n, int B) {
+hipError_t launch_set_base(Ctx& c, const int32_t* xyz, const int32_t* frame_of, const uint8_t* codes, int64_t n,
+                           int B) {
   ProfScope ps_(c, RENO_K_SET_BASE);
   (void)B;
   const int b0 = c.b0();
   int64_t blocks = (n + 255) / 256;
   if (blocks < 1) blocks = 1;
-  hipLaunchKernelGGL(k_set_base, dim3((unsigned)blocks), dim3(256), 0, c.stream, xyz, codes, n, b0,
+  hipLaunchKernelGGL(k_set_base, dim3((unsigned)blocks), dim3(256), 0, c.stream, xyz, frame_of, c.frames, codes, n, b0,
                      c.lv_key + c.lv(b0), c.lv_code + c.lv(b0), c.lv_parent + c.lv(b0), c.d_count,
                      c.d_moff, c.d_err);
   return hipGetLastError();
@@ -190,6 +206,7 @@ hipError_t launch_expand(Ctx& c, int b, const uint8_t* codes, int B) {
   a.codes_in = codes;
   a.b = b;
   a.B = B;
+  a.fb = c.fbits;
   a.cap_pts = c.cap_pts;
   a.cap_model = c.cap_model;
   a.key_b = c.lv_key + c.lv(b);

@@ -267,6 +267,7 @@ struct ConvArgs {
   int b_ext;              // scale whose rows live past the zero row (the base scale), or -1
   int64_t ext_off;        // first packed row of that scale (cap_model + 1)
   int64_t cap_rows;       // rows of the feature buffers
+  int fb;                 // frame-id bits above the Morton bits (frame batch), else 0
   // replication + octant embedding fused into the epilogue (Eqs. 7-8): each
   // voxel's result F, plus Emb_D[delta], goes to the rows of its children
   float* xb;              // child rows' input X_B (rows of scale b + 1), or NULL
@@ -338,8 +339,9 @@ __device__ __forceinline__ void stage_lds(const f4* __restrict__ src, f4* dst, i
 // first-child row, from which every neighbour row follows by the FCG order.
 // par is the 8-entry LDS slot of voxel r (shared by the 4 lanes of r); the
 // lane ends with the rows of offsets 8g .. 8g+7 (-1: absent or off-grid).
-__device__ __forceinline__ void parent_cell_rows(uint64_t key, int b, int g, const HashSlot* __restrict__ hash,
-                                                 int hash_lg, volatile uint64_t* par, int32_t (&nb)[8]) {
+__device__ __forceinline__ void parent_cell_rows(uint64_t kf, int b, int g, const HashSlot* __restrict__ hash,
+                                                 int hash_lg, int fb, volatile uint64_t* par, int32_t (&nb)[8]) {
+  const uint64_t key = morton_part(kf, b), fr = frame_part(kf, b) << (3 * (b - 1));
   const int x = (int)compact3(key), y = (int)compact3(key >> 1), z = (int)compact3(key >> 2);
   const int px = x >> 1, py = y >> 1, pz = z >> 1;
   const int sx = (x & 1) ? 1 : -1, sy = (y & 1) ? 1 : -1, sz = (z & 1) ? 1 : -1;
@@ -350,7 +352,7 @@ __device__ __forceinline__ void parent_cell_rows(uint64_t key, int b, int g, con
     const int e = 2 * g + i;
     const int cx = px + ((e & 1) ? sx : 0), cy = py + ((e & 2) ? sy : 0), cz = pz + ((e & 4) ? sz : 0);
     tk[i] = (cx >= 0 && cy >= 0 && cz >= 0 && cx < plim && cy < plim && cz < plim)
-                ? tag_key(morton3((uint32_t)cx, (uint32_t)cy, (uint32_t)cz), b - 1)
+                ? tag_key(fr | morton3((uint32_t)cx, (uint32_t)cy, (uint32_t)cz), b - 1, fb)
                 : 0ull;
   }
   uint2 hit[2];
@@ -460,7 +462,7 @@ __global__ void __launch_bounds__(CONV_THREADS) k_conv(ConvArgs a) {
     int4 nlo, nhi;
     if (FIRST) {
       int32_t nb[8];
-      parent_cell_rows(a.lv_key[lvb + (prow - mo)], b, g, a.hash, a.hash_lg, s_par[w][r], nb);
+      parent_cell_rows(a.lv_key[lvb + (prow - mo)], b, g, a.hash, a.hash_lg, a.fb, s_par[w][r], nb);
       nlo = make_int4(nb[0], nb[1], nb[2], nb[3]);
       nhi = make_int4(nb[4], nb[5], nb[6], nb[7]);
       if (valid) {
@@ -885,8 +887,9 @@ __device__ __forceinline__ int scale_of(const int64_t* pre, int64_t e) {
 // stored: the 8 cells of lane group g located among the scale's n sorted
 // Morton keys by 8 interleaved searches for the last key <= the cell
 // (wave-uniform trip count; every probe stays below n).
-__device__ __forceinline__ void base_cell_rows(uint64_t key, int b, int g, const uint64_t* __restrict__ keys,
+__device__ __forceinline__ void base_cell_rows(uint64_t kf, int b, int g, const uint64_t* __restrict__ keys,
                                                int64_t n, int32_t (&nb)[8]) {
+  const uint64_t key = morton_part(kf, b), fr = kf ^ key;  // frame id bits, in place
   const int x = (int)compact3(key), y = (int)compact3(key >> 1), z = (int)compact3(key >> 2);
   const int lim = 1 << b;
   uint64_t want[8];
@@ -897,7 +900,7 @@ __device__ __forceinline__ void base_cell_rows(uint64_t key, int b, int g, const
     const int k = 8 * g + j;
     const int ux = x + (k % 3) - 1, uy = y + (k / 3) % 3 - 1, uz = z + (k / 9) % 3 - 1;
     ok[j] = k < 27 && ux >= 0 && uy >= 0 && uz >= 0 && ux < lim && uy < lim && uz < lim;
-    want[j] = ok[j] ? morton3((uint32_t)ux, (uint32_t)uy, (uint32_t)uz) : 0ull;
+    want[j] = ok[j] ? (fr | morton3((uint32_t)ux, (uint32_t)uy, (uint32_t)uz)) : 0ull;
     at[j] = 0;
   }
   for (int64_t len = n; len > 1;) {
@@ -914,7 +917,7 @@ template <int C>
 __global__ void __launch_bounds__(256) k_top_prep(int lo, int nsc, int n_embed, int b0, RowMap rm,
                                                   const uint64_t* __restrict__ lv_key,
                                                   const uint8_t* __restrict__ lv_code, int64_t cap_pts,
-                                                  const HashSlot* __restrict__ hash, int hash_lg,
+                                                  const HashSlot* __restrict__ hash, int hash_lg, int fb,
                                                   const float* __restrict__ emb_o, int32_t* __restrict__ nbr,
                                                   float* __restrict__ X) {
   constexpr int Q = C / 16;  // f4 per lane of a row
@@ -950,7 +953,7 @@ __global__ void __launch_bounds__(256) k_top_prep(int lo, int nsc, int n_embed, 
     if (b == rm.b_ext)
       base_cell_rows(lv_key[lvb + vr], b, g, lv_key + lvb, n, nb);
     else
-      parent_cell_rows(lv_key[lvb + vr], b, g, hash, hash_lg, s_par[w][r], nb);
+      parent_cell_rows(lv_key[lvb + vr], b, g, hash, hash_lg, fb, s_par[w][r], nb);
     if (valid) {
       int4* dst = reinterpret_cast<int4*>(nbr + (mo + vr) * NBR_STRIDE + 8 * g);
       dst[0] = make_int4(nb[0], nb[1], nb[2], nb[3]);
@@ -1115,7 +1118,8 @@ hipError_t launch_top(Ctx& c, int b_lo, int b_hi, float* logits, bool second) {
     const int blocks = (int)std::min<int64_t>(2048, (c.cap_rows() + 63) / 64);
 #define RENO_PREP(CC)                                                                                         \
   hipLaunchKernelGGL(k_top_prep<CC>, dim3(blocks), dim3(256), 0, c.stream, n_lo, b_hi - n_lo + 1, b_hi - n_lo, b0, \
-                     rm, c.lv_key, c.lv_code, (int64_t)c.cap_pts, c.d_hash, c.hash_lg, c.w_embo, c.d_nbr, c.h_c)
+                     rm, c.lv_key, c.lv_code, (int64_t)c.cap_pts, c.d_hash, c.hash_lg, c.fbits, c.w_embo, c.d_nbr, \
+                     c.h_c)
     if (C == 32) RENO_PREP(32); else RENO_PREP(16);
 #undef RENO_PREP
   }
@@ -1129,6 +1133,7 @@ hipError_t launch_top(Ctx& c, int b_lo, int b_hi, float* logits, bool second) {
   a.lv_feat = c.lv_feat;
   a.hash = c.d_hash;
   a.hash_lg = c.hash_lg;
+  a.fb = c.fbits;
   a.nbr = c.d_nbr;
   a.zero_feat = (int64_t)c.nlv * c.cap_pts;
   a.hb = c.w_hbias;
@@ -1190,6 +1195,7 @@ hipError_t launch_model(Ctx& c, int b_lo, int b_hi, float* logits, bool second) 
   a.lv_feat = c.lv_feat;
   a.hash = c.d_hash;
   a.hash_lg = c.hash_lg;
+  a.fb = c.fbits;
   a.nbr = c.d_nbr;
   a.zero_feat = (int64_t)c.nlv * c.cap_pts;
   a.hb = c.w_hbias;

@@ -341,8 +341,9 @@ __global__ void k_coords(const uint64_t* __restrict__ key, const int32_t* __rest
   const int64_t n = count[b];
   for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n;
        i += (int64_t)gridDim.x * blockDim.x) {
-    const uint64_t k = key[i];
-    if (keys) keys[i] = k;
+    const uint64_t kf = key[i];
+    if (keys) keys[i] = kf;  // with the frame id of a batch above the Morton bits
+    const uint64_t k = morton_part(kf, b);
     if (xyz) {
       xyz[3 * i + 0] = (int32_t)compact3(k);
       xyz[3 * i + 1] = (int32_t)compact3(k >> 1);

@@ -59,12 +59,20 @@ __device__ __forceinline__ void digits_of_idle(int passes, uint32_t* sh) {
 // ---------------------------------------------------------------------------
 // Quantise + Morton + digit histograms of every sort pass.
 //   u = ((p + R) * 2^B) / (2R) in fp64, q = clamp(floor(u), 0, 2^B - 1).
+//   Frame batch: point i of frame f (frame_start[f] <= i < frame_start[f+1])
+//   gets the key f << 3B | Morton(q).
 __global__ void __launch_bounds__(256) k_quantize(const float* __restrict__ pts, int64_t n, int B,
-                                                  double R, uint64_t* __restrict__ keys,
+                                                  double R, const int64_t* __restrict__ frame_start,
+                                                  int frames, uint64_t* __restrict__ keys,
                                                   uint32_t* __restrict__ hist, int passes,
                                                   uint32_t* err) {
   __shared__ uint32_t sh[MAX_PASSES * RADIX];
   for (int i = threadIdx.x; i < passes * RADIX; i += blockDim.x) sh[i] = 0u;
+  if (frames > 1 && blockIdx.x == 0 && threadIdx.x == 0) {  // frame ranges: 0 = s_0 <= s_1 <= ... <= s_F = n
+    bool ok = frame_start[0] == 0 && frame_start[frames] == n;
+    for (int f = 0; f < frames; ++f) ok = ok && frame_start[f] <= frame_start[f + 1];
+    if (!ok) latch(err, ERR_FRAMES);
+  }
   __syncthreads();
   const double scale = (double)(int64_t(1) << B);
   const double span = 2.0 * R;
@@ -95,7 +103,13 @@ __global__ void __launch_bounds__(256) k_quantize(const float* __restrict__ pts,
       f = f > top ? top : f;
       q[a] = (uint32_t)f;
     }
-    const uint64_t k = morton3(q[0], q[1], q[2]);
+    uint64_t k = morton3(q[0], q[1], q[2]);
+    if (frames > 1) {  // last frame f with frame_start[f] <= i
+      int f = 0;
+      for (int step = 1 << 9; step; step >>= 1)
+        if (f + step < frames && frame_start[f + step] <= i) f += step;
+      k |= (uint64_t)f << (3 * B);
+    }
     keys[i] = k;
     digits_of(k, passes, sh);
   }
@@ -339,7 +353,7 @@ __global__ void __launch_bounds__(256) k_codes(const uint64_t* __restrict__ key,
                                                uint8_t* __restrict__ code,
                                                uint16_t* __restrict__ feat,
                                                const int32_t* __restrict__ count, int b0, int B,
-                                               int64_t cap_pts, HashSlot* hash, int hash_lg,
+                                               int64_t cap_pts, HashSlot* hash, int hash_lg, int fb,
                                                uint32_t* err) {
   __shared__ int64_t s_pre[NLEV + 1];
   if (threadIdx.x == 0) {
@@ -383,7 +397,7 @@ __global__ void __launch_bounds__(256) k_codes(const uint64_t* __restrict__ key,
       if (i < nk) feat[rc + lo + i] = (uint16_t)((kc[i] & 7ull) | (c << 3));
     // parents of model scales go into the coordinate hash with their code
     // and first child
-    if (b <= B - 2) hash_insert(hash, hash_lg, tag_key(key[rb + p], b), lo, c, err);
+    if (b <= B - 2) hash_insert(hash, hash_lg, tag_key(key[rb + p], b, fb), lo, c, err);
   }
 }
 
@@ -406,13 +420,14 @@ hipError_t launch_zero(Ctx& c, void* const* ptrs, const size_t* bytes, int n) {
   return hipGetLastError();
 }
 
-hipError_t launch_quantize(Ctx& c, const float* pts, int64_t n, int B, int passes) {
+hipError_t launch_quantize(Ctx& c, const float* pts, int64_t n, int B, int passes, const int64_t* frame_start,
+                           int frames) {
   ProfScope ps_(c, RENO_K_QUANTIZE);
   int64_t blocks = (n + 255) / 256;
   if (blocks > 1024) blocks = 1024;
   if (blocks < 1) blocks = 1;
   hipLaunchKernelGGL(k_quantize, dim3((unsigned)blocks), dim3(256), 0, c.stream, pts, n, B,
-                     c.p.range_m, c.keys_a, c.d_hist, passes, c.d_err);
+                     c.p.range_m, frame_start, frames, c.keys_a, c.d_hist, passes, c.d_err);
   return hipGetLastError();
 }
 
@@ -459,7 +474,7 @@ hipError_t launch_codes(Ctx& c, int B) {
   if (blocks < 1) blocks = 1;
   hipLaunchKernelGGL(k_codes, dim3((unsigned)blocks), dim3(256), 0, c.stream, c.lv_key, c.lv_fc,
                      c.lv_code, c.lv_feat, c.d_count, c.b0(), B, c.cap_pts, c.d_hash, c.hash_lg,
-                     c.d_err);
+                     c.fbits, c.d_err);
   return hipGetLastError();
 }
 
