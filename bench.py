@@ -70,18 +70,19 @@ def alg_bytes_per_frame(counts, b0, B, M, C, hash_slots, status_words):
 
 def alg_bytes_encoder(counts, b0, B, M, C, hash_slots, status_words, fb):
     """Minimum HBM bytes of one encoder pass over a frame batch (every input
-    read once, every output written once), per kernel kind; sort passes cover
-    the 3B Morton bits and the fb frame-id bits."""
+    read once, every output written once), per kernel kind.  The sort's
+    minimum is one read and one write per key; its LSD passes (over the 3B
+    Morton bits and the fb frame-id bits) each move that much, reported
+    separately."""
     N = {b0 + i: n for i, n in enumerate(counts)}
     model = [b for b in range(b0 + 1, B)]
     nm = sum(N[b] for b in model)
     parents_hashed = sum(N[b] for b in range(b0, B - 1))
-    passes = (3 * B + fb + 7) // 8
     row = 4 * C
     return {
         "zero": 16 * hash_slots + 4 * status_words,
         "quantize": M * (12 + 8),
-        "sort": passes * M * 16,
+        "sort": M * 16,
         "pyramid": M * 8 + sum(N[b] * 12 for b in range(b0, B + 1)) + sum(N[b] * 4 for b in range(b0, B)),
         "codes": sum(N[b + 1] * (8 + 2) + N[b] for b in range(b0, B)) + 16 * parents_hashed,
         "conv_first": sum(N[b] * (8 + 2 + 4 * 32 + row) + 16 * N[b - 1] for b in model),
@@ -361,6 +362,103 @@ class EndToEnd:
         self.dec.close()
 
 
+def run_stress(args, reno, torch, dev, stream):
+    """HBM stress: K frames of the streaming generator (its distinct frames,
+    cycled) batched into one key space, frame id above the Morton bits; one
+    encoder pass (pyramid, all model scales, code lengths) per batch, every
+    launch bracketed with HIP events.  At K = 512 the keys, levels and
+    feature rows far exceed the 256 MB Infinity Cache."""
+    from synth import BY_NAME, gen_scan, gen_weights
+    scfg = BY_NAME[args.stream_config]
+    sframes = [gen_scan(scfg, f) for f in range(scfg.frames)]
+    sB, sb0, sC, sL = scfg.bit_depth, scfg.min_bit_depth, scfg.channels, scfg.layers
+    sw = reno.weights_to_device(gen_weights(sC, sL, seed=scfg.weight_seed))
+    mv = []
+    for f in sframes:
+        with torch.cuda.stream(stream):
+            pr = reno.Context(f.shape[0], sB, sb0, scfg.range_m, sC, sL, stream=stream)
+            pr.build_pyramid(torch.from_numpy(f).to(dev), sB)
+            mv.append(sum(pr.num_voxels(b) for b in range(sb0 + 1, sB)))
+            pr.close()
+    stress = {"workload": f"{scfg.name}: K frames (its {len(sframes)} distinct scans cycled) in one key "
+                          f"space, {sB}-bit, encoder pass (pyramid, codes + hash, {sL} conv layers + head "
+                          "on every model scale, code lengths)", "runs": []}
+    skinds = ["zero", "quantize", "sort", "pyramid", "codes", "conv_first", "conv_mid", "conv_last",
+              "code_length", "other"]
+    for K in [int(x) for x in args.stress.split(",") if x]:
+        sel = [sframes[i % len(sframes)] for i in range(K)]
+        start = np.cumsum([0] + [f.shape[0] for f in sel]).astype(np.int64)
+        SM = int(start[-1])
+        cap = sum(mv[i % len(mv)] for i in range(K))
+        cap = (cap + cap // 8 + 4095) // 4096 * 4096
+        pts_d = torch.from_numpy(np.concatenate(sel)).to(dev)
+        st_d = torch.from_numpy(start).to(dev)
+        del sel
+        with torch.cuda.stream(stream):
+            sc = reno.Context(SM, sB, sb0, scfg.range_m, sC, sL, max_model_voxels=cap, stream=stream)
+            sc.set_weights(sw)
+
+            def enc():
+                sc.build_pyramid_frames(pts_d, st_d, sB)
+                sc.predict_probs(reno.RENO_ALL_SCALES)
+                sc.code_length(reno.RENO_ALL_SCALES, per_voxel=False, total=False)
+
+            enc()
+            sc.sync()
+            reps = max(1, min(20, 64 // K))
+            t0 = torch.cuda.Event(enable_timing=True)
+            t1 = torch.cuda.Event(enable_timing=True)
+            t0.record(stream)
+            for _ in range(reps):
+                enc()
+            t1.record(stream)
+            stream.synchronize()
+            ms = t0.elapsed_time(t1) / reps
+            sc.profile(skinds)
+            enc()
+            prof = sc.profile_read()
+            sc.profile([])
+            sc.sync()
+            cnt = sc.scale_counts()[sb0:sB + 1].tolist()
+            smem = sc.memory_info()
+        if sum(cnt[1:-1]) != sum(mv[i % len(mv)] for i in range(K)):
+            log("stress K", K, "model voxels of the batch differ from the sum over its frames")
+            sys.exit(1)
+        fb = max(0, (K - 1).bit_length())
+        alg = alg_bytes_encoder(cnt, sb0, sB, SM, sC, smem["hash_slots"], smem["status_words"], fb)
+        kinds_out = {}
+        for k in skinds:
+            if k not in prof:
+                continue
+            us = 1000.0 * prof[k][0]
+            e = {"us": round(us, 1), "launches": prof[k][1]}
+            if k in alg:
+                gbs = alg[k] / (us * 1e-6) / 1e9
+                e.update({"alg_MB": round(alg[k] / 1e6, 2), "alg_GBs": round(gbs, 1),
+                          "hbm_frac": round(gbs / PEAK_HBM_GBS, 4)})
+            if k == "sort":  # every LSD pass reads and writes each key once
+                passes = (3 * sB + fb + 7) // 8
+                pgbs = passes * alg[k] / (us * 1e-6) / 1e9
+                e.update({"passes": passes, "pass_MB": round(passes * alg[k] / 1e6, 2),
+                          "pass_GBs": round(pgbs, 1), "pass_hbm_frac": round(pgbs / PEAK_HBM_GBS, 4)})
+            kinds_out[k] = e
+        run = {"K": K, "points": SM, "voxels": int(sum(cnt)), "model_rows_capacity": cap,
+               "device_bytes": smem["device_bytes"], "encoder_ms_per_batch": round(ms, 4),
+               "encoder_frames_per_s": round(K * 1000.0 / ms, 1), "kinds": kinds_out}
+        stress["runs"].append(run)
+        log("stress K", K, {k: (v["us"], v.get("pass_hbm_frac", v.get("hbm_frac"))) for k, v in kinds_out.items()},
+            f"{ms:.3f} ms/batch")
+        sc.close()
+        del pts_d, st_d
+        torch.cuda.empty_cache()
+    stress["note"] = ("hbm_frac = algorithmic bytes (each input read once, each output written once) / "
+                      "kernel time / 8 TB/s; sort = all LSD passes (pass_* count every pass's read + write), "
+                      "codes = code words + hash build, conv_first = hash probes + first-layer gather, "
+                      "conv_mid = neighbour-row gather")
+
+    return stress
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawTextHelpFormatter)
     ap.add_argument("--gpus", type=int, default=1)
@@ -372,6 +470,8 @@ def main():
     ap.add_argument("--no-two-stage", action="store_true", help="skip the two-stage head measurement")
     ap.add_argument("--no-bf16x3", action="store_true", help="skip the split-bf16 precision measurement")
     ap.add_argument("--no-top", action="store_true", help="skip the full-predictor measurement")
+    ap.add_argument("--stress-only", action="store_true",
+                    help="run only the HBM stress pass and print its JSON (for counter runs)")
     ap.add_argument("--stress", default="1,8,64,512",
                     help="frame-batch sizes K of the HBM stress pass (encoder stages on K frames in one key "
                          "space); empty to skip")
@@ -406,6 +506,15 @@ def main():
     torch.cuda.set_device(dev)
     stream = torch.cuda.Stream(device=dev)
     pts = torch.from_numpy(pts_np).to(dev)
+    if args.stress_only:
+        if args.calib_copy:
+            src = torch.ones(64 << 20, dtype=torch.float32, device=dev)
+            dst = torch.empty_like(src)
+            torch.mul(src, 1.0, out=dst)
+            torch.cuda.synchronize()
+            del src, dst
+        print(json.dumps({"hbm_stress": run_stress(args, reno, torch, dev, stream)}), flush=True)
+        return
     if args.calib_copy:
         # plain kernels of known traffic: a fill (256 MiB written), then an
         # elementwise copy (256 MiB read, 256 MiB written)
@@ -599,90 +708,8 @@ def main():
                 c.close()
         del codecs
 
-    # ---- HBM stress: K frames of the streaming generator (its 10 distinct
-    # frames, cycled) batched into one key space, frame id above the Morton
-    # bits; one encoder pass (pyramid, all model scales, code lengths) per
-    # batch, every launch bracketed with HIP events.  At K = 512 the keys,
-    # levels and feature rows far exceed the 256 MB Infinity Cache ----
-    stress = None
-    if args.stress:
-        scfg = BY_NAME[args.stream_config]
-        sframes = [gen_scan(scfg, f) for f in range(scfg.frames)]
-        sB, sb0, sC, sL = scfg.bit_depth, scfg.min_bit_depth, scfg.channels, scfg.layers
-        sw = reno.weights_to_device(gen_weights(sC, sL, seed=scfg.weight_seed))
-        mv = []
-        for f in sframes:
-            with torch.cuda.stream(stream):
-                pr = reno.Context(f.shape[0], sB, sb0, scfg.range_m, sC, sL, stream=stream)
-                pr.build_pyramid(torch.from_numpy(f).to(dev), sB)
-                mv.append(sum(pr.num_voxels(b) for b in range(sb0 + 1, sB)))
-                pr.close()
-        stress = {"workload": f"{scfg.name}: K frames (its {len(sframes)} distinct scans cycled) in one key "
-                              f"space, {sB}-bit, encoder pass (pyramid, codes + hash, {sL} conv layers + head "
-                              "on every model scale, code lengths)", "runs": []}
-        skinds = ["zero", "quantize", "sort", "pyramid", "codes", "conv_first", "conv_mid", "conv_last",
-                  "code_length", "other"]
-        for K in [int(x) for x in args.stress.split(",") if x]:
-            sel = [sframes[i % len(sframes)] for i in range(K)]
-            start = np.cumsum([0] + [f.shape[0] for f in sel]).astype(np.int64)
-            SM = int(start[-1])
-            cap = sum(mv[i % len(mv)] for i in range(K))
-            cap = (cap + cap // 8 + 4095) // 4096 * 4096
-            pts_d = torch.from_numpy(np.concatenate(sel)).to(dev)
-            st_d = torch.from_numpy(start).to(dev)
-            del sel
-            with torch.cuda.stream(stream):
-                sc = reno.Context(SM, sB, sb0, scfg.range_m, sC, sL, max_model_voxels=cap, stream=stream)
-                sc.set_weights(sw)
-
-                def enc():
-                    sc.build_pyramid_frames(pts_d, st_d, sB)
-                    sc.predict_probs(reno.RENO_ALL_SCALES)
-                    sc.code_length(reno.RENO_ALL_SCALES, per_voxel=False, total=False)
-
-                enc()
-                sc.sync()
-                reps = max(1, min(20, 64 // K))
-                t0 = torch.cuda.Event(enable_timing=True)
-                t1 = torch.cuda.Event(enable_timing=True)
-                t0.record(stream)
-                for _ in range(reps):
-                    enc()
-                t1.record(stream)
-                stream.synchronize()
-                ms = t0.elapsed_time(t1) / reps
-                sc.profile(skinds)
-                enc()
-                prof = sc.profile_read()
-                sc.profile([])
-                sc.sync()
-                cnt = sc.scale_counts()[sb0:sB + 1].tolist()
-                smem = sc.memory_info()
-            fb = max(0, (K - 1).bit_length())
-            alg = alg_bytes_encoder(cnt, sb0, sB, SM, sC, smem["hash_slots"], smem["status_words"], fb)
-            kinds_out = {}
-            for k in skinds:
-                if k not in prof:
-                    continue
-                us = 1000.0 * prof[k][0]
-                e = {"us": round(us, 1), "launches": prof[k][1]}
-                if k in alg:
-                    gbs = alg[k] / (us * 1e-6) / 1e9
-                    e.update({"alg_MB": round(alg[k] / 1e6, 2), "alg_GBs": round(gbs, 1),
-                              "hbm_frac": round(gbs / PEAK_HBM_GBS, 4)})
-                kinds_out[k] = e
-            run = {"K": K, "points": SM, "voxels": int(sum(cnt)), "model_rows_capacity": cap,
-                   "device_bytes": smem["device_bytes"], "encoder_ms_per_batch": round(ms, 4),
-                   "encoder_frames_per_s": round(K * 1000.0 / ms, 1), "kinds": kinds_out}
-            stress["runs"].append(run)
-            log("stress K", K, {k: (v["us"], v.get("hbm_frac")) for k, v in kinds_out.items()},
-                f"{ms:.3f} ms/batch")
-            sc.close()
-            del pts_d, st_d
-            torch.cuda.empty_cache()
-        stress["note"] = ("hbm_frac = algorithmic bytes (each input read once, each output written once) / "
-                          "kernel time / 8 TB/s; sort = all LSD passes, codes = code words + hash build, "
-                          "conv_first = hash probes + first-layer gather, conv_mid = neighbour-row gather")
+    # ---- HBM stress: K frames of the streaming generator in one key space ----
+    stress = run_stress(args, reno, torch, dev, stream) if args.stress else None
 
     # ---- CPU baseline: the oracle (single-threaded C++, fp64), one frame per
     # process, first alone, then one process per available core at once ----

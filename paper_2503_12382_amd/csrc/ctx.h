@@ -18,6 +18,8 @@ constexpr int NLEV = RENO_MAX_BIT_DEPTH + 1;   // bit depths 0 .. 21
 constexpr int SORT_THREADS = 256;
 constexpr int SORT_KPT = 4;                     // keys per thread per sort tile
 constexpr int SORT_TILE = SORT_THREADS * SORT_KPT;
+constexpr int SORT_KPT_BIG = 16;                // keys per thread for inputs of SORT_BIG_N keys or more
+constexpr int64_t SORT_BIG_N = int64_t(1) << 22;
 constexpr int RADIX_BITS = 8;
 constexpr int RADIX = 1 << RADIX_BITS;
 constexpr int MAX_PASSES = (3 * RENO_MAX_BIT_DEPTH + RADIX_BITS - 1) / RADIX_BITS;

@@ -377,6 +377,17 @@ __device__ __forceinline__ void parent_cell_rows(uint64_t kf, int b, int g, cons
   }
 }
 
+// Tile of a block's slot, XCD-aware: workgroups are dealt round-robin to the
+// 8 XCDs (block b runs on XCD b % 8), so chunks of tch consecutive tiles are
+// dealt to the XCDs in turn and the blocks of one XCD sweep that XCD's chunks
+// together: tiles that gather the same neighbour rows run on one L2 at about
+// the same time.  Increasing in the slot for a fixed block.
+__device__ __forceinline__ int64_t conv_tile(int64_t slot, int64_t tch) {
+  const int64_t xcd = blockIdx.x & 7, j = blockIdx.x >> 3, nb = gridDim.x >> 3;
+  const int64_t k = j + nb * slot;  // the XCD's k-th tile
+  return ((k / tch) * 8 + xcd) * tch + k % tch;
+}
+
 template <int C, bool FIRST, bool LAST, bool TWO, bool BF>
 __global__ void __launch_bounds__(CONV_THREADS) k_conv(ConvArgs a) {
   constexpr int NCB = C / 16;
@@ -416,7 +427,9 @@ __global__ void __launch_bounds__(CONV_THREADS) k_conv(ConvArgs a) {
     scale_span(rm, a.b_lo + i, mo, nb);
     total_tiles += (nb + 15) / 16;
   }
-  if ((int64_t)blockIdx.x >= total_tiles) return;  // whole block idle: skip the weight staging
+  // chunk size: 64 chunks per launch (8 per XCD) between 16 and 256 tiles
+  const int64_t tch = total_tiles / 64 < 16 ? 16 : (total_tiles / 64 > 256 ? 256 : total_tiles / 64);
+  if (conv_tile(0, tch) >= total_tiles) return;  // whole block idle: skip the weight staging
   if (tid == 0) {
     s_next = 0;
     int64_t acc = 0;
@@ -436,14 +449,14 @@ __global__ void __launch_bounds__(CONV_THREADS) k_conv(ConvArgs a) {
                                      tid);
   __syncthreads();
 
-  // Tile order: block x owns tiles x, x + G, x + 2G, ... (G = grid size), a
-  // sample of every scale of the launch, so all blocks carry about the same
+  // Tile order (conv_tile): every XCD gets chunks from the whole tile range,
+  // a sample of every scale of the launch, so the XCDs carry about the same
   // mix of cheap and expensive tiles (coarse scales have far more occupied
   // offsets per tile).  Inside a block the waves take the block's tiles
   // dynamically from an LDS counter: the first CONV_WAVES slots statically,
   // the rest first come, first served.
   for (int64_t slot = w;;) {
-    const int64_t tile = (int64_t)blockIdx.x + slot * gridDim.x;
+    const int64_t tile = conv_tile(slot, tch);
     if (tile >= total_tiles) break;
     int si = 0;  // scale of the tile: all prefix loads issued together
 #pragma unroll

@@ -34,17 +34,24 @@ __global__ void __launch_bounds__(256) k_zero(ZeroArgs a) {
 
 // ---------------------------------------------------------------------------
 // Histogram update of every sort pass's digit of key k in LDS, aggregated over
-// the lanes of the wave that share a digit (one LDS atomic per distinct digit:
-// the coarse digits of Morton keys are few, so unaggregated atomics serialise).
+// runs of adjacent lanes with equal digits: one LDS atomic per run.  Input
+// points arrive in scan order, so the coarse digits of neighbouring lanes
+// mostly agree (unaggregated, those atomics would hit one address and
+// serialise), while the fine digits differ and cost one atomic per lane, as
+// without aggregation.
 __device__ __forceinline__ void digit_count(uint32_t dig, bool valid, uint32_t* h) {
-  uint64_t peers = __ballot(valid);
-#pragma unroll
-  for (int bit = 0; bit < RADIX_BITS; ++bit) {
-    const bool set = (dig >> bit) & 1u;
-    const uint64_t bm = __ballot(set);
-    peers &= set ? bm : ~bm;
+  const int lane = lane_id();
+  const uint32_t prev = (uint32_t)__shfl_up((int)dig, 1);
+  const uint64_t valids = __ballot(valid);
+  const bool vprev = lane > 0 && ((valids >> (lane - 1)) & 1ull);
+  const bool head = valid && (!vprev || prev != dig);
+  const uint64_t heads = __ballot(head);
+  if (head) {
+    const uint64_t above = lane == 63 ? 0ull : (heads >> (lane + 1)) << (lane + 1);
+    const uint64_t upto = above ? (above & (0ull - above)) - 1ull : ~0ull;  // lanes below the next head
+    const uint64_t run = valids & upto & ~((1ull << lane) - 1ull);
+    atomicAdd(&h[dig], (uint32_t)__popcll(run));
   }
-  if (valid && rank_below(peers) == 0u) atomicAdd(&h[dig], (uint32_t)__popcll(peers));
 }
 
 __device__ __forceinline__ void digits_of(uint64_t k, int passes, uint32_t* sh) {
@@ -67,51 +74,67 @@ __global__ void __launch_bounds__(256) k_quantize(const float* __restrict__ pts,
                                                   uint32_t* __restrict__ hist, int passes,
                                                   uint32_t* err) {
   __shared__ uint32_t sh[MAX_PASSES * RADIX];
+  __shared__ int64_t s_fs[RENO_MAX_FRAMES + 1];  // frame ranges of a batch
   for (int i = threadIdx.x; i < passes * RADIX; i += blockDim.x) sh[i] = 0u;
-  if (frames > 1 && blockIdx.x == 0 && threadIdx.x == 0) {  // frame ranges: 0 = s_0 <= s_1 <= ... <= s_F = n
-    bool ok = frame_start[0] == 0 && frame_start[frames] == n;
-    for (int f = 0; f < frames; ++f) ok = ok && frame_start[f] <= frame_start[f + 1];
-    if (!ok) latch(err, ERR_FRAMES);
+  if (frames > 1) {
+    for (int f = threadIdx.x; f <= frames; f += blockDim.x) s_fs[f] = frame_start[f];
+    if (blockIdx.x == 0 && threadIdx.x == 0) {  // 0 = s_0 <= s_1 <= ... <= s_F = n
+      bool ok = frame_start[0] == 0 && frame_start[frames] == n;
+      for (int f = 0; f < frames; ++f) ok = ok && frame_start[f] <= frame_start[f + 1];
+      if (!ok) latch(err, ERR_FRAMES);
+    }
   }
   __syncthreads();
+  int fcur = 0;  // a thread's points increase, so its frame only moves forward
   const double scale = (double)(int64_t(1) << B);
   const double span = 2.0 * R;
   const double top = (double)((int64_t(1) << B) - 1);
   bool bad = false;
   const int64_t stride = (int64_t)gridDim.x * blockDim.x;
-  // every lane of a wave runs the same number of iterations so that the
-  // wave-wide digit matching below sees all lanes; idle lanes carry no key
-  const int64_t nwaves_iter = (n + stride - 1) / stride;
+  const int64_t gid = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  // QU points per thread per iteration, all loads issued first.  Every lane
+  // of a wave runs the same number of iterations so that the wave-wide digit
+  // matching below sees all lanes; idle lanes carry no key.
+  constexpr int QU = 4;
+  const int64_t nwaves_iter = (n + stride * QU - 1) / (stride * QU);
   for (int64_t it = 0; it < nwaves_iter; ++it) {
-    const int64_t i = it * stride + (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-    if (i >= n) {
-      digits_of_idle(passes, sh);
-      continue;
-    }
-    uint32_t q[3];
+    float pv[QU][3];
 #pragma unroll
-    for (int a = 0; a < 3; ++a) {
-      const float p = pts[3 * i + a];
-      if (!isfinite(p)) {
-        bad = true;
-        q[a] = 0u;
+    for (int u = 0; u < QU; ++u) {
+      const int64_t i = (it * QU + u) * stride + gid;
+#pragma unroll
+      for (int a = 0; a < 3; ++a) pv[u][a] = i < n ? pts[3 * i + a] : 0.0f;
+    }
+#pragma unroll
+    for (int u = 0; u < QU; ++u) {
+      const int64_t i = (it * QU + u) * stride + gid;
+      if (i >= n) {
+        digits_of_idle(passes, sh);
         continue;
       }
-      const double u = ((double)p + R) * scale / span;
-      double f = floor(u);
-      f = f < 0.0 ? 0.0 : f;
-      f = f > top ? top : f;
-      q[a] = (uint32_t)f;
+      uint32_t q[3];
+#pragma unroll
+      for (int a = 0; a < 3; ++a) {
+        const float p = pv[u][a];
+        if (!isfinite(p)) {
+          bad = true;
+          q[a] = 0u;
+          continue;
+        }
+        const double uu = ((double)p + R) * scale / span;
+        double f = floor(uu);
+        f = f < 0.0 ? 0.0 : f;
+        f = f > top ? top : f;
+        q[a] = (uint32_t)f;
+      }
+      uint64_t k = morton3(q[0], q[1], q[2]);
+      if (frames > 1) {  // last frame f with s_fs[f] <= i
+        while (fcur + 1 < frames && s_fs[fcur + 1] <= i) ++fcur;
+        k |= (uint64_t)fcur << (3 * B);
+      }
+      keys[i] = k;
+      digits_of(k, passes, sh);
     }
-    uint64_t k = morton3(q[0], q[1], q[2]);
-    if (frames > 1) {  // last frame f with frame_start[f] <= i
-      int f = 0;
-      for (int step = 1 << 9; step; step >>= 1)
-        if (f + step < frames && frame_start[f + step] <= i) f += step;
-      k |= (uint64_t)f << (3 * B);
-    }
-    keys[i] = k;
-    digits_of(k, passes, sh);
   }
   if (bad) latch(err, ERR_NONFINITE);
   __syncthreads();
@@ -141,38 +164,40 @@ __device__ __forceinline__ uint32_t block_excl_scan256(uint32_t v, uint32_t* s_w
 // in ticket order; each tile ranks its keys with wave-level digit matching,
 // publishes per-digit counts, finds its global offsets by look-back, reorders
 // in LDS and writes out bucket runs.
+template <int KPT>
 __global__ void __launch_bounds__(SORT_THREADS) k_sort_pass(const uint64_t* __restrict__ in,
                                                             uint64_t* __restrict__ out, int64_t n,
                                                             int shift,
                                                             const uint32_t* __restrict__ hist,
                                                             uint32_t* status, uint32_t* ticket,
                                                             uint32_t* err) {
+  constexpr int TILE = SORT_THREADS * KPT;
   __shared__ uint32_t s_tile;
   __shared__ uint32_t s_wh[4][RADIX];
   __shared__ uint32_t s_dexcl[RADIX];
   __shared__ uint32_t s_gbase[RADIX];
   __shared__ uint32_t s_wsum[4];
-  __shared__ uint64_t s_keys[SORT_TILE];
+  __shared__ uint64_t s_keys[TILE];
 
   const int tid = threadIdx.x, w = tid >> 6, lane = tid & 63;
   if (tid == 0) s_tile = atomicAdd(ticket, 1u);
   for (int i = tid; i < 4 * RADIX; i += SORT_THREADS) (&s_wh[0][0])[i] = 0u;
   __syncthreads();
   const int tile = (int)s_tile;
-  const int64_t base = (int64_t)tile * SORT_TILE;
+  const int64_t base = (int64_t)tile * TILE;
 
-  uint64_t key[SORT_KPT];
-  uint32_t dig[SORT_KPT], rnk[SORT_KPT];
-  bool ok[SORT_KPT];
+  uint64_t key[KPT];
+  uint32_t dig[KPT], rnk[KPT];
+  bool ok[KPT];
 #pragma unroll
-  for (int j = 0; j < SORT_KPT; ++j) {
-    const int64_t idx = base + (int64_t)w * 64 * SORT_KPT + j * 64 + lane;
+  for (int j = 0; j < KPT; ++j) {
+    const int64_t idx = base + (int64_t)w * 64 * KPT + j * 64 + lane;
     ok[j] = idx < n;
     key[j] = ok[j] ? in[idx] : 0ull;
     dig[j] = (uint32_t)(key[j] >> shift) & (RADIX - 1);
   }
 #pragma unroll
-  for (int j = 0; j < SORT_KPT; ++j) {
+  for (int j = 0; j < KPT; ++j) {
     uint64_t peers = __ballot(ok[j]);
 #pragma unroll
     for (int bit = 0; bit < RADIX_BITS; ++bit) {
@@ -206,11 +231,11 @@ __global__ void __launch_bounds__(SORT_THREADS) k_sort_pass(const uint64_t* __re
   __syncthreads();
 
 #pragma unroll
-  for (int j = 0; j < SORT_KPT; ++j)
+  for (int j = 0; j < KPT; ++j)
     if (ok[j]) s_keys[s_dexcl[dig[j]] + s_wh[w][dig[j]] + rnk[j]] = key[j];
   __syncthreads();
 
-  const int cnt = (int)((n - base) < SORT_TILE ? (n - base) : SORT_TILE);
+  const int cnt = (int)((n - base) < TILE ? (n - base) : TILE);
   for (int q = tid; q < cnt; q += SORT_THREADS) {
     const uint64_t k = s_keys[q];
     const uint32_t dd = (uint32_t)(k >> shift) & (RADIX - 1);
@@ -423,8 +448,8 @@ hipError_t launch_zero(Ctx& c, void* const* ptrs, const size_t* bytes, int n) {
 hipError_t launch_quantize(Ctx& c, const float* pts, int64_t n, int B, int passes, const int64_t* frame_start,
                            int frames) {
   ProfScope ps_(c, RENO_K_QUANTIZE);
-  int64_t blocks = (n + 255) / 256;
-  if (blocks > 1024) blocks = 1024;
+  int64_t blocks = (n + 1023) / 1024;  // 4 points per thread per iteration
+  if (blocks > 2048) blocks = 2048;
   if (blocks < 1) blocks = 1;
   hipLaunchKernelGGL(k_quantize, dim3((unsigned)blocks), dim3(256), 0, c.stream, pts, n, B,
                      c.p.range_m, frame_start, frames, c.keys_a, c.d_hist, passes, c.d_err);
@@ -433,11 +458,18 @@ hipError_t launch_quantize(Ctx& c, const float* pts, int64_t n, int B, int passe
 
 hipError_t launch_sort_pass(Ctx& c, const uint64_t* in, uint64_t* out, int64_t n, int pass) {
   ProfScope ps_(c, RENO_K_SORT);
-  const int64_t tiles = (n + SORT_TILE - 1) / SORT_TILE;
   uint32_t* status = c.st_sort(pass);
-  hipLaunchKernelGGL(k_sort_pass, dim3((unsigned)tiles), dim3(SORT_THREADS), 0, c.stream, in, out,
-                     n, RADIX_BITS * pass, c.d_hist + pass * RADIX, status,
-                     c.d_ticket + TK_SORT + pass, c.d_err);
+  // large inputs: 4096-key tiles (digit runs of ~16 keys per tile, a quarter
+  // of the look-backs); small ones keep 1024-key tiles to fill the CUs
+  if (n >= SORT_BIG_N) {
+    const int64_t tiles = (n + SORT_THREADS * SORT_KPT_BIG - 1) / (SORT_THREADS * SORT_KPT_BIG);
+    hipLaunchKernelGGL(k_sort_pass<SORT_KPT_BIG>, dim3((unsigned)tiles), dim3(SORT_THREADS), 0, c.stream, in, out,
+                       n, RADIX_BITS * pass, c.d_hist + pass * RADIX, status, c.d_ticket + TK_SORT + pass, c.d_err);
+  } else {
+    const int64_t tiles = (n + SORT_TILE - 1) / SORT_TILE;
+    hipLaunchKernelGGL(k_sort_pass<SORT_KPT>, dim3((unsigned)tiles), dim3(SORT_THREADS), 0, c.stream, in, out,
+                       n, RADIX_BITS * pass, c.d_hist + pass * RADIX, status, c.d_ticket + TK_SORT + pass, c.d_err);
+  }
   return hipGetLastError();
 }
 

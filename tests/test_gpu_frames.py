@@ -177,3 +177,35 @@ def test_frame_batch_errors(scan_cache):
         ctx.sync()
     assert e.value.status == reno.RENO_E_INPUT
     ctx.close()
+
+
+def test_large_batch_pyramid_matches_oracle(scan_cache):
+    """36 copies of the 12-bit scan as one batch (4.6M points: the large-tile
+    sort path): every frame's scales, codes and parents equal the oracle's."""
+    cfg = CONFIGS[1]
+    B, b0 = cfg.bit_depth, cfg.min_bit_depth
+    scan = scan_cache(1)
+    K = 36
+    pts = np.concatenate([scan] * K)
+    start = (np.arange(K + 1) * len(scan)).astype(np.int64)
+    assert len(pts) >= 1 << 22
+    say("large frame batch", len(pts), "points")
+    ctx = _ctx(cfg, len(pts))
+    ctx.build_pyramid_frames(to_dev(pts), to_dev(start), B)
+    ctx.sync()
+    P = oracle.Pyramid.from_points(scan, B, b0, cfg.range_m)
+    for b in range(b0, B + 1):
+        n = P.num(b)
+        assert ctx.num_voxels(b) == K * n
+        xyz, keys = ctx.coords(b)
+        keys = keys.cpu().numpy().view(np.uint64)
+        want = np.concatenate([P.keys(b) | (np.uint64(f) << np.uint64(3 * b)) for f in range(K)])
+        np.testing.assert_array_equal(keys, want, err_msg=f"keys b={b}")
+        np.testing.assert_array_equal(xyz.cpu().numpy(), np.concatenate([P.xyz(b)] * K))
+        par = ctx.parent_rows(b).cpu().numpy()
+        if b > b0:
+            np.testing.assert_array_equal(
+                par, np.concatenate([P.parent(b) + f * P.num(b - 1) for f in range(K)]))
+        if b < B:
+            np.testing.assert_array_equal(ctx.occupancy_codes(b).cpu().numpy(), np.concatenate([P.codes(b)] * K))
+    ctx.close()
