@@ -139,10 +139,13 @@ class Codec:
     step over a resident frame.  The decoder's symbols come from the encoder
     (a stand-in for an instant entropy decoder)."""
 
-    def __init__(self, reno, torch, cfg, pts, M, cap_model, stream, w_np, two_stage, precision=0, top=False):
+    def __init__(self, reno, torch, cfg, pts, M, cap_model, stream, w_np, two_stage, precision=0, top=False,
+                 frame_start=None):
         self.reno, self.torch, self.stream = reno, torch, stream
         B, b0, C, L = cfg.bit_depth, cfg.min_bit_depth, cfg.channels, cfg.layers
         self.B, self.b0, self.C, self.two_stage = B, b0, C, two_stage
+        self.frame_start = frame_start     # a frame batch (int64 device tensor [K + 1]) or None
+        self.K = 1 if frame_start is None else int(frame_start.shape[0]) - 1
         wd = reno.weights_to_device(w_np)
         with torch.cuda.stream(stream):
             mk = lambda: reno.Context(M, B, b0, cfg.range_m, C, L, max_model_voxels=cap_model,
@@ -151,9 +154,10 @@ class Codec:
             self.enc.set_weights(wd)
             self.dec.set_weights(wd)
             # decoder inputs (resident before timing): initial state and every scale's codes
-            self.enc.build_pyramid(pts, B)
-            base, _ = self.enc.coords(b0)
+            self.build(pts)
+            base, keys = self.enc.coords(b0)
             self.base = base.clone()
+            self.fid = (keys >> (3 * b0)).to(torch.int32).contiguous()  # frame ids of a batch
             self.codes = {b: self.enc.occupancy_codes(b).clone() for b in range(b0, B)}
             self.s1 = {b: (self.codes[b] & 15).contiguous() for b in range(b0, B)}
             self.enc.predict_probs(reno.RENO_ALL_SCALES)
@@ -163,12 +167,21 @@ class Codec:
         self.pts = pts
         self.graph = None
 
+    def build(self, pts):
+        if self.frame_start is None:
+            self.enc.build_pyramid(pts, self.B)
+        else:
+            self.enc.build_pyramid_frames(pts, self.frame_start, self.B)
+
     def step(self):
         reno, enc, dec, B, b0 = self.reno, self.enc, self.dec, self.B, self.b0
-        enc.build_pyramid(self.pts, B)
+        self.build(self.pts)
         enc.predict_probs(reno.RENO_ALL_SCALES)
         enc.code_length(reno.RENO_ALL_SCALES, per_voxel=False, total=False)
-        dec.set_base(B, self.base, self.codes[b0])
+        if self.frame_start is None:
+            dec.set_base(B, self.base, self.codes[b0])
+        else:
+            dec.set_base_frames(B, self.base, self.fid, self.codes[b0], self.K)
         for b in range(b0 + 1, B):
             dec.expand(b - 1, None if b - 1 == b0 else self.codes[b - 1])
             dec.predict_probs(b)
@@ -704,6 +717,39 @@ def main():
             multi["runs"].append({"streams": S, "frames_per_s": round(len(cs) * 1000.0 / ms, 2),
                                   "ms_per_batch": round(ms, 4)})
             log(f"multi-frame {len(cs)} frames on {S} streams: {ms:.3f} ms, {len(cs) * 1000.0 / ms:.1f} frames/s")
+            for c in cs:
+                c.close()
+        # frame batches: the frames split into S batches (one key space each,
+        # frame id above the Morton bits), one encoder + decoder context pair
+        # and captured step per batch, batches replayed on S streams
+        for S in [x for x in (1, 2) if x <= len(codecs)]:
+            groups = [list(range(len(codecs)))[g::S] for g in range(S)]
+            cs = []
+            for g, idx in enumerate(groups):
+                bp = torch.cat([codecs[i][0] for i in idx])
+                st = torch.tensor(np.cumsum([0] + [codecs[i][0].shape[0] for i in idx]), dtype=torch.int64,
+                                  device=dev)
+                bcap = sum(codecs[i][1] for i in idx)
+                cs.append(Codec(reno, torch, mcfg, bp, int(bp.shape[0]), bcap, streams[g], mw, two_stage=False,
+                                frame_start=st))
+            for c in cs:
+                c.time(1, 2, "graph")
+            reps = max(args.steps // 10, 2)
+            torch.cuda.synchronize()
+            t = time.perf_counter()
+            for _ in range(reps):
+                for c in cs:
+                    with torch.cuda.stream(c.stream):
+                        c.graph.replay()
+            torch.cuda.synchronize()
+            ms = (time.perf_counter() - t) * 1000.0 / reps
+            for c in cs:
+                c.check("frame batch:")
+            multi["runs"].append({"frame_batches": S, "frames_per_batch": [len(x) for x in groups],
+                                  "streams": S, "frames_per_s": round(len(codecs) * 1000.0 / ms, 2),
+                                  "ms_per_batch": round(ms, 4)})
+            log(f"multi-frame {len(codecs)} frames as {S} frame batch(es) on {S} streams: {ms:.3f} ms, "
+                f"{len(codecs) * 1000.0 / ms:.1f} frames/s")
             for c in cs:
                 c.close()
         del codecs
