@@ -42,7 +42,8 @@ class OrcWeights(ctypes.Structure):
                 ("head2_b", ctypes.c_void_p),
                 ("model_mode", ctypes.c_int), ("pad3", ctypes.c_int),
                 ("emb_o", ctypes.c_void_p), ("emb_d", ctypes.c_void_p),
-                ("top_w", ctypes.c_void_p * 4), ("top_b", ctypes.c_void_p * 4)]
+                ("top_w", ctypes.c_void_p * 4), ("top_b", ctypes.c_void_p * 4),
+                ("kernel_size", ctypes.c_int), ("pad4", ctypes.c_int)]
 
 
 def lib():
@@ -66,9 +67,9 @@ def lib():
             "orc_codes": (c_int, [vp, c_int, vp]),
             "orc_parent": (None, [vp, c_int, vp]),
             "orc_expand": (i64, [vp, c_int, vp, vp]),
-            "orc_neighbors": (None, [vp, c_int, vp]),
+            "orc_neighbors": (None, [vp, c_int, c_int, vp]),
             "orc_features": (None, [vp, c_int, vp]),
-            "orc_sparse_conv": (c_int, [vp, i64, c_int, vp, c_int, vp, vp, c_int, c_int, vp]),
+            "orc_sparse_conv": (c_int, [vp, i64, c_int, vp, c_int, vp, vp, c_int, c_int, c_int, vp]),
             "orc_model": (c_int, [vp, c_int, ctypes.POINTER(OrcWeights), vp, i64, vp, vp, vp]),
             "orc_model2": (c_int, [vp, c_int, ctypes.POINTER(OrcWeights), vp, i64, vp, vp, vp, vp,
                                    vp, vp]),
@@ -100,6 +101,15 @@ def quantize(points: np.ndarray, B: int, R: float) -> np.ndarray:
     if lib().orc_quantize(_p(pts), pts.shape[0], B, R, _p(q)) != 0:
         raise ValueError("non-finite point")
     return q
+
+
+def kernel_size_of(w: np.ndarray) -> int:
+    """Kernel size ks of a conv weight array [ks^3][C_in][C_out]."""
+    kv = int(np.asarray(w).shape[0])
+    ks = int(round(kv ** (1.0 / 3.0)))
+    if ks ** 3 != kv or ks % 2 == 0:
+        raise ValueError(f"{kv} offsets is not an odd cube")
+    return ks
 
 
 class _W:
@@ -136,6 +146,7 @@ class _W:
                 a = np.ascontiguousarray(w[name], dtype=np.float32)
                 self.arrays.append(a)
                 setattr(s, name, a.ctypes.data)
+            s.kernel_size = kernel_size_of(w["top_w"][0])
             for i in range(4):
                 tw = np.ascontiguousarray(w["top_w"][i], dtype=np.float32)
                 tb = np.ascontiguousarray(w["top_b"][i], dtype=np.float32)
@@ -213,9 +224,10 @@ class Pyramid:
         lib().orc_expand(self._h, b, _p(c), _p(out))
         return out
 
-    def neighbors(self, b: int) -> np.ndarray:
-        out = np.empty((self.num(b), 27), dtype=np.int32)
-        lib().orc_neighbors(self._h, b, _p(out))
+    def neighbors(self, b: int, ks: int = 3) -> np.ndarray:
+        """Neighbour rows [N_b][ks^3] (-1: absent or off-grid)."""
+        out = np.empty((self.num(b), ks ** 3), dtype=np.int32)
+        lib().orc_neighbors(self._h, b, ks, _p(out))
         return out
 
     def features(self, b: int) -> np.ndarray:
@@ -282,9 +294,10 @@ def sparse_conv(xyz: np.ndarray, bits: int, feats: np.ndarray, W: np.ndarray, bi
     Wf = np.ascontiguousarray(W, dtype=np.float32)
     bf = np.ascontiguousarray(bias, dtype=np.float32)
     c_in, c_out = Wf.shape[1], Wf.shape[2]
+    ks = kernel_size_of(Wf)
     out = np.empty((v.shape[0], c_out), dtype=np.float64)
     if lib().orc_sparse_conv(_p(v), v.shape[0], bits, _p(f), c_in, _p(Wf), _p(bf), c_out,
-                             int(relu), _p(out)) != 0:
+                             int(relu), ks, _p(out)) != 0:
         raise ValueError("duplicate voxel")
     return out
 

@@ -148,11 +148,13 @@ std::vector<Vox> fcg_expand(const std::vector<Vox>& v, const std::vector<uint8_t
   return out;
 }
 
-// Neighbour k of v at scale b: k = (dx+1) + 3(dy+1) + 9(dz+1); the row of
-// v + (dx,dy,dz) among the voxels of the scale, or -1 when that cell is empty
-// or outside [0, 2^b)^3.
-int64_t neighbour(const std::map<Vox, int64_t>& rows, int b, const Vox& v, int k) {
-  int dx = k % 3 - 1, dy = (k / 3) % 3 - 1, dz = k / 9 - 1;
+// Neighbour k of v at scale b for a ks x ks x ks kernel (ks odd, radius
+// h = ks / 2): k = (dx+h) + ks(dy+h) + ks^2(dz+h), i.e. (dx+1) + 3(dy+1) +
+// 9(dz+1) for ks = 3; the row of v + (dx,dy,dz) among the voxels of the
+// scale, or -1 when that cell is empty or outside [0, 2^b)^3.
+int64_t neighbour(const std::map<Vox, int64_t>& rows, int b, const Vox& v, int k, int ks = 3) {
+  const int h = ks / 2;
+  int dx = k % ks - h, dy = (k / ks) % ks - h, dz = k / (ks * ks) - h;
   Vox u = {v[0] + dx, v[1] + dy, v[2] + dz};
   int64_t lim = int64_t(1) << b;
   for (int a = 0; a < 3; ++a)
@@ -161,27 +163,29 @@ int64_t neighbour(const std::map<Vox, int64_t>& rows, int b, const Vox& v, int k
   return it == rows.end() ? -1 : it->second;
 }
 
-// The 27 neighbour rows of voxel v (index k as above).
-std::array<int64_t, 27> neighbours_of(const std::map<Vox, int64_t>& rows, int b, const Vox& v) {
-  std::array<int64_t, 27> nb;
-  for (int k = 0; k < 27; ++k) nb[k] = neighbour(rows, b, v, k);
+// The ks^3 neighbour rows of voxel v (index k as above).
+typedef std::vector<int64_t> Nbrs;
+Nbrs neighbours_of(const std::map<Vox, int64_t>& rows, int b, const Vox& v, int ks = 3) {
+  Nbrs nb(ks * ks * ks);
+  for (int k = 0; k < ks * ks * ks; ++k) nb[k] = neighbour(rows, b, v, k, ks);
   return nb;
 }
 
-// One submanifold 3x3x3 sparse convolution (stride 1, outputs only on the
-// input voxels), as used by TOP's ResNet on the target coordinates (Eq. 9):
+// One submanifold ks x ks x ks sparse convolution (stride 1, outputs only on
+// the input voxels), as used by TOP's ResNet on the target coordinates (Eq. 9):
 //   y(v)[co] = bias[co] + sum_k sum_ci W[k][ci][co] * h(nbr(v,k))[ci]
 // over present neighbours, optionally followed by ReLU.  Cross-correlation
-// convention, zero for absent neighbours.  `nb[r]` are the neighbour rows of
-// output r; `h` is indexed by row.
-void sparse_conv(const std::vector<std::array<int64_t, 27>>& nb, const std::vector<double>& h,
+// convention, zero for absent neighbours.  `nb[r]` are the ks^3 neighbour rows
+// of output r; `h` is indexed by row.
+void sparse_conv(const std::vector<Nbrs>& nb, const std::vector<double>& h,
                  int c_in, const float* W, const float* bias, int c_out, bool relu,
                  std::vector<double>& y) {
   y.assign(nb.size() * c_out, 0.0);
   for (size_t r = 0; r < nb.size(); ++r) {
+    const int kv = (int)nb[r].size();
     for (int co = 0; co < c_out; ++co) {
       double acc = (double)bias[co];
-      for (int k = 0; k < 27; ++k) {
+      for (int k = 0; k < kv; ++k) {
         int64_t n = nb[r][k];
         if (n < 0) continue;
         for (int ci = 0; ci < c_in; ++ci)
@@ -213,8 +217,9 @@ struct OrcWeights {
   int model_mode, pad3;
   const float* emb_o;       // [256][C]  Emb(O^{d-1})
   const float* emb_d;       // [8][C]    Emb(delta)
-  const float* top_w[4];    // [27][C][C] residual blocks: A1, A2 (scale d-1), B1, B2 (scale d)
+  const float* top_w[4];    // [ks^3][C][C] residual blocks: A1, A2 (scale d-1), B1, B2 (scale d)
   const float* top_b[4];    // [C]
+  int kernel_size, pad4;    // ks of the full predictor's convs (0 reads as 3)
 };
 
 uint64_t orc_morton(int64_t x, int64_t y, int64_t z, int bits) {
@@ -357,11 +362,12 @@ int64_t orc_expand(void* h, int b, const uint8_t* codes, int64_t* out_xyz) {
   return (int64_t)ch.size();
 }
 
-// Neighbour map [N_b][27] of scale b.
-void orc_neighbors(void* h, int b, int32_t* out) {
+// Neighbour map [N_b][ks^3] of scale b for kernel size ks (odd).
+void orc_neighbors(void* h, int b, int ks, int32_t* out) {
   const Level& L = static_cast<Pyramid*>(h)->lv[b];
+  const int kv = ks * ks * ks;
   for (size_t i = 0; i < L.v.size(); ++i)
-    for (int k = 0; k < 27; ++k) out[i * 27 + k] = (int32_t)neighbour(L.row, b, L.v[i], k);
+    for (int k = 0; k < kv; ++k) out[i * kv + k] = (int32_t)neighbour(L.row, b, L.v[i], k, ks);
 }
 
 // Input features of the target voxels (target embedding, Eqs. 7-8, in the
@@ -387,7 +393,8 @@ void orc_features(void* h, int b, double* out /*[N][11]*/) {
 // Standalone sparse conv on an explicit voxel list (rows in the given order),
 // used to pin the layer against a dense 3D convolution.
 int orc_sparse_conv(const int64_t* xyz, int64_t n, int bits, const double* feats, int c_in,
-                    const float* W, const float* bias, int c_out, int relu, double* out) {
+                    const float* W, const float* bias, int c_out, int relu, int ks, double* out) {
+  if (ks < 1 || ks % 2 == 0) return -1;
   std::vector<Vox> v(n);
   std::map<Vox, int64_t> rows;
   for (int64_t i = 0; i < n; ++i) {
@@ -396,8 +403,8 @@ int orc_sparse_conv(const int64_t* xyz, int64_t n, int bits, const double* feats
     rows[v[i]] = i;
   }
   std::vector<double> h(feats, feats + n * c_in), y;
-  std::vector<std::array<int64_t, 27>> nb(n);
-  for (int64_t i = 0; i < n; ++i) nb[i] = neighbours_of(rows, bits, v[i]);
+  std::vector<Nbrs> nb(n);
+  for (int64_t i = 0; i < n; ++i) nb[i] = neighbours_of(rows, bits, v[i], ks);
   sparse_conv(nb, h, c_in, W, bias, c_out, relu != 0, y);
   std::copy(y.begin(), y.end(), out);
   return 0;
@@ -413,7 +420,7 @@ int orc_sparse_conv(const int64_t* xyz, int64_t n, int bits, const double* feats
 //   NULL), bits [nrows] (or NULL; needs b < B).
 // Residual block of the full predictor: x + conv2(ReLU(conv1(x))), then ReLU
 // (3x3x3 submanifold convs C -> C with bias, on the neighbour lists nb).
-static void res_block(const std::vector<std::array<int64_t, 27>>& nb, const std::vector<double>& x, int C,
+static void res_block(const std::vector<Nbrs>& nb, const std::vector<double>& x, int C,
                       const float* w1, const float* b1, const float* w2, const float* b2,
                       std::vector<double>& out) {
   std::vector<double> t, y;
@@ -433,9 +440,10 @@ static int top_features(Pyramid* P, int b, const OrcWeights* w, std::vector<doub
   const Level& Pl = P->lv[b - 1];
   const int C = w->channels;
   const int64_t Np = (int64_t)Pl.v.size(), N = (int64_t)L.v.size();
-  std::vector<std::array<int64_t, 27>> nbA(Np), nbB(N);
-  for (int64_t u = 0; u < Np; ++u) nbA[u] = neighbours_of(Pl.row, b - 1, Pl.v[u]);
-  for (int64_t v = 0; v < N; ++v) nbB[v] = neighbours_of(L.row, b, L.v[v]);
+  const int ks = w->kernel_size > 0 ? w->kernel_size : 3;
+  std::vector<Nbrs> nbA(Np), nbB(N);
+  for (int64_t u = 0; u < Np; ++u) nbA[u] = neighbours_of(Pl.row, b - 1, Pl.v[u], ks);
+  for (int64_t v = 0; v < N; ++v) nbB[v] = neighbours_of(L.row, b, L.v[v], ks);
   std::vector<double> xa(Np * C), fa, xb(N * C);
   for (int64_t u = 0; u < Np; ++u)
     for (int c = 0; c < C; ++c) xa[u * C + c] = (double)w->emb_o[(size_t)Pl.code[u] * C + c];
@@ -476,8 +484,8 @@ static int final_features(void* h, int b, const OrcWeights* w, const int64_t* ro
     if (rows[i] < 0 || rows[i] >= N) return -1;
     if (!mark[rows[i]]) { mark[rows[i]] = 1; need[w->layers].push_back(rows[i]); }
   }
-  std::map<int64_t, std::array<int64_t, 27>> nbmap;   // neighbour rows, computed once per row
-  auto nbrs = [&](int64_t r) -> const std::array<int64_t, 27>& {
+  std::map<int64_t, Nbrs> nbmap;   // neighbour rows, computed once per row
+  auto nbrs = [&](int64_t r) -> const Nbrs& {
     auto it = nbmap.find(r);
     if (it == nbmap.end()) it = nbmap.emplace(r, neighbours_of(L.row, b, L.v[r])).first;
     return it->second;
@@ -503,7 +511,7 @@ static int final_features(void* h, int b, const OrcWeights* w, const int64_t* ro
   for (int l = 1; l <= w->layers; ++l) {
     std::vector<int64_t> out_rows = need[l];
     std::sort(out_rows.begin(), out_rows.end());
-    std::vector<std::array<int64_t, 27>> nb;
+    std::vector<Nbrs> nb;
     for (int64_t r : out_rows) nb.push_back(nbrs(r));
     sparse_conv(nb, cur, c_in, w->conv_w[l - 1], w->conv_b[l - 1], C, true, y);
     std::vector<double> nxt(N * C, 0.0);

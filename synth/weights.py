@@ -35,7 +35,8 @@ _W_STREAM = 21
 
 def gen_weights(channels: int, layers: int, seed: int = 2, bias_std: float = 0.0,
                 head_scale: float = 1.0, in_features: int = IN_FEATURES,
-                two_stage: bool = False, emb_std: float = 1.0, top: bool = False) -> dict:
+                two_stage: bool = False, emb_std: float = 1.0, top: bool = False,
+                kernel_size: int = 3) -> dict:
     draw = [0]
 
     def normals(n):
@@ -71,8 +72,9 @@ def gen_weights(channels: int, layers: int, seed: int = 2, bias_std: float = 0.0
         out["emb_o"] = (normals(256 * channels) * emb_std).reshape(256, channels).astype(np.float32)
         out["emb_d"] = (normals(8 * channels) * emb_std).reshape(8, channels).astype(np.float32)
         out["top_w"], out["top_b"] = [], []
+        kv = kernel_size ** 3   # the full predictor's convs: ks^3 offsets
         for _ in range(4):
-            w_ = normals(KVOL * channels * channels) * np.sqrt(2.0 / (KVOL * channels))
-            out["top_w"].append(w_.reshape(KVOL, channels, channels).astype(np.float32))
+            w_ = normals(kv * channels * channels) * np.sqrt(2.0 / (kv * channels))
+            out["top_w"].append(w_.reshape(kv, channels, channels).astype(np.float32))
             out["top_b"].append((normals(channels) * bias_std).astype(np.float32))
     return out

@@ -208,6 +208,30 @@ def test_neighbor_map_brute_force():
         assert np.array_equal(nb[:, 13], np.arange(len(v)))
 
 
+def test_neighbor_map_brute_force_kernel5():
+    """5 x 5 x 5 neighbourhoods: k = (dx+2) + 5(dy+2) + 25(dz+2), centre 62."""
+    rs = np.random.default_rng(12)
+    B = 5
+    xyz = rs.integers(0, 1 << B, size=(250, 3))
+    P = oracle.Pyramid.from_voxels(xyz, B, 2)
+    for b in (3, 5):
+        v = P.xyz(b)
+        nb = P.neighbors(b, 5)
+        assert nb.shape == (len(v), 125)
+        index = {tuple(p): i for i, p in enumerate(v.tolist())}
+        lim = 1 << b
+        for i, p in enumerate(v.tolist()):
+            for dz, dy, dx in itertools.product(range(-2, 3), repeat=3):
+                k = (dx + 2) + 5 * (dy + 2) + 25 * (dz + 2)
+                q = (p[0] + dx, p[1] + dy, p[2] + dz)
+                inside = all(0 <= c < lim for c in q)
+                assert nb[i, k] == (index.get(q, -1) if inside else -1)
+        assert np.array_equal(nb[:, 62], np.arange(len(v)))
+        # the 3 x 3 x 3 map is the centre of the 5 x 5 x 5 one
+        sub = [(dx + 2) + 5 * (dy + 2) + 25 * (dz + 2) for dz in (-1, 0, 1) for dy in (-1, 0, 1) for dx in (-1, 0, 1)]
+        np.testing.assert_array_equal(nb[:, sub], P.neighbors(b))
+
+
 # ---- P7 / P8: sparse conv vs dense conv3d ------------------------------------------------
 
 def test_sparse_conv_equals_dense_conv3d():
@@ -233,6 +257,31 @@ def test_sparse_conv_equals_dense_conv3d():
         if relu:
             out = torch.relu(out)
         dense = out[0, :, xyz[:, 2], xyz[:, 1], xyz[:, 0]].T.numpy()       # mask to the voxels
+        np.testing.assert_allclose(y, dense, rtol=1e-12, atol=1e-12)
+
+
+def test_sparse_conv_kernel5_equals_dense_conv3d():
+    import torch
+    rs = np.random.default_rng(14)
+    b = 4
+    G = 1 << b
+    flat = rs.choice(G ** 3, size=500, replace=False)
+    xyz = np.stack([flat % G, (flat // G) % G, flat // (G * G)], axis=1)
+    for c_in, c_out, relu in [(16, 16, True), (6, 9, False)]:
+        feats = rs.normal(size=(500, c_in))
+        W = rs.normal(size=(125, c_in, c_out)).astype(np.float32)
+        bias = rs.normal(size=c_out).astype(np.float32)
+        y = oracle.sparse_conv(xyz, b, feats, W, bias, relu)
+        grid = torch.zeros((1, c_in, G, G, G), dtype=torch.float64)
+        grid[0, :, xyz[:, 2], xyz[:, 1], xyz[:, 0]] = torch.from_numpy(feats.T)
+        Wt = torch.zeros((c_out, c_in, 5, 5, 5), dtype=torch.float64)
+        for k in range(125):
+            dx, dy, dz = k % 5, (k // 5) % 5, k // 25
+            Wt[:, :, dz, dy, dx] = torch.from_numpy(W[k].astype(np.float64).T)
+        out = torch.nn.functional.conv3d(grid, Wt, torch.from_numpy(bias.astype(np.float64)), padding=2)
+        if relu:
+            out = torch.relu(out)
+        dense = out[0, :, xyz[:, 2], xyz[:, 1], xyz[:, 0]].T.numpy()
         np.testing.assert_allclose(y, dense, rtol=1e-12, atol=1e-12)
 
 
@@ -538,6 +587,23 @@ def test_top_equals_composition_of_pinned_pieces():
     xyz = rs.integers(0, 1 << B, size=(900, 3)) // 2 + 16
     P = oracle.Pyramid.from_voxels(xyz, B, b0)
     w = _top_weights(16)
+    for b in (b0 + 1, B - 1):
+        lg, lse, bits = P.model(b, w)
+        ref = _top_by_composition(P, b, w)
+        np.testing.assert_allclose(lg, ref, rtol=0, atol=1e-9)
+        code = P.codes(b).astype(np.int64)
+        np.testing.assert_allclose(bits, (lse - ref[np.arange(len(code)), code]) / math.log(2), atol=1e-9)
+
+
+@pytest.mark.parametrize("C,ks", [(16, 5), (64, 3), (128, 5)])
+def test_top_wide_and_kernel5_equal_composition(C, ks):
+    """Other widths and the 5 x 5 x 5 kernel (the large model: c128, k5)."""
+    rs = np.random.default_rng(18)
+    B, b0 = 6, 2
+    xyz = rs.integers(0, 1 << B, size=(300 if C == 128 else 600, 3)) // 2 + 8
+    P = oracle.Pyramid.from_voxels(xyz, B, b0)
+    w = _top_weights(C, kernel_size=ks)
+    assert w["top_w"][0].shape == (ks ** 3, C, C)
     for b in (b0 + 1, B - 1):
         lg, lse, bits = P.model(b, w)
         ref = _top_by_composition(P, b, w)
