@@ -96,7 +96,10 @@ typedef struct {
   int precision;             /* RENO_PREC_FP32 (0) or RENO_PREC_BF16X3 */
   int model_mode;            /* RENO_MODEL_PLAIN (0) or RENO_MODEL_TOP (layers is then
                                 unused: the full predictor has its four convs) */
-  int pad0;
+  int kernel_size;           /* full predictor: 3 (0 reads as 3) or 5; the plain model
+                                uses 3.  Channels: 16 or 32 for the plain model; 16,
+                                32, 64 or 128 for the full predictor (c128 with kernel
+                                5 is the large variant) */
 } reno_params;
 
 /* Model weights (fp32, device memory, row-major).  Layout:
@@ -113,7 +116,7 @@ typedef struct {
  * Full predictor (RENO_MODEL_TOP; conv_w / conv_b are then not read):
  *   emb_o      [256][C]  Emb_O, indexed by the code of a voxel of scale d-1
  *   emb_d      [8][C]    Emb_D, indexed by the octant delta of a voxel of scale d
- *   top_w[i]   [27][C][C], top_b[i] [C]: convs A1, A2 (residual block on scale
+ *   top_w[i]   [ks^3][C][C], top_b[i] [C]: convs A1, A2 (residual block on scale
  *              d-1) and B1, B2 (residual block on scale d); a block computes
  *              ReLU(x + conv2(ReLU(conv1(x)))) with biases inside both convs
  * Only the pointers of the context's model and head modes are read.        */
@@ -246,9 +249,11 @@ reno_status reno_predict_second(reno_ctx* ctx, int scale, const uint8_t* s1, flo
  * scales concatenated. */
 reno_status reno_code_length(reno_ctx* ctx, int scale, float* bits_per_voxel, double* total_host);
 
-/* Neighbour map of a model scale, int32 [N_scale][27]: entry k is the row in
- * V_scale of v + (dx,dy,dz), k = (dx+1) + 3(dy+1) + 9(dz+1), or -1 when absent
- * or outside [0, 2^scale)^3.  Available after predict_probs of that scale. */
+/* Neighbour map of a model scale, int32 [N_scale][ks^3] (ks = 3, or the full
+ * predictor's kernel size): entry k is the row in V_scale of v + (dx,dy,dz),
+ * k = (dx+h) + ks(dy+h) + ks^2(dz+h) with h = ks/2 (for ks = 3: (dx+1) +
+ * 3(dy+1) + 9(dz+1)), or -1 when absent or outside [0, 2^scale)^3.
+ * Available after predict_probs of that scale. */
 reno_status reno_neighbor_map(reno_ctx* ctx, int scale, int32_t* map);
 
 /* Quantised distribution for the host coder, uint16 [N_scale][256]:

@@ -51,7 +51,7 @@ class reno_params(ctypes.Structure):
                 ("range_m", ctypes.c_double), ("in_features", ctypes.c_int),
                 ("channels", ctypes.c_int), ("layers", ctypes.c_int),
                 ("head_mode", ctypes.c_int), ("precision", ctypes.c_int),
-                ("model_mode", ctypes.c_int), ("pad0", ctypes.c_int)]
+                ("model_mode", ctypes.c_int), ("kernel_size", ctypes.c_int)]
 
 
 class reno_weights(ctypes.Structure):
@@ -134,14 +134,15 @@ class Context:
 
     def __init__(self, max_points: int, max_bit_depth: int, min_bit_depth: int, range_m: float,
                  channels: int, layers: int, max_model_voxels: int = 0, stream=None,
-                 two_stage: bool = False, precision: int = RENO_PREC_FP32, top: bool = False):
+                 two_stage: bool = False, precision: int = RENO_PREC_FP32, top: bool = False,
+                 kernel_size: int = 3):
         import torch
         self.torch = torch
         self.device = torch.device("cuda", torch.cuda.current_device())
         self.stream = stream if stream is not None else torch.cuda.current_stream()
         p = reno_params(max_points, max_model_voxels, max_bit_depth, min_bit_depth, range_m, 11,
                         channels, layers, RENO_HEAD_TWO_STAGE if two_stage else RENO_HEAD_ONE_STAGE,
-                        precision, RENO_MODEL_TOP if top else RENO_MODEL_PLAIN, 0)
+                        precision, RENO_MODEL_TOP if top else RENO_MODEL_PLAIN, kernel_size)
         h = ctypes.c_void_p()
         rc = lib().reno_create(ctypes.byref(p), ctypes.c_void_p(self.stream.cuda_stream),
                                ctypes.byref(h))
@@ -154,6 +155,7 @@ class Context:
         self.layers = layers
         self.two_stage = two_stage
         self.top = top
+        self.kernel_size = kernel_size
         self.B = 0
         self._keep = []
 
@@ -320,7 +322,7 @@ class Context:
 
     def neighbor_map(self, scale: int):
         n = self.num_voxels(scale)
-        out = self._empty((max(n, 1), 27), self.torch.int32)
+        out = self._empty((max(n, 1), self.kernel_size ** 3 if self.top else 27), self.torch.int32)
         self._check(lib().reno_neighbor_map(self._h, scale, _ptr(out)))
         return out[:n]
 

@@ -139,8 +139,11 @@ reno_status reno_create(const reno_params* p, void* hip_stream, reno_ctx** out) 
     return fail(nullptr, RENO_E_INVALID, "range_m must be positive and finite");
   if (p->in_features != RENO_IN_FEATURES)
     return fail(nullptr, RENO_E_INVALID, "in_features must be 11");
-  if (p->channels != 16 && p->channels != 32)
-    return fail(nullptr, RENO_E_INVALID, "channels must be 16 or 32");
+  const bool top_mode = p->model_mode == RENO_MODEL_TOP;
+  if (!(p->channels == 16 || p->channels == 32 || (top_mode && (p->channels == 64 || p->channels == 128))))
+    return fail(nullptr, RENO_E_INVALID, "channels must be 16 or 32 (full predictor: 16, 32, 64 or 128)");
+  if (p->kernel_size != 0 && p->kernel_size != 3 && !(top_mode && p->kernel_size == 5))
+    return fail(nullptr, RENO_E_INVALID, "kernel_size must be 3 (full predictor: 3 or 5)");
   if (p->layers < 1 || p->layers > RENO_MAX_LAYERS)
     return fail(nullptr, RENO_E_INVALID, "layers must be in [1, 8]");
   if (p->head_mode != RENO_HEAD_ONE_STAGE && p->head_mode != RENO_HEAD_TWO_STAGE)
@@ -207,7 +210,7 @@ reno_status reno_create(const reno_params* p, void* hip_stream, reno_ctx** out) 
     A(dalloc(&c->w_embo, (size_t)256 * C, &c->device_bytes));
     A(dalloc(&c->w_embd, (size_t)8 * C, &c->device_bytes));
   }
-  A(dalloc(&c->d_nbr, rows * reno::NBR_STRIDE, &c->device_bytes));
+  A(dalloc(&c->d_nbr, rows * c->nbr_stride(), &c->device_bytes));
   A(dalloc(&c->d_lse, (size_t)cap_model, &c->device_bytes));
   A(dalloc(&c->d_lse2, (size_t)cap_model, &c->device_bytes));
   A(dalloc(&c->d_perm, rows, &c->device_bytes));
@@ -218,7 +221,8 @@ reno_status reno_create(const reno_params* p, void* hip_stream, reno_ctx** out) 
   for (int l = 0; l < (top ? 4 : p->layers); ++l) {
     const int KS = (c_in + 3) / 4, KSP = (KS + 3) & ~3;
     // fp32: KSP floats per (offset, column block, lane); bf16x3: 8 words
-    A(dalloc(&c->w_conv[l], (size_t)27 * (C / 16) * 64 * std::max(KSP, 8), &c->device_bytes));
+    A(dalloc(&c->w_conv[l], (size_t)(top ? c->kvol() : 27) * (C / 16) * 64 * std::max(KSP, 8),
+             &c->device_bytes));
     A(dalloc(&c->w_bias[l], (size_t)C, &c->device_bytes));
     c_in = C;
   }

@@ -134,6 +134,14 @@ struct Ctx {
   int b0() const { return p.min_bit_depth; }
   int64_t lv(int b) const { return (int64_t)(b - p.min_bit_depth) * cap_pts; }
   bool top() const { return p.model_mode == RENO_MODEL_TOP; }
+  // kernel size of the full predictor's convs (3 or 5) and its offsets
+  int ks() const { return p.kernel_size == 5 ? 5 : 3; }
+  int kvol() const { return ks() * ks() * ks(); }
+  // neighbour-map row: 27 offsets + 5 padding, or 125 + 3
+  int nbr_stride() const { return ks() == 5 ? 128 : NBR_STRIDE; }
+  // the full predictor runs on streamed-weight kernels when its weights do
+  // not fit the LDS-resident conv kernel (C above 32 or a 5x5x5 kernel)
+  bool wide() const { return top() && (p.channels > 32 || ks() == 5); }
   // rows of the feature buffers: the model rows, the zero row cap_model and,
   // for the full predictor, the base scale
   int64_t cap_rows() const { return cap_model + 1 + (top() ? cap_pts : 0); }

@@ -71,11 +71,11 @@ __device__ __forceinline__ f4 mfma_bf3(const uint4& ah, const uint4& al, const u
 // Weight packing.  Conv layer (C_in -> C): KS = ceil(C_in/4) MFMA k-steps per
 // offset; lane l (g = l/16) feeds input channel ci = g*KS + s at step s and
 // output channel co = 16*cb + l%16.  Packed [27][C/16][64][KSP], KSP = KS
-// rounded up to 4, zero padded.
-__global__ void k_pack_conv(const float* __restrict__ W, int c_in, int C, int KS, int KSP,
+// rounded up to 4, zero padded (kv offsets: 27, or 125 for a 5x5x5 kernel).
+__global__ void k_pack_conv(const float* __restrict__ W, int c_in, int C, int KS, int KSP, int kv,
                             float* __restrict__ out) {
   const int ncb = C / 16;
-  const int total = 27 * ncb * 64 * KSP;
+  const int total = kv * ncb * 64 * KSP;
   for (int i = blockIdx.x * blockDim.x + threadIdx.x; i < total; i += gridDim.x * blockDim.x) {
     const int s = i % KSP;
     const int lane = (i / KSP) % 64;
@@ -332,6 +332,29 @@ __device__ __forceinline__ void stage_lds(const f4* __restrict__ src, f4* dst, i
   }
 }
 
+// Register-staged copy of N16 16-byte words into LDS, in two halves: the
+// loads (issued early, so that their latency overlaps other work) and the
+// stores.
+template <int N16, int THREADS>
+struct Staged {
+  static constexpr int PER = (N16 + THREADS - 1) / THREADS;
+  f4 v[PER];
+  __device__ __forceinline__ void load(const f4* __restrict__ src, int tid) {
+#pragma unroll
+    for (int i = 0; i < PER; ++i) {
+      const int idx = i * THREADS + tid;
+      if (idx < N16) v[i] = src[idx];
+    }
+  }
+  __device__ __forceinline__ void store(f4* dst, int tid) const {
+#pragma unroll
+    for (int i = 0; i < PER; ++i) {
+      const int idx = i * THREADS + tid;
+      if (idx < N16) dst[idx] = v[i];
+    }
+  }
+};
+
 // Neighbour rows of a voxel from the parent scale.  The 27 cells around v lie
 // in at most 8 cells of the parent scale: the parent p and, per axis, the
 // neighbour of p on v's side.  Lane (r, g) probes cells e = 2g and 2g+1
@@ -374,6 +397,111 @@ __device__ __forceinline__ void parent_cell_rows(uint64_t kf, int b, int g, cons
       const uint32_t d = (uint32_t)((ux & 1) | ((uy & 1) << 1) | ((uz & 1) << 2));
       if ((code >> d) & 1u) nb[j] = (int32_t)first + __popc(code & ((1u << d) - 1u));
     }
+  }
+}
+
+// Head of the last conv layer's features h (the conv accumulators of a tile:
+// lane (r, g) holds channels 16 cb + 4 g .. + 3 of voxel r) in registers:
+// the one-stage 256-way head with its softmax normaliser (Eq. 10), or the
+// two-stage head (Eqs. 11-13).  Writes lse (lse2, S1) at row prow and, when
+// requested, the logits at row prow - mo_first.
+template <int C, bool TWO, bool BF>
+__device__ __forceinline__ void head_epilogue(const ConvArgs& a, const f4 (&acc)[C / 16], const float* s_h, int lane,
+                                              int g, bool valid, int64_t prow, int64_t mo, int64_t lvb,
+                                              int64_t mo_first) {
+  constexpr int KT = C / 4;
+  constexpr int NCB = C / 16;
+  if constexpr (TWO) {
+    // ---- two-stage head (Eqs. 11-13): stage 1 over S1; stage 2 over S2
+    // with h + Emb(S1) when the codes of the scale are known
+    const f4* hp = reinterpret_cast<const f4*>(s_h) + lane * (KT / 4);
+    const uint4* hpb = reinterpret_cast<const uint4*>(s_h) + lane * 2;
+    f4 z1;
+    if constexpr (BF) {
+      uint4 bh, bl;
+      head_operand_bf<C>(acc, bh, bl);
+      z1 = head16_bf<C>(hpb, a.hb, bh, bl, g);
+    } else {
+      z1 = head16<C>(hp, a.hb, acc, g);
+    }
+    const float l1 = lse16(z1);
+    if (valid && g == 0) a.lse[prow] = l1;
+    float* lo = (a.logits && valid) ? a.logits + (prow - mo_first) * 32 + 4 * g : nullptr;
+    if (lo) *reinterpret_cast<f4*>(lo) = z1;
+    if (a.s1_code) {
+      const int s1 = a.s1_code[lvb + (prow - mo)] & 15;
+      f4 h2[NCB];
+      add_emb<C>(acc, a.emb + s1 * C, g, h2);
+      f4 z2;
+      if constexpr (BF) {
+        uint4 bh, bl;
+        head_operand_bf<C>(h2, bh, bl);
+        z2 = head16_bf<C>(hpb + 64 * 2, a.hb + 16, bh, bl, g);
+      } else {
+        z2 = head16<C>(hp + 64 * (KT / 4), a.hb + 16, h2, g);
+      }
+      const float l2 = lse16(z2);
+      if (valid && g == 0) {
+        a.lse2[prow] = l2;
+        a.s1_out[prow] = (uint8_t)s1;
+      }
+      if (lo) *reinterpret_cast<f4*>(lo + 16) = z2;
+    }
+  }
+  if constexpr (!TWO) {
+    // ---- head: z^T[256][16] = H^T h^T with the conv accumulators as the B
+    // operand; 64 symbols at a time with a running (max, sum of exp)
+    float m = -INFINITY, ssum = 0.0f;
+    float* lo = (a.logits && valid) ? a.logits + (prow - mo_first) * 256 + 4 * g : nullptr;
+    uint4 bh = make_uint4(0, 0, 0, 0), bl = bh;
+    if constexpr (BF) head_operand_bf<C>(acc, bh, bl);
+#pragma unroll 1
+    for (int grp = 0; grp < 4; ++grp) {
+      f4 zz[4];
+#pragma unroll
+      for (int q4 = 0; q4 < 4; ++q4) {
+        const int sb = grp * 4 + q4;
+        if constexpr (BF) {
+          zz[q4] = head16_bf<C>(reinterpret_cast<const uint4*>(s_h) + (sb * 64 + lane) * 2, a.hb + 16 * sb,
+                                bh, bl, g);
+        } else {
+          zz[q4] = *reinterpret_cast<const f4*>(a.hb + 16 * sb + 4 * g);
+          const f4* hp = reinterpret_cast<const f4*>(s_h + (sb * 64 + lane) * KT);
+#pragma unroll
+          for (int q = 0; q < KT / 4; ++q) {
+            const f4 hv = hp[q];
+#pragma unroll
+            for (int e = 0; e < 4; ++e) zz[q4] = mfma4(hv[e], acc[q][e], zz[q4]);
+          }
+        }
+      }
+      float gm = zz[0][0];
+#pragma unroll
+      for (int q4 = 0; q4 < 4; ++q4)
+#pragma unroll
+        for (int e = 0; e < 4; ++e) gm = fmaxf(gm, zz[q4][e]);
+      const float mn = fmaxf(m, gm);
+      float part = 0.0f;
+#pragma unroll
+      for (int q4 = 0; q4 < 4; ++q4)
+#pragma unroll
+        for (int e = 0; e < 4; ++e) part += __expf(zz[q4][e] - mn);
+      ssum = ssum * __expf(m - mn) + part;
+      m = mn;
+      if (lo) {
+#pragma unroll
+        for (int q4 = 0; q4 < 4; ++q4) *reinterpret_cast<f4*>(lo + 16 * (grp * 4 + q4)) = zz[q4];
+      }
+    }
+    // the 4 lanes r, r+16, r+32, r+48 hold the 4 quarters of voxel r's symbols
+#pragma unroll
+    for (int o = 16; o <= 32; o <<= 1) {
+      const float om = __shfl_xor(m, o), os = __shfl_xor(ssum, o);
+      const float mn = fmaxf(m, om);
+      ssum = ssum * __expf(m - mn) + os * __expf(om - mn);
+      m = mn;
+    }
+    if (valid && g == 0) a.lse[prow] = m + __logf(ssum);
   }
 }
 
@@ -685,98 +813,7 @@ __global__ void __launch_bounds__(CONV_THREADS) k_conv(ConvArgs a) {
       }
     }
 
-    if constexpr (LAST && TWO) {
-      // ---- two-stage head (Eqs. 11-13): stage 1 over S1; stage 2 over S2
-      // with h + Emb(S1) when the codes of the scale are known
-      const f4* hp = reinterpret_cast<const f4*>(s_h) + lane * (KT / 4);
-      const uint4* hpb = reinterpret_cast<const uint4*>(s_h) + lane * 2;
-      f4 z1;
-      if constexpr (BF) {
-        uint4 bh, bl;
-        head_operand_bf<C>(acc, bh, bl);
-        z1 = head16_bf<C>(hpb, a.hb, bh, bl, g);
-      } else {
-        z1 = head16<C>(hp, a.hb, acc, g);
-      }
-      const float l1 = lse16(z1);
-      if (valid && g == 0) a.lse[prow] = l1;
-      float* lo = (a.logits && valid) ? a.logits + (prow - s_mo[0]) * 32 + 4 * g : nullptr;
-      if (lo) *reinterpret_cast<f4*>(lo) = z1;
-      if (a.s1_code) {
-        const int s1 = a.s1_code[lvb + (prow - mo)] & 15;
-        f4 h2[NCB];
-        add_emb<C>(acc, a.emb + s1 * C, g, h2);
-        f4 z2;
-        if constexpr (BF) {
-          uint4 bh, bl;
-          head_operand_bf<C>(h2, bh, bl);
-          z2 = head16_bf<C>(hpb + 64 * 2, a.hb + 16, bh, bl, g);
-        } else {
-          z2 = head16<C>(hp + 64 * (KT / 4), a.hb + 16, h2, g);
-        }
-        const float l2 = lse16(z2);
-        if (valid && g == 0) {
-          a.lse2[prow] = l2;
-          a.s1_out[prow] = (uint8_t)s1;
-        }
-        if (lo) *reinterpret_cast<f4*>(lo + 16) = z2;
-      }
-    }
-    if constexpr (LAST && !TWO) {
-      // ---- head: z^T[256][16] = H^T h^T with the conv accumulators as the B
-      // operand; 64 symbols at a time with a running (max, sum of exp)
-      float m = -INFINITY, ssum = 0.0f;
-      float* lo = (a.logits && valid) ? a.logits + (prow - s_mo[0]) * 256 + 4 * g : nullptr;
-      uint4 bh = make_uint4(0, 0, 0, 0), bl = bh;
-      if constexpr (BF) head_operand_bf<C>(acc, bh, bl);
-#pragma unroll 1
-      for (int grp = 0; grp < 4; ++grp) {
-        f4 zz[4];
-#pragma unroll
-        for (int q4 = 0; q4 < 4; ++q4) {
-          const int sb = grp * 4 + q4;
-          if constexpr (BF) {
-            zz[q4] = head16_bf<C>(reinterpret_cast<const uint4*>(s_h) + (sb * 64 + lane) * 2, a.hb + 16 * sb,
-                                  bh, bl, g);
-          } else {
-            zz[q4] = *reinterpret_cast<const f4*>(a.hb + 16 * sb + 4 * g);
-            const f4* hp = reinterpret_cast<const f4*>(s_h + (sb * 64 + lane) * KT);
-#pragma unroll
-            for (int q = 0; q < KT / 4; ++q) {
-              const f4 hv = hp[q];
-#pragma unroll
-              for (int e = 0; e < 4; ++e) zz[q4] = mfma4(hv[e], acc[q][e], zz[q4]);
-            }
-          }
-        }
-        float gm = zz[0][0];
-#pragma unroll
-        for (int q4 = 0; q4 < 4; ++q4)
-#pragma unroll
-          for (int e = 0; e < 4; ++e) gm = fmaxf(gm, zz[q4][e]);
-        const float mn = fmaxf(m, gm);
-        float part = 0.0f;
-#pragma unroll
-        for (int q4 = 0; q4 < 4; ++q4)
-#pragma unroll
-          for (int e = 0; e < 4; ++e) part += __expf(zz[q4][e] - mn);
-        ssum = ssum * __expf(m - mn) + part;
-        m = mn;
-        if (lo) {
-#pragma unroll
-          for (int q4 = 0; q4 < 4; ++q4) *reinterpret_cast<f4*>(lo + 16 * (grp * 4 + q4)) = zz[q4];
-        }
-      }
-      // the 4 lanes r, r+16, r+32, r+48 hold the 4 quarters of voxel r's symbols
-#pragma unroll
-      for (int o = 16; o <= 32; o <<= 1) {
-        const float om = __shfl_xor(m, o), os = __shfl_xor(ssum, o);
-        const float mn = fmaxf(m, om);
-        ssum = ssum * __expf(m - mn) + os * __expf(om - mn);
-        m = mn;
-      }
-      if (valid && g == 0) a.lse[prow] = m + __logf(ssum);
-    }
+    if constexpr (LAST) head_epilogue<C, TWO, BF>(a, acc, s_h, lane, g, valid, prow, mo, lvb, s_mo[0]);
     int nxt = 0;
     if (lane == 0) nxt = atomicAdd(&s_next, 1);
     slot = CONV_WAVES + __builtin_amdgcn_readfirstlane(__shfl(nxt, 0));
@@ -981,6 +1018,413 @@ __global__ void __launch_bounds__(256) k_top_prep(int lo, int nsc, int n_embed, 
   }
 }
 
+// ---------------------------------------------------------------------------
+// Large kernels and wide layers of the full predictor (5x5x5 kernels, C up to
+// 128: the paper's large variant is c128, k5).
+
+// Neighbour rows of a voxel for a 5x5x5 kernel.  The 125 cells around v span
+// x-2 .. x+2 on each axis, i.e. the parents p-1 .. p+1: 27 cells of the
+// parent scale.  Lane (r, g) probes parent cells e = g, g+4, ... (e = (ex+1) +
+// 3(ey+1) + 9(ez+1)), the hits are exchanged through par (27 LDS slots of
+// voxel r), and the lane ends with the rows of offsets k = 32g .. 32g+31,
+// k = (dx+2) + 5(dy+2) + 25(dz+2) (125 .. 127 padding; -1: absent or
+// off-grid).
+__device__ __forceinline__ void parent_cell_rows5(uint64_t kf, int b, int g, const HashSlot* __restrict__ hash,
+                                                  int hash_lg, int fb, volatile uint64_t* par, int32_t (&nb)[32]) {
+  const uint64_t key = morton_part(kf, b), fr = frame_part(kf, b) << (3 * (b - 1));
+  const int x = (int)compact3(key), y = (int)compact3(key >> 1), z = (int)compact3(key >> 2);
+  const int px = x >> 1, py = y >> 1, pz = z >> 1;
+  const int plim = 1 << (b - 1);
+  uint64_t tk[7];
+#pragma unroll
+  for (int i = 0; i < 7; ++i) {
+    const int e = g + 4 * i;
+    const int cx = px + e % 3 - 1, cy = py + (e / 3) % 3 - 1, cz = pz + e / 9 - 1;
+    tk[i] = (e < 27 && cx >= 0 && cy >= 0 && cz >= 0 && cx < plim && cy < plim && cz < plim)
+                ? tag_key(fr | morton3((uint32_t)cx, (uint32_t)cy, (uint32_t)cz), b - 1, fb)
+                : 0ull;
+  }
+  uint2 hit[7];
+  hash_find_n<7>(hash, hash_lg, tk, hit);
+#pragma unroll
+  for (int i = 0; i < 7; ++i)
+    if (g + 4 * i < 27) par[g + 4 * i] = ((uint64_t)hit[i].y << 32) | hit[i].x;
+  __builtin_amdgcn_wave_barrier();
+  const int lim = 1 << b;
+#pragma unroll
+  for (int j = 0; j < 32; ++j) {
+    const int k = 32 * g + j;
+    const int ux = x + k % 5 - 2, uy = y + (k / 5) % 5 - 2, uz = z + k / 25 - 2;
+    nb[j] = -1;
+    if (k < 125 && ux >= 0 && uy >= 0 && uz >= 0 && ux < lim && uy < lim && uz < lim) {
+      const int e = ((ux >> 1) - px + 1) + 3 * ((uy >> 1) - py + 1) + 9 * ((uz >> 1) - pz + 1);
+      const uint64_t pc = par[e];
+      const uint32_t first = (uint32_t)pc, code = (uint32_t)(pc >> 32);
+      const uint32_t d = (uint32_t)((ux & 1) | ((uy & 1) << 1) | ((uz & 1) << 2));
+      if ((code >> d) & 1u) nb[j] = (int32_t)first + __popc(code & ((1u << d) - 1u));
+    }
+  }
+}
+
+// Base-scale rows for a 5x5x5 kernel: the searches of base_cell_rows, eight
+// interleaved at a time over the 32 entries of the lane.
+__device__ __forceinline__ void base_cell_rows5(uint64_t kf, int b, int g, const uint64_t* __restrict__ keys,
+                                                int64_t n, int32_t (&nb)[32]) {
+  const uint64_t key = morton_part(kf, b), fr = kf ^ key;
+  const int x = (int)compact3(key), y = (int)compact3(key >> 1), z = (int)compact3(key >> 2);
+  const int lim = 1 << b;
+#pragma unroll
+  for (int j0 = 0; j0 < 32; j0 += 8) {
+    uint64_t want[8];
+    bool ok[8];
+    int64_t at[8];
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+      const int k = 32 * g + j0 + j;
+      const int ux = x + k % 5 - 2, uy = y + (k / 5) % 5 - 2, uz = z + k / 25 - 2;
+      ok[j] = k < 125 && ux >= 0 && uy >= 0 && uz >= 0 && ux < lim && uy < lim && uz < lim;
+      want[j] = ok[j] ? (fr | morton3((uint32_t)ux, (uint32_t)uy, (uint32_t)uz)) : 0ull;
+      at[j] = 0;
+    }
+    for (int64_t len = n; len > 1;) {
+      const int64_t half = len >> 1;
+#pragma unroll
+      for (int j = 0; j < 8; ++j) at[j] += (keys[at[j] + half] <= want[j]) ? half : 0;
+      len -= half;
+    }
+#pragma unroll
+    for (int j = 0; j < 8; ++j) nb[j0 + j] = (ok[j] && keys[at[j]] == want[j]) ? (int32_t)at[j] : -1;
+  }
+}
+
+// k_top_prep for a 5x5x5 kernel: neighbour maps of stride 128 and X_A rows.
+template <int C>
+__global__ void __launch_bounds__(256) k_top_prep5(int lo, int nsc, int n_embed, int b0, RowMap rm,
+                                                   const uint64_t* __restrict__ lv_key,
+                                                   const uint8_t* __restrict__ lv_code, int64_t cap_pts,
+                                                   const HashSlot* __restrict__ hash, int hash_lg, int fb,
+                                                   const float* __restrict__ emb_o, int32_t* __restrict__ nbr,
+                                                   float* __restrict__ X) {
+  constexpr int Q = C / 16;
+  __shared__ uint64_t s_par[4][16][27];
+  __shared__ int64_t s_n[32], s_mo[32], s_tpre[32];
+  const int tid = threadIdx.x, w = tid >> 6, lane = tid & 63, r = lane & 15, g = lane >> 4;
+  if (tid < nsc) {
+    int64_t o, n;
+    scale_span(rm, lo + tid, o, n);
+    s_n[tid] = n;
+    s_mo[tid] = o;
+  }
+  __syncthreads();
+  if (tid == 0) {
+    int64_t acc = 0;
+    for (int i = 0; i < nsc; ++i) {
+      s_tpre[i] = acc;
+      acc += (s_n[i] + 15) / 16;
+    }
+    for (int i = nsc; i < 32; ++i) s_tpre[i] = acc;
+  }
+  __syncthreads();
+  const int64_t total = s_tpre[31];
+  for (int64_t tile = (int64_t)blockIdx.x * 4 + w; tile < total; tile += (int64_t)gridDim.x * 4) {
+    const int si = scale_of(s_tpre, tile);
+    const int b = lo + si;
+    const int64_t n = s_n[si], mo = s_mo[si];
+    const int64_t row = (tile - s_tpre[si]) * 16 + r;
+    const bool valid = row < n;
+    const int64_t vr = valid ? row : n - 1;
+    const int64_t lvb = (int64_t)(b - b0) * cap_pts;
+    int32_t nb[32];
+    if (b == rm.b_ext)
+      base_cell_rows5(lv_key[lvb + vr], b, g, lv_key + lvb, n, nb);
+    else
+      parent_cell_rows5(lv_key[lvb + vr], b, g, hash, hash_lg, fb, s_par[w][r], nb);
+    if (valid) {
+      int4* dst = reinterpret_cast<int4*>(nbr + (mo + vr) * 128 + 32 * g);
+#pragma unroll
+      for (int q = 0; q < 8; ++q) dst[q] = make_int4(nb[4 * q], nb[4 * q + 1], nb[4 * q + 2], nb[4 * q + 3]);
+      if (si < n_embed) {
+        const f4* e = reinterpret_cast<const f4*>(emb_o + (int)lv_code[lvb + vr] * C) + g * Q;
+        f4* xr = reinterpret_cast<f4*>(X + (mo + vr) * C) + g * Q;
+#pragma unroll
+        for (int q = 0; q < Q; ++q) xr[q] = e[q];
+      }
+    }
+  }
+}
+
+// Offset set of up to 128 offsets (wave-uniform).
+struct OffMask {
+  uint64_t lo = 0, hi = 0;
+  __device__ __forceinline__ void set(int o) {
+    if (o < 64) lo |= 1ull << o;
+    else hi |= 1ull << (o - 64);
+  }
+  // lowest offset, removed from the set (-1 when empty)
+  __device__ __forceinline__ int pop() {
+    if (lo) {
+      const int k = __builtin_ctzll(lo);
+      lo &= lo - 1ull;
+      return k;
+    }
+    if (hi) {
+      const int k = 64 + __builtin_ctzll(hi);
+      hi &= hi - 1ull;
+      return k;
+    }
+    return -1;
+  }
+};
+
+constexpr int CW_THREADS = 512;
+constexpr int CW_WAVES = CW_THREADS / 64;
+
+// Sparse conv C -> C (ReLU, optional residual input, child scatter and row
+// store as in k_conv) with the weights streamed through LDS, for layers whose
+// weights do not fit in it (a 5x5x5 kernel at C = 128 holds 8 MB).  A block
+// takes groups of CW_WAVES tiles, one per wave.  For each offset in the union
+// of the group's occupied offsets, in ascending order, the block stages that
+// offset's C x C weights in LDS (double buffered: the next offset's loads are
+// issued before the current MFMAs), and each wave whose tile has the offset
+// accumulates its gathered neighbour rows on fp32 MFMA 16x16x4 in the layout
+// of k_conv; the wave's next gather is issued before its MFMAs.  A voxel sums
+// its offsets in ascending order whatever its group, so results do not depend
+// on the grouping.
+template <int C, int KV>
+__global__ void __launch_bounds__(CW_THREADS) k_convw(ConvArgs a) {
+  constexpr int NCB = C / 16;
+  constexpr int KS = C / 4;  // input channels of a lane group (one contiguous slice of a row)
+  constexpr int NBS = KV > 27 ? 128 : NBR_STRIDE;
+  constexpr int EPL = NBS / 4;  // map entries per lane
+  constexpr int WQ = C * C / 4;  // 16-byte words of one offset's packed weights
+  __shared__ __attribute__((aligned(16))) float s_w[2][C * C];
+  __shared__ uint64_t s_mask[CW_WAVES][2];
+  __shared__ int64_t s_tpre[NLEV + 1];
+  __shared__ int64_t s_nv[NLEV];
+  __shared__ int64_t s_mo[NLEV];
+  const int tid = threadIdx.x, w = tid >> 6, lane = tid & 63, r = lane & 15, g = lane >> 4;
+  const int nsc = a.b_hi - a.b_lo + 1;
+  const RowMap rm{a.count, a.moff, a.cap_model, a.b_ext, a.ext_off, a.cap_rows};
+  int64_t total_tiles = 0;
+  for (int i = 0; i < nsc; ++i) {
+    int64_t mo, nb;
+    scale_span(rm, a.b_lo + i, mo, nb);
+    total_tiles += (nb + 15) / 16;
+  }
+  const int64_t groups = (total_tiles + CW_WAVES - 1) / CW_WAVES;
+  const int64_t tch = groups / 64 < 4 ? 4 : (groups / 64 > 64 ? 64 : groups / 64);
+  if (conv_tile(0, tch) >= groups) return;  // whole block idle
+  if (tid == 0) {
+    int64_t acc = 0;
+    for (int i = 0; i < nsc; ++i) {
+      int64_t mo, nb;
+      scale_span(rm, a.b_lo + i, mo, nb);
+      s_tpre[i] = acc;
+      s_nv[i] = nb;
+      s_mo[i] = mo;
+      acc += (nb + 15) / 16;
+    }
+    for (int i = nsc; i <= NLEV; ++i) s_tpre[i] = acc;
+  }
+  const f4* wsrc = reinterpret_cast<const f4*>(a.w);
+  for (int64_t gs = 0;; ++gs) {
+    const int64_t grp = conv_tile(gs, tch);  // block-uniform
+    if (grp >= groups) break;
+    __syncthreads();  // prefix visible; the previous group is done with s_mask and s_w
+    const int64_t tile = grp * CW_WAVES + w;
+    const bool have = tile < total_tiles;
+    int b = a.b_lo;
+    int64_t mo = 0, prow = 0, lvb = 0;
+    bool valid = false;
+    if (have) {
+      int si = 0;
+#pragma unroll
+      for (int i = 1; i < NLEV; ++i) si += (s_tpre[i] <= tile) ? 1 : 0;
+      b = a.b_lo + si;
+      const int64_t nvox = s_nv[si];
+      mo = s_mo[si];
+      const int64_t row = (tile - s_tpre[si]) * 16 + r;
+      valid = row < nvox;
+      prow = mo + (valid ? row : nvox - 1);  // idle lanes read a real row
+      lvb = (int64_t)(b - a.b0) * a.cap_pts;
+    }
+    // occupied offsets of the wave's tile (wave-uniform), from the map rows
+    OffMask own;
+    {
+      int32_t nbv[EPL];
+#pragma unroll
+      for (int q = 0; q < EPL / 4; ++q) {
+        int4 t = make_int4(-1, -1, -1, -1);
+        if (have) t = reinterpret_cast<const int4*>(a.nbr + prow * NBS + EPL * g)[q];
+        nbv[4 * q] = t.x;
+        nbv[4 * q + 1] = t.y;
+        nbv[4 * q + 2] = t.z;
+        nbv[4 * q + 3] = t.w;
+      }
+#pragma unroll
+      for (int j = 0; j < EPL; ++j) {
+        const uint64_t bal = __ballot(valid && nbv[j] >= 0);
+#pragma unroll
+        for (int gg = 0; gg < 4; ++gg)
+          if ((bal >> (16 * gg)) & 0xFFFFull) own.set(gg * EPL + j);
+      }
+    }
+    if (lane == 0) {
+      s_mask[w][0] = own.lo;
+      s_mask[w][1] = own.hi;
+    }
+    __syncthreads();
+    OffMask uni;
+    for (int ww = 0; ww < CW_WAVES; ++ww) {
+      uni.lo |= s_mask[ww][0];
+      uni.hi |= s_mask[ww][1];
+    }
+    // each lane reads its own voxel's map entry of an offset two of the
+    // wave's offsets ahead of its use, and gathers one offset ahead
+    const int32_t* maprow = a.nbr + prow * NBS;
+    auto entry = [&](int k) -> int32_t { return (k >= 0 && have) ? maprow[k] : -1; };
+    auto gather = [&](int32_t nn, f4 (&x)[KS / 4]) {
+      const int64_t srow = (valid && nn >= 0) ? mo + nn : a.cap_model;  // absent: the zero row
+      const f4* src = reinterpret_cast<const f4*>(a.h_in + srow * C + g * KS);
+#pragma unroll
+      for (int q = 0; q < KS / 4; ++q) x[q] = src[q];
+    };
+    f4 acc[NCB];
+#pragma unroll
+    for (int cb = 0; cb < NCB; ++cb) acc[cb] = *reinterpret_cast<const f4*>(a.bias + 16 * cb + 4 * g);
+    f4 xa[KS / 4], xb[KS / 4];
+    int ko = own.pop();
+    const int32_t eo = entry(ko);
+    int kq = own.pop();
+    int32_t eq = entry(kq);
+    if (ko >= 0) gather(eo, xa);
+    int kc = uni.pop();
+    Staged<WQ, CW_THREADS> stw;
+    if (kc >= 0) {  // always: wave 0 has a valid voxel, whose own centre is occupied
+      stw.load(wsrc + (int64_t)kc * WQ, tid);
+      stw.store(reinterpret_cast<f4*>(s_w[0]), tid);
+    }
+    __syncthreads();
+    int buf = 0;
+    while (kc >= 0) {  // block-uniform
+      const int kn = uni.pop();
+      if (kn >= 0) stw.load(wsrc + (int64_t)kn * WQ, tid);
+      if (kc == ko) {
+        const int kr = own.pop();
+        const int32_t er = entry(kr);
+        if (kq >= 0) gather(eq, xb);
+        const float* wb = s_w[buf];
+#pragma unroll
+        for (int q = 0; q < KS / 4; ++q) {
+          f4 wv[NCB];
+#pragma unroll
+          for (int cb = 0; cb < NCB; ++cb) wv[cb] = reinterpret_cast<const f4*>(wb + (cb * 64 + lane) * KS)[q];
+#pragma unroll
+          for (int e = 0; e < 4; ++e)
+#pragma unroll
+            for (int cb = 0; cb < NCB; ++cb) acc[cb] = mfma4(wv[cb][e], xa[q][e], acc[cb]);
+        }
+#pragma unroll
+        for (int q = 0; q < KS / 4; ++q) xa[q] = xb[q];
+        ko = kq;
+        kq = kr;
+        eq = er;
+      }
+    if (kn >= 0) stw.store(reinterpret_cast<f4*>(s_w[buf ^ 1]), tid);
+      __syncthreads();
+      buf ^= 1;
+      kc = kn;
+    }
+    if (!have) continue;
+    if (a.res) {  // residual block: ReLU(x + conv(.)), x read at the voxel's own row
+#pragma unroll
+      for (int cb = 0; cb < NCB; ++cb) acc[cb] += *reinterpret_cast<const f4*>(a.res + prow * C + 16 * cb + 4 * g);
+    }
+#pragma unroll
+    for (int cb = 0; cb < NCB; ++cb)
+#pragma unroll
+      for (int e = 0; e < 4; ++e) acc[cb][e] = fmaxf(acc[cb][e], 0.0f);
+    if (a.xb && valid) {  // children v of this voxel u: X_B[v] = F[u] + Emb_D[delta(v)]
+      int64_t cmo = a.moff[b + 1];
+      const int64_t cn = a.count[b + 1];
+      const uint32_t code = a.code[lvb + (prow - mo)];
+      const int64_t first = a.fc[lvb + (prow - mo)];
+      if (cmo + cn > a.cap_model) cmo = -1;  // overflow (latched where the size was made): no writes
+      int rank = 0;
+#pragma unroll
+      for (int d = 0; d < 8; ++d) {
+        if (cmo >= 0 && ((code >> d) & 1u)) {
+          float* dst = a.xb + (cmo + first + rank) * C;
+#pragma unroll
+          for (int cb = 0; cb < NCB; ++cb)
+            *reinterpret_cast<f4*>(dst + 16 * cb + 4 * g) =
+                acc[cb] + *reinterpret_cast<const f4*>(a.emb_d + d * C + 16 * cb + 4 * g);
+          ++rank;
+        }
+      }
+    }
+    if (valid && a.h_out) {
+#pragma unroll
+      for (int cb = 0; cb < NCB; ++cb) *reinterpret_cast<f4*>(a.h_out + prow * C + 16 * cb + 4 * g) = acc[cb];
+    }
+  }
+}
+
+// The head on stored last-layer features h_in (rows of the scales b_lo ..
+// b_hi), for layers computed by k_convw: one wave per tile of 16 voxels, the
+// head weights in LDS, the same arithmetic as the fused head of k_conv.
+// threads of a k_headw block: the two-stage head at C >= 64 needs more
+// registers than 16 waves per CU allow
+template <int C, bool TWO>
+constexpr int headw_threads() { return (TWO && C >= 64) ? 256 : 1024; }
+
+template <int C, bool TWO>
+__global__ void __launch_bounds__((headw_threads<C, TWO>())) k_headw(ConvArgs a) {
+  constexpr int NCB = C / 16;
+  constexpr int HT = headw_threads<C, TWO>();
+  constexpr int HWV = HT / 64;
+  constexpr int HQ = (TWO ? 2 : 16) * 64 * (C / 4) / 4;  // 16-byte words of the packed head
+  __shared__ __attribute__((aligned(16))) float s_h[HQ * 4];
+  __shared__ int64_t s_tpre[NLEV + 1];
+  __shared__ int64_t s_nv[NLEV];
+  __shared__ int64_t s_mo[NLEV];
+  const int tid = threadIdx.x, w = tid >> 6, lane = tid & 63, r = lane & 15, g = lane >> 4;
+  const int nsc = a.b_hi - a.b_lo + 1;
+  const RowMap rm{a.count, a.moff, a.cap_model, -1, 0, a.cap_model + 1};
+  Staged<HQ, HT> sth;
+  sth.load(reinterpret_cast<const f4*>(a.hw), tid);
+  if (tid == 0) {
+    int64_t acc = 0;
+    for (int i = 0; i < nsc; ++i) {
+      int64_t mo, nb;
+      scale_span(rm, a.b_lo + i, mo, nb);
+      s_tpre[i] = acc;
+      s_nv[i] = nb;
+      s_mo[i] = mo;
+      acc += (nb + 15) / 16;
+    }
+    for (int i = nsc; i <= NLEV; ++i) s_tpre[i] = acc;
+  }
+  sth.store(reinterpret_cast<f4*>(s_h), tid);
+  __syncthreads();
+  const int64_t total = s_tpre[NLEV];
+  for (int64_t tile = (int64_t)blockIdx.x * HWV + w; tile < total; tile += (int64_t)gridDim.x * HWV) {
+    int si = 0;
+#pragma unroll
+    for (int i = 1; i < NLEV; ++i) si += (s_tpre[i] <= tile) ? 1 : 0;
+    const int b = a.b_lo + si;
+    const int64_t nvox = s_nv[si], mo = s_mo[si];
+    const int64_t row = (tile - s_tpre[si]) * 16 + r;
+    const bool valid = row < nvox;
+    const int64_t prow = mo + (valid ? row : nvox - 1);
+    const int64_t lvb = (int64_t)(b - a.b0) * a.cap_pts;
+    f4 acc[NCB];
+#pragma unroll
+    for (int cb = 0; cb < NCB; ++cb) acc[cb] = *reinterpret_cast<const f4*>(a.h_in + prow * C + 16 * cb + 4 * g);
+    head_epilogue<C, TWO, false>(a, acc, s_h, lane, g, valid, prow, mo, lvb, s_mo[0]);
+  }
+}
+
 template <int C, bool FIRST, bool LAST, bool TWO, bool BF>
 hipError_t run_conv(Ctx& c, const ConvArgs& a) {
   // one block per CU stages the weights once for its 16 waves
@@ -1058,8 +1502,8 @@ hipError_t launch_pack_weights(Ctx& c, const reno_weights& w) {
   const bool bf = c.p.precision == RENO_PREC_BF16X3;
   if (c.p.model_mode == RENO_MODEL_TOP) {  // four C -> C convs (fp32) and the two embeddings
     for (int l = 0; l < 4; ++l) {
-      hipLaunchKernelGGL(k_pack_conv, dim3(64), dim3(256), 0, c.stream, w.top_w[l], C, C, C / 4, C / 4,
-                         c.w_conv[l]);
+      hipLaunchKernelGGL(k_pack_conv, dim3(256), dim3(256), 0, c.stream, w.top_w[l], C, C, C / 4, C / 4,
+                         c.kvol(), c.w_conv[l]);
       hipLaunchKernelGGL(k_copy_f32, dim3(1), dim3(256), 0, c.stream, w.top_b[l], c.w_bias[l], C);
     }
     hipLaunchKernelGGL(k_copy_f32, dim3(32), dim3(256), 0, c.stream, w.emb_o, c.w_embo, 256 * C);
@@ -1072,7 +1516,7 @@ hipError_t launch_pack_weights(Ctx& c, const reno_weights& w) {
       hipLaunchKernelGGL(k_pack_conv_bf, dim3(64), dim3(256), 0, c.stream, w.conv_w[l], c_in, C,
                          reinterpret_cast<uint32_t*>(c.w_conv[l]));
     else
-      hipLaunchKernelGGL(k_pack_conv, dim3(64), dim3(256), 0, c.stream, w.conv_w[l], c_in, C, KS, KSP,
+      hipLaunchKernelGGL(k_pack_conv, dim3(64), dim3(256), 0, c.stream, w.conv_w[l], c_in, C, KS, KSP, 27,
                          c.w_conv[l]);
     hipLaunchKernelGGL(k_copy_f32, dim3(1), dim3(256), 0, c.stream, w.conv_b[l], c.w_bias[l], C);
     c_in = C;
@@ -1194,7 +1638,103 @@ hipError_t launch_top(Ctx& c, int b_lo, int b_hi, float* logits, bool second) {
   return e == hipSuccess ? hipGetLastError() : e;
 }
 
+// Full predictor with streamed weights (5x5x5 kernels or C above 32): the
+// steps of launch_top on k_convw and a separate head launch.
+template <int C, int KV>
+hipError_t launch_top_wide(Ctx& c, int b_lo, int b_hi, float* logits, bool second) {
+  const int b0 = c.b0();
+  const int64_t ext_off = c.cap_model + 1;
+  const RowMap rm{c.d_count, c.d_moff, (int64_t)c.cap_model, b0, ext_off, c.cap_rows()};
+  const int n_lo = b_lo - 1;
+  {
+    ProfScope ps_(c, RENO_K_TOP_INPUT);
+    const int blocks = (int)std::min<int64_t>(2048, (c.cap_rows() + 63) / 64);
+    if (KV == 125)
+      hipLaunchKernelGGL(k_top_prep5<C>, dim3(blocks), dim3(256), 0, c.stream, n_lo, b_hi - n_lo + 1, b_hi - n_lo,
+                         b0, rm, c.lv_key, c.lv_code, (int64_t)c.cap_pts, c.d_hash, c.hash_lg, c.fbits, c.w_embo,
+                         c.d_nbr, c.h_c);
+    else
+      hipLaunchKernelGGL(k_top_prep<C>, dim3(blocks), dim3(256), 0, c.stream, n_lo, b_hi - n_lo + 1, b_hi - n_lo,
+                         b0, rm, c.lv_key, c.lv_code, (int64_t)c.cap_pts, c.d_hash, c.hash_lg, c.fbits, c.w_embo,
+                         c.d_nbr, c.h_c);
+  }
+  ConvArgs a{};
+  a.b0 = b0;
+  a.count = c.d_count;
+  a.moff = c.d_moff;
+  a.cap_pts = c.cap_pts;
+  a.cap_model = c.cap_model;
+  a.lv_key = c.lv_key;
+  a.nbr = c.d_nbr;
+  a.hb = c.w_hbias;
+  a.hw = c.w_head;
+  a.lse = c.d_lse;
+  a.err = c.d_err;
+  a.emb = c.w_emb;
+  a.s1_code = second ? c.lv_code : nullptr;
+  a.lse2 = c.d_lse2;
+  a.s1_out = c.d_s1;
+  a.b_ext = b0;
+  a.ext_off = ext_off;
+  a.cap_rows = c.cap_rows();
+  a.emb_d = c.w_embd;
+  a.code = c.lv_code;
+  a.fc = c.lv_fc;
+  hipError_t e = hipSuccess;
+  auto conv = [&](int lo, int hi, int wi, const float* in, float* out, const float* res, float* xb) {
+    if (e != hipSuccess) return;
+    a.b_lo = lo;
+    a.b_hi = hi;
+    a.h_in = in;
+    a.h_out = out;
+    a.res = res;
+    a.xb = xb;
+    a.w = c.w_conv[wi];
+    a.bias = c.w_bias[wi];
+    ProfScope ps_(c, RENO_K_CONV_MID);
+    hipLaunchKernelGGL((k_convw<C, KV>), dim3(256), dim3(CW_THREADS), 0, c.stream, a);
+    e = hipGetLastError();
+  };
+  conv(n_lo, b_hi - 1, 0, c.h_c, c.h_b, nullptr, nullptr);
+  conv(n_lo, b_hi - 1, 1, c.h_b, nullptr, c.h_c, c.h_d);
+  conv(b_lo, b_hi, 2, c.h_d, c.h_b, nullptr, nullptr);
+  conv(b_lo, b_hi, 3, c.h_b, c.h_a, c.h_d, nullptr);
+  if (e != hipSuccess) return e;
+  {
+    ProfScope ps_(c, RENO_K_CONV_LAST);
+    a.b_lo = b_lo;
+    a.b_hi = b_hi;
+    a.h_in = c.h_a;
+    a.logits = logits;
+    if (c.p.head_mode == RENO_HEAD_TWO_STAGE) {
+      constexpr int HT = headw_threads<C, true>();
+      const int blocks = (int)std::min<int64_t>(4096, (c.cap_model + 16 * HT / 64 - 1) / (16 * HT / 64));
+      hipLaunchKernelGGL((k_headw<C, true>), dim3(blocks), dim3(HT), 0, c.stream, a);
+    } else {
+      constexpr int HT = headw_threads<C, false>();
+      const int blocks = (int)std::min<int64_t>(1024, (c.cap_model + 16 * HT / 64 - 1) / (16 * HT / 64));
+      hipLaunchKernelGGL((k_headw<C, false>), dim3(blocks), dim3(HT), 0, c.stream, a);
+    }
+  }
+  return hipGetLastError();
+}
+
+hipError_t launch_top_wide_any(Ctx& c, int b_lo, int b_hi, float* logits, bool second) {
+  const bool k5 = c.ks() == 5;
+  switch (c.p.channels) {
+    case 16: return k5 ? launch_top_wide<16, 125>(c, b_lo, b_hi, logits, second)
+                       : launch_top_wide<16, 27>(c, b_lo, b_hi, logits, second);
+    case 32: return k5 ? launch_top_wide<32, 125>(c, b_lo, b_hi, logits, second)
+                       : launch_top_wide<32, 27>(c, b_lo, b_hi, logits, second);
+    case 64: return k5 ? launch_top_wide<64, 125>(c, b_lo, b_hi, logits, second)
+                       : launch_top_wide<64, 27>(c, b_lo, b_hi, logits, second);
+    default: return k5 ? launch_top_wide<128, 125>(c, b_lo, b_hi, logits, second)
+                       : launch_top_wide<128, 27>(c, b_lo, b_hi, logits, second);
+  }
+}
+
 hipError_t launch_model(Ctx& c, int b_lo, int b_hi, float* logits, bool second) {
+  if (c.wide()) return launch_top_wide_any(c, b_lo, b_hi, logits, second);
   if (c.p.model_mode == RENO_MODEL_TOP) return launch_top(c, b_lo, b_hi, logits, second);
   ConvArgs a{};
   a.b_lo = b_lo;
@@ -1265,7 +1805,11 @@ hipError_t launch_head2(Ctx& c, int b, const uint8_t* s1, float* logits2) {
   hipLaunchKernelGGL((k_head2<CC, BFV>), dim3(blocks), dim3(256), 0, c.stream, b, c.d_count, c.d_moff, \
                      (int64_t)c.cap_model, c.hlast(), s1, code, hw2, c.w_hbias + 16, c.w_emb, c.d_lse2, \
                      logits2, c.d_s1, c.d_err)
-  if (c.p.channels == 32) {
+  if (c.p.channels == 128) {
+    RENO_HEAD2(128, false);
+  } else if (c.p.channels == 64) {
+    RENO_HEAD2(64, false);
+  } else if (c.p.channels == 32) {
     if (bf) RENO_HEAD2(32, true); else RENO_HEAD2(32, false);
   } else {
     if (bf) RENO_HEAD2(16, true); else RENO_HEAD2(16, false);

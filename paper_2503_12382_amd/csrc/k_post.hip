@@ -81,32 +81,39 @@ __global__ void __launch_bounds__(CL_THREADS) k_code_length(
     const int o = lv_code[(int64_t)(b - b0) * cap_pts + vv];
     const float l1 = lse[mo + vv];
     const float l2 = TWO ? lse2[mo + vv] : 0.0f;
-    float h[C];
+    // the row in chunks of HC channels (all of it for C <= 32); the dot
+    // products run over c in ascending order either way
+    constexpr int HC = C <= 32 ? C : 16;
     const float4* hr = reinterpret_cast<const float4*>(hL + (mo + vv) * C);
-#pragma unroll
-    for (int c4 = 0; c4 < C / 4; ++c4) {
-      const float4 t = hr[c4];
-      h[4 * c4] = t.x;
-      h[4 * c4 + 1] = t.y;
-      h[4 * c4 + 2] = t.z;
-      h[4 * c4 + 3] = t.w;
-    }
     float bt;
-    if constexpr (TWO) {
-      const int a1 = o & 15, a2 = 16 + (o >> 4);
-      float z1 = s_hb[a1], z2 = s_hb[a2];
+    const int a1 = o & 15, a2 = 16 + (o >> 4);
+    float z1 = TWO ? s_hb[a1] : s_hb[o], z2 = TWO ? s_hb[a2] : 0.0f;
 #pragma unroll
-      for (int c = 0; c < C; ++c) {
-        z1 = fmaf(s_HT[a1 * RS + c], h[c], z1);
-        z2 = fmaf(s_HT[a2 * RS + c], h[c] + s_emb[a1 * C + c], z2);
+    for (int c0 = 0; c0 < C; c0 += HC) {
+      float h[HC];
+#pragma unroll
+      for (int c4 = 0; c4 < HC / 4; ++c4) {
+        const float4 t = hr[c0 / 4 + c4];
+        h[4 * c4] = t.x;
+        h[4 * c4 + 1] = t.y;
+        h[4 * c4 + 2] = t.z;
+        h[4 * c4 + 3] = t.w;
       }
-      bt = ((l1 - z1) + (l2 - z2)) * INV_LN2;
-    } else {
-      float z = s_hb[o];
 #pragma unroll
-      for (int c = 0; c < C; ++c) z = fmaf(s_HT[o * RS + c], h[c], z);
-      bt = (l1 - z) * INV_LN2;
+      for (int cc = 0; cc < HC; ++cc) {
+        const int c = c0 + cc;
+        if constexpr (TWO) {
+          z1 = fmaf(s_HT[a1 * RS + c], h[cc], z1);
+          z2 = fmaf(s_HT[a2 * RS + c], h[cc] + s_emb[a1 * C + c], z2);
+        } else {
+          z1 = fmaf(s_HT[o * RS + c], h[cc], z1);
+        }
+      }
     }
+    if constexpr (TWO)
+      bt = ((l1 - z1) + (l2 - z2)) * INV_LN2;
+    else
+      bt = (l1 - z1) * INV_LN2;
     double acc = 0.0;
     if (v < n) {
       if (bits_out) bits_out[mo - moff[b_lo] + v] = bt;
@@ -370,15 +377,15 @@ __global__ void k_copy_i32(const int32_t* __restrict__ src, const int32_t* __res
 
 // neighbour map rows of scale b start at its packed model row (device value)
 __global__ void k_copy_map(const int32_t* __restrict__ nbr, const int32_t* __restrict__ moff,
-                           const int32_t* __restrict__ count, int b, int64_t cap_model,
+                           const int32_t* __restrict__ count, int b, int64_t cap_model, int kv, int stride,
                            int32_t* __restrict__ dst) {
   int64_t n = (int64_t)count[b];
   if (moff[b] + n > cap_model) n = 0;
-  n *= 27;
-  const int64_t o = (int64_t)moff[b] * NBR_STRIDE;
+  n *= kv;
+  const int64_t o = (int64_t)moff[b] * stride;
   for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n;
        i += (int64_t)gridDim.x * blockDim.x)
-    dst[i] = nbr[o + (i / 27) * NBR_STRIDE + i % 27];
+    dst[i] = nbr[o + (i / kv) * stride + i % kv];
 }
 
 unsigned grid_for(int64_t cap, int per_block) {
@@ -407,10 +414,19 @@ void run_code_length(Ctx& c, int b_lo, int b_hi, float* bits) {
 hipError_t launch_code_length(Ctx& c, int b_lo, int b_hi, float* bits) {
   ProfScope ps_(c, RENO_K_CODE_LENGTH);
   const bool two = c.p.head_mode == RENO_HEAD_TWO_STAGE;
-  if (c.p.channels == 32)
-    two ? run_code_length<32, true>(c, b_lo, b_hi, bits) : run_code_length<32, false>(c, b_lo, b_hi, bits);
-  else
-    two ? run_code_length<16, true>(c, b_lo, b_hi, bits) : run_code_length<16, false>(c, b_lo, b_hi, bits);
+  switch (c.p.channels) {
+    case 128:
+      two ? run_code_length<128, true>(c, b_lo, b_hi, bits) : run_code_length<128, false>(c, b_lo, b_hi, bits);
+      break;
+    case 64:
+      two ? run_code_length<64, true>(c, b_lo, b_hi, bits) : run_code_length<64, false>(c, b_lo, b_hi, bits);
+      break;
+    case 32:
+      two ? run_code_length<32, true>(c, b_lo, b_hi, bits) : run_code_length<32, false>(c, b_lo, b_hi, bits);
+      break;
+    default:
+      two ? run_code_length<16, true>(c, b_lo, b_hi, bits) : run_code_length<16, false>(c, b_lo, b_hi, bits);
+  }
   return hipGetLastError();
 }
 
@@ -471,8 +487,9 @@ hipError_t launch_copy_level_i32(Ctx& c, int b, const int32_t* src, int32_t* out
 
 hipError_t launch_neighbor_map(Ctx& c, int b, int32_t* out) {
   ProfScope ps_(c, RENO_K_OTHER);
-  hipLaunchKernelGGL(k_copy_map, dim3(grid_for(c.cap_pts * 27, 256)), dim3(256), 0, c.stream,
-                     c.d_nbr, c.d_moff, c.d_count, b, c.cap_model, out);
+  const int kv = c.top() ? c.kvol() : 27;
+  hipLaunchKernelGGL(k_copy_map, dim3(grid_for(c.cap_pts * kv, 256)), dim3(256), 0, c.stream,
+                     c.d_nbr, c.d_moff, c.d_count, b, c.cap_model, kv, c.nbr_stride(), out);
   return hipGetLastError();
 }
 
