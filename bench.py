@@ -140,16 +140,17 @@ class Codec:
     (a stand-in for an instant entropy decoder)."""
 
     def __init__(self, reno, torch, cfg, pts, M, cap_model, stream, w_np, two_stage, precision=0, top=False,
-                 frame_start=None):
+                 frame_start=None, channels=None, kernel_size=3):
         self.reno, self.torch, self.stream = reno, torch, stream
-        B, b0, C, L = cfg.bit_depth, cfg.min_bit_depth, cfg.channels, cfg.layers
+        B, b0, C, L = cfg.bit_depth, cfg.min_bit_depth, channels or cfg.channels, cfg.layers
         self.B, self.b0, self.C, self.two_stage = B, b0, C, two_stage
         self.frame_start = frame_start     # a frame batch (int64 device tensor [K + 1]) or None
         self.K = 1 if frame_start is None else int(frame_start.shape[0]) - 1
         wd = reno.weights_to_device(w_np)
         with torch.cuda.stream(stream):
             mk = lambda: reno.Context(M, B, b0, cfg.range_m, C, L, max_model_voxels=cap_model,
-                                      stream=stream, two_stage=two_stage, precision=precision, top=top)
+                                      stream=stream, two_stage=two_stage, precision=precision, top=top,
+                                      kernel_size=kernel_size)
             self.enc, self.dec = mk(), mk()
             self.enc.set_weights(wd)
             self.dec.set_weights(wd)
@@ -653,6 +654,39 @@ def main():
                           "us_per_frame_by_kind": kinds_us}
             log("full predictor", name, topm[name])
             tc.close()
+        # the large variant (c128, k5; the paper's RENO-L) with the two-stage
+        # head: streamed-weight conv kernels and a separate head launch
+        LC, LK = 128, 5
+        wl = gen_weights(LC, L, seed=cfg.weight_seed, two_stage=True, top=True, kernel_size=LK)
+        lc = Codec(reno, torch, cfg, pts, M, cap_model, stream, wl, two_stage=True, top=True, channels=LC,
+                   kernel_size=LK)
+        st = max(args.steps // 10, 5)
+        msl = lc.time(st, max(args.warmup // 2, 2), args.mode)
+        with torch.cuda.stream(stream):
+            lc.enc.profile(kinds)
+            lc.dec.profile(kinds)
+            for _ in range(5):
+                lc.step()
+            pe, pd = lc.enc.profile_read(), lc.dec.profile_read()
+            lc.enc.profile([])
+            lc.dec.profile([])
+        lk_us = {k: round(1000.0 * (pe.get(k, (0.0, 0))[0] + pd.get(k, (0.0, 0))[0]) / 5, 1)
+                 for k in kinds if k in pe or k in pd}
+        # algorithmic conv flops per frame (encoder + decoder): block B's two
+        # convs on every model scale, block A's on every scale below one
+        # (the base scale's map is not exposed: left out, a lower bound)
+        pl = lc.pairs
+        conv_flops = 2 * 2 * 2 * LC * LC * (sum(pl.values()) + sum(v for b, v in pl.items() if b < B - 1))
+        conv_us = lk_us.get("conv_mid", 0.0)
+        topm["large_c128_k5_two_stage"] = {
+            "value": round(1000.0 / msl, 2), "unit": "frames/s", "ms_per_step": round(msl, 4), "steps": st,
+            "bits_per_point": round(lc.enc_total / M, 4), "us_per_frame_by_kind": lk_us,
+            "conv_alg_gflop_per_frame": round(conv_flops / 1e9, 2),
+            "conv_achieved_tflops": round(conv_flops / (conv_us * 1e-6) / 1e12, 2) if conv_us else None,
+            "conv_frac": round(conv_flops / (conv_us * 1e-6) / 1e12 / PEAK_FP32_MFMA_TFLOPS, 4) if conv_us else None,
+            "paper_context_s": "RENO-L NN 0.184 s per 14-bit frame, encoder, RTX 4090 (Table S2)"}
+        log("full predictor large", topm["large_c128_k5_two_stage"])
+        lc.close()
 
     # ---- end to end: GPU model + host rANS per scale, both heads ----
     e2e = None
