@@ -87,6 +87,25 @@ __global__ void k_pack_conv(const float* __restrict__ W, int c_in, int C, int KS
   }
 }
 
+// Conv weights W [kv][C][C] for the streamed-weight kernel: the operands of
+// k_pack_conv (lane (r, g), step s = 4q + e: W[ci = g*KS + s][co = 16cb + r],
+// KS = C/4), stored lane-fastest as 16-byte words [kv][C/16][KS/4][64], so a
+// wave's LDS reads of one (cb, q) are 64 consecutive words (no bank conflicts).
+__global__ void k_pack_conv_wide(const float* __restrict__ W, int C, int kv, float* __restrict__ out) {
+  const int ncb = C / 16, KS = C / 4, nq = KS / 4;
+  const int total = kv * C * C;
+  for (int i = blockIdx.x * blockDim.x + threadIdx.x; i < total; i += gridDim.x * blockDim.x) {
+    const int e = i % 4;
+    const int lane = (i / 4) % 64;
+    const int q = (i / 256) % nq;
+    const int cb = (i / (256 * nq)) % ncb;
+    const int k = i / (256 * nq * ncb);
+    const int ci = (lane >> 4) * KS + 4 * q + e;
+    const int co = cb * 16 + (lane & 15);
+    out[i] = W[((size_t)k * C + ci) * C + co];
+  }
+}
+
 // Head H [C][NS] (NS = 256, or 16 per stage of the two-stage head): step
 // t = 4*cb + r carries channel c = 16*cb + 4*g + r (the conv accumulator
 // register r of column block cb); lane l carries symbol 16*sb + l%16.
@@ -833,7 +852,7 @@ constexpr int TO_W = 2048;
 constexpr int TO_THREADS = 1024;
 constexpr int TO_KEYS = 2048;
 
-__global__ void __launch_bounds__(TO_THREADS) k_tile_order(int b_lo, int nsc, RowMap rm,
+__global__ void __launch_bounds__(TO_THREADS) k_tile_order(int b_lo, int nsc, RowMap rm, int ks,
                                                            const int32_t* __restrict__ nbr, int32_t* __restrict__ perm) {
   __shared__ uint32_t s_cnt[TO_KEYS];
   __shared__ uint32_t s_wsum[TO_THREADS / 64];
@@ -871,7 +890,7 @@ __global__ void __launch_bounds__(TO_THREADS) k_tile_order(int b_lo, int nsc, Ro
   for (int e = 0; e < PER; ++e) {
     const int64_t i = w0 + e * TO_THREADS + tid;
     key[e] = TO_KEYS;  // absent
-    if (i < n) {
+    if (i < n && ks == 3) {
       const int32_t* r = nbr + (mo + i) * NBR_STRIDE;
       const int4 a = *reinterpret_cast<const int4*>(r + 8), c = *reinterpret_cast<const int4*>(r + 12);
       const int4 d = *reinterpret_cast<const int4*>(r + 16);
@@ -881,6 +900,15 @@ __global__ void __launch_bounds__(TO_THREADS) k_tile_order(int b_lo, int nsc, Ro
                ((uint32_t)(c.x >= 0) << 3) | ((uint32_t)(c.y >= 0) << 4) | ((uint32_t)(c.z >= 0) << 5) |
                ((uint32_t)(c.w >= 0) << 6) | ((uint32_t)(d.x >= 0) << 7) | ((uint32_t)(d.y >= 0) << 8) |
                ((uint32_t)(f4v >= 0) << 9) | ((uint32_t)(f22 >= 0) << 10);
+      rank[e] = atomicAdd(&s_cnt[key[e]], 1u);
+    } else if (i < n) {
+      // 5x5x5 map (stride 128): the same cells, k = (dx+2) + 5(dy+2) + 25(dz+2)
+      const int32_t* r = nbr + (mo + i) * 128;
+      const int32_t v[11] = {r[56], r[57], r[58], r[61], r[62], r[63], r[66], r[67], r[68], r[37], r[87]};
+      uint32_t kk = 0;
+#pragma unroll
+      for (int j = 0; j < 11; ++j) kk |= (uint32_t)(v[j] >= 0) << j;
+      key[e] = kk;
       rank[e] = atomicAdd(&s_cnt[key[e]], 1u);
     }
   }
@@ -1245,7 +1273,8 @@ __global__ void __launch_bounds__(CW_THREADS) k_convw(ConvArgs a) {
       mo = s_mo[si];
       const int64_t row = (tile - s_tpre[si]) * 16 + r;
       valid = row < nvox;
-      prow = mo + (valid ? row : nvox - 1);  // idle lanes read a real row
+      const int64_t pos = mo + (valid ? row : nvox - 1);  // idle lanes read a real row
+      prow = a.perm ? (int64_t)a.perm[pos] : pos;          // with a tile order, slot -> row
       lvb = (int64_t)(b - a.b0) * a.cap_pts;
     }
     // occupied offsets of the wave's tile (wave-uniform), from the map rows
@@ -1318,7 +1347,7 @@ __global__ void __launch_bounds__(CW_THREADS) k_convw(ConvArgs a) {
         for (int q = 0; q < KS / 4; ++q) {
           f4 wv[NCB];
 #pragma unroll
-          for (int cb = 0; cb < NCB; ++cb) wv[cb] = reinterpret_cast<const f4*>(wb + (cb * 64 + lane) * KS)[q];
+          for (int cb = 0; cb < NCB; ++cb) wv[cb] = reinterpret_cast<const f4*>(wb)[(cb * (KS / 4) + q) * 64 + lane];
 #pragma unroll
           for (int e = 0; e < 4; ++e)
 #pragma unroll
@@ -1502,8 +1531,12 @@ hipError_t launch_pack_weights(Ctx& c, const reno_weights& w) {
   const bool bf = c.p.precision == RENO_PREC_BF16X3;
   if (c.p.model_mode == RENO_MODEL_TOP) {  // four C -> C convs (fp32) and the two embeddings
     for (int l = 0; l < 4; ++l) {
-      hipLaunchKernelGGL(k_pack_conv, dim3(256), dim3(256), 0, c.stream, w.top_w[l], C, C, C / 4, C / 4,
-                         c.kvol(), c.w_conv[l]);
+      if (c.wide())
+        hipLaunchKernelGGL(k_pack_conv_wide, dim3(1024), dim3(256), 0, c.stream, w.top_w[l], C, c.kvol(),
+                           c.w_conv[l]);
+      else
+        hipLaunchKernelGGL(k_pack_conv, dim3(256), dim3(256), 0, c.stream, w.top_w[l], C, C, C / 4, C / 4,
+                           c.kvol(), c.w_conv[l]);
       hipLaunchKernelGGL(k_copy_f32, dim3(1), dim3(256), 0, c.stream, w.top_b[l], c.w_bias[l], C);
     }
     hipLaunchKernelGGL(k_copy_f32, dim3(32), dim3(256), 0, c.stream, w.emb_o, c.w_embo, 256 * C);
@@ -1612,8 +1645,8 @@ hipError_t launch_top(Ctx& c, int b_lo, int b_hi, float* logits, bool second) {
     ProfScope pso_(c, RENO_K_OTHER);
     const int nsc = b_hi - n_lo + 1;
     const int64_t windows = (c.cap_model + c.cap_pts + TO_W - 1) / TO_W + nsc;
-    hipLaunchKernelGGL(k_tile_order, dim3((unsigned)windows), dim3(TO_THREADS), 0, c.stream, n_lo, nsc, rm, c.d_nbr,
-                       c.d_perm);
+    hipLaunchKernelGGL(k_tile_order, dim3((unsigned)windows), dim3(TO_THREADS), 0, c.stream, n_lo, nsc, rm, 3,
+                       c.d_nbr, c.d_perm);
     a.perm = c.d_perm;
   }
   hipError_t e = hipSuccess;
@@ -1680,6 +1713,14 @@ hipError_t launch_top_wide(Ctx& c, int b_lo, int b_hi, float* logits, bool secon
   a.emb_d = c.w_embd;
   a.code = c.lv_code;
   a.fc = c.lv_fc;
+  {  // tiles of voxels with similar neighbourhoods: smaller offset unions per tile and group
+    ProfScope pso_(c, RENO_K_OTHER);
+    const int nsc = b_hi - n_lo + 1;
+    const int64_t windows = (c.cap_model + c.cap_pts + TO_W - 1) / TO_W + nsc;
+    hipLaunchKernelGGL(k_tile_order, dim3((unsigned)windows), dim3(TO_THREADS), 0, c.stream, n_lo, nsc, rm,
+                       KV == 125 ? 5 : 3, c.d_nbr, c.d_perm);
+    a.perm = c.d_perm;
+  }
   hipError_t e = hipSuccess;
   auto conv = [&](int lo, int hi, int wi, const float* in, float* out, const float* res, float* xb) {
     if (e != hipSuccess) return;
@@ -1774,7 +1815,7 @@ hipError_t launch_model(Ctx& c, int b_lo, int b_hi, float* logits, bool second) 
       ProfScope pso_(c, RENO_K_OTHER);
       const int nsc = b_hi - b_lo + 1;
       const int64_t windows = (c.cap_model + TO_W - 1) / TO_W + nsc;
-      hipLaunchKernelGGL(k_tile_order, dim3((unsigned)windows), dim3(TO_THREADS), 0, c.stream, b_lo, nsc, rm,
+      hipLaunchKernelGGL(k_tile_order, dim3((unsigned)windows), dim3(TO_THREADS), 0, c.stream, b_lo, nsc, rm, 3,
                          c.d_nbr, c.d_perm);
       a.perm = c.d_perm;
     }
