@@ -92,9 +92,10 @@ def alg_bytes_encoder(counts, b0, B, M, C, hash_slots, status_words, fb):
     }
 
 
-def read_traffic():
+def read_traffic(workload):
     """HBM traffic of conv_last per launch from the committed rocprofv3 PMC
-    summary, or None when the kernel source changed since it was taken."""
+    summary, or None when the kernel source changed since it was taken or the
+    summary is of another workload."""
     import hashlib
     if not os.path.exists(TRAFFIC_FILE):
         return None
@@ -104,7 +105,7 @@ def read_traffic():
             k, v = line.split("=", 1)
             kv[k.strip()] = v.strip()
     src = hashlib.sha256(open(MODEL_SRC, "rb").read()).hexdigest()[:16]
-    if kv.get("k_model_sha256_16") != src:
+    if kv.get("k_model_sha256_16") != src or kv.get("workload") != workload:
         return None
     return float(kv["bytes_per_launch"])
 
@@ -175,10 +176,17 @@ class Codec:
             self.enc.build_pyramid_frames(pts, self.frame_start, self.B)
 
     def step(self):
-        reno, enc, dec, B, b0 = self.reno, self.enc, self.dec, self.B, self.b0
+        self.enc_step()
+        self.dec_step()
+
+    def enc_step(self):
+        reno, enc = self.reno, self.enc
         self.build(self.pts)
         enc.predict_probs(reno.RENO_ALL_SCALES)
         enc.code_length(reno.RENO_ALL_SCALES, per_voxel=False, total=False)
+
+    def dec_step(self):
+        reno, dec, B, b0 = self.reno, self.dec, self.B, self.b0
         if self.frame_start is None:
             dec.set_base(B, self.base, self.codes[b0])
         else:
@@ -231,6 +239,33 @@ class Codec:
         self.check("after the timed steps:")  # the last replayed frame is consistent
         return t0.elapsed_time(t1) / steps
 
+    def time_sides(self, steps):
+        """(encoder ms, decoder ms) per frame, each side captured as its own
+        HIP graph and replayed `steps` times."""
+        torch, stream = self.torch, self.stream
+        out = []
+        for fn in (self.enc_step, self.dec_step):
+            g = torch.cuda.CUDAGraph()
+            with torch.cuda.stream(stream):
+                fn()
+                stream.synchronize()
+            with torch.cuda.graph(g, stream=stream):
+                fn()
+            with torch.cuda.stream(stream):
+                g.replay()
+            stream.synchronize()
+            t0 = torch.cuda.Event(enable_timing=True)
+            t1 = torch.cuda.Event(enable_timing=True)
+            with torch.cuda.stream(stream):
+                t0.record(stream)
+                for _ in range(steps):
+                    g.replay()
+                t1.record(stream)
+            torch.cuda.synchronize()
+            out.append(t0.elapsed_time(t1) / steps)
+        self.check("after the per-side timing:")
+        return tuple(out)
+
     def profile_conv_last(self, steps):
         """(total ms, launches) of conv_last over `steps` eager steps, each launch
         bracketed by HIP events on the context stream."""
@@ -274,7 +309,16 @@ class EndToEnd:
             self.enc, self.dec = mk(), mk()
             self.enc.set_weights(wd)
             self.dec.set_weights(wd)
-        self.pts = pts
+        # the frame arrives in (pinned) host memory and its bitstream leaves
+        # to host memory: the encoder copies the points in and the base
+        # voxels out, the decoder copies the base voxels in
+        self.pts_host = torch.empty(tuple(pts.shape), dtype=pts.dtype, pin_memory=True)
+        self.pts_host.copy_(pts.cpu())
+        self.pts = torch.empty_like(pts)
+        self.base_xyz_host = torch.empty((M, 3), dtype=torch.int32, pin_memory=True)
+        self.base_code_host = torch.empty(M, dtype=torch.uint8, pin_memory=True)
+        self.base_xyz_dev = torch.empty((M, 3), dtype=torch.int32, device=pts.device)
+        self.base_code_dev = torch.empty(M, dtype=torch.uint8, device=pts.device)
         per = 4 if two_stage else 2
         self.iv_host = torch.empty((cap_model, per), dtype=torch.int16, pin_memory=True)
         k = 16 if two_stage else 256
@@ -288,15 +332,20 @@ class EndToEnd:
         """-> (bitstream dict, N_b per scale, base xyz, base codes)."""
         reno, torch, enc, B, b0 = self.reno, self.torch, self.enc, self.B, self.b0
         with torch.cuda.stream(self.stream):
+            self.pts.copy_(self.pts_host, non_blocking=True)
             enc.build_pyramid(self.pts, B)
             enc.predict_probs(reno.RENO_ALL_SCALES)
             counts = enc.scale_counts()                       # synchronises once
             nm = int(counts[b0 + 1:B].sum())
+            n0 = int(counts[b0])
             iv = enc.symbol_intervals(reno.RENO_ALL_SCALES)
             self.iv_host[:nm].copy_(iv, non_blocking=True)
             base_xyz, _ = enc.coords(b0)
             base_codes = enc.occupancy_codes(b0)
+            self.base_xyz_host[:n0].copy_(base_xyz, non_blocking=True)
+            self.base_code_host[:n0].copy_(base_codes, non_blocking=True)
             self.stream.synchronize()
+        base_xyz, base_codes = self.base_xyz_host[:n0], self.base_code_host[:n0]
         ivh = self.iv_host.numpy().view(np.uint16)
         jobs, off = [], 0
         for b in range(b0 + 1, B):
@@ -313,7 +362,11 @@ class EndToEnd:
     def decode(self, words, counts, base_xyz, base_codes):
         reno, torch, dec, B, b0 = self.reno, self.torch, self.dec, self.B, self.b0
         with torch.cuda.stream(self.stream):
-            dec.set_base(B, base_xyz, base_codes)
+            n0 = int(base_xyz.shape[0])
+            bx, bc = self.base_xyz_dev[:n0], self.base_code_dev[:n0]
+            bx.copy_(base_xyz, non_blocking=True)
+            bc.copy_(base_codes, non_blocking=True)
+            dec.set_base(B, bx, bc)
             prev = None
             for b in range(b0 + 1, B):
                 n = int(counts[b])
@@ -556,6 +609,9 @@ def main():
     ms_step = one.time(args.steps, args.warmup, args.mode)
     fps = 1000.0 / ms_step
     log(f"{args.mode}: {ms_step * 1000:.1f} us/frame, {fps:.1f} frames/s")
+    enc_ms, dec_ms = one.time_sides(args.steps) if args.mode == "graph" else (None, None)
+    if enc_ms is not None:
+        log(f"encode {enc_ms * 1000:.1f} us, decode {dec_ms * 1000:.1f} us per frame")
     cl_ms, cl_launches = one.profile_conv_last(args.steps)
     achieved_tflops = one.conv_last_flops(counts) * args.steps / (cl_ms * 1e-3) / 1e12
     log(f"conv_last: {cl_launches} launches, {1000 * cl_ms / cl_launches:.1f} us avg, "
@@ -701,9 +757,10 @@ def main():
                          "coded_bits_per_point": round(bits / M, 4)}
             log("end-to-end", name, e2e[name])
             ee.close()
-        e2e["note"] = ("wall-clock per frame: GPU pyramid + model + symbol intervals (encoder) or tables "
-                       "(decoder), pinned copies, host rANS with one stream per scale (and stage); the decoder "
-                       "decodes each scale before expanding it; encoder streams coded on 8 host threads")
+        e2e["note"] = ("wall-clock per frame: points copied in from pinned host memory, GPU pyramid + model + "
+                       "symbol intervals (encoder) or tables (decoder), pinned copies out, host rANS with one "
+                       "stream per scale (and stage), base voxels out and back in; the decoder decodes each "
+                       "scale before expanding it; encoder streams coded on 8 host threads")
 
     # ---- multi-frame throughput: F different frames, each with its own encoder
     # and decoder context and captured step, replayed round-robin over S
@@ -818,7 +875,7 @@ def main():
         log("cpu baseline", cpu)
 
     voxels_frame = sum(counts)
-    traffic = read_traffic()
+    traffic = read_traffic(cfg.name)
     out = {
         "metric": "frames/s + Mvoxels/s, encode+decode model path, 14-bit 64-beam scan; bits/pt",
         "value": round(fps, 2),
@@ -833,6 +890,9 @@ def main():
         "dtype": "f32",
         "data": "synthetic",
         "mvoxels_per_s": round(fps * voxels_frame / 1e6, 2),
+        "model_mvoxels_per_s": round(fps * model_vox / 1e6, 2),
+        "encode_ms": None if enc_ms is None else round(enc_ms, 5),
+        "decode_ms": None if dec_ms is None else round(dec_ms, 5),
         "bits_per_point": round(enc_total / M, 4),
         "oracle_bits_per_point": None if oracle_bpp is None else round(oracle_bpp, 4),
         "config": {"workload": f"{cfg.name}: synthetic {cfg.beams}-beam x {cfg.azimuth_steps}-azimuth "
