@@ -94,6 +94,11 @@ __global__ void __launch_bounds__(EXP_THREADS) k_expand(ExpArgs a) {
     }
     return;
   }
+  // The grid is sized for the largest scale.  Only the first ntiles blocks
+  // take a ticket, so they get exactly tickets 0 .. ntiles-1; the others leave
+  // without touching the counter (same-address atomics serialise, and a ticket
+  // per idle block cost microseconds at the small scales).
+  if ((int64_t)blockIdx.x >= ntiles) return;
   if (tid == 0) s_tile = atomicAdd(a.ticket, 1u);
   __syncthreads();
   const int64_t tile = s_tile;
