@@ -14,8 +14,12 @@
 // last conv layer is exactly the B operand layout of the head, so the head
 // (16 x 256 logits per tile) runs from registers, followed by a row max / sum
 // of exp over the 64 logits a lane holds and the 4 lanes sharing a voxel.
-// Output-stationary: no atomics, a fixed summation order per voxel, so an
-// encoder and a decoder evaluating the same scale get bit-identical results.
+// Output-stationary: no atomics, a fixed summation order per voxel (4 offset
+// groups, each chained from zero and folded onto the bias in group order; the
+// softmax normaliser merged per 64-symbol group in group order), so an encoder
+// and a decoder evaluating the same scale get bit-identical results whether a
+// tile is computed by one wave (large launches) or split over a quad of waves
+// by offset group and symbol group (launches of at most 4 tiles per block).
 
 #include <type_traits>
 
@@ -419,6 +423,72 @@ __device__ __forceinline__ void parent_cell_rows(uint64_t kf, int b, int g, cons
   }
 }
 
+// One group of 64 symbols of the 256-way head (symbol blocks 4 grp .. 4 grp
+// + 3, 16 symbols each): logits z = H^T h + b on MFMA from the accumulator
+// layout of h, stored when requested, and the group's normaliser terms per
+// lane: gm = the max of the lane's 16 logits, part = the sum of exp(z - gm).
+template <int C, bool BF>
+__device__ __forceinline__ void head_group(const ConvArgs& a, const f4 (&acc)[C / 16], const float* s_h,
+                                           const float* hb, int lane, int g, bool valid, int64_t prow,
+                                           int64_t mo_first, int grp, float& gm, float& part) {
+  constexpr int KT = C / 4;
+  float* lo = (a.logits && valid) ? a.logits + (prow - mo_first) * 256 + 4 * g : nullptr;
+  uint4 bh = make_uint4(0, 0, 0, 0), bl = bh;
+  if constexpr (BF) head_operand_bf<C>(acc, bh, bl);
+  f4 zz[4];
+#pragma unroll
+  for (int q4 = 0; q4 < 4; ++q4) {
+    const int sb = grp * 4 + q4;
+    if constexpr (BF) {
+      zz[q4] = head16_bf<C>(reinterpret_cast<const uint4*>(s_h) + (sb * 64 + lane) * 2, hb + 16 * sb, bh, bl, g);
+    } else {
+      zz[q4] = *reinterpret_cast<const f4*>(hb + 16 * sb + 4 * g);
+      const f4* hp = reinterpret_cast<const f4*>(s_h + (sb * 64 + lane) * KT);
+#pragma unroll
+      for (int q = 0; q < KT / 4; ++q) {
+        const f4 hv = hp[q];
+#pragma unroll
+        for (int e = 0; e < 4; ++e) zz[q4] = mfma4(hv[e], acc[q][e], zz[q4]);
+      }
+    }
+  }
+  gm = zz[0][0];
+#pragma unroll
+  for (int q4 = 0; q4 < 4; ++q4)
+#pragma unroll
+    for (int e = 0; e < 4; ++e) gm = fmaxf(gm, zz[q4][e]);
+  part = 0.0f;
+#pragma unroll
+  for (int q4 = 0; q4 < 4; ++q4)
+#pragma unroll
+    for (int e = 0; e < 4; ++e) part += __expf(zz[q4][e] - gm);
+  if (lo) {
+#pragma unroll
+    for (int q4 = 0; q4 < 4; ++q4) *reinterpret_cast<f4*>(lo + 16 * (grp * 4 + q4)) = zz[q4];
+  }
+}
+
+// Running normaliser (m, s) of the logits seen so far, extended by a group
+// with terms (gm, part); starts from (-inf, 0).
+__device__ __forceinline__ void lse_merge(float& m, float& s, float gm, float part) {
+  const float mn = fmaxf(m, gm);
+  s = s * __expf(m - mn) + part * __expf(gm - mn);
+  m = mn;
+}
+
+// The 4 lanes r, r+16, r+32, r+48 hold the 4 quarters of voxel r's symbols:
+// merged by lane exchange, then lse = m + log(s) stored at row prow.
+__device__ __forceinline__ void lse_finish(const ConvArgs& a, float m, float ssum, int g, bool valid, int64_t prow) {
+#pragma unroll
+  for (int o = 16; o <= 32; o <<= 1) {
+    const float om = __shfl_xor(m, o), os = __shfl_xor(ssum, o);
+    const float mn = fmaxf(m, om);
+    ssum = ssum * __expf(m - mn) + os * __expf(om - mn);
+    m = mn;
+  }
+  if (valid && g == 0) a.lse[prow] = m + __logf(ssum);
+}
+
 // Head of the last conv layer's features h (the conv accumulators of a tile:
 // lane (r, g) holds channels 16 cb + 4 g .. + 3 of voxel r) in registers:
 // the one-stage 256-way head with its softmax normaliser (Eq. 10), or the
@@ -469,58 +539,17 @@ __device__ __forceinline__ void head_epilogue(const ConvArgs& a, const f4 (&acc)
   }
   if constexpr (!TWO) {
     // ---- head: z^T[256][16] = H^T h^T with the conv accumulators as the B
-    // operand; 64 symbols at a time with a running (max, sum of exp)
+    // operand, 64 symbols (4 blocks of 16) per group; the normaliser is
+    // combined group by group in a fixed order (head_group / lse_merge), the
+    // same order a tile split over several waves uses
     float m = -INFINITY, ssum = 0.0f;
-    float* lo = (a.logits && valid) ? a.logits + (prow - mo_first) * 256 + 4 * g : nullptr;
-    uint4 bh = make_uint4(0, 0, 0, 0), bl = bh;
-    if constexpr (BF) head_operand_bf<C>(acc, bh, bl);
 #pragma unroll 1
     for (int grp = 0; grp < 4; ++grp) {
-      f4 zz[4];
-#pragma unroll
-      for (int q4 = 0; q4 < 4; ++q4) {
-        const int sb = grp * 4 + q4;
-        if constexpr (BF) {
-          zz[q4] = head16_bf<C>(reinterpret_cast<const uint4*>(s_h) + (sb * 64 + lane) * 2, a.hb + 16 * sb,
-                                bh, bl, g);
-        } else {
-          zz[q4] = *reinterpret_cast<const f4*>(a.hb + 16 * sb + 4 * g);
-          const f4* hp = reinterpret_cast<const f4*>(s_h + (sb * 64 + lane) * KT);
-#pragma unroll
-          for (int q = 0; q < KT / 4; ++q) {
-            const f4 hv = hp[q];
-#pragma unroll
-            for (int e = 0; e < 4; ++e) zz[q4] = mfma4(hv[e], acc[q][e], zz[q4]);
-          }
-        }
-      }
-      float gm = zz[0][0];
-#pragma unroll
-      for (int q4 = 0; q4 < 4; ++q4)
-#pragma unroll
-        for (int e = 0; e < 4; ++e) gm = fmaxf(gm, zz[q4][e]);
-      const float mn = fmaxf(m, gm);
-      float part = 0.0f;
-#pragma unroll
-      for (int q4 = 0; q4 < 4; ++q4)
-#pragma unroll
-        for (int e = 0; e < 4; ++e) part += __expf(zz[q4][e] - mn);
-      ssum = ssum * __expf(m - mn) + part;
-      m = mn;
-      if (lo) {
-#pragma unroll
-        for (int q4 = 0; q4 < 4; ++q4) *reinterpret_cast<f4*>(lo + 16 * (grp * 4 + q4)) = zz[q4];
-      }
+      float gm, part;
+      head_group<C, BF>(a, acc, s_h, a.hb, lane, g, valid, prow, mo_first, grp, gm, part);
+      lse_merge(m, ssum, gm, part);
     }
-    // the 4 lanes r, r+16, r+32, r+48 hold the 4 quarters of voxel r's symbols
-#pragma unroll
-    for (int o = 16; o <= 32; o <<= 1) {
-      const float om = __shfl_xor(m, o), os = __shfl_xor(ssum, o);
-      const float mn = fmaxf(m, om);
-      ssum = ssum * __expf(m - mn) + os * __expf(om - mn);
-      m = mn;
-    }
-    if (valid && g == 0) a.lse[prow] = m + __logf(ssum);
+    lse_finish(a, m, ssum, g, valid, prow);
   }
 }
 
@@ -535,6 +564,13 @@ __device__ __forceinline__ int64_t conv_tile(int64_t slot, int64_t tch) {
   return ((k / tch) * 8 + xcd) * tch + k % tch;
 }
 
+// Offsets of group i of the conv's fixed summation order: k in [7i, 7i + 7),
+// the last group [21, 27).
+__device__ __forceinline__ uint32_t group_offsets(int i) {
+  const int lo = 7 * i, hi = i < 3 ? 7 * i + 7 : 27;
+  return ((1u << hi) - 1u) & ~((1u << lo) - 1u);
+}
+
 template <int C, bool FIRST, bool LAST, bool TWO, bool BF>
 __global__ void __launch_bounds__(CONV_THREADS) k_conv(ConvArgs a) {
   constexpr int NCB = C / 16;
@@ -544,7 +580,7 @@ __global__ void __launch_bounds__(CONV_THREADS) k_conv(ConvArgs a) {
   // packed weights per (offset, column block, lane): fp32 KSP floats, bf16x3 8 words
   constexpr int WSZ = 27 * NCB * 64 * (BF ? 8 : KSP);
   constexpr int HSZ = LAST ? (TWO ? 2 : 16) * 64 * (BF ? 8 : KT) : 4;
-  constexpr int PCH = FIRST ? 8 : 4;  // offsets per pipeline stage
+  constexpr int PCH = FIRST ? 8 : 3;  // offsets per pipeline stage
   struct Gath {                        // one gathered neighbour slice
     uint32_t word;                     // first layer: 11 input bits
     f4 v[FIRST ? 1 : KSP / 4];         // later layers, fp32: KS channels
@@ -576,7 +612,11 @@ __global__ void __launch_bounds__(CONV_THREADS) k_conv(ConvArgs a) {
   }
   // chunk size: 64 chunks per launch (8 per XCD) between 16 and 256 tiles
   const int64_t tch = total_tiles / 64 < 16 ? 16 : (total_tiles / 64 > 256 ? 256 : total_tiles / 64);
-  if (conv_tile(0, tch) >= total_tiles) return;  // whole block idle: skip the weight staging
+  // small launches: a quad of waves per tile (at most CONV_WAVES / 4 tiles per block)
+  const bool quads = total_tiles <= (int64_t)gridDim.x * (CONV_WAVES / 4);  // uniform
+  static_assert((16 * NCB * 64 * 16 + 16 * 64 * 8) <= WSZ * 4, "quad exchange area exceeds the weight area");
+  if (quads ? (int64_t)blockIdx.x >= total_tiles : conv_tile(0, tch) >= total_tiles)
+    return;  // whole block idle: skip the weight staging
   if (tid == 0) {
     s_next = 0;
     int64_t acc = 0;
@@ -596,15 +636,16 @@ __global__ void __launch_bounds__(CONV_THREADS) k_conv(ConvArgs a) {
                                      tid);
   __syncthreads();
 
-  // Tile order (conv_tile): every XCD gets chunks from the whole tile range,
-  // a sample of every scale of the launch, so the XCDs carry about the same
-  // mix of cheap and expensive tiles (coarse scales have far more occupied
-  // offsets per tile).  Inside a block the waves take the block's tiles
-  // dynamically from an LDS counter: the first CONV_WAVES slots statically,
-  // the rest first come, first served.
-  for (int64_t slot = w;;) {
-    const int64_t tile = conv_tile(slot, tch);
-    if (tile >= total_tiles) break;
+  // A tile as the epilogue and the head need it.
+  struct TileRef {
+    int b;
+    int64_t mo, prow, lvb;
+    bool valid;
+  };
+  // Opens tile `tile` (scale, rows, neighbour rows) and accumulates it: grp < 0
+  // gives the bias plus all 4 offset-group sums, folded in group order; grp in
+  // 0 .. 3 gives that group's sum alone (a wave of a quad sharing the tile).
+  auto conv_sum = [&](int64_t tile, int grp, TileRef& tr, f4 (&out)[NCB]) {
     int si = 0;  // scale of the tile: all prefix loads issued together
 #pragma unroll
     for (int i = 1; i < NLEV; ++i) si += (s_tpre[i] <= tile) ? 1 : 0;
@@ -625,7 +666,7 @@ __global__ void __launch_bounds__(CONV_THREADS) k_conv(ConvArgs a) {
       parent_cell_rows(a.lv_key[lvb + (prow - mo)], b, g, a.hash, a.hash_lg, a.fb, s_par[w][r], nb);
       nlo = make_int4(nb[0], nb[1], nb[2], nb[3]);
       nhi = make_int4(nb[4], nb[5], nb[6], nb[7]);
-      if (valid) {
+      if (valid && grp <= 0) {  // one wave of a quad stores the map rows
         int4* dst = reinterpret_cast<int4*>(a.nbr + prow * NBR_STRIDE + 8 * g);
         dst[0] = nlo;
         dst[1] = nhi;
@@ -649,14 +690,34 @@ __global__ void __launch_bounds__(CONV_THREADS) k_conv(ConvArgs a) {
       }
       offs &= 0x7FFFFFFu;
     }
+    if (grp >= 0) offs &= group_offsets(grp);
 
     // ---- accumulate over the occupied offsets, software-pipelined: the
     // gathers of the next PCH offsets are issued before the MFMAs of the
     // current ones (double buffer; loads are never skipped, an unused slot
     // reads the zero row, so the wait counts stay exact).
-    f4 acc[NCB];
+    // Summation order per output: the offsets fall into 4 fixed groups
+    // (k < 7, < 14, < 21, < 27); each group's products are chained on MFMA
+    // from zero, in ascending offset order, and the 4 group sums are added to
+    // the bias in group order: ((((bias + S0) + S1) + S2) + S3).
+    f4 acc[NCB], tsum[NCB];
 #pragma unroll
-    for (int cb = 0; cb < NCB; ++cb) acc[cb] = *reinterpret_cast<const f4*>(a.bias + 16 * cb + 4 * g);
+    for (int cb = 0; cb < NCB; ++cb) {
+      tsum[cb] = *reinterpret_cast<const f4*>(a.bias + 16 * cb + 4 * g);
+      acc[cb] = f4{0.0f, 0.0f, 0.0f, 0.0f};
+    }
+    int gcur = grp >= 0 ? grp : 0;  // group whose sum acc holds
+    auto fold = [&]() {
+#pragma unroll
+      for (int cb = 0; cb < NCB; ++cb) {
+        tsum[cb] += acc[cb];
+        acc[cb] = f4{0.0f, 0.0f, 0.0f, 0.0f};
+      }
+      ++gcur;
+    };
+    auto enter = [&](int k) {  // k: the next offset, wave-uniform
+      while (k >= (gcur < 3 ? 7 * (gcur + 1) : 27)) fold();
+    };
     auto take = [&](int (&ks)[PCH]) {
 #pragma unroll
       for (int c = 0; c < PCH; ++c) {
@@ -705,6 +766,7 @@ __global__ void __launch_bounds__(CONV_THREADS) k_conv(ConvArgs a) {
 #pragma unroll
       for (int c = 0; c < PCH; ++c) {
         if (ks[c] < 0) break;
+        enter(ks[c]);
         uint4 wa[NCB][2];
 #pragma unroll
         for (int cb = 0; cb < NCB; ++cb) {
@@ -745,6 +807,7 @@ __global__ void __launch_bounds__(CONV_THREADS) k_conv(ConvArgs a) {
 #pragma unroll
       for (int c = 0; c < PCH; ++c) {
         if (ks[c] < 0) break;
+        enter(ks[c]);
         f4 wv[NCB][KSP / 4];
         load_w(ks[c], wv);
         float bsrc[KSP];
@@ -786,6 +849,25 @@ __global__ void __launch_bounds__(CONV_THREADS) k_conv(ConvArgs a) {
         if (ksA[0] < 0) break;
       }
     }
+    if (grp < 0) {
+      while (gcur < 4) fold();  // every group folded, also the empty ones
+#pragma unroll
+      for (int cb = 0; cb < NCB; ++cb) out[cb] = tsum[cb];
+    } else {
+#pragma unroll
+      for (int cb = 0; cb < NCB; ++cb) out[cb] = acc[cb];
+    }
+    tr.b = b;
+    tr.mo = mo;
+    tr.prow = prow;
+    tr.lvb = lvb;
+    tr.valid = valid;
+  };
+  // Residual, ReLU, the children's X_B rows (full predictor) and the output row.
+  auto epilogue = [&](const TileRef& tr, f4 (&acc)[NCB]) {
+    const int b = tr.b;
+    const int64_t mo = tr.mo, prow = tr.prow, lvb = tr.lvb;
+    const bool valid = tr.valid;
     if (a.res) {  // residual block: ReLU(x + conv(.)), x read at the voxel's own row
 #pragma unroll
       for (int cb = 0; cb < NCB; ++cb) acc[cb] += *reinterpret_cast<const f4*>(a.res + prow * C + 16 * cb + 4 * g);
@@ -832,10 +914,90 @@ __global__ void __launch_bounds__(CONV_THREADS) k_conv(ConvArgs a) {
       }
     }
 
-    if constexpr (LAST) head_epilogue<C, TWO, BF>(a, acc, s_h, lane, g, valid, prow, mo, lvb, s_mo[0]);
-    int nxt = 0;
-    if (lane == 0) nxt = atomicAdd(&s_next, 1);
-    slot = CONV_WAVES + __builtin_amdgcn_readfirstlane(__shfl(nxt, 0));
+  };
+
+  if (!quads) {
+    // Tile order (conv_tile): every XCD gets chunks from the whole tile range,
+    // a sample of every scale of the launch, so the XCDs carry about the same
+    // mix of cheap and expensive tiles (coarse scales have far more occupied
+    // offsets per tile).  Inside a block the waves take the block's tiles
+    // dynamically from an LDS counter: the first CONV_WAVES slots statically,
+    // the rest first come, first served.
+    for (int64_t slot = w;;) {
+      const int64_t tile = conv_tile(slot, tch);
+      if (tile >= total_tiles) break;
+      TileRef tr;
+      f4 acc[NCB];
+      conv_sum(tile, -1, tr, acc);
+      epilogue(tr, acc);
+      if constexpr (LAST) head_epilogue<C, TWO, BF>(a, acc, s_h, lane, g, tr.valid, tr.prow, tr.mo, tr.lvb, s_mo[0]);
+      int nxt = 0;
+      if (lane == 0) nxt = atomicAdd(&s_next, 1);
+      slot = CONV_WAVES + __builtin_amdgcn_readfirstlane(__shfl(nxt, 0));
+    }
+    return;
+  }
+
+  // Small launch (at most one tile per quad of waves): quad q of block x takes
+  // tile x + q G, its wave i the offsets of group i, so a tile's serial MFMA
+  // chain is split four ways.  The group sums meet in the weight area of LDS
+  // (free once every conv loop is done) and are folded by wave 0 in the same
+  // order as above; the 256-way head is split by symbol group the same way.
+  // Every wave passes every barrier (no early exit below).
+  {
+    const int q = w >> 2, gi = w & 3;
+    const int64_t tile = (int64_t)blockIdx.x + (int64_t)gridDim.x * q;
+    const bool has = tile < total_tiles;  // wave-uniform
+    TileRef tr{};
+    f4 acc[NCB];
+    if (has) conv_sum(tile, gi, tr, acc);
+    __syncthreads();  // every conv loop of the block is done: the weight area is free
+    f4* s_x = reinterpret_cast<f4*>(s_w);  // [quad][slot 0..3][NCB][64]: group sums 1-3, h
+    float2* s_x2 = reinterpret_cast<float2*>(s_x + 16 * NCB * 64);  // [quad][group][64]: (gm, part)
+    auto xs = [&](int slot, int cb) -> f4* { return s_x + ((q * 4 + slot) * NCB + cb) * 64 + lane; };
+    if (has && gi > 0) {
+#pragma unroll
+      for (int cb = 0; cb < NCB; ++cb) *xs(gi - 1, cb) = acc[cb];
+    }
+    __syncthreads();
+    if (has && gi == 0) {
+#pragma unroll
+      for (int cb = 0; cb < NCB; ++cb) {
+        f4 t = *reinterpret_cast<const f4*>(a.bias + 16 * cb + 4 * g);
+        t += acc[cb];
+        t += *xs(0, cb);
+        t += *xs(1, cb);
+        t += *xs(2, cb);
+        acc[cb] = t;
+      }
+      epilogue(tr, acc);
+      if constexpr (LAST && !TWO) {
+#pragma unroll
+        for (int cb = 0; cb < NCB; ++cb) *xs(3, cb) = acc[cb];  // h for the quad's other waves
+      }
+      if constexpr (LAST && TWO) head_epilogue<C, TWO, BF>(a, acc, s_h, lane, g, tr.valid, tr.prow, tr.mo, tr.lvb, s_mo[0]);
+    }
+    if constexpr (LAST && !TWO) {
+      __syncthreads();
+      if (has) {
+        f4 h[NCB];
+#pragma unroll
+        for (int cb = 0; cb < NCB; ++cb) h[cb] = *xs(3, cb);
+        float gm, part;
+        head_group<C, BF>(a, h, s_h, a.hb, lane, g, tr.valid, tr.prow, s_mo[0], gi, gm, part);
+        s_x2[(q * 4 + gi) * 64 + lane] = make_float2(gm, part);
+      }
+      __syncthreads();
+      if (has && gi == 0) {
+        float m = -INFINITY, ssum = 0.0f;
+#pragma unroll
+        for (int k = 0; k < 4; ++k) {
+          const float2 v = s_x2[(q * 4 + k) * 64 + lane];
+          lse_merge(m, ssum, v.x, v.y);
+        }
+        lse_finish(a, m, ssum, g, tr.valid, tr.prow);
+      }
+    }
   }
 }
 
