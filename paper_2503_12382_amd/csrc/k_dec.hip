@@ -107,11 +107,13 @@ __global__ void __launch_bounds__(EXP_THREADS) k_expand(ExpArgs a) {
 
   // popcount scan over the tile's parents (element j of wave w: w*64*KPT + j*64 + lane)
   uint32_t code[EXP_KPT], incl[EXP_KPT];
+  uint64_t key[EXP_KPT];  // loaded with the codes: off the look-back's critical path
   uint32_t run = 0;
 #pragma unroll
   for (int j = 0; j < EXP_KPT; ++j) {
     const int64_t p = base + (int64_t)w * 64 * EXP_KPT + j * 64 + lane;
     uint32_t c = 0;
+    key[j] = p < np ? a.key_b[p] : 0ull;
     if (p < np) {
       c = a.codes_in ? a.codes_in[p] : a.code_b[p];
       if (a.codes_in) a.code_b[p] = (uint8_t)c;
@@ -165,7 +167,7 @@ __global__ void __launch_bounds__(EXP_THREADS) k_expand(ExpArgs a) {
     const uint32_t c = code[j];
     int64_t q = wbase + incl[j] - (uint32_t)__popc(c);
     a.fc_b[p] = (int32_t)q;
-    const uint64_t kp = a.key_b[p] << 3;
+    const uint64_t kp = key[j] << 3;
     for (uint32_t d = 0; d < 8; ++d) {
       if (!((c >> d) & 1u)) continue;
       if (q >= a.cap_pts) {
@@ -186,7 +188,7 @@ __global__ void __launch_bounds__(EXP_THREADS) k_expand(ExpArgs a) {
     const int64_t p = base + (int64_t)w * 64 * EXP_KPT + j * 64 + lane;
     if (p >= np) continue;
     const int64_t q = wbase + incl[j] - (uint32_t)__popc(code[j]);
-    hash_insert(a.hash, a.hash_lg, tag_key(a.key_b[p], a.b, a.fb), (int32_t)q, code[j], a.err);
+    hash_insert(a.hash, a.hash_lg, tag_key(key[j], a.b, a.fb), (int32_t)q, code[j], a.err);
   }
 }
 
