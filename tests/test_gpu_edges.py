@@ -236,3 +236,57 @@ def test_model_capacity_overflow_reported():
         ctx.sync()
     assert e.value.status == reno.RENO_E_CAPACITY
     ctx.close()
+
+
+@pytest.mark.parametrize("extra", [0, 1])
+def test_quad_split_boundary(extra):
+    """A model scale of exactly 1024 tiles (16384 voxels: a 32 x 32 x 16 block)
+    runs with a quad of waves per tile when launched alone; one voxel more
+    (1025 tiles) runs one wave per tile.  Either way the per-scale launches of
+    the encoder and of the decoder reproduce the all-scale launch (one wave per
+    tile) bit for bit, and match the oracle."""
+    B, b0, R, C, L = 8, 4, 10.0, 32, 3
+    g = np.stack(np.meshgrid(np.arange(32), np.arange(32), np.arange(16), indexing="ij"), -1).reshape(-1, 3)
+    cells7 = g + np.array([40, 50, 60])
+    if extra:
+        cells7 = np.concatenate([cells7, [[3, 120, 7]]])
+    pts = _points_from_voxels(2 * cells7, B, R)  # one finest-scale child per scale-7 voxel
+    w = gen_weights(C, L, seed=61, bias_std=0.1)
+    cfg = _cfg(B, b0, C, L, R)
+    say("quad split boundary, scale-7 voxels", len(cells7))
+    enc = make_ctx(cfg, len(pts))
+    encode(enc, pts, B)
+    assert enc.num_voxels(7) == 16384 + extra
+    enc.set_weights(reno.weights_to_device(w))
+    lg = enc.predict_probs(reno.RENO_ALL_SCALES, logits=True).cpu().numpy()
+    bits, total = enc.code_length(reno.RENO_ALL_SCALES)
+    P = oracle.Pyramid.from_points(pts, B, b0, R)
+    off = {}
+    o = 0
+    for b in range(b0 + 1, B):
+        off[b] = o
+        n = P.num(b)
+        olg, _, obits = P.model(b, w)
+        assert np.abs(lg[o:o + n] - olg).max() <= LOGIT_TOL, b
+        assert np.abs(bits.cpu().numpy()[o:o + n] - obits).max() <= BITS_ABS_TOL, b
+        o += n
+    # encoder, one scale per launch
+    for b in range(b0 + 1, B):
+        n = P.num(b)
+        np.testing.assert_array_equal(enc.predict_probs(b, logits=True).cpu().numpy(), lg[off[b]:off[b] + n])
+    # decoder
+    codes = {b: enc.occupancy_codes(b).clone() for b in range(b0, B)}
+    base, _ = enc.coords(b0)
+    dec = make_ctx(cfg, len(pts))
+    dec.set_weights(reno.weights_to_device(w))
+    dec.set_base(B, base.clone(), codes[b0])
+    for b in range(b0 + 1, B):
+        dec.expand(b - 1, None if b - 1 == b0 else codes[b - 1])
+        n = P.num(b)
+        np.testing.assert_array_equal(dec.predict_probs(b, logits=True).cpu().numpy(), lg[off[b]:off[b] + n])
+    dec.expand(B - 1, codes[B - 1])
+    dbits, dtotal = dec.code_length(reno.RENO_ALL_SCALES)
+    np.testing.assert_array_equal(dbits.cpu().numpy(), bits.cpu().numpy())
+    assert dtotal == total
+    enc.close()
+    dec.close()
