@@ -4,7 +4,8 @@
 // target coordinates (Eq. 9) and a linear head to 256 logits with the softmax
 // normaliser (Eq. 10).
 //
-// Work unit: a wavefront owns a tile of 16 consecutive voxels of one scale.
+// Work unit: a wavefront owns a tile of 16 consecutive voxels of one scale (in
+// launches of at most 4 tiles per block, a quad of waves shares it).
 // Each layer is computed transposed, out^T[c_out][16] = sum_k W_k^T in_k^T, on
 // fp32 MFMA 16x16x4: the A operand is the offset's weights (staged once per
 // block in LDS, pre-swizzled so each lane reads its operands with 128-bit
