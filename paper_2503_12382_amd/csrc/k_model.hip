@@ -1804,7 +1804,7 @@ hipError_t launch_top(Ctx& c, int b_lo, int b_hi, float* logits, bool second) {
   a.code = c.lv_code;
   a.fc = c.lv_fc;
   const bool two = c.p.head_mode == RENO_HEAD_TWO_STAGE;
-  if (b_lo != b_hi || b_lo >= c.B - 3) {  // sorted tiles, as for the plain model
+  if (b_lo != b_hi || b_lo >= c.B - 2) {  // sorted tiles, as for the plain model
     ProfScope pso_(c, RENO_K_OTHER);
     const int nsc = b_hi - n_lo + 1;
     const int64_t windows = (c.cap_model + c.cap_pts + TO_W - 1) / TO_W + nsc;
@@ -1966,9 +1966,10 @@ hipError_t launch_model(Ctx& c, int b_lo, int b_hi, float* logits, bool second) 
   const bool two = c.p.head_mode == RENO_HEAD_TWO_STAGE;
   const int L = c.p.layers;
   // sorted tiles where the launch is bound by matrix work: a batch of scales,
-  // or one of the three finest model scales (small scales are latency-bound
-  // and would only pay for the extra launch)
-  const bool order = L >= 2 && (b_lo != b_hi || b_lo >= c.B - 3);
+  // or one of the two finest model scales (smaller scales are latency-bound
+  // and would only pay for the extra launch; on the 14-bit scan ordering the
+  // third finest too cost 1 %)
+  const bool order = L >= 2 && (b_lo != b_hi || b_lo >= c.B - 2);
   a.b_ext = -1;
   a.cap_rows = c.cap_model + 1;
   const RowMap rm{c.d_count, c.d_moff, (int64_t)c.cap_model, -1, 0, (int64_t)c.cap_model + 1};
