@@ -1368,6 +1368,7 @@ struct OffMask {
 };
 
 constexpr int CW_THREADS = 512;
+constexpr int CW_SPLIT_ROUNDS = 2;  // column split while a block has at most this many tile sets
 constexpr int CW_WAVES = CW_THREADS / 64;
 
 // Sparse conv C -> C (ReLU, optional residual input, child scatter and row
@@ -1404,7 +1405,16 @@ __global__ void __launch_bounds__(CW_THREADS) k_convw(ConvArgs a) {
   }
   const int64_t groups = (total_tiles + CW_WAVES - 1) / CW_WAVES;
   const int64_t tch = groups / 64 < 4 ? 4 : (groups / 64 > 64 ? 64 : groups / 64);
-  if (conv_tile(0, tch) >= groups) return;  // whole block idle
+  // Column split for launches with few tiles: a block takes TPB tiles and
+  // wave w computes column block w % NCB of tile w / NCB, so a tile's serial
+  // walk over its offsets is spread over NCB waves (each output channel's
+  // MFMA chain is the same as with one wave per tile) and the block walks the
+  // union of TPB tiles instead of CW_WAVES.
+  constexpr int TPB = CW_WAVES / NCB;
+  const int64_t sets = (total_tiles + TPB - 1) / TPB;
+  const bool split = NCB > 1 && sets <= (int64_t)gridDim.x * CW_SPLIT_ROUNDS;  // uniform
+  const int64_t nwork = split ? sets : groups;
+  if (split ? (int64_t)blockIdx.x >= sets : conv_tile(0, tch) >= groups) return;  // whole block idle
   if (tid == 0) {
     int64_t acc = 0;
     for (int i = 0; i < nsc; ++i) {
@@ -1418,11 +1428,12 @@ __global__ void __launch_bounds__(CW_THREADS) k_convw(ConvArgs a) {
     for (int i = nsc; i <= NLEV; ++i) s_tpre[i] = acc;
   }
   const f4* wsrc = reinterpret_cast<const f4*>(a.w);
+  const int cb0 = split ? w % NCB : 0;  // the wave's (first) column block
   for (int64_t gs = 0;; ++gs) {
-    const int64_t grp = conv_tile(gs, tch);  // block-uniform
-    if (grp >= groups) break;
+    const int64_t grp = split ? (int64_t)blockIdx.x + gs * (int64_t)gridDim.x : conv_tile(gs, tch);  // block-uniform
+    if (grp >= nwork) break;
     __syncthreads();  // prefix visible; the previous group is done with s_mask and s_w
-    const int64_t tile = grp * CW_WAVES + w;
+    const int64_t tile = split ? grp * TPB + w / NCB : grp * CW_WAVES + w;
     const bool have = tile < total_tiles;
     int b = a.b_lo;
     int64_t mo = 0, prow = 0, lvb = 0;
@@ -1481,9 +1492,10 @@ __global__ void __launch_bounds__(CW_THREADS) k_convw(ConvArgs a) {
 #pragma unroll
       for (int q = 0; q < KS / 4; ++q) x[q] = src[q];
     };
+    // acc[j] holds column block cb0 + j (split: j = 0 only)
     f4 acc[NCB];
 #pragma unroll
-    for (int cb = 0; cb < NCB; ++cb) acc[cb] = *reinterpret_cast<const f4*>(a.bias + 16 * cb + 4 * g);
+    for (int cb = 0; cb < NCB; ++cb) acc[cb] = *reinterpret_cast<const f4*>(a.bias + 16 * (cb0 + (split ? 0 : cb)) + 4 * g);
     f4 xa[KS / 4], xb[KS / 4];
     int ko = own.pop();
     const int32_t eo = entry(ko);
@@ -1506,15 +1518,24 @@ __global__ void __launch_bounds__(CW_THREADS) k_convw(ConvArgs a) {
         const int32_t er = entry(kr);
         if (kq >= 0) gather(eq, xb);
         const float* wb = s_w[buf];
+        if (split) {
 #pragma unroll
-        for (int q = 0; q < KS / 4; ++q) {
-          f4 wv[NCB];
+          for (int q = 0; q < KS / 4; ++q) {
+            const f4 wv = reinterpret_cast<const f4*>(wb)[(cb0 * (KS / 4) + q) * 64 + lane];
 #pragma unroll
-          for (int cb = 0; cb < NCB; ++cb) wv[cb] = reinterpret_cast<const f4*>(wb)[(cb * (KS / 4) + q) * 64 + lane];
+            for (int e = 0; e < 4; ++e) acc[0] = mfma4(wv[e], xa[q][e], acc[0]);
+          }
+        } else {
 #pragma unroll
-          for (int e = 0; e < 4; ++e)
+          for (int q = 0; q < KS / 4; ++q) {
+            f4 wv[NCB];
 #pragma unroll
-            for (int cb = 0; cb < NCB; ++cb) acc[cb] = mfma4(wv[cb][e], xa[q][e], acc[cb]);
+            for (int cb = 0; cb < NCB; ++cb) wv[cb] = reinterpret_cast<const f4*>(wb)[(cb * (KS / 4) + q) * 64 + lane];
+#pragma unroll
+            for (int e = 0; e < 4; ++e)
+#pragma unroll
+              for (int cb = 0; cb < NCB; ++cb) acc[cb] = mfma4(wv[cb][e], xa[q][e], acc[cb]);
+          }
         }
 #pragma unroll
         for (int q = 0; q < KS / 4; ++q) xa[q] = xb[q];
@@ -1528,9 +1549,11 @@ __global__ void __launch_bounds__(CW_THREADS) k_convw(ConvArgs a) {
       kc = kn;
     }
     if (!have) continue;
+    const int ncw = split ? 1 : NCB;  // column blocks this wave holds: cb0 .. cb0 + ncw - 1
     if (a.res) {  // residual block: ReLU(x + conv(.)), x read at the voxel's own row
 #pragma unroll
-      for (int cb = 0; cb < NCB; ++cb) acc[cb] += *reinterpret_cast<const f4*>(a.res + prow * C + 16 * cb + 4 * g);
+      for (int j = 0; j < NCB; ++j)
+        if (j < ncw) acc[j] += *reinterpret_cast<const f4*>(a.res + prow * C + 16 * (cb0 + j) + 4 * g);
     }
 #pragma unroll
     for (int cb = 0; cb < NCB; ++cb)
@@ -1548,16 +1571,18 @@ __global__ void __launch_bounds__(CW_THREADS) k_convw(ConvArgs a) {
         if (cmo >= 0 && ((code >> d) & 1u)) {
           float* dst = a.xb + (cmo + first + rank) * C;
 #pragma unroll
-          for (int cb = 0; cb < NCB; ++cb)
-            *reinterpret_cast<f4*>(dst + 16 * cb + 4 * g) =
-                acc[cb] + *reinterpret_cast<const f4*>(a.emb_d + d * C + 16 * cb + 4 * g);
+          for (int j = 0; j < NCB; ++j)
+            if (j < ncw)
+              *reinterpret_cast<f4*>(dst + 16 * (cb0 + j) + 4 * g) =
+                  acc[j] + *reinterpret_cast<const f4*>(a.emb_d + d * C + 16 * (cb0 + j) + 4 * g);
           ++rank;
         }
       }
     }
     if (valid && a.h_out) {
 #pragma unroll
-      for (int cb = 0; cb < NCB; ++cb) *reinterpret_cast<f4*>(a.h_out + prow * C + 16 * cb + 4 * g) = acc[cb];
+      for (int j = 0; j < NCB; ++j)
+        if (j < ncw) *reinterpret_cast<f4*>(a.h_out + prow * C + 16 * (cb0 + j) + 4 * g) = acc[j];
     }
   }
 }
