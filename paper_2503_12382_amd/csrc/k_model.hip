@@ -604,12 +604,34 @@ __global__ void __launch_bounds__(CONV_THREADS) k_conv(ConvArgs a) {
   const int nsc = a.b_hi - a.b_lo + 1;
 
   const RowMap rm{a.count, a.moff, a.cap_model, a.b_ext, a.ext_off, a.cap_rows};
-  // tile prefix over the scales of this launch
-  int64_t total_tiles = 0;
-  for (int i = 0; i < nsc; ++i) {
+  // Sizes of the launch's scales.  One scale: scalar loads.  Several (the
+  // encoder's batched launch): all loaded at once, lane i of every wave
+  // reading scale b_lo + i, and the tile prefix over the scales is a scan
+  // across the lanes.  Lane i ends with scale i's rows (nb_l, mo_l), tiles
+  // tl and inclusive tile prefix incl (0 and the total beyond the last scale).
+  static_assert(NLEV < 32, "the scale scan covers 32 lanes");
+  int64_t nb_l = 0, mo_l = 0, total_tiles;
+  int tl = 0, incl;  // tiles of a scale and of a launch fit in 31 bits
+  if (nsc == 1) {
     int64_t mo, nb;
-    scale_span(rm, a.b_lo + i, mo, nb);
-    total_tiles += (nb + 15) / 16;
+    scale_span(rm, a.b_lo, mo, nb);
+    total_tiles = (nb + 15) / 16;
+    if (lane == 0) {
+      nb_l = nb;
+      mo_l = mo;
+      tl = (int)total_tiles;
+    }
+    incl = (int)total_tiles;
+  } else {
+    if (lane < nsc) scale_span(rm, a.b_lo + lane, mo_l, nb_l);
+    tl = (int)((nb_l + 15) / 16);
+    incl = tl;
+#pragma unroll
+    for (int o = 1; o < 32; o <<= 1) {
+      const int y = __shfl_up(incl, o);
+      if (lane >= o) incl += y;
+    }
+    total_tiles = __builtin_amdgcn_readlane(incl, 31);  // uniform (scalar register)
   }
   // chunk size: 64 chunks per launch (8 per XCD) between 16 and 256 tiles
   const int64_t tch = total_tiles / 64 < 16 ? 16 : (total_tiles / 64 > 256 ? 256 : total_tiles / 64);
@@ -617,24 +639,22 @@ __global__ void __launch_bounds__(CONV_THREADS) k_conv(ConvArgs a) {
   const bool quads = total_tiles <= (int64_t)gridDim.x * (CONV_WAVES / 4);  // uniform
   static_assert((16 * NCB * 64 * 16 + 16 * 64 * 8) <= WSZ * 4, "quad exchange area exceeds the weight area");
   if (quads ? (int64_t)blockIdx.x >= total_tiles : conv_tile(0, tch) >= total_tiles)
-    return;  // whole block idle: skip the weight staging
-  if (tid == 0) {
-    s_next = 0;
-    int64_t acc = 0;
-    for (int i = 0; i < nsc; ++i) {
-      int64_t mo, nb;
-      scale_span(rm, a.b_lo + i, mo, nb);
-      s_tpre[i] = acc;
-      s_nv[i] = nb;
-      s_mo[i] = mo;
-      acc += (nb + 15) / 16;
+    return;  // whole block idle: no weight staging
+  // weight and head loads of the whole block in one round trip
+  Staged<WSZ / 4, CONV_THREADS> stw;
+  Staged<LAST ? HSZ / 4 : 1, CONV_THREADS> sth;
+  stw.load(reinterpret_cast<const f4*>(a.w), tid);
+  if (LAST) sth.load(reinterpret_cast<const f4*>(a.hw), tid);
+  if (w == 0 && lane <= NLEV) {
+    if (lane == 0) s_next = 0;
+    s_tpre[lane] = lane < nsc ? incl - tl : total_tiles;  // padding: never below a valid tile
+    if (lane < NLEV) {
+      s_nv[lane] = nb_l;
+      s_mo[lane] = mo_l;
     }
-    for (int i = nsc; i <= NLEV; ++i) s_tpre[i] = acc;  // padding: never below a valid tile
   }
-  stage_lds<WSZ / 4, CONV_THREADS>(reinterpret_cast<const f4*>(a.w), reinterpret_cast<f4*>(s_w), tid);
-  if (LAST)
-    stage_lds<HSZ / 4, CONV_THREADS>(reinterpret_cast<const f4*>(a.hw), reinterpret_cast<f4*>(s_h),
-                                     tid);
+  stw.store(reinterpret_cast<f4*>(s_w), tid);
+  if (LAST) sth.store(reinterpret_cast<f4*>(s_h), tid);
   __syncthreads();
 
   // A tile as the epilogue and the head need it.

@@ -37,17 +37,28 @@ __global__ void __launch_bounds__(CL_THREADS) k_code_length(
   __shared__ float s_hb[NS];
   __shared__ float s_emb[TWO ? 16 * C : 1];
   __shared__ int64_t s_cpre[NLEV + 1];  // chunk prefix over the launch's scales
+  __shared__ int64_t s_n[NLEV], s_mo[NLEV];
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
-  if (tid == 0) {
-    int64_t acc = 0;
-    for (int i = 0; i < nsc; ++i) {
-      const int b = b_lo + i;
-      int64_t n = count[b];
-      if (moff[b] + n > cap_model) n = 0;  // capacity overflow, latched where the size was made
-      s_cpre[i] = acc;
-      acc += (n + CL_CHUNK - 1) / CL_CHUNK;
+  static_assert(NLEV < 32, "the scale scan covers 32 lanes");
+  if (w == 0) {  // sizes of all scales loaded at once (lane i: scale b_lo + i), prefix by a lane scan
+    int64_t n = 0, mo = 0;
+    if (lane < nsc) {
+      n = count[b_lo + lane];
+      mo = moff[b_lo + lane];
+      if (mo + n > cap_model) n = 0;  // capacity overflow, latched where the size was made
     }
-    s_cpre[nsc] = acc;
+    const int nc = (int)((n + CL_CHUNK - 1) / CL_CHUNK);
+    int incl = nc;
+#pragma unroll
+    for (int o = 1; o < 32; o <<= 1) {
+      const int y = __shfl_up(incl, o);
+      if (lane >= o) incl += y;
+    }
+    if (lane <= nsc) s_cpre[lane] = incl - nc;
+    if (lane < nsc) {
+      s_n[lane] = n;
+      s_mo[lane] = mo;
+    }
   }
   {  // staging: every load of a thread issued before its stores
     constexpr int PER = (NS * C + CL_THREADS - 1) / CL_THREADS;
@@ -73,8 +84,8 @@ __global__ void __launch_bounds__(CL_THREADS) k_code_length(
     int si = 0;
     while (si + 1 < nsc && s_cpre[si + 1] <= ch) ++si;
     const int b = b_lo + si;
-    const int64_t mo = moff[b];
-    const int64_t n = count[b];
+    const int64_t mo = s_mo[si];
+    const int64_t n = s_n[si];
     const int64_t cib = ch - s_cpre[si];  // chunk index inside the scale
     const int64_t v = cib * CL_CHUNK + lane;
     const int64_t vv = v < n ? v : n - 1;  // clamped: every load is issued
@@ -116,7 +127,7 @@ __global__ void __launch_bounds__(CL_THREADS) k_code_length(
       bt = (l1 - z1) * INV_LN2;
     double acc = 0.0;
     if (v < n) {
-      if (bits_out) bits_out[mo - moff[b_lo] + v] = bt;
+      if (bits_out) bits_out[mo - s_mo[0] + v] = bt;
       acc = (double)bt;
     }
     for (int d = 32; d > 0; d >>= 1) acc += __shfl_xor(acc, d);
