@@ -581,7 +581,9 @@ __global__ void __launch_bounds__(CONV_THREADS) k_conv(ConvArgs a) {
   // packed weights per (offset, column block, lane): fp32 KSP floats, bf16x3 8 words
   constexpr int WSZ = 27 * NCB * 64 * (BF ? 8 : KSP);
   constexpr int HSZ = LAST ? (TWO ? 2 : 16) * 64 * (BF ? 8 : KT) : 4;
-  constexpr int PCH = FIRST ? 8 : 3;  // offsets per pipeline stage
+  // offsets per pipeline stage: the first layer's gathers are 2-byte words behind a
+  // few MFMAs each, and a shallow pipeline measured fastest there
+  constexpr int PCH = FIRST ? 2 : 3;
   struct Gath {                        // one gathered neighbour slice
     uint32_t word;                     // first layer: 11 input bits
     f4 v[FIRST ? 1 : KSP / 4];         // later layers, fp32: KS channels
