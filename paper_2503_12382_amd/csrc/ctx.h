@@ -27,7 +27,7 @@ constexpr int PYR_THREADS = 256;
 constexpr int PYR_KPT = 4;
 constexpr int PYR_TILE = PYR_THREADS * PYR_KPT;
 constexpr int EXP_THREADS = 512;
-constexpr int EXP_KPT = 2;
+constexpr int EXP_KPT = 1;                      // parents per thread: a thread's hash inserts wait for their CAS in turn
 constexpr int EXP_TILE = EXP_THREADS * EXP_KPT;
 constexpr int TICKETS = 64;
 constexpr int NBR_STRIDE = 32;                  // neighbour-map row: 27 offsets + 5 padding
