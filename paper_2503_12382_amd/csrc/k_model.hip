@@ -635,8 +635,8 @@ __global__ void __launch_bounds__(CONV_THREADS) k_conv(ConvArgs a) {
     }
     total_tiles = __builtin_amdgcn_readlane(incl, 31);  // uniform (scalar register)
   }
-  // chunk size: 64 chunks per launch (8 per XCD) between 16 and 256 tiles
-  const int64_t tch = total_tiles / 64 < 16 ? 16 : (total_tiles / 64 > 256 ? 256 : total_tiles / 64);
+  // chunk size: 256 chunks per launch (32 per XCD) between 16 and 256 tiles
+  const int64_t tch = total_tiles / 256 < 16 ? 16 : (total_tiles / 256 > 256 ? 256 : total_tiles / 256);
   // small launches: a quad of waves per tile (at most CONV_WAVES / 4 tiles per block)
   const bool quads = total_tiles <= (int64_t)gridDim.x * (CONV_WAVES / 4);  // uniform
   static_assert((16 * NCB * 64 * 16 + 16 * 64 * 8) <= WSZ * 4, "quad exchange area exceeds the weight area");
