@@ -394,6 +394,49 @@ def test_model_two_layer_by_hand():
     np.testing.assert_allclose(lg, z, rtol=1e-12, atol=1e-12)
 
 
+def _plain_model_by_composition(P, b, w):
+    """The plain model of scale b (Sec. 3.2, Eqs. 7-10 in the configured form)
+    rebuilt from pinned pieces: input features written out with numpy from the
+    coordinates (octant bits of each voxel, bits of its parent's code, parent
+    found by halving the coordinates), then every layer l = 1..L through the
+    standalone sparse conv pinned against a dense conv3d, with layer l's own
+    weights and bias, then the linear head with numpy."""
+    xyz = P.xyz(b)
+    coarse = {tuple(v): i for i, v in enumerate(P.xyz(b - 1).tolist())}
+    par = np.array([coarse[tuple(v)] for v in (xyz >> 1).tolist()], dtype=np.int64)
+    pcode = P.codes(b - 1)[par].astype(np.int64)
+    x = np.zeros((len(xyz), 11))
+    for a in range(3):
+        x[:, a] = xyz[:, a] & 1
+    for j in range(8):
+        x[:, 3 + j] = (pcode >> j) & 1
+    h = x
+    for l in range(w["layers"]):
+        h = oracle.sparse_conv(xyz, b, h, w["conv_w"][l], w["conv_b"][l], True)
+    return h @ w["head_w"].astype(np.float64) + w["head_b"].astype(np.float64)
+
+
+@pytest.mark.parametrize("C,L", [(16, 2), (32, 3), (16, 4)])
+def test_model_layer_chain_equals_composition(scan_cache, C, L):
+    """Pins the layer loop of the plain model for L >= 2: a wrong layer-to-weight
+    index, a bias taken from another layer, or a broken C_in hand-over between
+    layers changes the logits far beyond the 1e-9 bound.  Biases are non-zero
+    and differ per layer so that each of them is exercised."""
+    c = CONFIGS[0]
+    P = oracle.Pyramid.from_points(scan_cache(0), c.bit_depth, c.min_bit_depth, c.range_m)
+    w = gen_weights(C, L, seed=31 + L, bias_std=0.2, head_scale=3.0)
+    for b in (c.min_bit_depth + 2, c.bit_depth - 1):
+        lg, lse, bits = P.model(b, w)
+        ref = _plain_model_by_composition(P, b, w)
+        np.testing.assert_allclose(lg, ref, rtol=0, atol=1e-9)
+        code = P.codes(b).astype(np.int64)
+        m = ref.max(1)
+        ref_lse = m + np.log(np.exp(ref - m[:, None]).sum(1))
+        np.testing.assert_allclose(lse, ref_lse, rtol=0, atol=1e-9)
+        np.testing.assert_allclose(bits, (ref_lse - ref[np.arange(len(code)), code]) / math.log(2),
+                                   rtol=0, atol=1e-9)
+
+
 # ---- P12: rANS ------------------------------------------------------------------------------
 
 def test_rans_round_trip_and_length():
