@@ -91,6 +91,18 @@ constexpr uint32_t LB_SPIN_LIMIT = 1u << 24;
 // instead of hanging.
 constexpr int LB_BATCH = 8;
 
+// An inclusive prefix beyond the 30-bit field (only reachable with corrupt
+// decoder codes on a context of more than 2^27 points) would spill into the
+// flag bits; it is published saturated and latches ERR_CAPACITY instead, so
+// the capacity checks downstream see a count above any context capacity.
+__device__ __forceinline__ uint32_t lb_saturate(uint32_t v, uint32_t* err) {
+  if (v > LB_VAL) {
+    latch(err, ERR_CAPACITY);
+    return LB_VAL;
+  }
+  return v;
+}
+
 __device__ __forceinline__ uint32_t lookback(uint32_t* status, int width, int tile, int c,
                                              uint32_t agg, uint32_t* err) {
   uint32_t* mine = status + (size_t)tile * width + c;
@@ -130,7 +142,7 @@ __device__ __forceinline__ uint32_t lookback(uint32_t* status, int width, int ti
       __builtin_amdgcn_s_sleep(1);
     }
   }
-  st_status(mine, LB_INC | (excl + agg));
+  st_status(mine, LB_INC | lb_saturate(excl + agg, err));
   return excl;
 }
 
@@ -173,7 +185,7 @@ __device__ __forceinline__ uint32_t lookback_wave(uint32_t* status, int tile, ui
       __builtin_amdgcn_s_sleep(1);
     }
   }
-  if (lane == 0) st_status(status + tile, LB_INC | (excl + agg));
+  if (lane == 0) st_status(status + tile, LB_INC | lb_saturate(excl + agg, err));
   return excl;
 }
 
