@@ -202,6 +202,40 @@ reno_status reno_set_base_frames(reno_ctx* ctx, int bit_depth, const int32_t* xy
  * RENO_E_INPUT. */
 reno_status reno_expand(reno_ctx* ctx, int scale, const uint8_t* codes);
 
+/* ALLOCATION-FREE FCG expansion, for callers that cannot allocate device
+ * memory: code under HIP graph capture, tight serving loops, harnesses that
+ * forbid hipMalloc.  The decoder step of reno_expand (same kernel) on plain
+ * arrays, without a context: each parent key in order emits 8*key + delta for
+ * every set bit delta of its code, in ascending delta.  Allocates nothing:
+ * its scratch (look-back status words, counters) is a static device array of
+ * (64 + RENO_NOALLOC_MAX_PARENTS / 512) * 4 bytes (256 KiB) that each device
+ * the library runs on holds until the process ends.
+ *   keys          [n] parent keys (Morton keys, optionally with frame bits above
+ *                 them), each below 2^61; their order is the output order
+ *   codes         [n] occupancy codes, each in [1, 255]
+ *   n             0 <= n <= RENO_NOALLOC_MAX_PARENTS
+ *   child_keys    [cap_children] out: the children's keys
+ *   child_parent  [cap_children] out: row of each child's parent in keys
+ *   cap_children  capacity of both child arrays, 0 <= cap_children < 2^31
+ *   first_child   [n] out, or NULL: row of each parent's first child
+ *   result        [2] int64 out: [0] children written (the total, clamped to
+ *                 cap_children), [1] RENO_OK, or RENO_E_CAPACITY when the
+ *                 children exceed cap_children, or RENO_E_INPUT for a zero code
+ *                 or a key of 2^61 or more (outputs then undefined)
+ *   hip_stream    stream of the current device (NULL: the null stream); every
+ *                 launch is enqueued there and the call returns without waiting
+ * All arrays are device pointers on the current device.  Argument errors
+ * return RENO_E_INVALID and launch errors RENO_E_HIP, with the message in
+ * reno_last_error(NULL) of the calling thread.  Every call on a device shares
+ * that device's scratch (cleared at the start of each call): calls that
+ * overlap on one device, on different streams, race and must be ordered by
+ * the caller. */
+#define RENO_NOALLOC_MAX_PARENTS (1 << 25)
+#define RENO_NOALLOC_MAX_DEVICES 64
+reno_status reno_expand_noalloc(const uint64_t* keys, const uint8_t* codes, int64_t n,
+                                uint64_t* child_keys, int32_t* child_parent, int64_t cap_children,
+                                int32_t* first_child, int64_t* result, void* hip_stream);
+
 /* Number of voxels of a scale (synchronises). */
 reno_status reno_num_voxels(reno_ctx* ctx, int scale, int64_t* n_host);
 /* N_b of every scale in one copy: counts_host[b] for b = 0 .. RENO_MAX_BIT_DEPTH

@@ -79,6 +79,7 @@ _SIGS = {
     "reno_build_pyramid_frames": (_int, [_vp, _vp, _i64, _vp, _int, _int]),
     "reno_set_base_frames": (_int, [_vp, _int, _vp, _vp, _vp, _i64, _int]),
     "reno_expand": (_int, [_vp, _int, _vp]),
+    "reno_expand_noalloc": (_int, [_vp, _vp, _i64, _vp, _vp, _i64, _vp, _vp, _vp]),
     "reno_num_voxels": (_int, [_vp, _int, ctypes.POINTER(_i64)]),
     "reno_scale_counts": (_int, [_vp, _vp]),
     "reno_coords": (_int, [_vp, _int, _vp, _vp]),
@@ -379,6 +380,30 @@ class Context:
         out = self._empty((max(n, 1), SYMBOLS), self.torch.int16)
         self._check(lib().reno_symbol_freqs(self._h, scale, _ptr(out)))
         return out[:n]
+
+
+RENO_NOALLOC_MAX_PARENTS = 1 << 25
+
+
+def expand_noalloc(keys, codes, child_keys, child_parent, result, first_child=None, stream=None):
+    """FCG expansion without a context and without device allocation
+    (reno_expand_noalloc): every argument is a caller-owned device tensor --
+    keys int64 [n], codes uint8 [n], child_keys int64 [cap], child_parent int32
+    [cap], result int64 [2] (children written, status), first_child int32 [n]
+    or None.  Enqueued on ``stream`` (default: torch's current stream)."""
+    import torch
+    n = int(keys.shape[0])
+    if int(codes.shape[0]) != n or (first_child is not None and int(first_child.shape[0]) < n):
+        raise ValueError("keys, codes and first_child must have n entries")
+    cap = min(int(child_keys.shape[0]), int(child_parent.shape[0]))
+    for t in (keys, codes, child_keys, child_parent, result) + ((first_child,) if first_child is not None else ()):
+        if not t.is_contiguous():
+            raise ValueError("arguments must be contiguous")
+    st = stream if stream is not None else torch.cuda.current_stream()
+    rc = lib().reno_expand_noalloc(_ptr(keys), _ptr(codes), n, _ptr(child_keys), _ptr(child_parent), cap,
+                                   _ptr(first_child), _ptr(result), ctypes.c_void_p(st.cuda_stream))
+    if rc != RENO_OK:
+        raise RenoError(rc, lib().reno_last_error(None).decode())
 
 
 def rans_encode(sym: np.ndarray, freq: np.ndarray) -> np.ndarray:

@@ -396,6 +396,21 @@ reno_status reno_expand(reno_ctx* c, int scale, const uint8_t* codes) {
   return RENO_OK;
 }
 
+reno_status reno_expand_noalloc(const uint64_t* keys, const uint8_t* codes, int64_t n,
+                                uint64_t* child_keys, int32_t* child_parent, int64_t cap_children,
+                                int32_t* first_child, int64_t* result, void* hip_stream) {
+  if (n < 0 || n > RENO_NOALLOC_MAX_PARENTS)
+    return fail(nullptr, RENO_E_INVALID, "n must be in [0, RENO_NOALLOC_MAX_PARENTS]");
+  if (cap_children < 0 || cap_children >= (int64_t(1) << 31))
+    return fail(nullptr, RENO_E_INVALID, "cap_children must be in [0, 2^31)");
+  if (!result) return fail(nullptr, RENO_E_INVALID, "null result");
+  if (n > 0 && (!keys || !codes)) return fail(nullptr, RENO_E_INVALID, "null input");
+  if (cap_children > 0 && (!child_keys || !child_parent)) return fail(nullptr, RENO_E_INVALID, "null output");
+  RENO_HIP(nullptr, reno::launch_expand_noalloc(keys, codes, n, child_keys, child_parent, cap_children,
+                                                first_child, result, static_cast<hipStream_t>(hip_stream)));
+  return RENO_OK;
+}
+
 reno_status reno_scale_counts(reno_ctx* c, int64_t* counts_host) {
   if (!c || !counts_host) return fail(c, RENO_E_INVALID, "null argument");
   RENO_HIP(c, hipMemcpyAsync(c->h_count, c->d_count, sizeof(int32_t) * reno::NLEV,

@@ -177,6 +177,9 @@ hipError_t launch_codes(Ctx& c, int B);
 hipError_t launch_set_base(Ctx& c, const int32_t* xyz, const int32_t* frame_of, const uint8_t* codes, int64_t n,
                            int B);
 hipError_t launch_expand(Ctx& c, int b, const uint8_t* codes, int B);
+hipError_t launch_expand_noalloc(const uint64_t* keys, const uint8_t* codes, int64_t n,
+                                 uint64_t* child_keys, int32_t* child_parent, int64_t cap_children,
+                                 int32_t* first_child, int64_t* result, hipStream_t stream);
 hipError_t launch_pack_weights(Ctx& c, const reno_weights& w);
 hipError_t launch_model(Ctx& c, int b_lo, int b_hi, float* logits, bool second);
 hipError_t launch_head2(Ctx& c, int b, const uint8_t* s1, float* logits2);

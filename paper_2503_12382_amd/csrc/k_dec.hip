@@ -4,6 +4,9 @@
 // children of a scale come out in ascending Morton order, identical to the
 // encoder's sorted scale, and are inserted into the coordinate hash.
 
+#include <algorithm>
+#include <mutex>
+
 #include "ctx.h"
 
 namespace reno {
@@ -65,10 +68,10 @@ struct ExpArgs {
   int64_t cap_model;
   const uint64_t* key_b;
   uint8_t* code_b;
-  int32_t* fc_b;
+  int32_t* fc_b;      // first-child row of each parent (or null)
   uint64_t* key_n;    // scale b+1
   int32_t* parent_n;
-  uint16_t* feat_n;
+  uint16_t* feat_n;   // layer-1 input word of each child (or null)
   int32_t* count;
   int32_t* moff;
   uint32_t* status;
@@ -76,6 +79,7 @@ struct ExpArgs {
   HashSlot* hash;
   int hash_lg;
   uint32_t* err;
+  int check_keys;     // latch ERR_KEY_RANGE for parent keys of 2^61 or more
 };
 
 __global__ void __launch_bounds__(EXP_THREADS) k_expand(ExpArgs a) {
@@ -118,6 +122,7 @@ __global__ void __launch_bounds__(EXP_THREADS) k_expand(ExpArgs a) {
       c = a.codes_in ? a.codes_in[p] : a.code_b[p];
       if (a.codes_in) a.code_b[p] = (uint8_t)c;
       if (c == 0u) latch(a.err, ERR_ZERO_CODE);
+      if (a.check_keys && (key[j] >> 61)) latch(a.err, ERR_KEY_RANGE);
     }
     code[j] = c;
     uint32_t x = (uint32_t)__popc(c);
@@ -166,7 +171,7 @@ __global__ void __launch_bounds__(EXP_THREADS) k_expand(ExpArgs a) {
     if (p >= np) continue;
     const uint32_t c = code[j];
     int64_t q = wbase + incl[j] - (uint32_t)__popc(c);
-    a.fc_b[p] = (int32_t)q;
+    if (a.fc_b) a.fc_b[p] = (int32_t)q;
     const uint64_t kp = key[j] << 3;
     for (uint32_t d = 0; d < 8; ++d) {
       if (!((c >> d) & 1u)) continue;
@@ -176,7 +181,7 @@ __global__ void __launch_bounds__(EXP_THREADS) k_expand(ExpArgs a) {
       }
       a.key_n[q] = kp | d;
       a.parent_n[q] = (int32_t)p;
-      a.feat_n[q] = (uint16_t)(d | (c << 3));
+      if (a.feat_n) a.feat_n[q] = (uint16_t)(d | (c << 3));
       ++q;
     }
   }
@@ -192,7 +197,100 @@ __global__ void __launch_bounds__(EXP_THREADS) k_expand(ExpArgs a) {
   }
 }
 
+// ---- FCG expansion without a context and without allocation ----
+// Scratch of reno_expand_noalloc, one copy per device for the life of the
+// process: NA_HEAD header words (parent count, child count, tile ticket, error
+// word) and one look-back status word per tile of EXP_TILE parents.  Host code
+// reaches it only through the address hipGetSymbolAddress returns for the
+// current device; calls that overlap on one device share it and race.
+constexpr int NA_HEAD = 64;
+constexpr int NA_COUNT = 0;   // int32 [2]: parents (scale "0"), children (scale "1")
+constexpr int NA_TICKET = 2;
+constexpr int NA_ERR = 3;
+constexpr int64_t NA_TILES = RENO_NOALLOC_MAX_PARENTS / EXP_TILE;
+static_assert(RENO_NOALLOC_MAX_PARENTS % EXP_TILE == 0, "whole tiles");
+static __device__ __align__(256) uint32_t scratch[NA_HEAD + NA_TILES];
+
+// Clears the header and the status words of the call's tiles (a fill kernel
+// rather than a memset, so that the call can be captured into a graph) and
+// records the parent count where k_expand reads it.
+__global__ void __launch_bounds__(256) k_noalloc_begin(uint32_t* s, int64_t n, int64_t words) {
+  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < words;
+       i += (int64_t)gridDim.x * blockDim.x)
+    s[i] = i == NA_COUNT ? (uint32_t)n : 0u;
+}
+
+// Child count and status of the call: result[0] = children written (clamped
+// to the capacity), result[1] = 0 or the reno_status of a data error.
+__global__ void k_noalloc_end(const uint32_t* s, int64_t* result) {
+  if (blockIdx.x != 0 || threadIdx.x != 0) return;
+  const uint32_t e = s[NA_ERR];
+  int64_t st = RENO_OK;
+  if (e & ERR_CAPACITY)
+    st = RENO_E_CAPACITY;
+  else if (e & (ERR_ZERO_CODE | ERR_KEY_RANGE))
+    st = RENO_E_INPUT;
+  else if (e)
+    st = RENO_E_HIP;   // a look-back wait ran out (never expected)
+  result[0] = (int64_t)(int32_t)s[NA_COUNT + 1];
+  result[1] = st;
+}
+
+std::mutex g_na_mu;
+uint32_t* g_na_ptr[RENO_NOALLOC_MAX_DEVICES] = {};
+
 }  // namespace
+
+hipError_t noalloc_scratch(uint32_t** out) {
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  if (dev < 0 || dev >= RENO_NOALLOC_MAX_DEVICES) return hipErrorInvalidDevice;
+  std::lock_guard<std::mutex> lock(g_na_mu);
+  if (!g_na_ptr[dev]) {
+    void* p = nullptr;
+    e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess) return e;
+    g_na_ptr[dev] = static_cast<uint32_t*>(p);
+  }
+  *out = g_na_ptr[dev];
+  return hipSuccess;
+}
+
+hipError_t launch_expand_noalloc(const uint64_t* keys, const uint8_t* codes, int64_t n,
+                                 uint64_t* child_keys, int32_t* child_parent, int64_t cap_children,
+                                 int32_t* first_child, int64_t* result, hipStream_t stream) {
+  uint32_t* s = nullptr;
+  hipError_t e = noalloc_scratch(&s);
+  if (e != hipSuccess) return e;
+  const int64_t ntiles = (n + EXP_TILE - 1) / EXP_TILE;
+  const int64_t words = NA_HEAD + ntiles;
+  hipLaunchKernelGGL(k_noalloc_begin, dim3((unsigned)std::min<int64_t>((words + 255) / 256, 1024)), dim3(256), 0, stream, s, n, words);
+  ExpArgs a;
+  a.codes_in = nullptr;                       // the codes are read, never written
+  a.b = 0;                                    // count[0]: parents, count[1]: children
+  a.B = 1;                                    // no next model scale: no hash inserts, no row offsets
+  a.fb = 0;
+  a.cap_pts = cap_children;
+  a.cap_model = 0;
+  a.key_b = keys;
+  a.code_b = const_cast<uint8_t*>(codes);
+  a.fc_b = first_child;
+  a.key_n = child_keys;
+  a.parent_n = child_parent;
+  a.feat_n = nullptr;
+  a.count = reinterpret_cast<int32_t*>(s + NA_COUNT);
+  a.moff = nullptr;                           // only touched when b + 1 < B
+  a.status = s + NA_HEAD;
+  a.ticket = s + NA_TICKET;
+  a.hash = nullptr;
+  a.hash_lg = 0;
+  a.err = s + NA_ERR;
+  a.check_keys = 1;
+  hipLaunchKernelGGL(k_expand, dim3((unsigned)(ntiles > 0 ? ntiles : 1)), dim3(EXP_THREADS), 0, stream, a);
+  hipLaunchKernelGGL(k_noalloc_end, dim3(1), dim3(64), 0, stream, s, result);
+  return hipGetLastError();
+}
 
 hipError_t launch_set_base(Ctx& c, const int32_t* xyz, const int32_t* frame_of, const uint8_t* codes, int64_t n,
                            int B) {
@@ -230,6 +328,7 @@ hipError_t launch_expand(Ctx& c, int b, const uint8_t* codes, int B) {
   a.hash = c.d_hash;
   a.hash_lg = c.hash_lg;
   a.err = c.d_err;
+  a.check_keys = 0;                           // context keys hold at most 3 * 20 + 10 bits
   hipLaunchKernelGGL(k_expand, dim3((unsigned)max_tiles), dim3(EXP_THREADS), 0, c.stream, a);
   return hipGetLastError();
 }

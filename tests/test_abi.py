@@ -25,7 +25,7 @@ def declared_functions():
 def test_header_and_binding_agree():
     decl = declared_functions()
     assert decl == set(reno._SIGS), decl ^ set(reno._SIGS)
-    assert len(decl) == 29
+    assert len(decl) == 30
 
 
 def _struct_fields(name):
@@ -115,3 +115,24 @@ def test_host_rans_empty_stream():
     words = reno.rans_encode(np.zeros(0, np.uint8), f)
     assert words.size == 2
     assert reno.rans_decode(words, f, 0).size == 0
+
+
+def test_expand_noalloc_rejects_bad_arguments_without_gpu():
+    """Argument checks of the allocation-free expansion come before any HIP call."""
+    L = reno.lib()
+    res = ctypes.c_void_p(16)            # never dereferenced: every case fails its checks first
+    one = ctypes.c_void_p(8)
+    cases = [
+        (one, one, reno.RENO_NOALLOC_MAX_PARENTS + 1, one, one, 8, None, res),   # too many parents
+        (one, one, -1, one, one, 8, None, res),                                  # negative count
+        (one, one, 4, one, one, 1 << 31, None, res),                             # capacity too large
+        (one, one, 4, one, one, -1, None, res),                                  # negative capacity
+        (one, one, 4, one, one, 8, None, None),                                  # no result array
+        (None, one, 4, one, one, 8, None, res),                                  # no keys
+        (one, None, 4, one, one, 8, None, res),                                  # no codes
+        (one, one, 4, None, one, 8, None, res),                                  # no child keys
+        (one, one, 4, one, None, 8, None, res),                                  # no child parents
+    ]
+    for args in cases:
+        assert L.reno_expand_noalloc(*args, None) == reno.RENO_E_INVALID, args
+        assert L.reno_last_error(None)
