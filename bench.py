@@ -31,7 +31,13 @@ PEAK_FP32_MFMA_TFLOPS = 157.3
 PEAK_BF16_MFMA_TFLOPS = 2500.0
 PEAK_HBM_GBS = 8000.0
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "conv_last_traffic_hdl64_b14.txt")
-MODEL_SRC = os.path.join(ROOT, "paper_2503_12382_amd", "csrc", "k_model.hip")
+TRACE_FILE = os.path.join(ROOT, "profiles", "conv_last_headline_trace_hdl64_b14.txt")
+MODEL_SRCS = [os.path.join(ROOT, "paper_2503_12382_amd", "csrc", f) for f in ("k_model.hip", "dev.h", "ctx.h")]
+# a neighbour-map row as the method defines it: 27 int32 entries (the stored
+# rows are padded to 32 for alignment; the padding is not algorithmic traffic)
+MAP_ROW_BYTES = 4 * 27
+# interleaved rANS streams per scale (and stage) in the end-to-end coder
+RANS_STREAMS = 16
 
 
 def alg_bytes_per_frame(counts, b0, B, M, C, hash_slots, status_words):
@@ -59,8 +65,8 @@ def alg_bytes_per_frame(counts, b0, B, M, C, hash_slots, status_words):
         16 * parents_hashed
     # conv layers (encoder + decoder): first reads keys, parent slots and feature
     # words, writes the neighbour map and h; later layers read map + h, write h
-    first = sum(N[b] * (8 + 2 + 4 * 32 + row) + 16 * N[b - 1] for b in model)
-    mid = nm * (4 * 32 + 2 * row)
+    first = sum(N[b] * (8 + 2 + MAP_ROW_BYTES + row) + 16 * N[b - 1] for b in model)
+    mid = nm * (MAP_ROW_BYTES + 2 * row)
     out["conv_first"] = 2 * first
     out["conv_mid"] = 2 * mid
     out["conv_last"] = 2 * (mid + nm * 4)
@@ -85,29 +91,93 @@ def alg_bytes_encoder(counts, b0, B, M, C, hash_slots, status_words, fb):
         "sort": M * 16,
         "pyramid": M * 8 + sum(N[b] * 12 for b in range(b0, B + 1)) + sum(N[b] * 4 for b in range(b0, B)),
         "codes": sum(N[b + 1] * (8 + 2) + N[b] for b in range(b0, B)) + 16 * parents_hashed,
-        "conv_first": sum(N[b] * (8 + 2 + 4 * 32 + row) + 16 * N[b - 1] for b in model),
-        "conv_mid": nm * (4 * 32 + 2 * row),
-        "conv_last": nm * (4 * 32 + 2 * row) + nm * 4,
+        "conv_first": sum(N[b] * (8 + 2 + MAP_ROW_BYTES + row) + 16 * N[b - 1] for b in model),
+        "conv_mid": nm * (MAP_ROW_BYTES + 2 * row),
+        "conv_last": nm * (MAP_ROW_BYTES + 2 * row) + nm * 4,
         "code_length": nm * (1 + 4 + row),
     }
 
 
-def read_traffic(workload):
-    """HBM traffic of conv_last per launch from the committed rocprofv3 PMC
-    summary, or None when the kernel source changed since it was taken or the
-    summary is of another workload."""
+def model_source_hash():
+    """sha256 prefix of the sources the conv kernels are built from (the
+    launcher declarations of ctx.h, which other files' changes add to, are
+    left out)."""
     import hashlib
-    if not os.path.exists(TRAFFIC_FILE):
+    h = hashlib.sha256()
+    for f in MODEL_SRCS:
+        text = open(f, "rb").read()
+        if f.endswith("ctx.h"):
+            text = text.split(b"\nhipError_t launch_", 1)[0]
+        h.update(text)
+    return h.hexdigest()[:16]
+
+
+def read_profile_kv(path, workload):
+    """key = value lines of a committed rocprofv3 summary, or None when the
+    kernel sources changed since it was taken or it covers another workload."""
+    if not os.path.exists(path):
         return None
     kv = {}
-    for line in open(TRAFFIC_FILE):
+    for line in open(path):
         if "=" in line and not line.startswith("#"):
             k, v = line.split("=", 1)
             kv[k.strip()] = v.strip()
-    src = hashlib.sha256(open(MODEL_SRC, "rb").read()).hexdigest()[:16]
-    if kv.get("k_model_sha256_16") != src or kv.get("workload") != workload:
+    if kv.get("model_sources_sha256_16") != model_source_hash() or kv.get("workload") != workload:
         return None
-    return float(kv["bytes_per_launch"])
+    return kv
+
+
+def read_traffic(workload):
+    """HBM traffic of conv_last per launch from the committed rocprofv3 PMC
+    summary (FETCH_SIZE and WRITE_SIZE runs scaled by a copy kernel's counts),
+    or None when it is stale."""
+    kv = read_profile_kv(TRAFFIC_FILE, workload)
+    return None if kv is None else float(kv["bytes_per_launch"])
+
+
+def read_trace(workload):
+    """conv_last's average dispatch duration (us) and dispatch count from the
+    committed rocprofv3 kernel trace of this bench's headline run alone
+    (--headline-only), or None when it is stale."""
+    kv = read_profile_kv(TRACE_FILE, workload)
+    return None if kv is None else (float(kv["avg_us"]), int(kv["dispatches"]))
+
+
+def measure_copy_peak(torch, dev, stream, mib=2048, reps=20):
+    """Device-to-device copy bandwidth (GB/s counting the bytes read and the
+    bytes written), the measured stand-in for the HBM peak beside the nominal
+    8 TB/s."""
+    n = mib << 20
+    src = torch.empty(n, dtype=torch.uint8, device=dev)
+    dst = torch.empty(n, dtype=torch.uint8, device=dev)
+    src.fill_(1)
+    with torch.cuda.stream(stream):
+        for _ in range(3):
+            dst.copy_(src)
+        t0 = torch.cuda.Event(enable_timing=True)
+        t1 = torch.cuda.Event(enable_timing=True)
+        t0.record(stream)
+        for _ in range(reps):
+            dst.copy_(src)
+        t1.record(stream)
+    stream.synchronize()
+    gbs = 2.0 * n * reps / (t0.elapsed_time(t1) * 1e-3) / 1e9
+    del src, dst
+    torch.cuda.empty_cache()
+    return gbs
+
+
+def host_info():
+    """Core count and CPU model of the host the oracle baseline runs on."""
+    model = None
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                model = line.split(":", 1)[1].strip()
+                break
+    except OSError:
+        pass
+    return {"nproc": os.cpu_count(), "affinity_cpus": len(os.sched_getaffinity(0)), "cpu_model": model}
 
 
 def oracle_frame(args):
@@ -239,6 +309,21 @@ class Codec:
         self.check("after the timed steps:")  # the last replayed frame is consistent
         return t0.elapsed_time(t1) / steps
 
+    def frame_times(self, frames):
+        """Milliseconds of each of `frames` single graph replays (one frame
+        encoded + decoded each), every replay bracketed by its own HIP events."""
+        torch, stream = self.torch, self.stream
+        ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+              for _ in range(frames)]
+        with torch.cuda.stream(stream):
+            for a, b in ev:
+                a.record(stream)
+                self.graph.replay()
+                b.record(stream)
+        stream.synchronize()
+        self.check("after the per-frame timing:")
+        return [a.elapsed_time(b) for a, b in ev]
+
     def time_sides(self, steps):
         """(encoder ms, decoder ms) per frame, each side captured as its own
         HIP graph and replayed `steps` times."""
@@ -267,8 +352,10 @@ class Codec:
         return tuple(out)
 
     def profile_conv_last(self, steps):
-        """(total ms, launches) of conv_last over `steps` eager steps, each launch
-        bracketed by HIP events on the context stream."""
+        """(total ms, launches) of conv_last over `steps` eager steps: the
+        library launches each timed conv kernel with two HIP events bound to
+        its dispatch (hipExtLaunchKernelGGL), so each interval is the kernel's
+        execution on the context stream."""
         with self.torch.cuda.stream(self.stream):
             self.enc.profile(["conv_last"])
             self.dec.profile(["conv_last"])
@@ -294,12 +381,12 @@ class Codec:
 
 class EndToEnd:
     """True end-to-end coding of one frame: GPU pyramid + model, the symbol
-    intervals (encoder) or tables (decoder) copied to pinned host memory, and
-    host rANS with one stream per scale (and per stage with the two-stage
-    head); the decoder decodes each scale's symbols before it expands them."""
+    intervals (encoder) or cumulative tables (decoder) copied to pinned host
+    memory, and host rANS with each scale (and each stage of the two-stage
+    head) split into interleaved streams coded on the library's host threads;
+    the decoder decodes each scale's symbols before it expands them."""
 
-    def __init__(self, reno, torch, cfg, pts, M, cap_model, stream, w_np, two_stage, threads=8):
-        from concurrent.futures import ThreadPoolExecutor
+    def __init__(self, reno, torch, cfg, pts, M, cap_model, stream, w_np, two_stage):
         self.reno, self.torch, self.stream, self.two = reno, torch, stream, two_stage
         self.B, self.b0 = cfg.bit_depth, cfg.min_bit_depth
         wd = reno.weights_to_device(w_np)
@@ -323,10 +410,11 @@ class EndToEnd:
         self.iv_host = torch.empty((cap_model, per), dtype=torch.int16, pin_memory=True)
         k = 16 if two_stage else 256
         self.tab_host = torch.empty((M, k), dtype=torch.int16, pin_memory=True)
+        self.tab_dev = torch.empty((M, k), dtype=torch.int16, device=pts.device)
         self.code_host = torch.empty(M, dtype=torch.uint8, pin_memory=True)
+        self.s1_host = torch.empty(M, dtype=torch.uint8, pin_memory=True)
         # decoded codes of consecutive scales alternate between two buffers; S1 has its own
         self.code_dev = [torch.empty(M, dtype=torch.uint8, device=pts.device) for _ in range(3)]
-        self.pool = ThreadPoolExecutor(threads)
 
     def encode(self):
         """-> (bitstream dict, N_b per scale, base xyz, base codes)."""
@@ -355,8 +443,8 @@ class EndToEnd:
             else:
                 jobs.append((b, 0, rows, 2, 0))
             off += counts[b]
-        words = dict(zip([(j[0], j[1]) for j in jobs],
-                         self.pool.map(lambda j: reno.rans_encode_intervals(j[2], j[3], j[4]), jobs)))
+        # each scale (and stage) as RANS_STREAMS interleaved streams coded on the library's host threads
+        words = {(j[0], j[1]): reno.rans_encode_streams(j[2], RANS_STREAMS, j[3], j[4]) for j in jobs}
         return words, counts, base_xyz, base_codes
 
     def decode(self, words, counts, base_xyz, base_codes):
@@ -372,26 +460,29 @@ class EndToEnd:
                 n = int(counts[b])
                 dec.expand(b - 1, prev)
                 dec.predict_probs(b)
+                # cumulative tables from the GPU; each scale's interleaved
+                # streams decoded on the library's host threads
                 if self.two:
-                    t1 = dec.symbol_freqs16(b, 1)
+                    t1 = dec.symbol_cdf(b, 1, out=self.tab_dev)
                     self.tab_host[:n].copy_(t1, non_blocking=True)
                     self.stream.synchronize()
-                    s1 = reno.rans_decode(words[(b, 0)], self.tab_host[:n].numpy().view(np.uint16), n)
-                    self.code_host[:n].copy_(torch.from_numpy(s1))
+                    s1 = reno.rans_decode_streams(*words[(b, 0)], self.tab_host[:n].numpy().view(np.uint16), n,
+                                                  out=self.s1_host[:n].numpy())
                     s1_dev = self.code_dev[2][:n]
-                    s1_dev.copy_(self.code_host[:n], non_blocking=True)
+                    s1_dev.copy_(self.s1_host[:n], non_blocking=True)
                     dec.predict_second(b, s1_dev)
-                    t2 = dec.symbol_freqs16(b, 2)
+                    t2 = dec.symbol_cdf(b, 2, out=self.tab_dev)
                     self.tab_host[:n].copy_(t2, non_blocking=True)
                     self.stream.synchronize()
-                    s2 = reno.rans_decode(words[(b, 1)], self.tab_host[:n].numpy().view(np.uint16), n)
-                    codes = s1 | (s2 << 4)
+                    s2 = reno.rans_decode_streams(*words[(b, 1)], self.tab_host[:n].numpy().view(np.uint16), n,
+                                                  out=self.code_host[:n].numpy())
+                    np.bitwise_or(s1, s2 << 4, out=s2)
                 else:
-                    t = dec.symbol_freqs(b)
+                    t = dec.symbol_cdf(b, 0, out=self.tab_dev)
                     self.tab_host[:n].copy_(t, non_blocking=True)
                     self.stream.synchronize()
-                    codes = reno.rans_decode(words[(b, 0)], self.tab_host[:n].numpy().view(np.uint16), n)
-                self.code_host[:n].copy_(torch.from_numpy(codes))
+                    reno.rans_decode_streams(*words[(b, 0)], self.tab_host[:n].numpy().view(np.uint16), n,
+                                             out=self.code_host[:n].numpy())
                 cd = self.code_dev[b & 1][:n]
                 cd.copy_(self.code_host[:n], non_blocking=True)
                 prev = cd
@@ -420,16 +511,15 @@ class EndToEnd:
                 if not same:
                     log("end-to-end: decoded frame differs from the input")
                     sys.exit(1)
-            bits = 32 + int(counts[self.b0]) * (3 * self.b0 + 8) + sum(32 * w.size for w in words.values())
+            bits = 32 + int(counts[self.b0]) * (3 * self.b0 + 8) + sum(32 * w[0].size for w in words.values())
         return te / frames, td / frames, bits
 
     def close(self):
-        self.pool.shutdown()
         self.enc.close()
         self.dec.close()
 
 
-def run_stress(args, reno, torch, dev, stream):
+def run_stress(args, reno, torch, dev, stream, copy_peak=None):
     """HBM stress: K frames of the streaming generator (its distinct frames,
     cycled) batched into one key space, frame id above the Morton bits; one
     encoder pass (pyramid, all model scales, code lengths) per batch, every
@@ -503,11 +593,15 @@ def run_stress(args, reno, torch, dev, stream):
                 gbs = alg[k] / (us * 1e-6) / 1e9
                 e.update({"alg_MB": round(alg[k] / 1e6, 2), "alg_GBs": round(gbs, 1),
                           "hbm_frac": round(gbs / PEAK_HBM_GBS, 4)})
+                if copy_peak:
+                    e["hbm_frac_of_copy"] = round(gbs / copy_peak, 4)
             if k == "sort":  # every LSD pass reads and writes each key once
                 passes = (3 * sB + fb + 7) // 8
                 pgbs = passes * alg[k] / (us * 1e-6) / 1e9
                 e.update({"passes": passes, "pass_MB": round(passes * alg[k] / 1e6, 2),
                           "pass_GBs": round(pgbs, 1), "pass_hbm_frac": round(pgbs / PEAK_HBM_GBS, 4)})
+                if copy_peak:
+                    e["pass_hbm_frac_of_copy"] = round(pgbs / copy_peak, 4)
             kinds_out[k] = e
         run = {"K": K, "points": SM, "voxels": int(sum(cnt)), "model_rows_capacity": cap,
                "device_bytes": smem["device_bytes"], "encoder_ms_per_batch": round(ms, 4),
@@ -519,7 +613,7 @@ def run_stress(args, reno, torch, dev, stream):
         del pts_d, st_d
         torch.cuda.empty_cache()
     stress["note"] = ("hbm_frac = algorithmic bytes (each input read once, each output written once) / "
-                      "kernel time / 8 TB/s; sort = all LSD passes (pass_* count every pass's read + write), "
+                      "kernel time / 8 TB/s (hbm_frac_of_copy: / the measured device copy rate); sort = all LSD passes (pass_* count every pass's read + write), "
                       "codes = code words + hash build, conv_first = hash probes + first-layer gather, "
                       "conv_mid = neighbour-row gather")
 
@@ -550,6 +644,9 @@ def main():
                     help="stream counts for the multi-frame measurement ('' to skip)")
     ap.add_argument("--cpu-workers", type=int, default=0,
                     help="processes for the all-cores oracle baseline (0: the CPUs this process may use, at most 16)")
+    ap.add_argument("--headline-only", action="store_true",
+                    help="only the headline timed region (warm-up, graph capture, timed replays): the run "
+                         "whose rocprofv3 kernel trace gives conv_last's per-dispatch duration")
     ap.add_argument("--calib-copy", action="store_true",
                     help="run one 256 MiB device-to-device copy first (counter calibration for PMC runs)")
     args = ap.parse_args()
@@ -580,7 +677,9 @@ def main():
             torch.mul(src, 1.0, out=dst)
             torch.cuda.synchronize()
             del src, dst
-        print(json.dumps({"hbm_stress": run_stress(args, reno, torch, dev, stream)}), flush=True)
+        cp = measure_copy_peak(torch, dev, stream)
+        print(json.dumps({"hbm_copy_peak_GBs": round(cp, 1),
+                          "hbm_stress": run_stress(args, reno, torch, dev, stream, cp)}), flush=True)
         return
     if args.calib_copy:
         # plain kernels of known traffic: a fill (256 MiB written), then an
@@ -609,6 +708,17 @@ def main():
     ms_step = one.time(args.steps, args.warmup, args.mode)
     fps = 1000.0 / ms_step
     log(f"{args.mode}: {ms_step * 1000:.1f} us/frame, {fps:.1f} frames/s")
+    if args.headline_only:
+        print(json.dumps({"metric": "frames/s (headline timed region only)", "value": round(fps, 2),
+                          "unit": "frames/s", "ms_per_step": round(ms_step, 5), "steps": args.steps,
+                          "warmup": args.warmup, "mode": args.mode, "workload": cfg.name,
+                          "conv_last_launches_per_frame": 1 + (B - b0 - 1)}), flush=True)
+        one.close()
+        return
+    per_frame = one.frame_times(50) if args.mode == "graph" else None
+    if per_frame:
+        med = float(np.median(per_frame))
+        log(f"per-frame graph replays: median {med * 1000:.1f} us over {len(per_frame)} frames")
     enc_ms, dec_ms = one.time_sides(args.steps) if args.mode == "graph" else (None, None)
     if enc_ms is not None:
         log(f"encode {enc_ms * 1000:.1f} us, decode {dec_ms * 1000:.1f} us per frame")
@@ -630,6 +740,8 @@ def main():
         dec.profile([])
     mem = enc.memory_info()
     alg = alg_bytes_per_frame(counts, b0, B, M, C, mem["hash_slots"], mem["status_words"])
+    copy_peak = measure_copy_peak(torch, dev, stream)
+    log(f"measured device copy: {copy_peak:.0f} GB/s (read + write)")
     breakdown = {}
     for k in kinds:
         ms = be.get(k, (0.0, 0))[0] + bd.get(k, (0.0, 0))[0]
@@ -640,7 +752,8 @@ def main():
             if k in alg:
                 gbs = alg[k] / (us * 1e-6) / 1e9
                 breakdown[k].update({"alg_bytes_per_frame": alg[k], "alg_GBs": round(gbs, 1),
-                                     "hbm_frac": round(gbs / PEAK_HBM_GBS, 4)})
+                                     "hbm_frac": round(gbs / PEAK_HBM_GBS, 4),
+                                     "hbm_frac_of_copy": round(gbs / copy_peak, 4)})
 
     # ---- the bitwise two-stage head (the paper's default head), same frame ----
     two = None
@@ -758,9 +871,10 @@ def main():
             log("end-to-end", name, e2e[name])
             ee.close()
         e2e["note"] = ("wall-clock per frame: points copied in from pinned host memory, GPU pyramid + model + "
-                       "symbol intervals (encoder) or tables (decoder), pinned copies out, host rANS with one "
-                       "stream per scale (and stage), base voxels out and back in; the decoder decodes each "
-                       "scale before expanding it; encoder streams coded on 8 host threads")
+                       "symbol intervals (encoder) or cumulative tables (decoder), pinned copies out, host rANS "
+                       f"with each scale (and stage) as {RANS_STREAMS} interleaved streams, coded and decoded on the "
+                       "library's host threads (the decoder from GPU cumulative tables), base voxels out and "
+                       "back in; the decoder decodes each scale before expanding it")
 
     # ---- multi-frame throughput: F different frames, each with its own encoder
     # and decoder context and captured step, replayed round-robin over S
@@ -846,7 +960,7 @@ def main():
         del codecs
 
     # ---- HBM stress: K frames of the streaming generator in one key space ----
-    stress = run_stress(args, reno, torch, dev, stream) if args.stress else None
+    stress = run_stress(args, reno, torch, dev, stream, copy_peak) if args.stress else None
 
     # ---- CPU baseline: the oracle (single-threaded C++, fp64), one frame per
     # process, first alone, then one process per available core at once ----
@@ -866,7 +980,7 @@ def main():
             log("oracle runs disagree")
             sys.exit(1)
         cpu = {"value": round(workers / wall, 4), "unit": "frames/s", "cores": workers,
-               "kind": "oracle",
+               "kind": "oracle", "host": host_info(),
                "sample": f"{workers} copies of one {cfg.name} frame ({M} points), one process per core, "
                          f"{wall:.1f} s wall; each: oracle encode (pyramid, codes, model, bits) + decode "
                          f"(FCG expansion, model, bits) in single-threaded C++ fp64",
@@ -876,6 +990,11 @@ def main():
 
     voxels_frame = sum(counts)
     traffic = read_traffic(cfg.name)
+    trace = read_trace(cfg.name)
+    flops_launch = one.conv_last_flops(counts) / (cl_launches / args.steps)
+    frac_trace = None
+    if trace is not None:
+        frac_trace = round(flops_launch / (trace[0] * 1e-6) / 1e12 / PEAK_FP32_MFMA_TFLOPS, 4)
     out = {
         "metric": "frames/s + Mvoxels/s, encode+decode model path, 14-bit 64-beam scan; bits/pt",
         "value": round(fps, 2),
@@ -907,7 +1026,15 @@ def main():
                      "unit": "TFLOP/s", "frac": round(achieved_tflops / PEAK_FP32_MFMA_TFLOPS, 4),
                      "traffic": traffic,
                      "avg_launch_us": round(1000 * cl_ms / cl_launches, 2),
-                     "launches": cl_launches},
+                     "launches": cl_launches,
+                     "flops_per_launch": round(flops_launch),
+                     "timing": "HIP events bound to each conv_last dispatch (hipExtLaunchKernelGGL), eager steps",
+                     "trace_avg_launch_us": None if trace is None else trace[0],
+                     "trace_dispatches": None if trace is None else trace[1],
+                     "frac_trace": frac_trace},
+        "hbm_copy_peak_GBs": round(copy_peak, 1),
+        "median_ms_per_frame": None if not per_frame else round(float(np.median(per_frame)), 5),
+        "median_frames_per_s": None if not per_frame else round(1000.0 / float(np.median(per_frame)), 2),
         "cpu_baseline": cpu,
         "kernels": breakdown,
         "two_stage_head": two,

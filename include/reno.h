@@ -307,6 +307,13 @@ reno_status reno_symbol_freqs16(reno_ctx* ctx, int scale, int stage, uint16_t* f
  * then S2 in the stage-2 table).  Needs the codes and predict_probs (and
  * stage 2).  RENO_ALL_SCALES: every model scale, concatenated in order. */
 reno_status reno_symbol_intervals(reno_ctx* ctx, int scale, uint16_t* iv);
+/* Decoder side in cumulative form: for each voxel of the scale the start of
+ * every symbol in its table (start_s = sum of f_t for t < s, so start_0 = 0 and
+ * f_s = start_{s+1} - start_s with start_K = 2^16), uint16 [N_scale][256] for
+ * the one-stage head (stage 0), [N_scale][16] for stage 1 or 2 of the
+ * two-stage head; the same tables as reno_symbol_freqs(16), summed on the
+ * device.  Preconditions as for those calls. */
+reno_status reno_symbol_cdf(reno_ctx* ctx, int scale, int stage, uint16_t* start);
 
 /* Host rANS coder (Duda, arXiv:1311.2540) for one scale's stream; HOST
  * pointers.  64-bit state in [2^31, 2^63), 32-bit renormalisation words.
@@ -326,10 +333,30 @@ reno_status reno_rans_decode16(const uint32_t* in, int64_t nwords, const uint16_
 reno_status reno_rans_decode(const uint32_t* in, int64_t nwords, const uint16_t* freq, int64_t n,
                              uint8_t* sym);
 
+/* Interleaved multi-stream form of the same coder (host memory), for coding
+ * one scale on several host threads: symbol i goes to stream i mod S (S =
+ * nstreams, 1 .. RENO_RANS_MAX_STREAMS), and each stream is exactly the
+ * single-stream coding of its symbols (the format of reno_rans_encode).
+ * encode: intervals as reno_rans_encode_intervals; the S streams are written
+ * back to back to out (at most cap words in all) and their word counts to
+ * nwords_host [S].  decode: the S streams back to back in `in` with their
+ * counts, and the cumulative tables start [n][k] (k = 256 or 16, from
+ * reno_symbol_cdf) instead of frequencies, so that no table is summed on the
+ * host; writes sym [n].  threads = host threads to use (0: up to 16 of the
+ * available cores); the threads belong to a pool the library keeps for the
+ * life of the process.  Errors as for the single-stream calls. */
+#define RENO_RANS_MAX_STREAMS 256
+reno_status reno_rans_encode_streams(const uint16_t* iv, int64_t n, int64_t stride, int nstreams, int threads,
+                                     uint32_t* out, int64_t cap, int64_t* nwords_host);
+reno_status reno_rans_decode_streams(const uint32_t* in, const int64_t* nwords_host, int nstreams, int threads,
+                                     const uint16_t* start, int k, int64_t n, uint8_t* sym);
+
 /* Kernel timing for measurement.  While a kind's bit is set in `kind_mask`,
  * every launch of that kind is bracketed by two HIP events recorded on the
  * context stream (event pairs come from a pool created by this call; launches
- * beyond the pool are not timed).  reno_profile resets the accumulators;
+ * beyond the pool are not timed); the plain model's conv launches take the
+ * two events as their own dispatch start and end (hipExtLaunchKernelGGL), so
+ * those intervals are kernel execution alone.  reno_profile resets the accumulators;
  * reno_profile_read synchronises and returns, per kind, the summed
  * event-to-event milliseconds and the number of timed launches (arrays of
  * RENO_K_COUNT).  Launches captured into a HIP graph are not timed. */

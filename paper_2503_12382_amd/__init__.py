@@ -92,10 +92,13 @@ _SIGS = {
     "reno_symbol_freqs": (_int, [_vp, _int, _vp]),
     "reno_symbol_freqs16": (_int, [_vp, _int, _int, _vp]),
     "reno_symbol_intervals": (_int, [_vp, _int, _vp]),
+    "reno_symbol_cdf": (_int, [_vp, _int, _int, _vp]),
     "reno_rans_encode_intervals": (_int, [_vp, _i64, _i64, _vp, _i64, ctypes.POINTER(_i64)]),
     "reno_rans_decode16": (_int, [_vp, _i64, _vp, _i64, _vp]),
     "reno_rans_encode": (_int, [_vp, _vp, _i64, _vp, _i64, ctypes.POINTER(_i64)]),
     "reno_rans_decode": (_int, [_vp, _i64, _vp, _i64, _vp]),
+    "reno_rans_encode_streams": (_int, [_vp, _i64, _i64, _int, _int, _vp, _i64, _vp]),
+    "reno_rans_decode_streams": (_int, [_vp, _vp, _int, _int, _vp, _int, _i64, _vp]),
     "reno_profile": (_int, [_vp, ctypes.c_uint32]),
     "reno_profile_read": (_int, [_vp, _vp, _vp]),
 }
@@ -375,6 +378,17 @@ class Context:
         self._check(lib().reno_symbol_intervals(self._h, scale, _ptr(out)))
         return out[:n]
 
+    def symbol_cdf(self, scale: int, stage: int = 0, out=None):
+        """Cumulative tables (start of every symbol): int16-typed uint16
+        [N][256] (one-stage head, stage 0) or [N][16] (two-stage head, stage 1
+        or 2).  ``out`` may be a preallocated device tensor."""
+        n = self.num_voxels(scale)
+        k = 16 if stage else SYMBOLS
+        if out is None:
+            out = self._empty((max(n, 1), k), self.torch.int16)
+        self._check(lib().reno_symbol_cdf(self._h, scale, stage, _ptr(out)))
+        return out[:n]
+
     def symbol_freqs(self, scale: int):
         n = self.num_voxels(scale)
         out = self._empty((max(n, 1), SYMBOLS), self.torch.int16)
@@ -447,6 +461,41 @@ def rans_encode_intervals(iv: np.ndarray, stride: int = 2, offset: int = 0) -> n
     if rc != RENO_OK:
         raise RenoError(rc, "rANS encode failed")
     return out[:nw.value].copy()
+
+
+RENO_RANS_MAX_STREAMS = 256
+
+
+def rans_encode_streams(iv: np.ndarray, nstreams: int, stride: int = 2, offset: int = 0, threads: int = 0):
+    """Interleaved multi-stream rANS encode from (start, freq) intervals (host
+    memory, layout as rans_encode_intervals): symbol i goes to stream i mod S.
+    Returns (words of all streams back to back, word count of each stream)."""
+    a = np.ascontiguousarray(iv, dtype=np.uint16).reshape(-1)
+    n = (a.size - offset - 2) // stride + 1 if a.size >= offset + 2 else 0
+    cap = n + 16 * nstreams
+    out = np.empty(cap, dtype=np.uint32)
+    counts = np.zeros(nstreams, dtype=np.int64)
+    rc = lib().reno_rans_encode_streams(a[offset:].ctypes.data_as(_vp), n, stride, nstreams, threads,
+                                        out.ctypes.data_as(_vp), cap, counts.ctypes.data_as(_vp))
+    if rc != RENO_OK:
+        raise RenoError(rc, "rANS multi-stream encode failed")
+    return out[:int(counts.sum())].copy(), counts
+
+
+def rans_decode_streams(words: np.ndarray, counts: np.ndarray, start: np.ndarray, n: int, threads: int = 0,
+                        out: np.ndarray | None = None) -> np.ndarray:
+    """Decodes S interleaved streams (words back to back, counts [S]) with
+    cumulative tables start [n][k] (k = 256 or 16) into n symbols."""
+    w = np.ascontiguousarray(words, dtype=np.uint32)
+    c = np.ascontiguousarray(counts, dtype=np.int64)
+    st = np.ascontiguousarray(start, dtype=np.uint16)
+    k = st.shape[1] if st.ndim == 2 else SYMBOLS
+    sym = out if out is not None else np.empty(n, dtype=np.uint8)
+    rc = lib().reno_rans_decode_streams(w.ctypes.data_as(_vp), c.ctypes.data_as(_vp), c.size, threads,
+                                        st.ctypes.data_as(_vp), k, n, sym.ctypes.data_as(_vp))
+    if rc != RENO_OK:
+        raise RenoError(rc, "rANS multi-stream decode failed")
+    return sym
 
 
 def weights_to_device(w: dict, device="cuda") -> dict:

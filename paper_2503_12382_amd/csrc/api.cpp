@@ -565,6 +565,19 @@ reno_status reno_symbol_freqs16(reno_ctx* c, int scale, int stage, uint16_t* fre
   return RENO_OK;
 }
 
+reno_status reno_symbol_cdf(reno_ctx* c, int scale, int stage, uint16_t* start) {
+  if (!c || !start) return fail(c, RENO_E_INVALID, "null argument");
+  if (!model_scale(c, scale)) return fail(c, RENO_E_INVALID, "not a model scale");
+  const bool two = c->p.head_mode == RENO_HEAD_TWO_STAGE;
+  if (two ? (stage != 1 && stage != 2) : stage != 0)
+    return fail(c, RENO_E_INVALID, two ? "stage must be 1 or 2 with the two-stage head"
+                                       : "stage must be 0 with the one-stage head");
+  if (!has(stage == 2 ? c->have_pred2 : c->have_pred, scale))
+    return fail(c, RENO_E_STATE, stage == 2 ? "stage 2 of the scale not run" : "predict_probs of the scale not run");
+  RENO_HIP(c, reno::launch_symbol_cdf(*c, scale, stage, start));
+  return RENO_OK;
+}
+
 reno_status reno_symbol_intervals(reno_ctx* c, int scale, uint16_t* iv) {
   if (!c || !iv) return fail(c, RENO_E_INVALID, "null argument");
   if (c->B == 0) return fail(c, RENO_E_STATE, "no frame");

@@ -3,6 +3,7 @@
 // launchers.
 #pragma once
 
+#include <hip/hip_ext.h>
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
@@ -120,6 +121,9 @@ struct Ctx {
   std::vector<hipEvent_t> prof_pool;
   size_t prof_used = 0;
   std::vector<ProfRec> prof_recs;
+  // events a timed conv launch binds to its dispatch (hipExtLaunchKernelGGL),
+  // set by a dispatch-bound ProfScope and consumed by that launch
+  hipEvent_t ext_start = nullptr, ext_stop = nullptr;
 
   int64_t pyr_tiles = 0;    // max tiles of the pyramid pass
   int64_t exp_tiles = 0;    // max tiles of one expansion
@@ -154,16 +158,33 @@ struct Ctx {
 struct ProfScope {
   Ctx& c;
   int kind;
-  hipEvent_t end = nullptr;
-  ProfScope(Ctx& ctx, int k) : c(ctx), kind(k) {
+  bool bound;
+  hipEvent_t start = nullptr, end = nullptr;
+  // bound = the scope holds exactly one kernel launch, which takes the two
+  // events as its dispatch start / end timestamps (hipExtLaunchKernelGGL):
+  // the interval is then the kernel's execution, without the launch gap or
+  // the inter-kernel barrier that events recorded between launches include
+  ProfScope(Ctx& ctx, int k, bool bind = false) : c(ctx), kind(k), bound(bind) {
     if (!((c.prof_mask >> kind) & 1u) || c.prof_used + 2 > c.prof_pool.size()) return;
-    hipEvent_t a = c.prof_pool[c.prof_used++];
+    start = c.prof_pool[c.prof_used++];
     end = c.prof_pool[c.prof_used++];
-    (void)hipEventRecord(a, c.stream);
-    c.prof_recs.push_back(ProfRec{kind, a, end});
+    if (bound) {
+      c.ext_start = start;
+      c.ext_stop = end;
+    } else {
+      (void)hipEventRecord(start, c.stream);
+    }
+    c.prof_recs.push_back(ProfRec{kind, start, end});
   }
   ~ProfScope() {
-    if (end) (void)hipEventRecord(end, c.stream);
+    if (!end) return;
+    if (!bound) {
+      (void)hipEventRecord(end, c.stream);
+    } else if (c.ext_start == start) {  // no launch took the events: an empty interval
+      (void)hipEventRecord(start, c.stream);
+      (void)hipEventRecord(end, c.stream);
+    }
+    if (bound) c.ext_start = c.ext_stop = nullptr;
   }
 };
 
@@ -187,6 +208,7 @@ hipError_t launch_code_length(Ctx& c, int b_lo, int b_hi, float* bits);
 hipError_t launch_symbol_freqs(Ctx& c, int b, uint16_t* freq);
 hipError_t launch_symbol_freqs16(Ctx& c, int b, int stage, uint16_t* freq);
 hipError_t launch_symbol_intervals(Ctx& c, int b_lo, int b_hi, uint16_t* iv);
+hipError_t launch_symbol_cdf(Ctx& c, int b, int stage, uint16_t* start);
 hipError_t launch_coords(Ctx& c, int b, int32_t* xyz, uint64_t* keys);
 hipError_t launch_copy_level_u8(Ctx& c, int b, uint8_t* out);
 hipError_t launch_copy_level_i32(Ctx& c, int b, const int32_t* src, int32_t* out);

@@ -1667,7 +1667,13 @@ __global__ void __launch_bounds__((headw_threads<C, TWO>())) k_headw(ConvArgs a)
 template <int C, bool FIRST, bool LAST, bool TWO, bool BF>
 hipError_t run_conv(Ctx& c, const ConvArgs& a) {
   // one block per CU stages the weights once for its 16 waves
-  hipLaunchKernelGGL((k_conv<C, FIRST, LAST, TWO, BF>), dim3(256), dim3(CONV_THREADS), 0, c.stream, a);
+  if (c.ext_start) {  // timed: the events are the dispatch's own start and end
+    hipExtLaunchKernelGGL((k_conv<C, FIRST, LAST, TWO, BF>), dim3(256), dim3(CONV_THREADS), 0, c.stream,
+                          c.ext_start, c.ext_stop, 0u, a);
+    c.ext_start = c.ext_stop = nullptr;
+  } else {
+    hipLaunchKernelGGL((k_conv<C, FIRST, LAST, TWO, BF>), dim3(256), dim3(CONV_THREADS), 0, c.stream, a);
+  }
   return hipGetLastError();
 }
 
@@ -2036,7 +2042,7 @@ hipError_t launch_model(Ctx& c, int b_lo, int b_hi, float* logits, bool second) 
     a.bias = c.w_bias[l];
     a.logits = (l == L - 1) ? logits : nullptr;
     const bool first = l == 0, last = l == L - 1;
-    ProfScope ps_(c, last ? RENO_K_CONV_LAST : (first ? RENO_K_CONV_FIRST : RENO_K_CONV_MID));
+    ProfScope ps_(c, last ? RENO_K_CONV_LAST : (first ? RENO_K_CONV_FIRST : RENO_K_CONV_MID), true);
     if (c.p.precision == RENO_PREC_BF16X3)
       e = (c.p.channels == 32) ? run_layer<32, true>(c, first, last, two, a)
                                : run_layer<16, true>(c, first, last, two, a);

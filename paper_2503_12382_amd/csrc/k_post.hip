@@ -261,6 +261,65 @@ __global__ void __launch_bounds__(256) k_symbol_freqs(const int32_t* __restrict_
   }
 }
 
+// One-stage cumulative tables [N][256]: the start of every symbol in the
+// voxel's table (exclusive prefix of the frequencies), one wavefront per voxel.
+__global__ void __launch_bounds__(256) k_symbol_cdf(const int32_t* __restrict__ count,
+                                                    const int32_t* __restrict__ moff, int b,
+                                                    int64_t cap_model,
+                                                    const float* __restrict__ hL, int C,
+                                                    const float* __restrict__ H,
+                                                    const float* __restrict__ hb,
+                                                    const float* __restrict__ lse,
+                                                    uint16_t* __restrict__ out) {
+  const int lane = threadIdx.x & 63;
+  const int64_t mo = moff[b];
+  int64_t n = count[b];
+  if (mo + n > cap_model) n = 0;
+  const int64_t wstride = (int64_t)gridDim.x * (blockDim.x / 64);
+  for (int64_t v = (int64_t)blockIdx.x * (blockDim.x / 64) + (threadIdx.x >> 6); v < n; v += wstride) {
+    uint32_t f[4];
+    table256(hL + (mo + v) * C, lse[mo + v], H, hb, C, lane, f);
+    const uint32_t mine = f[0] + f[1] + f[2] + f[3];
+    uint32_t inc = mine;
+    for (int d = 1; d < 64; d <<= 1) {
+      const uint32_t t = (uint32_t)__shfl_up((int)inc, d);
+      if (lane >= d) inc += t;
+    }
+    uint32_t st = inc - mine;
+    uint16_t* dst = out + v * 256 + lane * 4;
+    for (int e = 0; e < 4; ++e) {
+      dst[e] = (uint16_t)st;
+      st += f[e];
+    }
+  }
+}
+
+// Two-stage cumulative tables [N][16] of one scale and stage: 4 voxels per
+// wavefront, the same tables as k_symbol_freqs16 summed over the 16 lanes.
+__global__ void __launch_bounds__(256) k_symbol_cdf16(const int32_t* __restrict__ count,
+                                                      const int32_t* __restrict__ moff, int b, int stage,
+                                                      int64_t cap_model, const float* __restrict__ hL, int C,
+                                                      const float* __restrict__ Hp, const float* __restrict__ hb,
+                                                      const float* __restrict__ emb, const uint8_t* __restrict__ s1,
+                                                      const float* __restrict__ lse, const float* __restrict__ lse2,
+                                                      uint16_t* __restrict__ out) {
+  const int s = threadIdx.x & 15;
+  const int64_t mo = moff[b];
+  int64_t n = count[b];
+  if (mo + n > cap_model) n = 0;
+  const int64_t gstride = (int64_t)gridDim.x * (blockDim.x / 16);
+  for (int64_t v0 = (int64_t)blockIdx.x * (blockDim.x / 16); v0 < n; v0 += gstride) {
+    // the whole wavefront runs the shuffles; lanes past the last voxel write nothing
+    const int64_t v = v0 + (threadIdx.x >> 4);
+    const int64_t pr = mo + (v < n ? v : n - 1);
+    const float* h = hL + pr * C;
+    const uint32_t f = stage == 1 ? table16(h, nullptr, lse[pr], Hp, 0, hb, C, s)
+                                  : table16(h, emb + (int)s1[pr] * C, lse2[pr], Hp, 16, hb, C, s);
+    const uint32_t st = excl16(f, s);
+    if (v < n) out[v * 16 + s] = (uint16_t)st;
+  }
+}
+
 // One-stage encoder intervals [N][2] = (start, freq) of O_b[v] in its table.
 __global__ void __launch_bounds__(256) k_symbol_intervals(const int32_t* __restrict__ count,
                                                           const int32_t* __restrict__ moff, int b, int b_lo,
@@ -454,6 +513,19 @@ hipError_t launch_symbol_freqs16(Ctx& c, int b, int stage, uint16_t* freq) {
   hipLaunchKernelGGL(k_symbol_freqs16, dim3(grid_for(c.cap_pts, 16)), dim3(256), 0, c.stream,
                      c.d_count, c.d_moff, b, stage, c.cap_model, c.hlast(), c.p.channels, c.w_head_plain,
                      c.w_hbias, c.w_emb, c.d_s1, c.d_lse, c.d_lse2, freq);
+  return hipGetLastError();
+}
+
+hipError_t launch_symbol_cdf(Ctx& c, int b, int stage, uint16_t* start) {
+  ProfScope ps_(c, RENO_K_OTHER);
+  if (stage == 0)
+    hipLaunchKernelGGL(k_symbol_cdf, dim3(grid_for(c.cap_pts, 4)), dim3(256), 0, c.stream,
+                       c.d_count, c.d_moff, b, c.cap_model, c.hlast(), c.p.channels, c.w_head_plain,
+                       c.w_hbias, c.d_lse, start);
+  else
+    hipLaunchKernelGGL(k_symbol_cdf16, dim3(grid_for(c.cap_pts, 16)), dim3(256), 0, c.stream,
+                       c.d_count, c.d_moff, b, stage, c.cap_model, c.hlast(), c.p.channels, c.w_head_plain,
+                       c.w_hbias, c.w_emb, c.d_s1, c.d_lse, c.d_lse2, start);
   return hipGetLastError();
 }
 

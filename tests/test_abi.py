@@ -25,7 +25,7 @@ def declared_functions():
 def test_header_and_binding_agree():
     decl = declared_functions()
     assert decl == set(reno._SIGS), decl ^ set(reno._SIGS)
-    assert len(decl) == 30
+    assert len(decl) == 33
 
 
 def _struct_fields(name):
@@ -136,3 +136,67 @@ def test_expand_noalloc_rejects_bad_arguments_without_gpu():
     for args in cases:
         assert L.reno_expand_noalloc(*args, None) == reno.RENO_E_INVALID, args
         assert L.reno_last_error(None)
+
+
+def _intervals_and_starts(f, sym):
+    """(start, freq) of each symbol and the cumulative tables of f."""
+    start = np.zeros_like(f, dtype=np.int64)
+    start[:, 1:] = np.cumsum(f[:, :-1].astype(np.int64), axis=1)
+    n = len(sym)
+    iv = np.stack([start[np.arange(n), sym], f[np.arange(n), sym].astype(np.int64)], 1).astype(np.uint16)
+    return iv, start.astype(np.uint16)
+
+
+@pytest.mark.parametrize("nstreams,threads", [(1, 1), (7, 3), (16, 0), (64, 16)])
+def test_host_rans_streams_are_single_streams_and_round_trip(nstreams, threads):
+    """Stream j of the interleaved coder is exactly the single-stream coding of
+    symbols j, j + S, ...: word for word equal to the CPU oracle's independent
+    rANS write-up of that subsequence; the threaded decoder with cumulative
+    tables restores every symbol."""
+    import oracle
+    rs = np.random.default_rng(40 + nstreams)
+    n = 5000
+    p, f = _random_tables(rs, n, peaked=True)
+    sym = np.array([rs.choice(256, p=pi) for pi in p], dtype=np.uint8)
+    iv, start = _intervals_and_starts(f, sym)
+    words, counts = reno.rans_encode_streams(iv, nstreams, threads=threads)
+    assert counts.size == nstreams and words.size == counts.sum()
+    off = np.concatenate([[0], np.cumsum(counts)])
+    for j in range(nstreams):
+        ref = oracle.rans_encode(sym[j::nstreams], f[j::nstreams].astype(np.uint32))
+        np.testing.assert_array_equal(words[off[j]:off[j + 1]], ref, err_msg=f"stream {j}")
+    dec = reno.rans_decode_streams(words, counts, start, n, threads=threads)
+    np.testing.assert_array_equal(dec, sym)
+
+
+def test_host_rans_streams_16_symbol_tables_and_errors():
+    rs = np.random.default_rng(44)
+    n, S = 3001, 8
+    logits = rs.normal(size=(n, 16)) * 3
+    pr = np.exp(logits - logits.max(1, keepdims=True))
+    pr /= pr.sum(1, keepdims=True)
+    f = 1 + np.floor(pr.astype(np.float32) * np.float32(65504)).astype(np.int64)
+    f[np.arange(n), f.argmax(1)] += 65536 - f.sum(1)
+    f = f.astype(np.uint16)
+    sym = np.array([rs.choice(16, p=pi) for pi in pr], dtype=np.uint8)
+    iv, start = _intervals_and_starts(f, sym)
+    words, counts = reno.rans_encode_streams(iv, S)
+    assert np.array_equal(reno.rans_decode_streams(words, counts, start, n), sym)
+    single = reno.rans_decode(reno.rans_encode_intervals(iv), f, n)     # the single-stream coder agrees
+    assert np.array_equal(single, sym)
+    with pytest.raises(reno.RenoError):                                   # a stream cut short
+        bad = counts.copy()
+        bad[3] -= 1
+        reno.rans_decode_streams(np.delete(words, counts[:3].sum()), bad, start, n)
+    with pytest.raises(reno.RenoError):                                   # a table that does not start at 0
+        s2 = start.copy()
+        s2[10, 0] = 1
+        reno.rans_decode_streams(words, counts, s2, n)
+    with pytest.raises(reno.RenoError):                                   # an empty interval
+        iv2 = iv.copy()
+        iv2[5, 1] = 0
+        reno.rans_encode_streams(iv2, S)
+    # fewer symbols than streams: the empty streams hold the two flush words
+    w2, c2 = reno.rans_encode_streams(iv[:3], S)
+    assert list(c2[3:]) == [2] * (S - 3)
+    assert np.array_equal(reno.rans_decode_streams(w2, c2, start[:3], 3), sym[:3])

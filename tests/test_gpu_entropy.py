@@ -135,3 +135,57 @@ def test_round_trip_per_scale_streams(ci, two, scan_cache):
     assert dtotal == ideal
     enc.close()
     dec.close()
+
+
+@pytest.mark.parametrize("ci,two", [(0, False), (0, True), (2, False), (2, True)])
+def test_cdf_tables_and_multi_stream_round_trip(ci, two, scan_cache):
+    """Cumulative tables (reno_symbol_cdf) are the exclusive prefix sums of
+    the frequency tables, entry for entry; the frame round-trips through
+    interleaved multi-stream rANS decoded on host threads from those tables
+    (16 streams per scale and stage), up to the full 14-bit scan."""
+    cfg, pts, w, wd, enc, P = _setup(ci, two, scan_cache)
+    b0, B = cfg.min_bit_depth, cfg.bit_depth
+    S = 16
+    say("cdf + multi-stream round trip", cfg.name, "two-stage" if two else "one-stage")
+    iv = enc.symbol_intervals(reno.RENO_ALL_SCALES).cpu().numpy().view(np.uint16)
+    streams, off = {}, 0
+    for b in range(b0 + 1, B):
+        n = enc.num_voxels(b)
+        rows = iv[off:off + n]
+        if two:
+            streams[b] = (reno.rans_encode_streams(rows, S, 4, 0), reno.rans_encode_streams(rows, S, 4, 2))
+        else:
+            streams[b] = (reno.rans_encode_streams(rows, S, 2, 0),)
+        off += n
+    truth = {b: enc.occupancy_codes(b).cpu().numpy() for b in range(b0, B)}
+    base_xyz, _ = enc.coords(b0)
+    base_codes = enc.occupancy_codes(b0)
+    dec = reno.Context(len(pts), B, b0, cfg.range_m, cfg.channels, cfg.layers, two_stage=two)
+    dec.set_weights(wd)
+    dec.set_base(B, base_xyz.clone(), base_codes.clone())
+    prev = None
+    for b in range(b0 + 1, B):
+        dec.expand(b - 1, prev)
+        dec.predict_probs(b)
+        n = dec.num_voxels(b)
+        stages = (1, 2) if two else (0,)
+        sym = []
+        for i, st in enumerate(stages):
+            if st == 2:
+                dec.predict_second(b, to_dev(sym[0]))
+            cdf = dec.symbol_cdf(b, st).cpu().numpy().view(np.uint16)
+            f = (dec.symbol_freqs16(b, st) if two else dec.symbol_freqs(b)).cpu().numpy().view(np.uint16)
+            want = (np.cumsum(f.astype(np.int64), 1) - f).astype(np.uint16)
+            np.testing.assert_array_equal(cdf, want, err_msg=f"cdf b={b} stage={st}")
+            words, counts = streams[b][i]
+            sym.append(reno.rans_decode_streams(words, counts, cdf, n))
+        codes = sym[0] if not two else (sym[0] | (sym[1] << 4)).astype(np.uint8)
+        assert np.array_equal(codes, truth[b]), b
+        prev = to_dev(codes)
+    dec.expand(B - 1, prev)
+    assert torch.equal(dec.coords(B)[1], enc.coords(B)[1])
+    # wrong stage for the head is rejected
+    with pytest.raises(reno.RenoError):
+        dec.symbol_cdf(B - 1, 0 if two else 1)
+    enc.close()
+    dec.close()
