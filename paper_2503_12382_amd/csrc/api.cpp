@@ -51,7 +51,7 @@ uint32_t bits_range(int lo, int hi) {  // bits lo..hi inclusive
 void free_all(Ctx* c) {
   void* ptrs[] = {c->keys_a,  c->keys_b,    c->lv_key,   c->lv_code,  c->lv_parent, c->lv_fc,
                   c->lv_feat, c->d_count,   c->d_moff,   c->d_err,    c->d_hist,    c->d_ticket,
-                  c->d_status, c->d_hash,   c->h_a,      c->h_b,      c->d_nbr,     c->d_lse,
+                  c->d_status, c->d_hash,   c->d_hreg,   c->h_a,      c->h_b,      c->d_nbr,     c->d_lse,
                   c->d_partial, c->d_total, c->w_head,   c->w_hbias,  c->w_head_plain,
                   c->d_lse2,    c->w_emb,   c->d_s1,     c->w_head_t, c->d_perm,
                   c->h_c,       c->h_d,     c->w_embo,   c->w_embd};
@@ -200,6 +200,7 @@ reno_status reno_create(const reno_params* p, void* hip_stream, reno_ctx** out) 
   A(dalloc(&c->d_ticket, reno::TICKETS, &c->device_bytes));
   A(dalloc(&c->d_status, (size_t)c->status_words, &c->device_bytes));
   A(dalloc(&c->d_hash, size_t(1) << c->hash_lg, &c->device_bytes));
+  A(dalloc(&c->d_hreg, (size_t)RENO_MAX_FRAMES + 1, &c->device_bytes));
   const bool top = c->top();
   const size_t rows = (size_t)c->cap_rows();  // row cap_model stays zero
   A(dalloc(&c->h_a, rows * C, &c->device_bytes));

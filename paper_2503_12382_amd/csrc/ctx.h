@@ -76,6 +76,7 @@ struct Ctx {
   uint32_t* d_ticket = nullptr; // [TICKETS]
   uint32_t* d_status = nullptr; // look-back status words
   HashSlot* d_hash = nullptr;   // [1 << hash_lg]
+  uint64_t* d_hreg = nullptr;   // [RENO_MAX_FRAMES + 1] hash region starts of a frame batch
 
   // model buffers (packed model rows: scale b at d_moff[b] ..)
   float* h_a = nullptr;         // [cap_rows][C]
@@ -115,6 +116,8 @@ struct Ctx {
   int64_t npoints = 0;
   int frames = 1;               // frames batched in this frame's keys
   int fbits = 0;                // frame-id bits above the Morton bits (ceil(log2(frames)))
+  // hash region table of the current frame batch, null for a single frame
+  const uint64_t* hreg() const { return frames > 1 ? d_hreg : nullptr; }
 
   // kernel timing (reno_profile)
   uint32_t prof_mask = 0;

@@ -215,15 +215,33 @@ __device__ __forceinline__ uint64_t morton_part(uint64_t key, int b) {
 }
 __device__ __forceinline__ uint64_t frame_part(uint64_t key, int b) { return b >= 21 ? 0ull : key >> (3 * b); }
 
-__device__ __forceinline__ uint32_t hash_home(uint64_t tk, int lg) {
-  return (uint32_t)((tk * 0x9E3779B97F4A7C15ull) >> (64 - lg));
+// Home slots of a frame: a frame batch gives each frame its own region
+// [base, base + size) of the table (sized by the frame's share of the batch),
+// so that the inserts and probes of the frames in flight stay within a few
+// regions instead of the whole table; probing still runs on linearly through
+// the whole table, so a region that fills up spills into the next one.  A
+// single frame's region is the whole table.
+struct HashReg {
+  uint64_t base, size;
+};
+
+// Region of frame f from the table of region starts (null: one frame).
+__device__ __forceinline__ HashReg hash_region(const uint64_t* reg, int lg, uint64_t f) {
+  if (!reg) return HashReg{0ull, 1ull << lg};
+  return HashReg{reg[f], reg[f + 1] - reg[f]};
+}
+
+// Multiplicative hash scaled to the region: base + floor(mix * size / 2^64)
+// (for the whole table, the top lg bits of the product).
+__device__ __forceinline__ uint32_t hash_home(uint64_t tk, const HashReg& r) {
+  return (uint32_t)(r.base + __umul64hi(tk * 0x9E3779B97F4A7C15ull, r.size));
 }
 
 // Inserts tagged key -> (first, code) with linear probing (64-bit CAS on the key).
-__device__ __forceinline__ void hash_insert(HashSlot* tab, int lg, uint64_t tk, int32_t first,
-                                            uint32_t code, uint32_t* err) {
+__device__ __forceinline__ void hash_insert(HashSlot* tab, int lg, const HashReg& reg, uint64_t tk,
+                                            int32_t first, uint32_t code, uint32_t* err) {
   const uint32_t mask = (1u << lg) - 1u;
-  uint32_t h = hash_home(tk, lg);
+  uint32_t h = hash_home(tk, reg) & mask;
   for (uint32_t step = 0; step <= mask; ++step) {
     unsigned long long prev = atomicCAS(&tab[h].key, 0ull, (unsigned long long)tk);
     if (prev == 0ull) {
@@ -242,9 +260,9 @@ __device__ __forceinline__ void hash_insert(HashSlot* tab, int lg, uint64_t tk, 
 
 // (first, code) of a tagged key; code 0 (no children) when absent.  The
 // table was built by an earlier kernel.
-__device__ __forceinline__ uint2 hash_find(const HashSlot* tab, int lg, uint64_t tk) {
+__device__ __forceinline__ uint2 hash_find(const HashSlot* tab, int lg, const HashReg& reg, uint64_t tk) {
   const uint32_t mask = (1u << lg) - 1u;
-  uint32_t h = hash_home(tk, lg);
+  uint32_t h = hash_home(tk, reg) & mask;
   for (uint32_t step = 0; step <= mask; ++step) {
     const uint4 s = *reinterpret_cast<const uint4*>(&tab[h]);
     const uint64_t k = ((uint64_t)s.y << 32) | s.x;
@@ -255,16 +273,17 @@ __device__ __forceinline__ uint2 hash_find(const HashSlot* tab, int lg, uint64_t
   return make_uint2(0u, 0u);
 }
 
-// N lookups at once (tk == 0: no query, result code 0): the home slots of all
-// queries are loaded together, so a lane pays one memory round trip unless a
-// query lands on a slot holding another key.
+// N lookups at once, all of one frame (tk == 0: no query, result code 0): the
+// home slots of all queries are loaded together, so a lane pays one memory
+// round trip unless a query lands on a slot holding another key.
 template <int N>
-__device__ __forceinline__ void hash_find_n(const HashSlot* tab, int lg, const uint64_t* tk,
+__device__ __forceinline__ void hash_find_n(const HashSlot* tab, int lg, const HashReg& reg, const uint64_t* tk,
                                             uint2* out) {
+  const uint32_t mask = (1u << lg) - 1u;
   uint4 s[N];
 #pragma unroll
   for (int j = 0; j < N; ++j)
-    s[j] = *reinterpret_cast<const uint4*>(&tab[hash_home(tk[j] ? tk[j] : 1ull, lg)]);
+    s[j] = *reinterpret_cast<const uint4*>(&tab[hash_home(tk[j] ? tk[j] : 1ull, reg) & mask]);
 #pragma unroll
   for (int j = 0; j < N; ++j) {
     const uint64_t k = ((uint64_t)s[j].y << 32) | s[j].x;
@@ -273,7 +292,7 @@ __device__ __forceinline__ void hash_find_n(const HashSlot* tab, int lg, const u
     if (k == tk[j])
       out[j] = make_uint2(s[j].z, s[j].w);
     else if (k != 0ull)  // collision: continue linear probing from the home slot
-      out[j] = hash_find(tab, lg, tk[j]);
+      out[j] = hash_find(tab, lg, reg, tk[j]);
   }
 }
 

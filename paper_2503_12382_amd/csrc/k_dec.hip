@@ -20,11 +20,27 @@ __global__ void __launch_bounds__(256) k_set_base(const int32_t* __restrict__ xy
                                                   int b0, uint64_t* __restrict__ key,
                                                   uint8_t* __restrict__ code,
                                                   int32_t* __restrict__ parent, int32_t* count,
-                                                  int32_t* moff, uint32_t* err) {
+                                                  int32_t* moff, uint64_t* __restrict__ hreg, int hash_lg,
+                                                  uint32_t* err) {
   const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   if (i == 0) {
     count[b0] = (int32_t)n;
     moff[b0 + 1] = 0;
+  }
+  // hash regions of a frame batch in proportion to each frame's base voxels:
+  // the thread of the first voxel of a frame (ids ascending; out-of-range ids
+  // clamped, they are latched below) writes the starts of the frames since
+  // the previous voxel's frame
+  if (frame_of && i <= n) {
+    const uint64_t T = 1ull << hash_lg;
+    auto fid = [&](int64_t j) {
+      const int32_t f = frame_of[j];
+      return f < 0 ? 0 : (f >= frames ? frames - 1 : f);
+    };
+    const int f_hi = i < n ? fid(i) : frames;            // frames f_lo+1 .. f_hi start at voxel i
+    const int f_lo = i > 0 ? fid(i - 1) : -1;
+    const uint64_t st = n > 0 ? (uint64_t)i * T / (uint64_t)n : 0ull;
+    for (int f = f_lo + 1; f <= f_hi; ++f) hreg[f] = f == frames ? T : st;
   }
   if (i >= n) return;
   const int32_t lim = 1 << b0;
@@ -78,6 +94,7 @@ struct ExpArgs {
   uint32_t* ticket;
   HashSlot* hash;
   int hash_lg;
+  const uint64_t* hreg;  // hash region starts of a frame batch (null: one frame)
   uint32_t* err;
   int check_keys;     // latch ERR_KEY_RANGE for parent keys of 2^61 or more
 };
@@ -193,7 +210,8 @@ __global__ void __launch_bounds__(EXP_THREADS) k_expand(ExpArgs a) {
     const int64_t p = base + (int64_t)w * 64 * EXP_KPT + j * 64 + lane;
     if (p >= np) continue;
     const int64_t q = wbase + incl[j] - (uint32_t)__popc(code[j]);
-    hash_insert(a.hash, a.hash_lg, tag_key(key[j], a.b, a.fb), (int32_t)q, code[j], a.err);
+    hash_insert(a.hash, a.hash_lg, hash_region(a.hreg, a.hash_lg, frame_part(key[j], a.b)),
+                tag_key(key[j], a.b, a.fb), (int32_t)q, code[j], a.err);
   }
 }
 
@@ -285,6 +303,7 @@ hipError_t launch_expand_noalloc(const uint64_t* keys, const uint8_t* codes, int
   a.ticket = s + NA_TICKET;
   a.hash = nullptr;
   a.hash_lg = 0;
+  a.hreg = nullptr;
   a.err = s + NA_ERR;
   a.check_keys = 1;
   hipLaunchKernelGGL(k_expand, dim3((unsigned)(ntiles > 0 ? ntiles : 1)), dim3(EXP_THREADS), 0, stream, a);
@@ -297,11 +316,11 @@ hipError_t launch_set_base(Ctx& c, const int32_t* xyz, const int32_t* frame_of, 
   ProfScope ps_(c, RENO_K_SET_BASE);
   (void)B;
   const int b0 = c.b0();
-  int64_t blocks = (n + 255) / 256;
+  int64_t blocks = (n + 1 + 255) / 256;   // thread n closes the hash region table
   if (blocks < 1) blocks = 1;
   hipLaunchKernelGGL(k_set_base, dim3((unsigned)blocks), dim3(256), 0, c.stream, xyz, frame_of, c.frames, codes, n, b0,
                      c.lv_key + c.lv(b0), c.lv_code + c.lv(b0), c.lv_parent + c.lv(b0), c.d_count,
-                     c.d_moff, c.d_err);
+                     c.d_moff, c.d_hreg, c.hash_lg, c.d_err);
   return hipGetLastError();
 }
 
@@ -327,6 +346,7 @@ hipError_t launch_expand(Ctx& c, int b, const uint8_t* codes, int B) {
   a.ticket = c.d_ticket + TK_EXPAND + b;
   a.hash = c.d_hash;
   a.hash_lg = c.hash_lg;
+  a.hreg = c.hreg();
   a.err = c.d_err;
   a.check_keys = 0;                           // context keys hold at most 3 * 20 + 10 bits
   hipLaunchKernelGGL(k_expand, dim3((unsigned)max_tiles), dim3(EXP_THREADS), 0, c.stream, a);

@@ -269,6 +269,7 @@ struct ConvArgs {
   const uint16_t* lv_feat;
   const HashSlot* hash;
   int hash_lg;
+  const uint64_t* hreg;   // hash region starts of a frame batch (null: one frame)
   int32_t* nbr;           // [cap_model][NBR_STRIDE], entries 27.. are -1
   const float* h_in;      // [cap_model + 1][C_in], row cap_model all zero (unused by layer 1)
   int64_t zero_feat;      // index of a zero entry of lv_feat
@@ -387,7 +388,8 @@ struct Staged {
 // par is the 8-entry LDS slot of voxel r (shared by the 4 lanes of r); the
 // lane ends with the rows of offsets 8g .. 8g+7 (-1: absent or off-grid).
 __device__ __forceinline__ void parent_cell_rows(uint64_t kf, int b, int g, const HashSlot* __restrict__ hash,
-                                                 int hash_lg, int fb, volatile uint64_t* par, int32_t (&nb)[8]) {
+                                                 int hash_lg, const uint64_t* __restrict__ hreg, int fb,
+                                                 volatile uint64_t* par, int32_t (&nb)[8]) {
   const uint64_t key = morton_part(kf, b), fr = frame_part(kf, b) << (3 * (b - 1));
   const int x = (int)compact3(key), y = (int)compact3(key >> 1), z = (int)compact3(key >> 2);
   const int px = x >> 1, py = y >> 1, pz = z >> 1;
@@ -403,7 +405,7 @@ __device__ __forceinline__ void parent_cell_rows(uint64_t kf, int b, int g, cons
                 : 0ull;
   }
   uint2 hit[2];
-  hash_find_n<2>(hash, hash_lg, tk, hit);
+  hash_find_n<2>(hash, hash_lg, hash_region(hreg, hash_lg, frame_part(kf, b)), tk, hit);
   // cross-lane exchange through LDS (volatile: every read goes to LDS)
   par[2 * g] = ((uint64_t)hit[0].y << 32) | hit[0].x;
   par[2 * g + 1] = ((uint64_t)hit[1].y << 32) | hit[1].x;
@@ -686,7 +688,7 @@ __global__ void __launch_bounds__(CONV_THREADS) k_conv(ConvArgs a) {
     int4 nlo, nhi;
     if (FIRST) {
       int32_t nb[8];
-      parent_cell_rows(a.lv_key[lvb + (prow - mo)], b, g, a.hash, a.hash_lg, a.fb, s_par[w][r], nb);
+      parent_cell_rows(a.lv_key[lvb + (prow - mo)], b, g, a.hash, a.hash_lg, a.hreg, a.fb, s_par[w][r], nb);
       nlo = make_int4(nb[0], nb[1], nb[2], nb[3]);
       nhi = make_int4(nb[4], nb[5], nb[6], nb[7]);
       if (valid && grp <= 0) {  // one wave of a quad stores the map rows
@@ -1180,7 +1182,8 @@ template <int C>
 __global__ void __launch_bounds__(256) k_top_prep(int lo, int nsc, int n_embed, int b0, RowMap rm,
                                                   const uint64_t* __restrict__ lv_key,
                                                   const uint8_t* __restrict__ lv_code, int64_t cap_pts,
-                                                  const HashSlot* __restrict__ hash, int hash_lg, int fb,
+                                                  const HashSlot* __restrict__ hash, int hash_lg,
+                                                  const uint64_t* __restrict__ hreg, int fb,
                                                   const float* __restrict__ emb_o, int32_t* __restrict__ nbr,
                                                   float* __restrict__ X) {
   constexpr int Q = C / 16;  // f4 per lane of a row
@@ -1216,7 +1219,7 @@ __global__ void __launch_bounds__(256) k_top_prep(int lo, int nsc, int n_embed, 
     if (b == rm.b_ext)
       base_cell_rows(lv_key[lvb + vr], b, g, lv_key + lvb, n, nb);
     else
-      parent_cell_rows(lv_key[lvb + vr], b, g, hash, hash_lg, fb, s_par[w][r], nb);
+      parent_cell_rows(lv_key[lvb + vr], b, g, hash, hash_lg, hreg, fb, s_par[w][r], nb);
     if (valid) {
       int4* dst = reinterpret_cast<int4*>(nbr + (mo + vr) * NBR_STRIDE + 8 * g);
       dst[0] = make_int4(nb[0], nb[1], nb[2], nb[3]);
@@ -1243,7 +1246,8 @@ __global__ void __launch_bounds__(256) k_top_prep(int lo, int nsc, int n_embed, 
 // k = (dx+2) + 5(dy+2) + 25(dz+2) (125 .. 127 padding; -1: absent or
 // off-grid).
 __device__ __forceinline__ void parent_cell_rows5(uint64_t kf, int b, int g, const HashSlot* __restrict__ hash,
-                                                  int hash_lg, int fb, volatile uint64_t* par, int32_t (&nb)[32]) {
+                                                  int hash_lg, const uint64_t* __restrict__ hreg, int fb,
+                                                  volatile uint64_t* par, int32_t (&nb)[32]) {
   const uint64_t key = morton_part(kf, b), fr = frame_part(kf, b) << (3 * (b - 1));
   const int x = (int)compact3(key), y = (int)compact3(key >> 1), z = (int)compact3(key >> 2);
   const int px = x >> 1, py = y >> 1, pz = z >> 1;
@@ -1258,7 +1262,7 @@ __device__ __forceinline__ void parent_cell_rows5(uint64_t kf, int b, int g, con
                 : 0ull;
   }
   uint2 hit[7];
-  hash_find_n<7>(hash, hash_lg, tk, hit);
+  hash_find_n<7>(hash, hash_lg, hash_region(hreg, hash_lg, frame_part(kf, b)), tk, hit);
 #pragma unroll
   for (int i = 0; i < 7; ++i)
     if (g + 4 * i < 27) par[g + 4 * i] = ((uint64_t)hit[i].y << 32) | hit[i].x;
@@ -1315,7 +1319,8 @@ template <int C>
 __global__ void __launch_bounds__(256) k_top_prep5(int lo, int nsc, int n_embed, int b0, RowMap rm,
                                                    const uint64_t* __restrict__ lv_key,
                                                    const uint8_t* __restrict__ lv_code, int64_t cap_pts,
-                                                   const HashSlot* __restrict__ hash, int hash_lg, int fb,
+                                                   const HashSlot* __restrict__ hash, int hash_lg,
+                                                  const uint64_t* __restrict__ hreg, int fb,
                                                    const float* __restrict__ emb_o, int32_t* __restrict__ nbr,
                                                    float* __restrict__ X) {
   constexpr int Q = C / 16;
@@ -1351,7 +1356,7 @@ __global__ void __launch_bounds__(256) k_top_prep5(int lo, int nsc, int n_embed,
     if (b == rm.b_ext)
       base_cell_rows5(lv_key[lvb + vr], b, g, lv_key + lvb, n, nb);
     else
-      parent_cell_rows5(lv_key[lvb + vr], b, g, hash, hash_lg, fb, s_par[w][r], nb);
+      parent_cell_rows5(lv_key[lvb + vr], b, g, hash, hash_lg, hreg, fb, s_par[w][r], nb);
     if (valid) {
       int4* dst = reinterpret_cast<int4*>(nbr + (mo + vr) * 128 + 32 * g);
 #pragma unroll
@@ -1824,8 +1829,8 @@ hipError_t launch_top(Ctx& c, int b_lo, int b_hi, float* logits, bool second) {
     const int blocks = (int)std::min<int64_t>(2048, (c.cap_rows() + 63) / 64);
 #define RENO_PREP(CC)                                                                                         \
   hipLaunchKernelGGL(k_top_prep<CC>, dim3(blocks), dim3(256), 0, c.stream, n_lo, b_hi - n_lo + 1, b_hi - n_lo, b0, \
-                     rm, c.lv_key, c.lv_code, (int64_t)c.cap_pts, c.d_hash, c.hash_lg, c.fbits, c.w_embo, c.d_nbr, \
-                     c.h_c)
+                     rm, c.lv_key, c.lv_code, (int64_t)c.cap_pts, c.d_hash, c.hash_lg, c.hreg(), c.fbits, c.w_embo, \
+                     c.d_nbr, c.h_c)
     if (C == 32) RENO_PREP(32); else RENO_PREP(16);
 #undef RENO_PREP
   }
@@ -1839,6 +1844,7 @@ hipError_t launch_top(Ctx& c, int b_lo, int b_hi, float* logits, bool second) {
   a.lv_feat = c.lv_feat;
   a.hash = c.d_hash;
   a.hash_lg = c.hash_lg;
+  a.hreg = c.hreg();
   a.fb = c.fbits;
   a.nbr = c.d_nbr;
   a.zero_feat = (int64_t)c.nlv * c.cap_pts;
@@ -1900,11 +1906,11 @@ hipError_t launch_top_wide(Ctx& c, int b_lo, int b_hi, float* logits, bool secon
     const int blocks = (int)std::min<int64_t>(2048, (c.cap_rows() + 63) / 64);
     if (KV == 125)
       hipLaunchKernelGGL(k_top_prep5<C>, dim3(blocks), dim3(256), 0, c.stream, n_lo, b_hi - n_lo + 1, b_hi - n_lo,
-                         b0, rm, c.lv_key, c.lv_code, (int64_t)c.cap_pts, c.d_hash, c.hash_lg, c.fbits, c.w_embo,
+                         b0, rm, c.lv_key, c.lv_code, (int64_t)c.cap_pts, c.d_hash, c.hash_lg, c.hreg(), c.fbits, c.w_embo,
                          c.d_nbr, c.h_c);
     else
       hipLaunchKernelGGL(k_top_prep<C>, dim3(blocks), dim3(256), 0, c.stream, n_lo, b_hi - n_lo + 1, b_hi - n_lo,
-                         b0, rm, c.lv_key, c.lv_code, (int64_t)c.cap_pts, c.d_hash, c.hash_lg, c.fbits, c.w_embo,
+                         b0, rm, c.lv_key, c.lv_code, (int64_t)c.cap_pts, c.d_hash, c.hash_lg, c.hreg(), c.fbits, c.w_embo,
                          c.d_nbr, c.h_c);
   }
   ConvArgs a{};
@@ -2005,6 +2011,7 @@ hipError_t launch_model(Ctx& c, int b_lo, int b_hi, float* logits, bool second) 
   a.lv_feat = c.lv_feat;
   a.hash = c.d_hash;
   a.hash_lg = c.hash_lg;
+  a.hreg = c.hreg();
   a.fb = c.fbits;
   a.nbr = c.d_nbr;
   a.zero_feat = (int64_t)c.nlv * c.cap_pts;

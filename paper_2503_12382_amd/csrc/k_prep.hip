@@ -72,6 +72,7 @@ __global__ void __launch_bounds__(256) k_quantize(const float* __restrict__ pts,
                                                   double R, const int64_t* __restrict__ frame_start,
                                                   int frames, uint64_t* __restrict__ keys,
                                                   uint32_t* __restrict__ hist, int passes,
+                                                  uint64_t* __restrict__ hreg, int hash_lg,
                                                   uint32_t* err) {
   __shared__ uint32_t sh[MAX_PASSES * RADIX];
   __shared__ int64_t s_fs[RENO_MAX_FRAMES + 1];  // frame ranges of a batch
@@ -82,6 +83,18 @@ __global__ void __launch_bounds__(256) k_quantize(const float* __restrict__ pts,
       bool ok = frame_start[0] == 0 && frame_start[frames] == n;
       for (int f = 0; f < frames; ++f) ok = ok && frame_start[f] <= frame_start[f + 1];
       if (!ok) latch(err, ERR_FRAMES);
+    }
+    // hash region of each frame in proportion to its points (region starts
+    // ascending from 0 to the table size even for malformed ranges)
+    if (blockIdx.x == 0) {
+      const uint64_t T = 1ull << hash_lg;
+      for (int f = threadIdx.x; f <= frames; f += blockDim.x) {
+        int64_t sf = f == frames ? n : frame_start[f];
+        sf = sf < 0 ? 0 : (sf > n ? n : sf);
+        uint64_t st = n > 0 ? (uint64_t)sf * T / (uint64_t)n : (uint64_t)f * T / (uint64_t)frames;
+        if (f == frames) st = T;
+        hreg[f] = st;
+      }
     }
   }
   __syncthreads();
@@ -378,8 +391,8 @@ __global__ void __launch_bounds__(256) k_codes(const uint64_t* __restrict__ key,
                                                uint8_t* __restrict__ code,
                                                uint16_t* __restrict__ feat,
                                                const int32_t* __restrict__ count, int b0, int B,
-                                               int64_t cap_pts, HashSlot* hash, int hash_lg, int fb,
-                                               uint32_t* err) {
+                                               int64_t cap_pts, HashSlot* hash, int hash_lg,
+                                               const uint64_t* __restrict__ hreg, int fb, uint32_t* err) {
   __shared__ int64_t s_pre[NLEV + 1];
   if (threadIdx.x == 0) {
     int64_t acc = 0;
@@ -422,7 +435,10 @@ __global__ void __launch_bounds__(256) k_codes(const uint64_t* __restrict__ key,
       if (i < nk) feat[rc + lo + i] = (uint16_t)((kc[i] & 7ull) | (c << 3));
     // parents of model scales go into the coordinate hash with their code
     // and first child
-    if (b <= B - 2) hash_insert(hash, hash_lg, tag_key(key[rb + p], b, fb), lo, c, err);
+    if (b <= B - 2) {
+      const uint64_t kp = key[rb + p];
+      hash_insert(hash, hash_lg, hash_region(hreg, hash_lg, frame_part(kp, b)), tag_key(kp, b, fb), lo, c, err);
+    }
   }
 }
 
@@ -452,7 +468,8 @@ hipError_t launch_quantize(Ctx& c, const float* pts, int64_t n, int B, int passe
   if (blocks > 2048) blocks = 2048;
   if (blocks < 1) blocks = 1;
   hipLaunchKernelGGL(k_quantize, dim3((unsigned)blocks), dim3(256), 0, c.stream, pts, n, B,
-                     c.p.range_m, frame_start, frames, c.keys_a, c.d_hist, passes, c.d_err);
+                     c.p.range_m, frame_start, frames, c.keys_a, c.d_hist, passes, c.d_hreg, c.hash_lg,
+                     c.d_err);
   return hipGetLastError();
 }
 
@@ -506,7 +523,7 @@ hipError_t launch_codes(Ctx& c, int B) {
   if (blocks < 1) blocks = 1;
   hipLaunchKernelGGL(k_codes, dim3((unsigned)blocks), dim3(256), 0, c.stream, c.lv_key, c.lv_fc,
                      c.lv_code, c.lv_feat, c.d_count, c.b0(), B, c.cap_pts, c.d_hash, c.hash_lg,
-                     c.fbits, c.d_err);
+                     c.hreg(), c.fbits, c.d_err);
   return hipGetLastError();
 }
 
