@@ -542,7 +542,12 @@ def run_stress(args, reno, torch, dev, stream, copy_peak=None):
                           "on every model scale, code lengths)", "runs": []}
     skinds = ["zero", "quantize", "sort", "pyramid", "codes", "conv_first", "conv_mid", "conv_last",
               "code_length", "other"]
-    for K in [int(x) for x in args.stress.split(",") if x]:
+    ks = [int(x) for x in args.stress.split(",") if x]
+    # every K in fp32, and the largest K again with the split-bf16 contraction
+    # (about 5x less MFMA time per product than fp32), where the conv layers
+    # are no longer bound by the contraction and the gather shows its own rate
+    runs = [(K, reno.RENO_PREC_FP32) for K in ks] + ([(max(ks), reno.RENO_PREC_BF16X3)] if ks else [])
+    for K, prec in runs:
         sel = [sframes[i % len(sframes)] for i in range(K)]
         start = np.cumsum([0] + [f.shape[0] for f in sel]).astype(np.int64)
         SM = int(start[-1])
@@ -552,7 +557,8 @@ def run_stress(args, reno, torch, dev, stream, copy_peak=None):
         st_d = torch.from_numpy(start).to(dev)
         del sel
         with torch.cuda.stream(stream):
-            sc = reno.Context(SM, sB, sb0, scfg.range_m, sC, sL, max_model_voxels=cap, stream=stream)
+            sc = reno.Context(SM, sB, sb0, scfg.range_m, sC, sL, max_model_voxels=cap, stream=stream,
+                              precision=prec)
             sc.set_weights(sw)
 
             def enc():
@@ -603,11 +609,13 @@ def run_stress(args, reno, torch, dev, stream, copy_peak=None):
                 if copy_peak:
                     e["pass_hbm_frac_of_copy"] = round(pgbs / copy_peak, 4)
             kinds_out[k] = e
-        run = {"K": K, "points": SM, "voxels": int(sum(cnt)), "model_rows_capacity": cap,
+        run = {"K": K, "precision": "fp32" if prec == reno.RENO_PREC_FP32 else "bf16x3",
+               "points": SM, "voxels": int(sum(cnt)), "model_rows_capacity": cap,
                "device_bytes": smem["device_bytes"], "encoder_ms_per_batch": round(ms, 4),
                "encoder_frames_per_s": round(K * 1000.0 / ms, 1), "kinds": kinds_out}
         stress["runs"].append(run)
-        log("stress K", K, {k: (v["us"], v.get("pass_hbm_frac", v.get("hbm_frac"))) for k, v in kinds_out.items()},
+        log("stress K", K, run["precision"],
+            {k: (v["us"], v.get("pass_hbm_frac", v.get("hbm_frac"))) for k, v in kinds_out.items()},
             f"{ms:.3f} ms/batch")
         sc.close()
         del pts_d, st_d
