@@ -5,7 +5,9 @@ chunk-capped tile mode (more than 256 x 256 tiles per launch) and the sort in
 its large-tile mode.  Against the oracle, frame by frame: every scale's keys,
 coordinates and codes bit-exact (hence exact per-frame counts), neighbour
 maps, logits and per-voxel bits on sampled rows of every frame of every model
-scale, and the batch's total bits."""
+scale, and the batch's total bits; then the batched decoder from the frames'
+initial states and the encoder's codes, bit-identical to the encoder on every
+scale (keys, logits, bits, total)."""
 from concurrent.futures import ThreadPoolExecutor
 
 import numpy as np
@@ -96,6 +98,32 @@ def test_frame_batch_64_matches_oracle_per_frame(scan_cache):
     T = sum(Ts[s] for s in src)
     say(f"total bits gpu={total:.1f} oracle={T:.1f}")
     assert abs(total - T) <= BITS_REL_TOL * T
+
+    # the batched decoder: initial state of every frame plus the encoder's
+    # codes -> every scale's keys, every logit and every bit identical to the
+    # encoder's (compared on the device)
+    say("stress batch: decoder")
+    codes = {b: ctx.occupancy_codes(b).clone() for b in range(b0, B)}
+    base, bkeys = ctx.coords(b0)
+    fid = (bkeys >> (3 * b0)).to(torch.int32).contiguous()
+    dec = reno.Context(len(pts), B, b0, cfg.range_m, cfg.channels, cfg.layers, max_model_voxels=cap)
+    dec.set_weights(reno.weights_to_device(w))
+    dec.set_base_frames(B, base.clone(), fid, codes[b0], K)
+    off = 0
+    for b in range(b0 + 1, B):
+        dec.expand(b - 1, None if b - 1 == b0 else codes[b - 1])
+        assert torch.equal(dec.coords(b)[1], ctx.coords(b)[1]), f"decoder keys b={b}"
+        dl = dec.predict_probs(b, logits=True)
+        n = dl.shape[0]
+        assert torch.equal(dl.view(torch.int32), lg[off:off + n].view(torch.int32)), f"decoder logits b={b}"
+        off += n
+        del dl
+    dec.expand(B - 1, codes[B - 1])
+    assert torch.equal(dec.coords(B)[1], ctx.coords(B)[1])
+    dbits, dtotal = dec.code_length(reno.RENO_ALL_SCALES)
+    assert torch.equal(dbits.view(torch.int32), bits.view(torch.int32))
+    assert dtotal == total
+    dec.close()
     ctx.close()
-    del lg, bits
+    del lg, bits, dbits
     torch.cuda.empty_cache()
