@@ -380,11 +380,13 @@ class Codec:
 
 
 class EndToEnd:
-    """True end-to-end coding of one frame: GPU pyramid + model, the symbol
-    intervals (encoder) or cumulative tables (decoder) copied to pinned host
-    memory, and host rANS with each scale (and each stage of the two-stage
-    head) split into interleaved streams coded on the library's host threads;
-    the decoder decodes each scale's symbols before it expands them."""
+    """True end-to-end coding of one frame through the library's whole-frame
+    calls: the points copied in from pinned host memory, then
+    reno_encode_frame (GPU pyramid + model + symbol intervals, host rANS with
+    each scale and stage as interleaved streams on the library's host threads)
+    into a host bitstream, and reno_decode_frame from that bitstream alone
+    (per scale: expand, predict, cumulative tables out, streams decoded on the
+    host threads, codes back in)."""
 
     def __init__(self, reno, torch, cfg, pts, M, cap_model, stream, w_np, two_stage):
         self.reno, self.torch, self.stream, self.two = reno, torch, stream, two_stage
@@ -396,122 +398,41 @@ class EndToEnd:
             self.enc, self.dec = mk(), mk()
             self.enc.set_weights(wd)
             self.dec.set_weights(wd)
-        # the frame arrives in (pinned) host memory and its bitstream leaves
-        # to host memory: the encoder copies the points in and the base
-        # voxels out, the decoder copies the base voxels in
         self.pts_host = torch.empty(tuple(pts.shape), dtype=pts.dtype, pin_memory=True)
         self.pts_host.copy_(pts.cpu())
         self.pts = torch.empty_like(pts)
-        self.base_xyz_host = torch.empty((M, 3), dtype=torch.int32, pin_memory=True)
-        self.base_code_host = torch.empty(M, dtype=torch.uint8, pin_memory=True)
-        self.base_xyz_dev = torch.empty((M, 3), dtype=torch.int32, device=pts.device)
-        self.base_code_dev = torch.empty(M, dtype=torch.uint8, device=pts.device)
-        per = 4 if two_stage else 2
-        self.iv_host = torch.empty((cap_model, per), dtype=torch.int16, pin_memory=True)
-        k = 16 if two_stage else 256
-        self.tab_host = torch.empty((M, k), dtype=torch.int16, pin_memory=True)
-        self.tab_dev = torch.empty((M, k), dtype=torch.int16, device=pts.device)
-        self.code_host = torch.empty(M, dtype=torch.uint8, pin_memory=True)
-        self.s1_host = torch.empty(M, dtype=torch.uint8, pin_memory=True)
-        # decoded codes of consecutive scales alternate between two buffers; S1 has its own
-        self.code_dev = [torch.empty(M, dtype=torch.uint8, device=pts.device) for _ in range(3)]
+        self.buf = np.empty(2 * M + 65536, np.uint32)
 
     def encode(self):
-        """-> (bitstream dict, N_b per scale, base xyz, base codes)."""
-        reno, torch, enc, B, b0 = self.reno, self.torch, self.enc, self.B, self.b0
-        with torch.cuda.stream(self.stream):
+        with self.torch.cuda.stream(self.stream):
             self.pts.copy_(self.pts_host, non_blocking=True)
-            enc.build_pyramid(self.pts, B)
-            enc.predict_probs(reno.RENO_ALL_SCALES)
-            counts = enc.scale_counts()                       # synchronises once
-            nm = int(counts[b0 + 1:B].sum())
-            n0 = int(counts[b0])
-            iv = enc.symbol_intervals(reno.RENO_ALL_SCALES)
-            self.iv_host[:nm].copy_(iv, non_blocking=True)
-            base_xyz, _ = enc.coords(b0)
-            base_codes = enc.occupancy_codes(b0)
-            self.base_xyz_host[:n0].copy_(base_xyz, non_blocking=True)
-            self.base_code_host[:n0].copy_(base_codes, non_blocking=True)
-            self.stream.synchronize()
-        base_xyz, base_codes = self.base_xyz_host[:n0], self.base_code_host[:n0]
-        ivh = self.iv_host.numpy().view(np.uint16)
-        jobs, off = [], 0
-        for b in range(b0 + 1, B):
-            rows = ivh[off:off + counts[b]]
-            if self.two:
-                jobs += [(b, 0, rows, 4, 0), (b, 1, rows, 4, 2)]
-            else:
-                jobs.append((b, 0, rows, 2, 0))
-            off += counts[b]
-        # each scale (and stage) as RANS_STREAMS interleaved streams coded on the library's host threads
-        words = {(j[0], j[1]): reno.rans_encode_streams(j[2], RANS_STREAMS, j[3], j[4]) for j in jobs}
-        return words, counts, base_xyz, base_codes
+            return self.enc.encode_frame(self.pts, self.B, nstreams=RANS_STREAMS, out=self.buf)
 
-    def decode(self, words, counts, base_xyz, base_codes):
-        reno, torch, dec, B, b0 = self.reno, self.torch, self.dec, self.B, self.b0
-        with torch.cuda.stream(self.stream):
-            n0 = int(base_xyz.shape[0])
-            bx, bc = self.base_xyz_dev[:n0], self.base_code_dev[:n0]
-            bx.copy_(base_xyz, non_blocking=True)
-            bc.copy_(base_codes, non_blocking=True)
-            dec.set_base(B, bx, bc)
-            prev = None
-            for b in range(b0 + 1, B):
-                n = int(counts[b])
-                dec.expand(b - 1, prev)
-                dec.predict_probs(b)
-                # cumulative tables from the GPU; each scale's interleaved
-                # streams decoded on the library's host threads
-                if self.two:
-                    t1 = dec.symbol_cdf(b, 1, out=self.tab_dev)
-                    self.tab_host[:n].copy_(t1, non_blocking=True)
-                    self.stream.synchronize()
-                    s1 = reno.rans_decode_streams(*words[(b, 0)], self.tab_host[:n].numpy().view(np.uint16), n,
-                                                  out=self.s1_host[:n].numpy())
-                    s1_dev = self.code_dev[2][:n]
-                    s1_dev.copy_(self.s1_host[:n], non_blocking=True)
-                    dec.predict_second(b, s1_dev)
-                    t2 = dec.symbol_cdf(b, 2, out=self.tab_dev)
-                    self.tab_host[:n].copy_(t2, non_blocking=True)
-                    self.stream.synchronize()
-                    s2 = reno.rans_decode_streams(*words[(b, 1)], self.tab_host[:n].numpy().view(np.uint16), n,
-                                                  out=self.code_host[:n].numpy())
-                    np.bitwise_or(s1, s2 << 4, out=s2)
-                else:
-                    t = dec.symbol_cdf(b, 0, out=self.tab_dev)
-                    self.tab_host[:n].copy_(t, non_blocking=True)
-                    self.stream.synchronize()
-                    reno.rans_decode_streams(*words[(b, 0)], self.tab_host[:n].numpy().view(np.uint16), n,
-                                             out=self.code_host[:n].numpy())
-                cd = self.code_dev[b & 1][:n]
-                cd.copy_(self.code_host[:n], non_blocking=True)
-                prev = cd
-            dec.expand(B - 1, prev)
-            self.stream.synchronize()
+    def decode(self, words):
+        with self.torch.cuda.stream(self.stream):
+            self.dec.decode_frame(words)
 
     def run(self, frames, check=True):
         """Mean seconds per frame of encode and of decode, coded bits."""
-        reno, torch = self.reno, self.torch
+        torch = self.torch
         te = td = 0.0
         bits = None
         for i in range(frames + 1):                        # first pass: warm-up
             t = time.perf_counter()
-            words, counts, bx, bc = self.encode()
+            words = self.encode()
             t1 = time.perf_counter()
-            self.decode(words, counts, bx, bc)
+            self.decode(words)
             t2 = time.perf_counter()
             if i:
                 te += t1 - t
                 td += t2 - t1
             if check and i in (0, frames):
                 with torch.cuda.stream(self.stream):
-                    a, _ = self.dec.coords(self.B)
-                    e, _ = self.enc.coords(self.B)
-                    same = bool(torch.equal(a, e))
+                    same = bool(torch.equal(self.dec.coords(self.B)[0], self.enc.coords(self.B)[0]))
                 if not same:
                     log("end-to-end: decoded frame differs from the input")
                     sys.exit(1)
-            bits = 32 + int(counts[self.b0]) * (3 * self.b0 + 8) + sum(32 * w[0].size for w in words.values())
+            bits = 32 * words.size
         return te / frames, td / frames, bits
 
     def close(self):
@@ -878,11 +799,12 @@ def main():
                          "coded_bits_per_point": round(bits / M, 4)}
             log("end-to-end", name, e2e[name])
             ee.close()
-        e2e["note"] = ("wall-clock per frame: points copied in from pinned host memory, GPU pyramid + model + "
-                       "symbol intervals (encoder) or cumulative tables (decoder), pinned copies out, host rANS "
-                       f"with each scale (and stage) as {RANS_STREAMS} interleaved streams, coded and decoded on the "
-                       "library's host threads (the decoder from GPU cumulative tables), base voxels out and "
-                       "back in; the decoder decodes each scale before expanding it")
+        e2e["note"] = ("wall-clock per frame through reno_encode_frame / reno_decode_frame: points copied in "
+                       "from pinned host memory, GPU pyramid + model + symbol intervals (encoder) or cumulative "
+                       "tables (decoder) copied to pinned host memory, host rANS with each scale (and stage) as "
+                       f"{RANS_STREAMS} interleaved streams on the library's host threads; the decoder starts from "
+                       "the bitstream alone and decodes each scale before expanding it; coded bits = the whole "
+                       "bitstream (header, bit-packed base voxels, stream lengths, streams)")
 
     # ---- multi-frame throughput: F different frames, each with its own encoder
     # and decoder context and captured step, replayed round-robin over S
@@ -935,7 +857,7 @@ def main():
         # frame batches: the frames split into S batches (one key space each,
         # frame id above the Morton bits), one encoder + decoder context pair
         # and captured step per batch, batches replayed on S streams
-        for S in [x for x in (1, 2) if x <= len(codecs)]:
+        for S in [x for x in (1, 2) if x <= len(codecs) and x <= len(streams)]:
             groups = [list(range(len(codecs)))[g::S] for g in range(S)]
             cs = []
             for g, idx in enumerate(groups):

@@ -351,6 +351,37 @@ reno_status reno_rans_encode_streams(const uint16_t* iv, int64_t n, int64_t stri
 reno_status reno_rans_decode_streams(const uint32_t* in, const int64_t* nwords_host, int nstreams, int threads,
                                      const uint16_t* start, int k, int64_t n, uint8_t* sym);
 
+/* WHOLE-FRAME CODING: the codec of Sec. 3 with the arithmetic coder of
+ * Sec. 4.2 realised as the interleaved rANS streams above, one frame's points
+ * to a self-describing bitstream and back in one call each.
+ * encode: points device float [n][3] as for reno_build_pyramid; builds the
+ * pyramid, evaluates the model on every model scale, takes the symbol
+ * intervals on the device and codes every model scale (and each stage of the
+ * two-stage head) as nstreams (1 .. RENO_RANS_MAX_STREAMS) interleaved
+ * streams on the library's host threads.  Writes the bitstream to the HOST
+ * array out (at most cap_words words) and its length to *nwords_host (also
+ * when it fails with RENO_E_CAPACITY because cap_words is too small).  The
+ * context then holds the frame as after build_pyramid + predict_probs.
+ * decode: the bitstream in HOST memory; rebuilds V_b0 .. V_B on the device
+ * scale by scale (expand, predict, cumulative tables to the host, the scale's
+ * streams decoded on the host threads, codes back to the device), so that
+ * reno_coords(ctx, B, ...) afterwards returns the decoded voxels.  Fails with
+ * RENO_E_INPUT on a bitstream that is not well formed (bad magic, sizes out
+ * of range, a stream that ends early, words left over, a zero code), that was
+ * made with another min_bit_depth or head, or whose frame exceeds the
+ * context's capacities (RENO_E_CAPACITY).
+ * Both need min_bit_depth <= 8, weights set, and synchronise the context
+ * stream (the decoder at every scale); device and pinned host staging is
+ * allocated by the first call that needs it and kept until reno_destroy.
+ * Bitstream (uint32 words): 0x4F4E4552, B, b0, stages (1 or 2), S, N_b0; the
+ * base voxels bit-packed low bits first as x, y, z (b0 bits each) and the
+ * code (8 bits), padded to a word; then for each model scale b0 < b < B in
+ * order and each stage: the S stream lengths in words, then the S streams
+ * (stream j codes the scale's voxels j, j + S, ...). */
+reno_status reno_encode_frame(reno_ctx* ctx, const float* points, int64_t n, int bit_depth, int nstreams,
+                              uint32_t* out, int64_t cap_words, int64_t* nwords_host);
+reno_status reno_decode_frame(reno_ctx* ctx, const uint32_t* in, int64_t nwords);
+
 /* Kernel timing for measurement.  While a kind's bit is set in `kind_mask`,
  * every launch of that kind is bracketed by two HIP events recorded on the
  * context stream (event pairs come from a pool created by this call; launches

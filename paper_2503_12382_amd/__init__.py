@@ -99,6 +99,8 @@ _SIGS = {
     "reno_rans_decode": (_int, [_vp, _i64, _vp, _i64, _vp]),
     "reno_rans_encode_streams": (_int, [_vp, _i64, _i64, _int, _int, _vp, _i64, _vp]),
     "reno_rans_decode_streams": (_int, [_vp, _vp, _int, _int, _vp, _int, _i64, _vp]),
+    "reno_encode_frame": (_int, [_vp, _vp, _i64, _int, _int, _vp, _i64, ctypes.POINTER(_i64)]),
+    "reno_decode_frame": (_int, [_vp, _vp, _i64]),
     "reno_profile": (_int, [_vp, ctypes.c_uint32]),
     "reno_profile_read": (_int, [_vp, _vp, _vp]),
 }
@@ -388,6 +390,34 @@ class Context:
             out = self._empty((max(n, 1), k), self.torch.int16)
         self._check(lib().reno_symbol_cdf(self._h, scale, stage, _ptr(out)))
         return out[:n]
+
+    def encode_frame(self, points, bit_depth: int, nstreams: int = 16, out: np.ndarray | None = None):
+        """Whole frame to bitstream (reno_encode_frame): points device float
+        [n][3]; returns the bitstream as a host uint32 array (a view of ``out``
+        when given and large enough)."""
+        n = int(points.shape[0])
+        pts = points.contiguous()
+        nw = ctypes.c_int64()
+        buf = out if out is not None else np.empty(2 * n + 4096, np.uint32)
+        cap = int(buf.size)
+        for _ in range(2):              # a second try with the size the first one reported
+            rc = lib().reno_encode_frame(self._h, _ptr(pts) if n else None, n, bit_depth, nstreams,
+                                         buf.ctypes.data_as(_vp) if buf.size else None, cap, ctypes.byref(nw))
+            if rc != RENO_E_CAPACITY or nw.value <= cap:
+                break
+            cap = int(nw.value)
+            buf = np.empty(cap, np.uint32)
+        self._check(rc)
+        self._points = pts
+        self.B = bit_depth
+        return buf[:nw.value]
+
+    def decode_frame(self, words: np.ndarray):
+        """Bitstream (host uint32 array) to frame (reno_decode_frame): every
+        scale rebuilt on the device; coords(B) are the decoded voxels."""
+        w = np.ascontiguousarray(words, dtype=np.uint32)
+        self._check(lib().reno_decode_frame(self._h, w.ctypes.data_as(_vp), w.size))
+        self.B = int(w[1])
 
     def symbol_freqs(self, scale: int):
         n = self.num_voxels(scale)

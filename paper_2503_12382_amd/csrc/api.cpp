@@ -9,8 +9,6 @@
 
 #include "ctx.h"
 
-struct reno_ctx : reno::Ctx {};
-
 namespace {
 
 using reno::Ctx;
@@ -66,6 +64,7 @@ void free_all(Ctx* c) {
   if (c->h_err) (void)hipHostFree(c->h_err);
   for (hipEvent_t ev : c->prof_pool) (void)hipEventDestroy(ev);
   c->prof_pool.clear();
+  reno::frame_free(*c);
 }
 
 // Waits for the stream and turns latched device errors into a status.

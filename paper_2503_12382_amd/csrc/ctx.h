@@ -128,6 +128,15 @@ struct Ctx {
   // set by a dispatch-bound ProfScope and consumed by that launch
   hipEvent_t ext_start = nullptr, ext_stop = nullptr;
 
+  // whole-frame coding staging, device + pinned host pairs grown on demand:
+  // symbol intervals / cumulative tables, and base voxels + decoded codes
+  void* fc_tab_dev = nullptr;
+  void* fc_tab_host = nullptr;
+  size_t fc_tab_bytes = 0;
+  void* fc_aux_dev = nullptr;
+  void* fc_aux_host = nullptr;
+  size_t fc_aux_bytes = 0;
+
   int64_t pyr_tiles = 0;    // max tiles of the pyramid pass
   int64_t exp_tiles = 0;    // max tiles of one expansion
 
@@ -217,4 +226,10 @@ hipError_t launch_copy_level_u8(Ctx& c, int b, uint8_t* out);
 hipError_t launch_copy_level_i32(Ctx& c, int b, const int32_t* src, int32_t* out);
 hipError_t launch_neighbor_map(Ctx& c, int b, int32_t* out);
 
+// releases the whole-frame coding staging
+void frame_free(Ctx& c);
+
 }  // namespace reno
+
+// the opaque handle of the C ABI
+struct reno_ctx : reno::Ctx {};

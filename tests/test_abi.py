@@ -25,7 +25,7 @@ def declared_functions():
 def test_header_and_binding_agree():
     decl = declared_functions()
     assert decl == set(reno._SIGS), decl ^ set(reno._SIGS)
-    assert len(decl) == 33
+    assert len(decl) == 35
 
 
 def _struct_fields(name):
@@ -136,6 +136,15 @@ def test_expand_noalloc_rejects_bad_arguments_without_gpu():
     for args in cases:
         assert L.reno_expand_noalloc(*args, None) == reno.RENO_E_INVALID, args
         assert L.reno_last_error(None)
+
+
+def test_frame_coding_rejects_bad_arguments_without_gpu():
+    """Whole-frame calls check their arguments before any HIP call."""
+    L = reno.lib()
+    nw = ctypes.c_int64()
+    buf = (ctypes.c_uint32 * 8)()
+    assert L.reno_encode_frame(None, None, 0, 10, 16, buf, 8, ctypes.byref(nw)) == reno.RENO_E_INVALID
+    assert L.reno_decode_frame(None, buf, 8) == reno.RENO_E_INVALID
 
 
 def _intervals_and_starts(f, sym):
