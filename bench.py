@@ -37,7 +37,7 @@ MODEL_SRCS = [os.path.join(ROOT, "paper_2503_12382_amd", "csrc", f) for f in ("k
 # rows are padded to 32 for alignment; the padding is not algorithmic traffic)
 MAP_ROW_BYTES = 4 * 27
 # interleaved rANS streams per scale (and stage) in the end-to-end coder
-RANS_STREAMS = 16
+STREAM_SYMBOLS = 1024  # whole-frame coding: symbols per rANS stream
 
 
 def alg_bytes_per_frame(counts, b0, B, M, C, hash_slots, status_words):
@@ -382,14 +382,13 @@ class Codec:
 class EndToEnd:
     """True end-to-end coding of one frame through the library's whole-frame
     calls: the points copied in from pinned host memory, then
-    reno_encode_frame (GPU pyramid + model + symbol intervals, host rANS with
-    each scale and stage as interleaved streams on the library's host threads)
+    reno_encode_frame (GPU pyramid + model + symbol intervals + rANS streams)
     into a host bitstream, and reno_decode_frame from that bitstream alone
-    (per scale: expand, predict, cumulative tables out, streams decoded on the
-    host threads, codes back in)."""
+    (copied in once; per scale expand, predict, cumulative tables and stream
+    decoding on the GPU, one synchronisation at the end)."""
 
-    def __init__(self, reno, torch, cfg, pts, M, cap_model, stream, w_np, two_stage):
-        self.reno, self.torch, self.stream, self.two = reno, torch, stream, two_stage
+    def __init__(self, reno, torch, cfg, pts, M, cap_model, stream, w_np, two_stage, L=STREAM_SYMBOLS):
+        self.reno, self.torch, self.stream, self.two, self.L = reno, torch, stream, two_stage, L
         self.B, self.b0 = cfg.bit_depth, cfg.min_bit_depth
         wd = reno.weights_to_device(w_np)
         mk = lambda: reno.Context(M, self.B, self.b0, cfg.range_m, cfg.channels, cfg.layers,
@@ -406,7 +405,7 @@ class EndToEnd:
     def encode(self):
         with self.torch.cuda.stream(self.stream):
             self.pts.copy_(self.pts_host, non_blocking=True)
-            return self.enc.encode_frame(self.pts, self.B, nstreams=RANS_STREAMS, out=self.buf)
+            return self.enc.encode_frame(self.pts, self.B, stream_symbols=self.L, out=self.buf)
 
     def decode(self, words):
         with self.torch.cuda.stream(self.stream):
@@ -800,11 +799,12 @@ def main():
             log("end-to-end", name, e2e[name])
             ee.close()
         e2e["note"] = ("wall-clock per frame through reno_encode_frame / reno_decode_frame: points copied in "
-                       "from pinned host memory, GPU pyramid + model + symbol intervals (encoder) or cumulative "
-                       "tables (decoder) copied to pinned host memory, host rANS with each scale (and stage) as "
-                       f"{RANS_STREAMS} interleaved streams on the library's host threads; the decoder starts from "
-                       "the bitstream alone and decodes each scale before expanding it; coded bits = the whole "
-                       "bitstream (header, bit-packed base voxels, stream lengths, streams)")
+                       "from pinned host memory; GPU pyramid + model + symbol intervals + rANS streams "
+                       f"(ceil(N_b / {STREAM_SYMBOLS}) streams per scale and stage, one thread each), bitstream "
+                       "copied out; the decoder starts from the host bitstream alone, copies it in once and runs "
+                       "expand, predict, cumulative tables and stream decoding (one wavefront per stream) scale "
+                       "by scale on the GPU; coded bits = the whole bitstream (header, bit-packed base voxels, "
+                       "16-bit stream lengths, streams)")
 
     # ---- multi-frame throughput: F different frames, each with its own encoder
     # and decoder context and captured step, replayed round-robin over S

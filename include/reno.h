@@ -352,33 +352,37 @@ reno_status reno_rans_decode_streams(const uint32_t* in, const int64_t* nwords_h
                                      const uint16_t* start, int k, int64_t n, uint8_t* sym);
 
 /* WHOLE-FRAME CODING: the codec of Sec. 3 with the arithmetic coder of
- * Sec. 4.2 realised as the interleaved rANS streams above, one frame's points
- * to a self-describing bitstream and back in one call each.
+ * Sec. 4.2 realised as rANS (the stream format of reno_rans_encode), one
+ * frame's points to a self-describing bitstream and back in one call each,
+ * every step on the GPU.
  * encode: points device float [n][3] as for reno_build_pyramid; builds the
  * pyramid, evaluates the model on every model scale, takes the symbol
- * intervals on the device and codes every model scale (and each stage of the
- * two-stage head) as nstreams (1 .. RENO_RANS_MAX_STREAMS) interleaved
- * streams on the library's host threads.  Writes the bitstream to the HOST
- * array out (at most cap_words words) and its length to *nwords_host (also
- * when it fails with RENO_E_CAPACITY because cap_words is too small).  The
- * context then holds the frame as after build_pyramid + predict_probs.
- * decode: the bitstream in HOST memory; rebuilds V_b0 .. V_B on the device
- * scale by scale (expand, predict, cumulative tables to the host, the scale's
- * streams decoded on the host threads, codes back to the device), so that
- * reno_coords(ctx, B, ...) afterwards returns the decoded voxels.  Fails with
- * RENO_E_INPUT on a bitstream that is not well formed (bad magic, sizes out
- * of range, a stream that ends early, words left over, a zero code), that was
- * made with another min_bit_depth or head, or whose frame exceeds the
- * context's capacities (RENO_E_CAPACITY).
- * Both need min_bit_depth <= 8, weights set, and synchronise the context
- * stream (the decoder at every scale); device and pinned host staging is
- * allocated by the first call that needs it and kept until reno_destroy.
- * Bitstream (uint32 words): 0x4F4E4552, B, b0, stages (1 or 2), S, N_b0; the
- * base voxels bit-packed low bits first as x, y, z (b0 bits each) and the
- * code (8 bits), padded to a word; then for each model scale b0 < b < B in
- * order and each stage: the S stream lengths in words, then the S streams
- * (stream j codes the scale's voxels j, j + S, ...). */
-reno_status reno_encode_frame(reno_ctx* ctx, const float* points, int64_t n, int bit_depth, int nstreams,
+ * intervals and codes each model scale (and each stage of the two-stage
+ * head) as S = ceil(N_b / stream_symbols) interleaved streams, one GPU thread
+ * per stream (1 <= stream_symbols <= 65533).  Copies the bitstream to the
+ * HOST array out (at most cap_words words) and its length to *nwords_host
+ * (also when it fails with RENO_E_CAPACITY because cap_words is too small).
+ * The context then holds the frame as after build_pyramid + predict_probs.
+ * decode: the bitstream in HOST memory; copies it to the device once and
+ * rebuilds V_b0 .. V_B scale by scale (expand, predict, cumulative tables,
+ * one wavefront per stream decoding the scale's codes) without waiting on the
+ * host, so that reno_coords(ctx, B, ...) afterwards returns the decoded
+ * voxels.  Fails with RENO_E_INPUT on a bitstream that is not well formed
+ * (bad magic, sizes out of range, a stream that ends early or does not end
+ * in the coder's initial state, words left over, a zero code), or that was
+ * made with another min_bit_depth or head; RENO_E_CAPACITY when its frame
+ * exceeds the context's capacities.
+ * Both need min_bit_depth <= 8 and weights set, and synchronise the context
+ * stream; device and pinned host staging is allocated by the first call that
+ * needs it (and grown by later ones) and kept until reno_destroy.
+ * Bitstream (uint32 words): 0x4F4E4552, B, b0, stages (1 or 2),
+ * stream_symbols L, N_b0; the base voxels bit-packed from the lowest bit up
+ * as fields x | y << b0 | z << 2 b0 | code << 3 b0 of 3 b0 + 8 bits, padded
+ * to a word; then for each model scale b0 < b < B in order and each stage:
+ * the S stream lengths in words as 16-bit fields (two per word, the even
+ * stream in the low half), then the S streams, stream j coding the scale's
+ * voxels j, j + S, ... (an empty scale has one stream of two words). */
+reno_status reno_encode_frame(reno_ctx* ctx, const float* points, int64_t n, int bit_depth, int stream_symbols,
                               uint32_t* out, int64_t cap_words, int64_t* nwords_host);
 reno_status reno_decode_frame(reno_ctx* ctx, const uint32_t* in, int64_t nwords);
 
@@ -405,6 +409,7 @@ typedef enum {
   RENO_K_CODE_LENGTH,   /* ideal bits and per-scale sums */
   RENO_K_OTHER,         /* weight packing, getters, symbol tables */
   RENO_K_TOP_INPUT,     /* full predictor: neighbour maps and embedding inputs */
+  RENO_K_ENTROPY,       /* whole-frame coding: rANS streams, their layout, base packing */
   RENO_K_COUNT
 } reno_kernel;
 

@@ -106,7 +106,7 @@ _SIGS = {
 }
 
 KERNELS = ["zero", "quantize", "sort", "pyramid", "codes", "set_base", "expand", "conv_first",
-           "conv_mid", "conv_last", "code_length", "other", "top_input"]
+           "conv_mid", "conv_last", "code_length", "other", "top_input", "entropy"]
 
 _lib = None
 
@@ -391,17 +391,18 @@ class Context:
         self._check(lib().reno_symbol_cdf(self._h, scale, stage, _ptr(out)))
         return out[:n]
 
-    def encode_frame(self, points, bit_depth: int, nstreams: int = 16, out: np.ndarray | None = None):
+    def encode_frame(self, points, bit_depth: int, stream_symbols: int = 1024, out: np.ndarray | None = None):
         """Whole frame to bitstream (reno_encode_frame): points device float
-        [n][3]; returns the bitstream as a host uint32 array (a view of ``out``
-        when given and large enough)."""
+        [n][3]; each scale's symbols go to ceil(N / stream_symbols)
+        interleaved rANS streams.  Returns the bitstream as a host uint32
+        array (a view of ``out`` when given and large enough)."""
         n = int(points.shape[0])
         pts = points.contiguous()
         nw = ctypes.c_int64()
         buf = out if out is not None else np.empty(2 * n + 4096, np.uint32)
         cap = int(buf.size)
         for _ in range(2):              # a second try with the size the first one reported
-            rc = lib().reno_encode_frame(self._h, _ptr(pts) if n else None, n, bit_depth, nstreams,
+            rc = lib().reno_encode_frame(self._h, _ptr(pts) if n else None, n, bit_depth, stream_symbols,
                                          buf.ctypes.data_as(_vp) if buf.size else None, cap, ctypes.byref(nw))
             if rc != RENO_E_CAPACITY or nw.value <= cap:
                 break

@@ -19,7 +19,7 @@ BUILD = os.path.join(ROOT, "_build")
 LIB = os.path.join(HERE, "libreno.so")
 ARCH = "gfx950"
 
-HIP_SOURCES = ["k_prep.hip", "k_dec.hip", "k_model.hip", "k_post.hip", "api.cpp", "frame.cpp"]
+HIP_SOURCES = ["k_prep.hip", "k_dec.hip", "k_model.hip", "k_post.hip", "k_code.hip", "api.cpp", "frame.cpp"]
 HOST_SOURCES = ["rans.cpp"]
 HEADERS = ["dev.h", "ctx.h"]
 

@@ -85,6 +85,10 @@ reno_status sync_check(Ctx* c) {
   if (e & reno::ERR_INTERNAL) msg += " internal: consistency check failed;";
   if (e & reno::ERR_SYMBOL) msg += " first sub-code outside 0..15;";
   if (e & reno::ERR_FRAMES) msg += " frame ranges or frame ids of the batch malformed;";
+  if (e & reno::ERR_STREAM) msg += " entropy-coded stream of the bitstream malformed;";
+  // a malformed bitstream explains what follows from decoding it (codes of
+  // zero, scales past the capacity)
+  if (e & reno::ERR_STREAM) return fail(c, RENO_E_INPUT, msg);
   if (e & (reno::ERR_CAPACITY | reno::ERR_HASH_FULL)) return fail(c, RENO_E_CAPACITY, msg);
   if (e & (reno::ERR_SPIN | reno::ERR_DUP_KEY | reno::ERR_INTERNAL)) return fail(c, RENO_E_HIP, msg);
   return fail(c, RENO_E_INPUT, msg);

@@ -7,6 +7,7 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include <algorithm>
 #include <string>
 #include <vector>
 
@@ -128,14 +129,14 @@ struct Ctx {
   // set by a dispatch-bound ProfScope and consumed by that launch
   hipEvent_t ext_start = nullptr, ext_stop = nullptr;
 
-  // whole-frame coding staging, device + pinned host pairs grown on demand:
-  // symbol intervals / cumulative tables, and base voxels + decoded codes
-  void* fc_tab_dev = nullptr;
-  void* fc_tab_host = nullptr;
-  size_t fc_tab_bytes = 0;
-  void* fc_aux_dev = nullptr;
-  void* fc_aux_host = nullptr;
-  size_t fc_aux_bytes = 0;
+  // whole-frame coding staging, grown on demand (device: bitstream, stream
+  // regions, stream bookkeeping, symbol tables, base voxels and codes;
+  // pinned host: bitstream, base voxels)
+  static constexpr int FC_DEV = 5, FC_HOST = 2;
+  void* fc_dev[FC_DEV] = {};
+  size_t fc_dev_bytes[FC_DEV] = {};
+  void* fc_host[FC_HOST] = {};
+  size_t fc_host_bytes[FC_HOST] = {};
 
   int64_t pyr_tiles = 0;    // max tiles of the pyramid pass
   int64_t exp_tiles = 0;    // max tiles of one expansion
@@ -221,10 +222,26 @@ hipError_t launch_symbol_freqs(Ctx& c, int b, uint16_t* freq);
 hipError_t launch_symbol_freqs16(Ctx& c, int b, int stage, uint16_t* freq);
 hipError_t launch_symbol_intervals(Ctx& c, int b_lo, int b_hi, uint16_t* iv);
 hipError_t launch_symbol_cdf(Ctx& c, int b, int stage, uint16_t* start);
+// the decoder's tables, entries start | f << 16 per symbol ([N][256] or
+// [N][16]); scratch ([N][K] uint16) is used only by contexts whose head
+// does not fit the register-resident table kernels
+hipError_t launch_symbol_entries(Ctx& c, int b, int stage, uint32_t* entries, uint16_t* scratch);
 hipError_t launch_coords(Ctx& c, int b, int32_t* xyz, uint64_t* keys);
 hipError_t launch_copy_level_u8(Ctx& c, int b, uint8_t* out);
 hipError_t launch_copy_level_i32(Ctx& c, int b, const int32_t* src, int32_t* out);
 hipError_t launch_neighbor_map(Ctx& c, int b, int32_t* out);
+
+// whole-frame entropy coder (k_code.hip)
+int64_t rans_stream_bound(const Ctx& c, int sections, int L);
+hipError_t launch_rans_encode(Ctx& c, const uint16_t* iv, int b_lo, int b_hi, int stages, int L, uint32_t* region,
+                              uint32_t* lens, int64_t G);
+hipError_t launch_rans_layout(Ctx& c, int b_lo, int b_hi, int stages, int L, int B, const uint32_t* lens,
+                              int64_t G, int64_t* offs, uint32_t* out, int64_t cap_words, int64_t* total);
+hipError_t launch_rans_pack(Ctx& c, const uint32_t* region, const uint32_t* lens, const int64_t* offs, int L,
+                            int64_t G, const int64_t* total, const int32_t* xyz, uint32_t* out, int64_t cap_words);
+hipError_t launch_rans_decode(Ctx& c, const uint32_t* words, int64_t nwords, int b, int L, int K,
+                              const uint32_t* tab, const uint8_t* s1, uint8_t* out, uint64_t* fpos, int t,
+                              int64_t p0, bool last);
 
 // releases the whole-frame coding staging
 void frame_free(Ctx& c);

@@ -23,6 +23,7 @@ enum : uint32_t {
   ERR_SYMBOL = 512u,     // a decoded sub-code outside its alphabet (S1 above 15)
   ERR_FRAMES = 1024u,    // frame ranges or base frame ids of a frame batch malformed
   ERR_KEY_RANGE = 2048u, // a parent key of 2^61 or more (its children would not fit in 64 bits)
+  ERR_STREAM = 4096u,    // an entropy-coded section or stream of a frame bitstream malformed
 };
 
 __device__ __forceinline__ void latch(uint32_t* err, uint32_t bit) { atomicOr(err, bit); }

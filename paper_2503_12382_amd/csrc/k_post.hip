@@ -413,6 +413,220 @@ __global__ void __launch_bounds__(256) k_symbol_intervals16(const int32_t* __res
   }
 }
 
+// ---- the same tables with the head held in registers (C = 16 or 32) ----
+// One wavefront per voxel for 256 symbols, four voxels per wavefront (16
+// lanes each) for 16; each lane keeps its symbols' head columns in registers
+// for the whole launch and the voxel's row h_L is read once per wavefront
+// (uniform loads).  Logits accumulate over c in ascending order exactly as in
+// table256 / table16, so every table is bit-identical to theirs.
+// TB_ENTRY: the decoder's entries, uint32 start | f << 16 per symbol
+enum { TB_FREQ = 0, TB_CDF = 1, TB_IV = 2, TB_ENTRY = 3 };
+
+__device__ __forceinline__ int uniform_wave() { return __builtin_amdgcn_readfirstlane((int)(threadIdx.x >> 6)); }
+
+// frequencies of symbols 4 lane .. 4 lane + 3 from their logits (the
+// quantisation of table256)
+__device__ __forceinline__ void quantise256(const float (&z)[4], float l, int lane, uint32_t (&f)[4]) {
+  uint32_t sum = 0, best = 0;
+  int besti = 0;
+  for (int e = 0; e < 4; ++e) {
+    const float p = __expf(z[e] - l);
+    f[e] = 1u + (uint32_t)floorf(p * 65024.0f);
+    sum += f[e];
+    if (f[e] > best) {
+      best = f[e];
+      besti = lane * 4 + e;
+    }
+  }
+  for (int o = 32; o > 0; o >>= 1) {
+    sum += (uint32_t)__shfl_xor((int)sum, o);
+    const uint32_t ob = (uint32_t)__shfl_xor((int)best, o);
+    const int oi = __shfl_xor(besti, o);
+    if (ob > best || (ob == best && oi < besti)) {
+      best = ob;
+      besti = oi;
+    }
+  }
+  const uint32_t left = 65536u - sum;
+  for (int e = 0; e < 4; ++e) f[e] += (lane * 4 + e == besti) ? left : 0u;
+}
+
+template <int C, int MODE>
+__global__ void __launch_bounds__(256) k_table256r(const int32_t* __restrict__ count,
+                                                   const int32_t* __restrict__ moff, int b, int b_lo,
+                                                   int64_t cap_model, const uint8_t* __restrict__ code,
+                                                   const float* __restrict__ hL, const float* __restrict__ H,
+                                                   const float* __restrict__ hb, const float* __restrict__ lse,
+                                                   uint16_t* __restrict__ out) {
+  const int lane = threadIdx.x & 63;
+  const int64_t mo = moff[b];
+  int64_t n = count[b];
+  if (mo + n > cap_model) n = 0;
+  const int64_t wstride = (int64_t)gridDim.x * (blockDim.x / 64);
+  const int64_t v_first = (int64_t)blockIdx.x * (blockDim.x / 64) + uniform_wave();
+  if (v_first >= n) return;  // no voxel for this wavefront: the head is not loaded
+  float w[C][4];
+#pragma unroll
+  for (int c = 0; c < C; ++c) {
+    const float4 t = reinterpret_cast<const float4*>(H + c * 256)[lane];
+    w[c][0] = t.x;
+    w[c][1] = t.y;
+    w[c][2] = t.z;
+    w[c][3] = t.w;
+  }
+  const float4 bias = reinterpret_cast<const float4*>(hb)[lane];
+  for (int64_t v = v_first; v < n; v += wstride) {
+    const float* h = hL + (mo + v) * C;
+    float z[4] = {bias.x, bias.y, bias.z, bias.w};
+#pragma unroll
+    for (int c = 0; c < C; ++c) {
+      const float hc = h[c];
+#pragma unroll
+      for (int e = 0; e < 4; ++e) z[e] = fmaf(w[c][e], hc, z[e]);
+    }
+    uint32_t f[4];
+    quantise256(z, lse[mo + v], lane, f);
+    if constexpr (MODE == TB_FREQ) {
+      uint16_t* dst = out + v * 256 + lane * 4;
+      for (int e = 0; e < 4; ++e) dst[e] = (uint16_t)f[e];
+    } else {
+      const uint32_t mine = f[0] + f[1] + f[2] + f[3];
+      uint32_t inc = mine;  // inclusive prefix over lanes
+      for (int d = 1; d < 64; d <<= 1) {
+        const uint32_t t = (uint32_t)__shfl_up((int)inc, d);
+        if (lane >= d) inc += t;
+      }
+      uint32_t st = inc - mine;
+      if constexpr (MODE == TB_CDF) {
+        uint16_t* dst = out + v * 256 + lane * 4;
+        for (int e = 0; e < 4; ++e) {
+          dst[e] = (uint16_t)st;
+          st += f[e];
+        }
+      } else if constexpr (MODE == TB_ENTRY) {
+        uint4 ent;
+        ent.x = st | (f[0] << 16);
+        st += f[0];
+        ent.y = st | (f[1] << 16);
+        st += f[1];
+        ent.z = st | (f[2] << 16);
+        st += f[2];
+        ent.w = st | (f[3] << 16);
+        reinterpret_cast<uint4*>(out)[v * 64 + lane] = ent;
+      } else {
+        const int o = code[v];
+        if (lane == (o >> 2)) {
+          for (int e = 0; e < (o & 3); ++e) st += f[e];
+          const int64_t ro = mo - moff[b_lo] + v;  // row in the concatenated output
+          out[ro * 2] = (uint16_t)st;
+          out[ro * 2 + 1] = (uint16_t)f[o & 3];
+        }
+      }
+    }
+  }
+}
+
+// 16-symbol table of the voxel of this lane's group from its logit z (the
+// quantisation of table16); returns f_s
+__device__ __forceinline__ uint32_t quantise16(float z, float l, int s) {
+  const float p = __expf(z - l);
+  uint32_t f = 1u + (uint32_t)floorf(p * 65504.0f);
+  uint32_t sum = f, best = f;
+  int besti = s;
+  for (int o = 1; o < 16; o <<= 1) {
+    sum += (uint32_t)__shfl_xor((int)sum, o);
+    const uint32_t ob = (uint32_t)__shfl_xor((int)best, o);
+    const int oi = __shfl_xor(besti, o);
+    if (ob > best || (ob == best && oi < besti)) {
+      best = ob;
+      besti = oi;
+    }
+  }
+  return f + (s == besti ? 65536u - sum : 0u);
+}
+
+// Two-stage tables: STAGE 1 or 2 (MODE TB_FREQ / TB_CDF), or both stages'
+// encoder intervals (MODE TB_IV, STAGE ignored).
+template <int C, int MODE, int STAGE>
+__global__ void __launch_bounds__(256) k_table16r(const int32_t* __restrict__ count,
+                                                  const int32_t* __restrict__ moff, int b, int b_lo,
+                                                  int64_t cap_model, const uint8_t* __restrict__ code,
+                                                  const float* __restrict__ hL, const float* __restrict__ Hp,
+                                                  const float* __restrict__ hb, const float* __restrict__ emb,
+                                                  const uint8_t* __restrict__ s1, const float* __restrict__ lse,
+                                                  const float* __restrict__ lse2, uint16_t* __restrict__ out) {
+  constexpr bool ONE = MODE == TB_IV || STAGE == 1;
+  constexpr bool TWO = MODE == TB_IV || STAGE == 2;
+  const int s = threadIdx.x & 15;
+  const int64_t mo = moff[b];
+  int64_t n = count[b];
+  if (mo + n > cap_model) n = 0;
+  const int64_t gstride = (int64_t)gridDim.x * (blockDim.x / 16);
+  const int64_t v_first = (int64_t)blockIdx.x * (blockDim.x / 16) + 4 * uniform_wave();
+  if (v_first >= n) return;  // no voxel for this wavefront: the head is not loaded
+  float w1[ONE ? C : 1], w2[TWO ? C : 1];
+#pragma unroll
+  for (int c = 0; c < C; ++c) {
+    if constexpr (ONE) w1[c] = Hp[c * 32 + s];
+    if constexpr (TWO) w2[c] = Hp[c * 32 + 16 + s];
+  }
+  const float b1 = ONE ? hb[s] : 0.0f, b2 = TWO ? hb[16 + s] : 0.0f;
+  for (int64_t v0 = v_first; v0 < n; v0 += gstride) {
+    // the whole wavefront runs the shuffles; groups past the last voxel write nothing
+    const int64_t v = v0 + ((threadIdx.x >> 4) & 3);
+    const int64_t pr = mo + (v < n ? v : n - 1);
+    const float* h = hL + pr * C;
+    const int o = MODE == TB_IV ? (int)code[v < n ? v : n - 1] : 0;
+    uint32_t f1 = 0, f2 = 0;
+    if constexpr (ONE) {
+      float z = b1;
+#pragma unroll
+      for (int c = 0; c < C; ++c) z = fmaf(w1[c], h[c], z);
+      f1 = quantise16(z, lse[pr], s);
+    }
+    if constexpr (TWO) {
+      const int a1 = MODE == TB_IV ? (o & 15) : (int)s1[pr];
+      const float* e = emb + a1 * C;
+      float z = b2;
+#pragma unroll
+      for (int c = 0; c < C; ++c) z = fmaf(w2[c], h[c] + e[c], z);
+      f2 = quantise16(z, lse2[pr], s);
+    }
+    if constexpr (MODE == TB_FREQ) {
+      if (v < n) out[v * 16 + s] = (uint16_t)(STAGE == 1 ? f1 : f2);
+    } else if constexpr (MODE == TB_CDF) {
+      const uint32_t st = excl16(STAGE == 1 ? f1 : f2, s);
+      if (v < n) out[v * 16 + s] = (uint16_t)st;
+    } else if constexpr (MODE == TB_ENTRY) {
+      const uint32_t f = STAGE == 1 ? f1 : f2;
+      const uint32_t st = excl16(f, s);
+      if (v < n) reinterpret_cast<uint32_t*>(out)[v * 16 + s] = st | (f << 16);
+    } else {
+      const uint32_t st1 = excl16(f1, s), st2 = excl16(f2, s);
+      const int64_t ro = mo - moff[b_lo] + v;  // row in the concatenated output
+      if (v < n && s == (o & 15)) {
+        out[ro * 4] = (uint16_t)st1;
+        out[ro * 4 + 1] = (uint16_t)f1;
+      }
+      if (v < n && s == (o >> 4)) {
+        out[ro * 4 + 2] = (uint16_t)st2;
+        out[ro * 4 + 3] = (uint16_t)f2;
+      }
+    }
+  }
+}
+
+// Cumulative tables [N][K] to the decoder's entries start | f << 16.
+__global__ void k_cdf_entries(const int32_t* __restrict__ count, int b, int K, const uint16_t* __restrict__ start,
+                              uint32_t* __restrict__ entries) {
+  const int64_t n = (int64_t)count[b] * K;
+  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += (int64_t)gridDim.x * blockDim.x) {
+    const uint32_t st = start[i];
+    const uint32_t nx = (i % K) + 1 < K ? (uint32_t)start[i + 1] : 65536u;
+    entries[i] = st | ((nx - st) << 16);
+  }
+}
+
 __global__ void k_coords(const uint64_t* __restrict__ key, const int32_t* __restrict__ count, int b,
                          int32_t* __restrict__ xyz, uint64_t* __restrict__ keys) {
   const int64_t n = count[b];
@@ -500,8 +714,51 @@ hipError_t launch_code_length(Ctx& c, int b_lo, int b_hi, float* bits) {
   return hipGetLastError();
 }
 
+// register-resident table kernels: C = 16 or 32; wavefronts of 64 voxels
+// (256 symbols) or 256 voxels (16 symbols) each, up to 2048 workgroups
+template <int C>
+void run_table256r(Ctx& c, int mode, int b, int b_lo, const uint8_t* code, uint16_t* out) {
+  const dim3 g(grid_for(c.cap_pts, 4 * 64)), t(256);
+  const auto args = [&](auto kern) {
+    hipLaunchKernelGGL(kern, g, t, 0, c.stream, c.d_count, c.d_moff, b, b_lo, c.cap_model, code, c.hlast(),
+                       c.w_head_plain, c.w_hbias, c.d_lse, out);
+  };
+  if (mode == TB_FREQ) args(k_table256r<C, TB_FREQ>);
+  else if (mode == TB_CDF) args(k_table256r<C, TB_CDF>);
+  else if (mode == TB_ENTRY) args(k_table256r<C, TB_ENTRY>);
+  else args(k_table256r<C, TB_IV>);
+}
+
+template <int C>
+void run_table16r(Ctx& c, int mode, int stage, int b, int b_lo, const uint8_t* code, uint16_t* out) {
+  const dim3 g(grid_for(c.cap_pts, 16 * 64)), t(256);
+  const auto args = [&](auto kern) {
+    hipLaunchKernelGGL(kern, g, t, 0, c.stream, c.d_count, c.d_moff, b, b_lo, c.cap_model, code, c.hlast(),
+                       c.w_head_plain, c.w_hbias, c.w_emb, c.d_s1, c.d_lse, c.d_lse2, out);
+  };
+  if (mode == TB_IV) args(k_table16r<C, TB_IV, 0>);
+  else if (mode == TB_FREQ) stage == 1 ? args(k_table16r<C, TB_FREQ, 1>) : args(k_table16r<C, TB_FREQ, 2>);
+  else if (mode == TB_ENTRY) stage == 1 ? args(k_table16r<C, TB_ENTRY, 1>) : args(k_table16r<C, TB_ENTRY, 2>);
+  else stage == 1 ? args(k_table16r<C, TB_CDF, 1>) : args(k_table16r<C, TB_CDF, 2>);
+}
+
+bool table_regs(const Ctx& c) { return c.p.channels == 16 || c.p.channels == 32; }
+
+void run_table(Ctx& c, bool sixteen, int mode, int stage, int b, int b_lo, const uint8_t* code, uint16_t* out) {
+  if (sixteen)
+    c.p.channels == 32 ? run_table16r<32>(c, mode, stage, b, b_lo, code, out)
+                       : run_table16r<16>(c, mode, stage, b, b_lo, code, out);
+  else
+    c.p.channels == 32 ? run_table256r<32>(c, mode, b, b_lo, code, out)
+                       : run_table256r<16>(c, mode, b, b_lo, code, out);
+}
+
 hipError_t launch_symbol_freqs(Ctx& c, int b, uint16_t* freq) {
   ProfScope ps_(c, RENO_K_OTHER);
+  if (table_regs(c)) {
+    run_table(c, false, TB_FREQ, 0, b, b, nullptr, freq);
+    return hipGetLastError();
+  }
   hipLaunchKernelGGL(k_symbol_freqs, dim3(grid_for(c.cap_pts, 4)), dim3(256), 0, c.stream,
                      c.d_count, c.d_moff, b, c.cap_model, c.hlast(), c.p.channels, c.w_head_plain,
                      c.w_hbias, c.d_lse, freq);
@@ -510,6 +767,10 @@ hipError_t launch_symbol_freqs(Ctx& c, int b, uint16_t* freq) {
 
 hipError_t launch_symbol_freqs16(Ctx& c, int b, int stage, uint16_t* freq) {
   ProfScope ps_(c, RENO_K_OTHER);
+  if (table_regs(c)) {
+    run_table(c, true, TB_FREQ, stage, b, b, nullptr, freq);
+    return hipGetLastError();
+  }
   hipLaunchKernelGGL(k_symbol_freqs16, dim3(grid_for(c.cap_pts, 16)), dim3(256), 0, c.stream,
                      c.d_count, c.d_moff, b, stage, c.cap_model, c.hlast(), c.p.channels, c.w_head_plain,
                      c.w_hbias, c.w_emb, c.d_s1, c.d_lse, c.d_lse2, freq);
@@ -518,6 +779,10 @@ hipError_t launch_symbol_freqs16(Ctx& c, int b, int stage, uint16_t* freq) {
 
 hipError_t launch_symbol_cdf(Ctx& c, int b, int stage, uint16_t* start) {
   ProfScope ps_(c, RENO_K_OTHER);
+  if (table_regs(c)) {
+    run_table(c, stage != 0, TB_CDF, stage, b, b, nullptr, start);
+    return hipGetLastError();
+  }
   if (stage == 0)
     hipLaunchKernelGGL(k_symbol_cdf, dim3(grid_for(c.cap_pts, 4)), dim3(256), 0, c.stream,
                        c.d_count, c.d_moff, b, c.cap_model, c.hlast(), c.p.channels, c.w_head_plain,
@@ -529,13 +794,30 @@ hipError_t launch_symbol_cdf(Ctx& c, int b, int stage, uint16_t* start) {
   return hipGetLastError();
 }
 
+hipError_t launch_symbol_entries(Ctx& c, int b, int stage, uint32_t* entries, uint16_t* scratch) {
+  if (table_regs(c)) {
+    ProfScope ps_(c, RENO_K_OTHER);
+    run_table(c, stage != 0, TB_ENTRY, stage, b, b, nullptr, reinterpret_cast<uint16_t*>(entries));
+    return hipGetLastError();
+  }
+  hipError_t e = launch_symbol_cdf(c, b, stage, scratch);
+  if (e != hipSuccess) return e;
+  ProfScope ps_(c, RENO_K_OTHER);
+  const int K = stage == 0 ? 256 : 16;
+  hipLaunchKernelGGL(k_cdf_entries, dim3(grid_for(c.cap_pts * K, 256)), dim3(256), 0, c.stream, c.d_count, b, K,
+                     scratch, entries);
+  return hipGetLastError();
+}
+
 hipError_t launch_symbol_intervals(Ctx& c, int b_lo, int b_hi, uint16_t* iv) {
   ProfScope ps_(c, RENO_K_OTHER);
   const bool two = c.p.head_mode == RENO_HEAD_TWO_STAGE;
   // model rows of consecutive scales are consecutive, so each scale's output
   // starts at its model-row offset relative to b_lo (read on the device)
   for (int b = b_lo; b <= b_hi; ++b) {
-    if (two)
+    if (table_regs(c))
+      run_table(c, two, TB_IV, 0, b, b_lo, c.lv_code + c.lv(b), iv);
+    else if (two)
       hipLaunchKernelGGL(k_symbol_intervals16, dim3(grid_for(c.cap_pts, 16)), dim3(256), 0, c.stream,
                          c.d_count, c.d_moff, b, b_lo, c.cap_model, c.lv_code + c.lv(b), c.hlast(),
                          c.p.channels, c.w_head_plain, c.w_hbias, c.w_emb, c.d_lse, c.d_lse2, iv);

@@ -1,13 +1,15 @@
-"""Whole-frame coding (reno_encode_frame / reno_decode_frame), both heads, up
-to the full 14-bit scan.  The bitstream is checked piece by piece against the
-oracle: the header holds the oracle's bit depth, base scale and N_b0; the
-bit-packed base voxels are the oracle's V_b0 and O_b0; every stream of every
-scale and stage, decoded by the oracle's own rANS decoder with the encoder
-context's frequency tables, gives the oracle's codes of that stream's voxels.
-A fresh decoder context then rebuilds the frame from the bitstream alone:
-every scale's codes and V_B equal the oracle's.  Malformed bitstreams are
-rejected with RENO_E_INPUT and leave the context usable; an empty frame and a
-frame without model scales round-trip."""
+"""Whole-frame coding (reno_encode_frame / reno_decode_frame, the rANS
+streams coded and decoded on the GPU), both heads, up to the full 14-bit
+scan.  The bitstream is checked piece by piece against the oracle: the header
+holds the oracle's bit depth, base scale and N_b0; the bit-packed base voxels
+are the oracle's V_b0 and O_b0; every section holds ceil(N_b / L) streams, and
+every stream is word for word the oracle's own rANS encoding of the oracle's
+codes of that stream's voxels under the encoder context's frequency tables
+(and decodes back with the oracle's decoder).  A fresh decoder context then
+rebuilds the frame from the bitstream alone: every scale's codes and V_B equal
+the oracle's.  Malformed bitstreams are rejected with RENO_E_INPUT and leave
+the context usable; an empty frame and a frame without model scales
+round-trip; stream lengths from one symbol per stream to the 16-bit limit."""
 import numpy as np
 import pytest
 import torch
@@ -20,7 +22,6 @@ from synth import CONFIGS, gen_weights
 pytestmark = pytest.mark.gpu
 
 MAGIC = 0x4F4E4552
-S = 16
 
 
 def _ctx(cfg, n, two, w, B=None):
@@ -42,8 +43,13 @@ def _unpack_base(words, n0, b0):
 
 
 def _split_streams(words, pos, nstreams):
-    counts = words[pos:pos + nstreams].astype(np.int64)
-    pos += nstreams
+    """A section: nstreams 16-bit lengths (two per word, low half first), then the streams."""
+    nl = (nstreams + 1) // 2
+    half = np.stack([words[pos:pos + nl] & 0xFFFF, words[pos:pos + nl] >> 16], 1).reshape(-1)
+    counts = half[:nstreams].astype(np.int64)
+    if nstreams % 2:
+        assert half[nstreams] == 0                  # the unused high half is zero
+    pos += nl
     out = []
     for c in counts:
         out.append(words[pos:pos + c])
@@ -57,25 +63,28 @@ def _pad256(f16):
     return f
 
 
-@pytest.mark.parametrize("ci,two", [(0, False), (0, True), (2, False), (2, True)])
-def test_frame_bitstream_is_the_oracles_and_decodes(ci, two, scan_cache):
+@pytest.mark.parametrize("ci,two,L", [(0, False, 1024), (0, True, 1024), (0, False, 1), (0, True, 37),
+                                      (0, False, 65533), (2, False, 1024), (2, True, 1024), (2, False, 4096)])
+def test_frame_bitstream_is_the_oracles_and_decodes(ci, two, L, scan_cache):
     cfg = CONFIGS[ci]
     B, b0 = cfg.bit_depth, cfg.min_bit_depth
     pts = scan_cache(ci)
     w = gen_weights(cfg.channels, cfg.layers, seed=cfg.weight_seed + 3, bias_std=0.1, head_scale=4.0,
                     two_stage=two)
-    say("frame codec", cfg.name, "two-stage" if two else "one-stage")
+    say("frame codec", cfg.name, "two-stage" if two else "one-stage", "L =", L)
     P = oracle.Pyramid.from_points(pts, B, b0, cfg.range_m)
     enc = _ctx(cfg, len(pts), two, w)
-    words = enc.encode_frame(to_dev(pts), B, nstreams=S).copy()
+    words = enc.encode_frame(to_dev(pts), B, stream_symbols=L).copy()
     stages = 2 if two else 1
-    assert list(words[:6]) == [MAGIC, B, b0, stages, S, P.num(b0)]
+    assert list(words[:6]) == [MAGIC, B, b0, stages, L, P.num(b0)]
     xyz, code, nw = _unpack_base(words[6:], P.num(b0), b0)
     np.testing.assert_array_equal(xyz, P.xyz(b0))
     np.testing.assert_array_equal(code, P.codes(b0))
     pos = 6 + nw
+    nstreams = 0
     for b in range(b0 + 1, B):
         truth = P.codes(b)
+        S = max(1, -(-truth.size // L))
         for st in range(stages):
             streams, pos = _split_streams(words, pos, S)
             if two:
@@ -84,14 +93,21 @@ def test_frame_bitstream_is_the_oracles_and_decodes(ci, two, scan_cache):
             else:
                 f = enc.symbol_freqs(b).cpu().numpy().view(np.uint16).astype(np.uint32)
                 want = truth
-            for j in range(S):
+            # the oracle's rANS encoder on the oracle's symbols gives the same words
+            # (checked on every stream of small sections, a spread of them otherwise)
+            check = range(S) if S <= 64 else sorted(set(np.linspace(0, S - 1, 64).astype(int)))
+            for j in check:
+                ref = oracle.rans_encode(want[j::S], f[j::S])
+                np.testing.assert_array_equal(streams[j], ref, err_msg=f"b={b} stage={st} stream={j}")
                 got = oracle.rans_decode(streams[j], f[j::S], len(want[j::S]))
                 np.testing.assert_array_equal(got, want[j::S], err_msg=f"b={b} stage={st} stream={j}")
+            nstreams += S
     assert pos == words.size
     _, ideal = enc.code_length(reno.RENO_ALL_SCALES, per_voxel=False)
     body = 32 * (words.size - 6 - nw)
-    say(f"  {words.size} words; model scales {body} bits vs ideal {ideal:.0f}")
-    assert body <= ideal * 1.001 + 32 * S * stages * (B - b0 - 1) * 3
+    say(f"  {words.size} words, {nstreams} streams; model scales {body} bits vs ideal {ideal:.0f}")
+    # flush words and 16-bit lengths of every stream on top of the table length
+    assert body <= ideal * 1.001 + 96 * nstreams + 32 * stages * (B - b0 - 1)
     # decoding from the bitstream alone
     dec = _ctx(cfg, len(pts), two, w)
     dec.decode_frame(words)
@@ -103,7 +119,7 @@ def test_frame_bitstream_is_the_oracles_and_decodes(ci, two, scan_cache):
     if ci == 0:
         pts2 = scan_cache(ci, 1) if cfg.frames > 1 else pts[: len(pts) // 2]
         P2 = oracle.Pyramid.from_points(pts2, B, b0, cfg.range_m)
-        w2 = enc.encode_frame(to_dev(pts2), B, nstreams=3)
+        w2 = enc.encode_frame(to_dev(pts2), B, stream_symbols=300)
         dec.decode_frame(w2)
         np.testing.assert_array_equal(dec.coords(B)[0].cpu().numpy(), P2.xyz(B))
     enc.close()
@@ -127,7 +143,8 @@ def test_frame_codec_rejects_malformed_bitstreams(two, scan_cache):
         "extra word": np.append(words, np.uint32(7)),
         "magic": np.concatenate([[np.uint32(0x12345678)], words[1:]]),
         "bit depth": np.concatenate([words[:1], [np.uint32(B + 30)], words[2:]]),
-        "stream count": np.concatenate([words[:4], [np.uint32(0)], words[5:]]),
+        "stream length 0": np.concatenate([words[:4], [np.uint32(0)], words[5:]]),
+        "stream length 2^16": np.concatenate([words[:4], [np.uint32(65536)], words[5:]]),
         "header only": words[:6],
         "short": words[:3],
     }
@@ -166,9 +183,10 @@ def test_frame_codec_empty_and_single_scale(two, scan_cache):
     dec = _ctx(cfg, len(pts), two, w)
     empty = enc.encode_frame(torch.zeros((0, 3), dtype=torch.float32, device="cuda"), cfg.bit_depth)
     stages = 2 if two else 1
-    assert list(empty[:6]) == [MAGIC, cfg.bit_depth, b0, stages, 16, 0]
-    # every model scale and stage: S counts of 2 and the S empty streams' two flush words
-    assert empty.size == 6 + (cfg.bit_depth - b0 - 1) * stages * 3 * 16
+    assert list(empty[:6]) == [MAGIC, cfg.bit_depth, b0, stages, 1024, 0]
+    # every model scale and stage: one empty stream (its length word, its two flush words)
+    assert empty.size == 6 + (cfg.bit_depth - b0 - 1) * stages * 3
+    assert list(empty[6:9]) == [2, 0, 1 << 31]
     dec.decode_frame(empty)
     assert dec.coords(cfg.bit_depth)[0].shape[0] == 0
     # bit depth b0 + 1: the base scale and its codes only, no model scale
