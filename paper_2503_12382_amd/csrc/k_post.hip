@@ -424,31 +424,68 @@ enum { TB_FREQ = 0, TB_CDF = 1, TB_IV = 2, TB_ENTRY = 3 };
 
 __device__ __forceinline__ int uniform_wave() { return __builtin_amdgcn_readfirstlane((int)(threadIdx.x >> 6)); }
 
-// frequencies of symbols 4 lane .. 4 lane + 3 from their logits (the
-// quantisation of table256)
-__device__ __forceinline__ void quantise256(const float (&z)[4], float l, int lane, uint32_t (&f)[4]) {
-  uint32_t sum = 0, best = 0;
-  int besti = 0;
+// DPP lane moves (CDNA): row_shr:k (0x110 + k) takes the value of lane
+// l - k of the same 16-lane row, row_ror:k (0x120 + k) of lane l - k mod 16
+// of the row, row_bcast:15 (0x142) lane 15 of the previous row, row_bcast:31
+// (0x143) lane 31.  Lanes whose source lies outside are fixed by the callers.
+template <int CTRL>
+__device__ __forceinline__ uint32_t dpp(uint32_t v) {
+  return (uint32_t)__builtin_amdgcn_mov_dpp((int)v, CTRL, 0xF, 0xF, false);
+}
+
+// The moves run in every lane and their results are masked with bit
+// operations: a move under a lane mask would read disabled source lanes.
+__device__ __forceinline__ uint32_t keep(bool c) { return c ? 0xFFFFFFFFu : 0u; }
+
+// inclusive prefix sum over the 64 lanes
+__device__ __forceinline__ uint32_t scan_add64(uint32_t v, int lane) {
+  const int r = lane & 15;
+  v += dpp<0x111>(v) & keep(r >= 1);
+  v += dpp<0x112>(v) & keep(r >= 2);
+  v += dpp<0x114>(v) & keep(r >= 4);
+  v += dpp<0x118>(v) & keep(r >= 8);
+  v += dpp<0x142>(v) & keep((lane & 31) >= 16);
+  v += dpp<0x143>(v) & keep(lane >= 32);
+  return v;
+}
+
+// running maximum over the 64 lanes (lane 63 ends with the maximum)
+__device__ __forceinline__ uint32_t scan_max64(uint32_t v, int lane) {
+  const int r = lane & 15;
+  v = max(v, dpp<0x111>(v) & keep(r >= 1));
+  v = max(v, dpp<0x112>(v) & keep(r >= 2));
+  v = max(v, dpp<0x114>(v) & keep(r >= 4));
+  v = max(v, dpp<0x118>(v) & keep(r >= 8));
+  v = max(v, dpp<0x142>(v) & keep((lane & 31) >= 16));
+  v = max(v, dpp<0x143>(v) & keep(lane >= 32));
+  return v;
+}
+
+// Quantisation of table256 from the logits of symbols 4 lane .. 4 lane + 3:
+// f_s = 1 + floor(p_s (2^16 - 512)), the leftover 2^16 - sum f to the
+// lowest-index largest f_s.  Returns the final f of the lane's symbols and
+// the start (sum of the final f below) of its first symbol.
+__device__ __forceinline__ uint32_t quantise256(const float (&z)[4], float l, int lane, uint32_t (&f)[4]) {
+  uint32_t lmax = 0, lsum = 0;
+  int lidx = 0;
   for (int e = 0; e < 4; ++e) {
     const float p = __expf(z[e] - l);
     f[e] = 1u + (uint32_t)floorf(p * 65024.0f);
-    sum += f[e];
-    if (f[e] > best) {
-      best = f[e];
-      besti = lane * 4 + e;
+    lsum += f[e];
+    if (f[e] > lmax) {
+      lmax = f[e];
+      lidx = e;
     }
   }
-  for (int o = 32; o > 0; o >>= 1) {
-    sum += (uint32_t)__shfl_xor((int)sum, o);
-    const uint32_t ob = (uint32_t)__shfl_xor((int)best, o);
-    const int oi = __shfl_xor(besti, o);
-    if (ob > best || (ob == best && oi < besti)) {
-      best = ob;
-      besti = oi;
-    }
-  }
-  const uint32_t left = 65536u - sum;
-  for (int e = 0; e < 4; ++e) f[e] += (lane * 4 + e == besti) ? left : 0u;
+  const uint32_t incl = scan_add64(lsum, lane);
+  const uint32_t total = (uint32_t)__builtin_amdgcn_readlane((int)incl, 63);
+  const uint32_t gmax = (uint32_t)__builtin_amdgcn_readlane((int)scan_max64(lmax, lane), 63);
+  const uint64_t ball = __ballot(lmax == gmax);
+  const int l0 = __ffsll((long long)ball) - 1;  // lowest lane holding the maximum
+  const int besti = 4 * l0 + __builtin_amdgcn_readlane(lidx, l0);
+  const uint32_t left = 65536u - total;
+  for (int e = 0; e < 4; ++e) f[e] += (4 * lane + e == besti) ? left : 0u;
+  return incl - lsum + (besti < 4 * lane ? left : 0u);
 }
 
 template <int C, int MODE>
@@ -485,18 +522,11 @@ __global__ void __launch_bounds__(256) k_table256r(const int32_t* __restrict__ c
       for (int e = 0; e < 4; ++e) z[e] = fmaf(w[c][e], hc, z[e]);
     }
     uint32_t f[4];
-    quantise256(z, lse[mo + v], lane, f);
+    uint32_t st = quantise256(z, lse[mo + v], lane, f);
     if constexpr (MODE == TB_FREQ) {
       uint16_t* dst = out + v * 256 + lane * 4;
       for (int e = 0; e < 4; ++e) dst[e] = (uint16_t)f[e];
     } else {
-      const uint32_t mine = f[0] + f[1] + f[2] + f[3];
-      uint32_t inc = mine;  // inclusive prefix over lanes
-      for (int d = 1; d < 64; d <<= 1) {
-        const uint32_t t = (uint32_t)__shfl_up((int)inc, d);
-        if (lane >= d) inc += t;
-      }
-      uint32_t st = inc - mine;
       if constexpr (MODE == TB_CDF) {
         uint16_t* dst = out + v * 256 + lane * 4;
         for (int e = 0; e < 4; ++e) {
@@ -526,23 +556,36 @@ __global__ void __launch_bounds__(256) k_table256r(const int32_t* __restrict__ c
   }
 }
 
-// 16-symbol table of the voxel of this lane's group from its logit z (the
-// quantisation of table16); returns f_s
-__device__ __forceinline__ uint32_t quantise16(float z, float l, int s) {
+// 16-symbol table of the voxel of this lane's row (16 lanes, s = lane % 16)
+// from its logit z (the quantisation of table16): returns f_s and its
+// exclusive start in the row.  Row totals by rotations, the start by row
+// shifts.
+__device__ __forceinline__ uint32_t quantise16(float z, float l, int lane, uint32_t* start) {
+  const int s = lane & 15;
   const float p = __expf(z - l);
   uint32_t f = 1u + (uint32_t)floorf(p * 65504.0f);
-  uint32_t sum = f, best = f;
-  int besti = s;
-  for (int o = 1; o < 16; o <<= 1) {
-    sum += (uint32_t)__shfl_xor((int)sum, o);
-    const uint32_t ob = (uint32_t)__shfl_xor((int)best, o);
-    const int oi = __shfl_xor(besti, o);
-    if (ob > best || (ob == best && oi < besti)) {
-      best = ob;
-      besti = oi;
-    }
-  }
-  return f + (s == besti ? 65536u - sum : 0u);
+  uint32_t sum = f, mx = f;
+  sum += dpp<0x128>(sum);  // row_ror:8, 4, 2, 1: every lane ends with the row total
+  sum += dpp<0x124>(sum);
+  sum += dpp<0x122>(sum);
+  sum += dpp<0x121>(sum);
+  mx = max(mx, dpp<0x128>(mx));
+  mx = max(mx, dpp<0x124>(mx));
+  mx = max(mx, dpp<0x122>(mx));
+  mx = max(mx, dpp<0x121>(mx));
+  // the lowest symbol of the row holding the maximum
+  const uint64_t ball = __ballot(f == mx);
+  const uint32_t rowbits = (uint32_t)(ball >> (lane & 48)) & 0xFFFFu;
+  const int besti = __ffs(rowbits) - 1;
+  const uint32_t left = 65536u - sum;
+  f += s == besti ? left : 0u;
+  uint32_t inc = f;  // inclusive prefix within the row
+  inc += dpp<0x111>(inc) & keep(s >= 1);
+  inc += dpp<0x112>(inc) & keep(s >= 2);
+  inc += dpp<0x114>(inc) & keep(s >= 4);
+  inc += dpp<0x118>(inc) & keep(s >= 8);
+  *start = inc - f;
+  return f;
 }
 
 // Two-stage tables: STAGE 1 or 2 (MODE TB_FREQ / TB_CDF), or both stages'
@@ -577,12 +620,13 @@ __global__ void __launch_bounds__(256) k_table16r(const int32_t* __restrict__ co
     const int64_t pr = mo + (v < n ? v : n - 1);
     const float* h = hL + pr * C;
     const int o = MODE == TB_IV ? (int)code[v < n ? v : n - 1] : 0;
-    uint32_t f1 = 0, f2 = 0;
+    const int lane = threadIdx.x & 63;
+    uint32_t f1 = 0, f2 = 0, st1 = 0, st2 = 0;
     if constexpr (ONE) {
       float z = b1;
 #pragma unroll
       for (int c = 0; c < C; ++c) z = fmaf(w1[c], h[c], z);
-      f1 = quantise16(z, lse[pr], s);
+      f1 = quantise16(z, lse[pr], lane, &st1);
     }
     if constexpr (TWO) {
       const int a1 = MODE == TB_IV ? (o & 15) : (int)s1[pr];
@@ -590,19 +634,16 @@ __global__ void __launch_bounds__(256) k_table16r(const int32_t* __restrict__ co
       float z = b2;
 #pragma unroll
       for (int c = 0; c < C; ++c) z = fmaf(w2[c], h[c] + e[c], z);
-      f2 = quantise16(z, lse2[pr], s);
+      f2 = quantise16(z, lse2[pr], lane, &st2);
     }
     if constexpr (MODE == TB_FREQ) {
       if (v < n) out[v * 16 + s] = (uint16_t)(STAGE == 1 ? f1 : f2);
     } else if constexpr (MODE == TB_CDF) {
-      const uint32_t st = excl16(STAGE == 1 ? f1 : f2, s);
-      if (v < n) out[v * 16 + s] = (uint16_t)st;
+      if (v < n) out[v * 16 + s] = (uint16_t)(STAGE == 1 ? st1 : st2);
     } else if constexpr (MODE == TB_ENTRY) {
-      const uint32_t f = STAGE == 1 ? f1 : f2;
-      const uint32_t st = excl16(f, s);
+      const uint32_t f = STAGE == 1 ? f1 : f2, st = STAGE == 1 ? st1 : st2;
       if (v < n) reinterpret_cast<uint32_t*>(out)[v * 16 + s] = st | (f << 16);
     } else {
-      const uint32_t st1 = excl16(f1, s), st2 = excl16(f2, s);
       const int64_t ro = mo - moff[b_lo] + v;  // row in the concatenated output
       if (v < n && s == (o & 15)) {
         out[ro * 4] = (uint16_t)st1;
