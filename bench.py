@@ -795,12 +795,22 @@ def main():
             te, td, bits = ee.run(args.e2e_frames)
             e2e[name] = {"encode_frames_per_s": round(1.0 / te, 2), "decode_frames_per_s": round(1.0 / td, 2),
                          "encode_ms": round(1000 * te, 3), "decode_ms": round(1000 * td, 3),
-                         "coded_bits_per_point": round(bits / M, 4)}
+                         "coded_bits_per_point": round(bits / M, 4), "stream_symbols": STREAM_SYMBOLS}
             log("end-to-end", name, e2e[name])
+            # shorter streams: more of them decode in parallel, each costs its
+            # final state and length (80 bits)
+            trade = []
+            for L in (256, 512, 2048):
+                ee.L = L
+                te2, td2, bits2 = ee.run(max(args.e2e_frames // 2, 2))
+                trade.append({"stream_symbols": L, "encode_ms": round(1000 * te2, 3),
+                              "decode_ms": round(1000 * td2, 3), "coded_bits_per_point": round(bits2 / M, 4)})
+            e2e[name]["stream_length_tradeoff"] = trade
+            log("end-to-end", name, "stream lengths", trade)
             ee.close()
         e2e["note"] = ("wall-clock per frame through reno_encode_frame / reno_decode_frame: points copied in "
                        "from pinned host memory; GPU pyramid + model + symbol intervals + rANS streams "
-                       f"(ceil(N_b / {STREAM_SYMBOLS}) streams per scale and stage, one thread each), bitstream "
+                       f"(ceil(N_b / {STREAM_SYMBOLS}) streams per scale and stage, one wavefront each), bitstream "
                        "copied out; the decoder starts from the host bitstream alone, copies it in once and runs "
                        "expand, predict, cumulative tables and stream decoding (one wavefront per stream) scale "
                        "by scale on the GPU; coded bits = the whole bitstream (header, bit-packed base voxels, "
