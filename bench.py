@@ -439,6 +439,59 @@ class EndToEnd:
         self.dec.close()
 
 
+def e2e_in_flight(reno, torch, args, dev, workers=(1, 2, 4, 8), per_worker=12):
+    """Throughput of whole-frame coding with W frames in flight: W host
+    threads (the library's calls release the interpreter), each encoding and
+    decoding its share of the streaming workload's scans through its own pair
+    of contexts on its own stream; every decoded frame is checked."""
+    from concurrent.futures import ThreadPoolExecutor
+    from synth import BY_NAME, gen_scan, gen_weights
+    mcfg = BY_NAME[args.stream_config]
+    scans = [gen_scan(mcfg, f) for f in range(mcfg.frames)]
+    w = reno.weights_to_device(gen_weights(mcfg.channels, mcfg.layers, seed=mcfg.weight_seed))
+    M = max(f.shape[0] for f in scans)
+    out = {"workload": f"{mcfg.name}: its {mcfg.frames} distinct scans cycled, one-stage head, "
+                       f"L = {STREAM_SYMBOLS}, each frame encoded to host memory and decoded from it", "runs": []}
+    for W in workers:
+        lanes = []
+        for i in range(W):
+            st = torch.cuda.Stream(device=dev)
+            with torch.cuda.stream(st):
+                mk = lambda: reno.Context(M, mcfg.bit_depth, mcfg.min_bit_depth, mcfg.range_m, mcfg.channels,
+                                          mcfg.layers, stream=st)
+                enc, dec = mk(), mk()
+                enc.set_weights(w)
+                dec.set_weights(w)
+                pts = [torch.from_numpy(scans[(i + k * W) % len(scans)]).to(dev) for k in range(per_worker)]
+            lanes.append((st, enc, dec, pts, np.empty(2 * M + 65536, np.uint32)))
+        torch.cuda.synchronize()
+
+        def work(lane, check=False):
+            st, enc, dec, pts, buf = lane
+            with torch.cuda.stream(st):
+                for p in pts:
+                    words = enc.encode_frame(p, mcfg.bit_depth, stream_symbols=STREAM_SYMBOLS, out=buf)
+                    dec.decode_frame(words)
+                    if check and not torch.equal(dec.coords(mcfg.bit_depth)[0], enc.coords(mcfg.bit_depth)[0]):
+                        return False
+            return True
+
+        with ThreadPoolExecutor(max_workers=W) as ex:
+            if not all(ex.map(lambda l: work(l, True), lanes)):      # warm-up pass, every frame checked
+                log("end-to-end in flight: decoded frame differs from the input")
+                sys.exit(1)
+            t = time.perf_counter()
+            list(ex.map(work, lanes))
+            dt = time.perf_counter() - t
+        n = W * per_worker
+        out["runs"].append({"frames_in_flight": W, "frames": n, "frames_per_s": round(n / dt, 1),
+                            "ms_per_frame": round(1000 * dt / n, 3)})
+        for _, enc, dec, _, _ in lanes:
+            enc.close()
+            dec.close()
+    return out
+
+
 def run_stress(args, reno, torch, dev, stream, copy_peak=None):
     """HBM stress: K frames of the streaming generator (its distinct frames,
     cycled) batched into one key space, frame id above the Morton bits; one
@@ -808,6 +861,12 @@ def main():
             e2e[name]["stream_length_tradeoff"] = trade
             log("end-to-end", name, "stream lengths", trade)
             ee.close()
+        # frames in flight: W host threads, each with its own encoder and
+        # decoder context on its own HIP stream, coding the streaming
+        # workload's distinct scans; a frame's coder kernels occupy few CUs,
+        # so frames overlap
+        e2e["frames_in_flight"] = e2e_in_flight(reno, torch, args, dev)
+        log("end-to-end frames in flight", e2e["frames_in_flight"])
         e2e["note"] = ("wall-clock per frame through reno_encode_frame / reno_decode_frame: points copied in "
                        "from pinned host memory; GPU pyramid + model + symbol intervals + rANS streams "
                        f"(ceil(N_b / {STREAM_SYMBOLS}) streams per scale and stage, one wavefront each), bitstream "
