@@ -439,7 +439,7 @@ class EndToEnd:
         self.dec.close()
 
 
-def e2e_in_flight(reno, torch, args, dev, workers=(1, 2, 4, 8), per_worker=12):
+def e2e_in_flight(reno, torch, args, dev, workers=(1, 2, 3, 4, 8), per_worker=12):
     """Throughput of whole-frame coding with W frames in flight: W host
     threads (the library's calls release the interpreter), each encoding and
     decoding its share of the streaming workload's scans through its own pair
@@ -452,10 +452,13 @@ def e2e_in_flight(reno, torch, args, dev, workers=(1, 2, 4, 8), per_worker=12):
     M = max(f.shape[0] for f in scans)
     out = {"workload": f"{mcfg.name}: its {mcfg.frames} distinct scans cycled, one-stage head, "
                        f"L = {STREAM_SYMBOLS}, each frame encoded to host memory and decoded from it", "runs": []}
+    # the streams are created once, together, so that the first few land on
+    # different hardware queues (the runtime hands queues out in turn)
+    pool = [torch.cuda.Stream(device=dev) for _ in range(max(workers))]
     for W in workers:
         lanes = []
         for i in range(W):
-            st = torch.cuda.Stream(device=dev)
+            st = pool[i]
             with torch.cuda.stream(st):
                 mk = lambda: reno.Context(M, mcfg.bit_depth, mcfg.min_bit_depth, mcfg.range_m, mcfg.channels,
                                           mcfg.layers, stream=st)
