@@ -402,8 +402,12 @@ __device__ __forceinline__ void find_symbol(const Table<K>& tb, uint32_t slot, i
 // register window of the stream (a lane read), and stores its symbol to LDS;
 // the trip's symbols are written out together at its end (with the trip's S1
 // values for stage 2).  Full trips run without per-step bounds; the last,
-// partial trip checks them.  A stream that runs past its end reads zeros and
-// is caught by the final check of its length and state.
+// partial trip checks them.  The window moves between trips only: a trip
+// reads at most 64 words, from the two registers win0 and win1 (128 words),
+// while the third, win2, is loaded a whole trip ahead (unconditionally, at
+// a fixed point), so that no step waits on a window load issued after its
+// own table loads.  A stream that runs past its end reads its last word
+// again and is caught by the final check of its length and state.
 template <int K, bool S1>
 __global__ void __launch_bounds__(64 * kDecWaves) k_rans_decode(DecArgs a, const uint32_t* __restrict__ words,
                                                                 const uint32_t* __restrict__ tab,
@@ -459,11 +463,16 @@ __global__ void __launch_bounds__(64 * kDecWaves) k_rans_decode(DecArgs a, const
   const int i_last = m > 0 ? ws + (m - 1) * Ss : 0;
   uint64_t x = ((uint64_t)in[0] << 32) | in[1];
   int p = 2;
-  // renormalisation words: lane l of win0 holds word wb + l, win1 the next
-  // 64 (zero past the stream's end)
+  // renormalisation words: lane l of win0 holds word wb + l, win1 and win2
+  // the next 64 each (the last word repeated past the stream's end, so that
+  // the loads are unconditional)
   int wb = 2;
-  auto word_at = [&](int q) -> uint32_t { return q < lens ? in[q] : 0u; };
+  auto word_at = [&](int q) -> uint32_t { return in[min(q, lens - 1)]; };
   uint32_t win0 = word_at(wb + lane), win1 = word_at(wb + 64 + lane);
+  // both complete before any table load is issued: the trips' window reads
+  // then never wait behind the table loads in flight
+  __builtin_amdgcn_s_waitcnt(0);
+  uint32_t win2 = word_at(wb + 128 + lane);
   Table<K> ring[kRing];
 #pragma unroll
   for (int u = 0; u < kRing; ++u) ring[u] = load_table<K>(tab, min(ws + u * Ss, i_last), lane);
@@ -489,12 +498,10 @@ __global__ void __launch_bounds__(64 * kDecWaves) k_rans_decode(DecArgs a, const
         find_symbol<K>(cur, slot, lane, &sym, &lo_s, &f_s);
         x = (uint64_t)f_s * (x >> kProb) + slot - lo_s;
         if ((uint32_t)(x >> 31) == 0) {  // x < 2^31 (x < 2^63 always)
-          x = (x << 32) | rdl(win0, p - wb);
-          if (++p - wb == 64) {  // next window (uniform, once per 64 words)
-            wb += 64;
-            win0 = win1;
-            win1 = word_at(wb + 64 + lane);
-          }
+          const int q = p - wb;          // below 128 inside a trip
+          const uint32_t w0 = rdl(win0, q & 63), w1 = rdl(win1, q & 63);
+          x = (x << 32) | (q < 64 ? w0 : w1);
+          ++p;
         }
         // every lane stores the same byte: no lane mask to set up
         ssymb[u] = (uint8_t)sym;
@@ -504,6 +511,13 @@ __global__ void __launch_bounds__(64 * kDecWaves) k_rans_decode(DecArgs a, const
     // are visible here
     const uint32_t symv = ssymb[lane];
     if (!GUARD || k0 + lane < m) out[i_mine] = (uint8_t)(S1 ? (s1v | (symv << 4)) : symv);
+    // the window moves on once its first 64 words are used up; win2 is
+    // reloaded either way (the same words when the window did not move)
+    const bool shift = p - wb >= 64;  // uniform
+    win0 = shift ? win1 : win0;
+    win1 = shift ? win2 : win1;
+    wb = shift ? wb + 64 : wb;
+    win2 = word_at(wb + 128 + lane);
   };
   const int full = m & ~63;
   for (int k0 = 0; k0 < full; k0 += 64) trip(k0, std::false_type{});
