@@ -387,42 +387,73 @@ struct Staged {
 // first-child row, from which every neighbour row follows by the FCG order.
 // par is the 8-entry LDS slot of voxel r (shared by the 4 lanes of r); the
 // lane ends with the rows of offsets 8g .. 8g+7 (-1: absent or off-grid).
+//
+// The cells are stepped to directly on the Morton key (dilated-integer
+// increments and decrements of one axis's bits), so no coordinate is ever
+// unpacked; a step off the grid leaves the probe empty, and every neighbour
+// in such a cell reads as absent, so the offsets need no bounds of their own.
+
+// Per entry slot j of the 8 a lane holds, the four lane groups' offsets
+// k = 8g + j packed one byte each: bit 6 the offset exists (k < 27), bits 3..5
+// the axes it moves up, bits 0..2 the axes it moves at all (k = dx+1 +
+// 3 (dy+1) + 9 (dz+1)).
+__host__ __device__ constexpr uint32_t offset_moves(int j) {
+  uint32_t v = 0;
+  for (int g = 0; g < 4; ++g) {
+    const int k = 8 * g + j;
+    if (k < 27) {
+      const int dx = k % 3 - 1, dy = (k / 3) % 3 - 1, dz = k / 9 - 1;
+      const uint32_t nz = (dx != 0 ? 1u : 0u) | (dy != 0 ? 2u : 0u) | (dz != 0 ? 4u : 0u);
+      const uint32_t up = (dx == 1 ? 1u : 0u) | (dy == 1 ? 2u : 0u) | (dz == 1 ? 4u : 0u);
+      v |= (64u | (up << 3) | nz) << (8 * g);
+    }
+  }
+  return v;
+}
+
+// One step of the cell with Morton key k (axis bits m) towards +1 (up) or -1
+// along that axis; `off` is set when the step leaves the grid.
+__device__ __forceinline__ uint64_t morton_step(uint64_t k, uint64_t m, bool up, bool& off) {
+  const uint64_t a = k & m, rest = k & ~m;
+  off = up ? a == m : a == 0ull;
+  const uint64_t na = up ? ((a | ~m) + 1ull) & m : (a - 1ull) & m;
+  return na | rest;
+}
+
 __device__ __forceinline__ void parent_cell_rows(uint64_t kf, int b, int g, const HashSlot* __restrict__ hash,
                                                  int hash_lg, const uint64_t* __restrict__ hreg, int fb,
                                                  volatile uint64_t* par, int32_t (&nb)[8]) {
   const uint64_t key = morton_part(kf, b), fr = frame_part(kf, b) << (3 * (b - 1));
-  const int x = (int)compact3(key), y = (int)compact3(key >> 1), z = (int)compact3(key >> 2);
-  const int px = x >> 1, py = y >> 1, pz = z >> 1;
-  const int sx = (x & 1) ? 1 : -1, sy = (y & 1) ? 1 : -1, sz = (z & 1) ? 1 : -1;
-  const int plim = 1 << (b - 1);
+  const uint32_t oct = (uint32_t)key & 7u;  // v's octant in its parent: the side of each neighbour cell
+  const uint64_t pk = key >> 3;
+  const uint64_t all = (1ull << (3 * (b - 1))) - 1ull;
+  const uint64_t mx = 0x1249249249249249ull & all, my = (mx << 1) & all, mz = (mx << 2) & all;
+  // lane group g probes cells 2g and 2g + 1: the y and z steps of g, then x
+  bool off_y = false, off_z = false, off_x = false;
+  uint64_t c0 = pk;
+  if (g & 1) c0 = morton_step(c0, my, (oct & 2u) != 0u, off_y);
+  if (g & 2) c0 = morton_step(c0, mz, (oct & 4u) != 0u, off_z);
+  const uint64_t c1 = morton_step(c0, mx, (oct & 1u) != 0u, off_x);
+  const bool ok0 = !(off_y || off_z), ok1 = ok0 && !off_x;
   uint64_t tk[2];
-#pragma unroll
-  for (int i = 0; i < 2; ++i) {
-    const int e = 2 * g + i;
-    const int cx = px + ((e & 1) ? sx : 0), cy = py + ((e & 2) ? sy : 0), cz = pz + ((e & 4) ? sz : 0);
-    tk[i] = (cx >= 0 && cy >= 0 && cz >= 0 && cx < plim && cy < plim && cz < plim)
-                ? tag_key(fr | morton3((uint32_t)cx, (uint32_t)cy, (uint32_t)cz), b - 1, fb)
-                : 0ull;
-  }
+  tk[0] = ok0 ? tag_key(fr | c0, b - 1, fb) : 0ull;
+  tk[1] = ok1 ? tag_key(fr | c1, b - 1, fb) : 0ull;
   uint2 hit[2];
   hash_find_n<2>(hash, hash_lg, hash_region(hreg, hash_lg, frame_part(kf, b)), tk, hit);
   // cross-lane exchange through LDS (volatile: every read goes to LDS)
   par[2 * g] = ((uint64_t)hit[0].y << 32) | hit[0].x;
   par[2 * g + 1] = ((uint64_t)hit[1].y << 32) | hit[1].x;
   __builtin_amdgcn_wave_barrier();
-  const int lim = 1 << b;
 #pragma unroll
   for (int j = 0; j < 8; ++j) {
-    const int k = 8 * g + j;
-    const int ux = x + (k % 3) - 1, uy = y + (k / 3) % 3 - 1, uz = z + (k / 9) % 3 - 1;
-    nb[j] = -1;
-    if (k < 27 && ux >= 0 && uy >= 0 && uz >= 0 && ux < lim && uy < lim && uz < lim) {
-      const int e = ((ux >> 1) != px ? 1 : 0) | ((uy >> 1) != py ? 2 : 0) | ((uz >> 1) != pz ? 4 : 0);
-      const uint64_t pc = par[e];
-      const uint32_t first = (uint32_t)pc, code = (uint32_t)(pc >> 32);
-      const uint32_t d = (uint32_t)((ux & 1) | ((uy & 1) << 1) | ((uz & 1) << 2));
-      if ((code >> d) & 1u) nb[j] = (int32_t)first + __popc(code & ((1u << d) - 1u));
-    }
+    const uint32_t c = (offset_moves(j) >> (8 * g)) & 0xFFu;
+    const uint32_t nz = c & 7u, up = (c >> 3) & 7u;
+    // the parent-scale cell of the neighbour: a moved axis leaves v's parent
+    // when the move points to v's side; its octant flips every moved axis
+    const uint32_t e = nz & ~(oct ^ up), d = oct ^ nz;
+    const uint64_t pc = par[e];
+    const uint32_t first = (uint32_t)pc, code = (uint32_t)(pc >> 32);
+    nb[j] = ((c & 64u) && ((code >> d) & 1u)) ? (int32_t)(first + __popc(code & ((1u << d) - 1u))) : -1;
   }
 }
 
@@ -598,12 +629,18 @@ __global__ void __launch_bounds__(CONV_THREADS) k_conv(ConvArgs a) {
   __shared__ __attribute__((aligned(16))) float s_w[WSZ];
   __shared__ __attribute__((aligned(16))) float s_h[HSZ];
   __shared__ uint64_t s_par[FIRST ? CONV_WAVES : 1][16][8];  // per wave: parent cells (code<<32|first)
+  // per wave: the tile's neighbour rows, voxel by voxel (32 entries, the last 5 are -1), so that
+  // a lane reads the row of any offset directly (the last layer has no room for them)
+  constexpr bool ROWS = FIRST && !LAST;
+  __shared__ int32_t s_rows[ROWS ? CONV_WAVES : 1][16][32];
   __shared__ int64_t s_tpre[NLEV + 1];
   __shared__ int64_t s_nv[NLEV];   // N_b of the launch's scales
   __shared__ int64_t s_mo[NLEV];   // first packed row of each scale
   __shared__ int s_next;           // next dynamically handed-out tile slot of this block
 
-  const int tid = threadIdx.x, w = tid >> 6, lane = tid & 63;
+  // the wave index through a lane read: the compiler then keeps the tile loop,
+  // the offset sets and the group folds in scalar registers and branches
+  const int tid = threadIdx.x, w = __builtin_amdgcn_readfirstlane(tid >> 6), lane = tid & 63;
   const int r = lane & 15, g = lane >> 4;
   const int nsc = a.b_hi - a.b_lo + 1;
 
@@ -701,6 +738,12 @@ __global__ void __launch_bounds__(CONV_THREADS) k_conv(ConvArgs a) {
       nlo = src[0];
       nhi = src[1];
     }
+    if constexpr (ROWS) {
+      int4* rr = reinterpret_cast<int4*>(&s_rows[w][r][8 * g]);
+      rr[0] = nlo;
+      rr[1] = nhi;
+      __builtin_amdgcn_wave_barrier();
+    }
     // occupied offsets of the tile: one ballot per entry slot j, lanes of
     // group g covering offsets 8g + j (the 5 padding entries are -1)
     uint32_t offs = 0;
@@ -753,7 +796,10 @@ __global__ void __launch_bounds__(CONV_THREADS) k_conv(ConvArgs a) {
     auto gather = [&](const int (&ks)[PCH], G (&gb)[PCH]) {
       int32_t nn[PCH];
 #pragma unroll
-      for (int c = 0; c < PCH; ++c) nn[c] = __shfl(pick8(nlo, nhi, ks[c] & 7), r + 16 * ((ks[c] & 31) >> 3));
+      for (int c = 0; c < PCH; ++c) {
+        if constexpr (ROWS) nn[c] = s_rows[w][r][ks[c] & 31];
+        else nn[c] = __shfl(pick8(nlo, nhi, ks[c] & 7), r + 16 * ((ks[c] & 31) >> 3));
+      }
       __builtin_amdgcn_sched_barrier(0);  // keep the exchanges back to back (one wait for all)
 #pragma unroll
       for (int c = 0; c < PCH; ++c) {
