@@ -457,6 +457,8 @@ __device__ __forceinline__ void parent_cell_rows(uint64_t kf, int b, int g, cons
   }
 }
 
+constexpr float LOG2E_F = 1.4426950408889634f;
+
 // One group of 64 symbols of the 256-way head (symbol blocks 4 grp .. 4 grp
 // + 3, 16 symbols each): logits z = H^T h + b on MFMA from the accumulator
 // layout of h, stored when requested, and the group's normaliser terms per
@@ -491,11 +493,14 @@ __device__ __forceinline__ void head_group(const ConvArgs& a, const f4 (&acc)[C 
   for (int q4 = 0; q4 < 4; ++q4)
 #pragma unroll
     for (int e = 0; e < 4; ++e) gm = fmaxf(gm, zz[q4][e]);
-  part = 0.0f;
+  // exp(z - gm) as 2^(z log2(e) - gm log2(e)): one fused multiply-add per term
+  const float gml = gm * LOG2E_F;
+  part = __builtin_amdgcn_exp2f(fmaf(zz[0][0], LOG2E_F, -gml));
 #pragma unroll
   for (int q4 = 0; q4 < 4; ++q4)
 #pragma unroll
-    for (int e = 0; e < 4; ++e) part += __expf(zz[q4][e] - gm);
+    for (int e = 0; e < 4; ++e)
+      if (q4 || e) part += __builtin_amdgcn_exp2f(fmaf(zz[q4][e], LOG2E_F, -gml));
   if (lo) {
 #pragma unroll
     for (int q4 = 0; q4 < 4; ++q4) *reinterpret_cast<f4*>(lo + 16 * (grp * 4 + q4)) = zz[q4];
