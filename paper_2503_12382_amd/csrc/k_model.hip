@@ -633,11 +633,15 @@ __global__ void __launch_bounds__(CONV_THREADS) k_conv(ConvArgs a) {
   using G = typename std::conditional<BF, GathB, Gath>::type;
   __shared__ __attribute__((aligned(16))) float s_w[WSZ];
   __shared__ __attribute__((aligned(16))) float s_h[HSZ];
-  __shared__ uint64_t s_par[FIRST ? CONV_WAVES : 1][16][8];  // per wave: parent cells (code<<32|first)
+  // per wave: parent cells (code<<32|first), rows padded to 9 so that the 16 voxels' cells lie in
+  // different banks
+  __shared__ uint64_t s_par[FIRST ? CONV_WAVES : 1][16][9];
   // per wave: the tile's neighbour rows, voxel by voxel (32 entries, the last 5 are -1), so that
-  // a lane reads the row of any offset directly (the last layer has no room for them)
-  constexpr bool ROWS = FIRST && !LAST;
-  __shared__ int32_t s_rows[ROWS ? CONV_WAVES : 1][16][32];
+  // a lane reads the row of any offset directly (the last layer has no room for them); rows
+  // padded to 36 words, so that the 16 voxels' entries of one offset lie in 16 different banks
+  constexpr bool ROWS = FIRST && !LAST && !BF;
+  constexpr int RW = 36;
+  __shared__ int32_t s_rows[ROWS ? CONV_WAVES : 1][16][RW];
   __shared__ int64_t s_tpre[NLEV + 1];
   __shared__ int64_t s_nv[NLEV];   // N_b of the launch's scales
   __shared__ int64_t s_mo[NLEV];   // first packed row of each scale
@@ -1238,7 +1242,7 @@ __global__ void __launch_bounds__(256) k_top_prep(int lo, int nsc, int n_embed, 
                                                   const float* __restrict__ emb_o, int32_t* __restrict__ nbr,
                                                   float* __restrict__ X) {
   constexpr int Q = C / 16;  // f4 per lane of a row
-  __shared__ uint64_t s_par[4][16][8];
+  __shared__ uint64_t s_par[4][16][9];  // rows padded: the 16 voxels' cells in different banks
   __shared__ int64_t s_n[32], s_mo[32], s_tpre[32];
   const int tid = threadIdx.x, w = tid >> 6, lane = tid & 63, r = lane & 15, g = lane >> 4;
   if (tid < nsc) {  // sizes of the launch's scales, loaded in parallel
