@@ -918,15 +918,32 @@ __global__ void __launch_bounds__(CONV_THREADS) k_conv(ConvArgs a) {
       G gA[PCH], gB[PCH];
       take(ksA);
       gather(ksA, gA);
-      while (true) {
-        take(ksB);
-        gather(ksB, gB);
-        mma(ksA, gA);
-        if (ksB[0] < 0) break;
-        take(ksA);
-        gather(ksA, gA);
-        mma(ksB, gB);
-        if (ksA[0] < 0) break;
+      if constexpr (FIRST) {
+        // fully unrolled (at most 27 offsets): straight-line code keeps the
+        // compiler's wait counts exact across the pipeline's stages
+        constexpr int ROUNDS = (27 + 2 * PCH - 1) / (2 * PCH);
+#pragma unroll
+        for (int it = 0; it < ROUNDS; ++it) {
+          take(ksB);
+          gather(ksB, gB);
+          mma(ksA, gA);
+          if (ksB[0] < 0) break;
+          take(ksA);
+          gather(ksA, gA);
+          mma(ksB, gB);
+          if (ksA[0] < 0) break;
+        }
+      } else {
+        while (true) {
+          take(ksB);
+          gather(ksB, gB);
+          mma(ksA, gA);
+          if (ksB[0] < 0) break;
+          take(ksA);
+          gather(ksA, gA);
+          mma(ksB, gB);
+          if (ksA[0] < 0) break;
+        }
       }
     }
     if (grp < 0) {
