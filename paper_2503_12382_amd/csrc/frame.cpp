@@ -76,6 +76,17 @@ hipError_t host_buf(Ctx& c, int i, size_t bytes) {
 
 int64_t base_words(int64_t n0, int b0) { return (n0 * (3 * b0 + 8) + 31) / 32; }
 
+// Once copies from the pinned staging buffers are enqueued, a call that
+// returns early still waits for its stream, so that the next call never
+// refills a staging buffer that a copy is still reading.
+struct DrainOnExit {
+  Ctx* c;
+  bool armed = false;
+  ~DrainOnExit() {
+    if (armed) (void)hipStreamSynchronize(c->stream);
+  }
+};
+
 }  // namespace
 
 void frame_free(Ctx& c) {
@@ -135,15 +146,20 @@ reno_status reno_encode_frame(reno_ctx* c, const float* points, int64_t n, int b
   FRAME_HIP(c, launch_rans_layout(*c, b0 + 1, B - 1, stages, L, B, lens, G, offs, words, cap_dev, total));
   FRAME_HIP(c, launch_rans_pack(*c, region, lens, offs, L, G, total, xyz, words, cap_dev));
   int64_t* tot_host = static_cast<int64_t*>(c->fc_host[H_AUX]);
+  DrainOnExit drain{c};
+  drain.armed = true;
   FRAME_HIP(c, hipMemcpyAsync(tot_host, total, 2 * sizeof(int64_t), hipMemcpyDeviceToHost, c->stream));
   FRAME_OK(reno_sync(c));
+  drain.armed = false;  // reno_sync waited for the stream
   const int64_t nw = tot_host[0];
   *nwords_host = nw;
   if (nw > cap_words) return frame_fail(c, RENO_E_CAPACITY, "bitstream exceeds cap_words");
   FRAME_HIP(c, host_buf(*c, H_WORDS, sizeof(uint32_t) * (size_t)nw));
+  drain.armed = true;
   FRAME_HIP(c, hipMemcpyAsync(c->fc_host[H_WORDS], words, sizeof(uint32_t) * (size_t)nw, hipMemcpyDeviceToHost,
                               c->stream));
   FRAME_HIP(c, hipStreamSynchronize(c->stream));
+  drain.armed = false;
   std::memcpy(out_host, c->fc_host[H_WORDS], sizeof(uint32_t) * (size_t)nw);
   return RENO_OK;
 }
@@ -208,6 +224,8 @@ reno_status reno_decode_frame(reno_ctx* c, const uint32_t* in_host, int64_t nwor
   uint32_t* tab = static_cast<uint32_t*>(c->fc_dev[D_TAB]);
   uint16_t* tab_scratch = reinterpret_cast<uint16_t*>(tab + (size_t)K * c->cap_pts);
   std::memcpy(c->fc_host[H_WORDS], in_host, sizeof(uint32_t) * (size_t)nwords);
+  DrainOnExit drain{c};
+  drain.armed = true;
   FRAME_HIP(c, hipMemcpyAsync(words_d, c->fc_host[H_WORDS], sizeof(uint32_t) * (size_t)nwords,
                               hipMemcpyHostToDevice, c->stream));
   if (n0 > 0) {
@@ -239,7 +257,9 @@ reno_status reno_decode_frame(reno_ctx* c, const uint32_t* in_host, int64_t nwor
     prev = code_d;
   }
   FRAME_OK(reno_expand(c, (int)B - 1, prev));
-  return reno_sync(c);
+  const reno_status st = reno_sync(c);
+  drain.armed = false;  // the stream has been waited for
+  return st;
 }
 
 }  // extern "C"
