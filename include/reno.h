@@ -358,7 +358,7 @@ reno_status reno_rans_decode_streams(const uint32_t* in, const int64_t* nwords_h
  * encode: points device float [n][3] as for reno_build_pyramid; builds the
  * pyramid, evaluates the model on every model scale, takes the symbol
  * intervals and codes each model scale (and each stage of the two-stage
- * head) as S = ceil(N_b / stream_symbols) interleaved streams, one GPU thread
+ * head) as S = ceil(N_b / stream_symbols) interleaved streams, one wavefront
  * per stream (1 <= stream_symbols <= 65533).  Copies the bitstream to the
  * HOST array out (at most cap_words words) and its length to *nwords_host
  * (also when it fails with RENO_E_CAPACITY because cap_words is too small).
@@ -373,8 +373,9 @@ reno_status reno_rans_decode_streams(const uint32_t* in, const int64_t* nwords_h
  * made with another min_bit_depth or head; RENO_E_CAPACITY when its frame
  * exceeds the context's capacities.
  * Both need min_bit_depth <= 8 and weights set, and synchronise the context
- * stream; device and pinned host staging is allocated by the first call that
- * needs it (and grown by later ones) and kept until reno_destroy.
+ * stream (also when they fail after enqueuing work); device and pinned host
+ * staging is allocated by the first call that needs it (and grown by later
+ * ones) and kept until reno_destroy.
  * Bitstream (uint32 words): 0x4F4E4552, B, b0, stages (1 or 2),
  * stream_symbols L, N_b0; the base voxels bit-packed from the lowest bit up
  * as fields x | y << b0 | z << 2 b0 | code << 3 b0 of 3 b0 + 8 bits, padded
