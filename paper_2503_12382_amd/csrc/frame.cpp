@@ -76,9 +76,9 @@ hipError_t host_buf(Ctx& c, int i, size_t bytes) {
 
 int64_t base_words(int64_t n0, int b0) { return (n0 * (3 * b0 + 8) + 31) / 32; }
 
-// Once copies from the pinned staging buffers are enqueued, a call that
-// returns early still waits for its stream, so that the next call never
-// refills a staging buffer that a copy is still reading.
+// Once a call has enqueued work (kernels, copies through the pinned staging
+// buffers), an early return still waits for its stream, so that the next
+// call never refills a staging buffer that a copy is still reading.
 struct DrainOnExit {
   Ctx* c;
   bool armed = false;
@@ -117,6 +117,8 @@ reno_status reno_encode_frame(reno_ctx* c, const float* points, int64_t n, int b
   const int b0 = c->b0();
   if (3 * b0 + 8 > 32) return frame_fail(c, RENO_E_INVALID, "frame coding needs min_bit_depth <= 8");
   if (!c->have_weights) return frame_fail(c, RENO_E_STATE, "no weights set");
+  DrainOnExit drain{c};
+  drain.armed = true;
   FRAME_OK(reno_build_pyramid(c, points, n, bit_depth));
   FRAME_OK(reno_predict_probs(c, RENO_ALL_SCALES, nullptr, nullptr));
   const int B = bit_depth;
@@ -146,8 +148,6 @@ reno_status reno_encode_frame(reno_ctx* c, const float* points, int64_t n, int b
   FRAME_HIP(c, launch_rans_layout(*c, b0 + 1, B - 1, stages, L, B, lens, G, offs, words, cap_dev, total));
   FRAME_HIP(c, launch_rans_pack(*c, region, lens, offs, L, G, total, xyz, words, cap_dev));
   int64_t* tot_host = static_cast<int64_t*>(c->fc_host[H_AUX]);
-  DrainOnExit drain{c};
-  drain.armed = true;
   FRAME_HIP(c, hipMemcpyAsync(tot_host, total, 2 * sizeof(int64_t), hipMemcpyDeviceToHost, c->stream));
   FRAME_OK(reno_sync(c));
   drain.armed = false;  // reno_sync waited for the stream
