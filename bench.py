@@ -621,7 +621,10 @@ def main():
                     help="frame-batch sizes K of the HBM stress pass (encoder stages on K frames in one key "
                          "space); empty to skip")
     ap.add_argument("--e2e-frames", type=int, default=20,
-                    help="frames for the end-to-end (GPU + host rANS) measurement (0 to skip)")
+                    help="frames for the end-to-end measurement through the whole-frame calls (0 to skip)")
+    ap.add_argument("--in-flight", default="1,2,3,4,8",
+                    help="frames in flight (host threads) for the end-to-end throughput measurement "
+                         "('' to skip)")
     ap.add_argument("--stream-config", default="stream10_hdl64_b14",
                     help="multi-frame workload measured with frames in flight on several streams")
     ap.add_argument("--streams", default="1,2,4",
@@ -868,8 +871,10 @@ def main():
         # decoder context on its own HIP stream, coding the streaming
         # workload's distinct scans; a frame's coder kernels occupy few CUs,
         # so frames overlap
-        e2e["frames_in_flight"] = e2e_in_flight(reno, torch, args, dev)
-        log("end-to-end frames in flight", e2e["frames_in_flight"])
+        workers = tuple(int(x) for x in args.in_flight.split(",") if x.strip())
+        if workers:
+            e2e["frames_in_flight"] = e2e_in_flight(reno, torch, args, dev, workers=workers)
+            log("end-to-end frames in flight", e2e["frames_in_flight"])
         e2e["note"] = ("wall-clock per frame through reno_encode_frame / reno_decode_frame: points copied in "
                        "from pinned host memory; GPU pyramid + model + symbol intervals + rANS streams "
                        f"(ceil(N_b / {STREAM_SYMBOLS}) streams per scale and stage, one wavefront each), bitstream "
