@@ -140,7 +140,7 @@ def test_dense_cube_neighbourhoods():
                  gen_weights(32, 3, seed=7, bias_std=0.1))
 
 
-@pytest.mark.parametrize("C,L", [(16, 1), (32, 1), (32, 4)])
+@pytest.mark.parametrize("C,L", [(16, 1), (32, 1), (32, 4), (16, 8), (32, 8)])  # L = 8: the most layers a context takes
 def test_other_model_shapes(C, L):
     rs = np.random.default_rng(C + L)
     B = 9
