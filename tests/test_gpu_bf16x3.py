@@ -52,7 +52,7 @@ def _logit_errors(ci, w, scan_cache, two=False):
     return out, T, float(np.abs(ref).max())
 
 
-@pytest.mark.parametrize("ci,head_scale", [(0, 1.0), (0, 10.0), (1, 1.0), (1, 10.0), (2, 1.0)])
+@pytest.mark.parametrize("ci,head_scale", [(0, 1.0), (0, 10.0), (1, 1.0), (1, 10.0), (2, 1.0), (3, 1.0)])
 def test_bf16x3_tolerance_one_stage(ci, head_scale, scan_cache):
     cfg = CONFIGS[ci]
     w = gen_weights(cfg.channels, cfg.layers, seed=cfg.weight_seed, bias_std=0.1, head_scale=head_scale)

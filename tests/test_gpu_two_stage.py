@@ -36,7 +36,7 @@ def _encode(cfg, pts, w):
     return ctx, lg.cpu().numpy(), bits.cpu().numpy(), total
 
 
-@pytest.mark.parametrize("ci,head_scale", [(0, 1.0), (0, 10.0), (1, 1.0), (2, 1.0)])
+@pytest.mark.parametrize("ci,head_scale", [(0, 1.0), (0, 10.0), (1, 1.0), (2, 1.0), (3, 1.0)])
 def test_two_stage_encoder_matches_oracle(ci, head_scale, scan_cache):
     cfg = CONFIGS[ci]
     B, b0 = cfg.bit_depth, cfg.min_bit_depth
