@@ -9,7 +9,8 @@ codes of that stream's voxels under the encoder context's frequency tables
 rebuilds the frame from the bitstream alone: every scale's codes and V_B equal
 the oracle's.  Malformed bitstreams are rejected with RENO_E_INPUT and leave
 the context usable; an empty frame and a frame without model scales
-round-trip; stream lengths from one symbol per stream to the 16-bit limit."""
+round-trip; stream lengths from one symbol per stream to the 16-bit limit; scans up to
+the 16-bit dense one."""
 import numpy as np
 import pytest
 import torch
@@ -64,7 +65,8 @@ def _pad256(f16):
 
 
 @pytest.mark.parametrize("ci,two,L", [(0, False, 1024), (0, True, 1024), (0, False, 1), (0, True, 37),
-                                      (0, False, 65533), (2, False, 1024), (2, True, 1024), (2, False, 4096)])
+                                      (0, False, 65533), (2, False, 1024), (2, True, 1024), (2, False, 4096),
+                                      (3, False, 1024), (3, True, 1024)])
 def test_frame_bitstream_is_the_oracles_and_decodes(ci, two, L, scan_cache):
     cfg = CONFIGS[ci]
     B, b0 = cfg.bit_depth, cfg.min_bit_depth
