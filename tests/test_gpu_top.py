@@ -58,7 +58,8 @@ def _check_against_oracle(pts, B, b0, R, C, w, two):
     ctx.close()
 
 
-@pytest.mark.parametrize("ci,two", [(0, False), (0, True), (1, False), (1, True), (2, False), (2, True)])
+@pytest.mark.parametrize("ci,two", [(0, False), (0, True), (1, False), (1, True), (2, False), (2, True),
+                                    (3, False), (3, True)])
 def test_top_encoder_matches_oracle(ci, two, scan_cache):
     cfg = CONFIGS[ci]
     pts = scan_cache(ci)
