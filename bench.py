@@ -52,13 +52,17 @@ def alg_bytes_per_frame(counts, b0, B, M, C, hash_slots, status_words):
     passes = (3 * B + 7) // 8
     row = 4 * C
     out = {}
-    out["zero"] = 2 * (16 * hash_slots + 4 * status_words)
+    clear = 16 * hash_slots + 4 * status_words
+    # the decoder clears its frame in the launch that writes a base scale of
+    # fewer than 256 voxels (one block), else in a launch of its own
+    dec_clear_in_base = N[b0] < 256
+    out["zero"] = clear * (1 if dec_clear_in_base else 2)
     out["quantize"] = M * (12 + 8)
     out["sort"] = passes * M * 16
     out["pyramid"] = M * 8 + sum(N[b] * 12 for b in range(b0, B + 1)) + sum(N[b] * 4 for b in range(b0, B))
     # codes: child keys read, codes + child feature words written, parents hashed
     out["codes"] = sum(N[b + 1] * (8 + 2) + N[b] for b in range(b0, B)) + 16 * parents_hashed
-    out["set_base"] = N[b0] * (12 + 1 + 8)
+    out["set_base"] = N[b0] * (12 + 1 + 8) + (clear if dec_clear_in_base else 0)
     # expand: parent key + code read; child key, parent row, feature word and the
     # parent's first-child row written; parents hashed
     out["expand"] = sum(N[b] * (8 + 1 + 4) + N[b + 1] * (8 + 4 + 2) for b in range(b0, B)) + \

@@ -96,15 +96,10 @@ reno_status sync_check(Ctx* c) {
 
 // Zeroes the per-frame counters, tickets, look-back state and hash.
 reno_status frame_init(Ctx* c) {
-  void* p[8] = {c->d_err, c->d_count, c->d_moff, c->d_hist, c->d_ticket, c->d_status, c->d_hash};
-  size_t n[8] = {16,
-                 sizeof(int32_t) * reno::NLEV,
-                 sizeof(int32_t) * (reno::NLEV + 1),
-                 sizeof(uint32_t) * reno::MAX_PASSES * reno::RADIX,
-                 sizeof(uint32_t) * reno::TICKETS,
-                 sizeof(uint32_t) * (size_t)c->status_words,
-                 sizeof(reno::HashSlot) << c->hash_lg};
-  RENO_HIP(c, reno::launch_zero(*c, p, n, 7));
+  void* p[8];
+  size_t n[8];
+  const int k = reno::frame_clear(*c, p, n);
+  RENO_HIP(c, reno::launch_zero(*c, p, n, k));
   return RENO_OK;
 }
 
@@ -380,6 +375,10 @@ reno_status reno_set_base_frames(reno_ctx* c, int bit_depth, const int32_t* xyz,
   c->have_codes = 1u << c->b0();
   c->have_pred = 0;
   c->have_pred2 = 0;
+  if (reno::clear_set_base_fits(n)) {  // a small base scale: the clear and the base scale in one launch
+    RENO_HIP(c, reno::launch_clear_set_base(*c, xyz, frames > 1 ? frame_of : nullptr, codes, n));
+    return RENO_OK;
+  }
   reno_status s = frame_init(c);
   if (s != RENO_OK) return s;
   RENO_HIP(c, reno::launch_set_base(*c, xyz, frames > 1 ? frame_of : nullptr, codes, n, bit_depth));

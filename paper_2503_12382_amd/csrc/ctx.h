@@ -210,6 +210,31 @@ hipError_t launch_pyramid(Ctx& c, const uint64_t* sorted, int64_t n, int B);
 hipError_t launch_codes(Ctx& c, int B);
 hipError_t launch_set_base(Ctx& c, const int32_t* xyz, const int32_t* frame_of, const uint8_t* codes, int64_t n,
                            int B);
+// What a new frame clears, as (pointer, bytes) pairs: first the error word,
+// the scale counts and the row offsets (CLEAR_SMALL entries, which the
+// base-scale kernels write next), then histograms, tickets, look-back status
+// and the hash.  Returns the number of entries (at most 8).
+constexpr int CLEAR_SMALL = 3;
+inline int frame_clear(const Ctx& c, void** ptr, size_t* bytes) {
+  void* const p_[7] = {c.d_err, c.d_count, c.d_moff, c.d_hist, c.d_ticket, c.d_status, c.d_hash};
+  const size_t n_[7] = {16,
+                        sizeof(int32_t) * NLEV,
+                        sizeof(int32_t) * (NLEV + 1),
+                        sizeof(uint32_t) * MAX_PASSES * RADIX,
+                        sizeof(uint32_t) * TICKETS,
+                        sizeof(uint32_t) * (size_t)c.status_words,
+                        sizeof(HashSlot) << c.hash_lg};
+  for (int i = 0; i < 7; ++i) {
+    ptr[i] = p_[i];
+    bytes[i] = n_[i];
+  }
+  return 7;
+}
+// The frame's clear and the base scale in one launch, for a base scale of
+// fewer than 256 voxels (clear_set_base_fits).
+bool clear_set_base_fits(int64_t n);
+hipError_t launch_clear_set_base(Ctx& c, const int32_t* xyz, const int32_t* frame_of, const uint8_t* codes,
+                                 int64_t n);
 hipError_t launch_expand(Ctx& c, int b, const uint8_t* codes, int B);
 hipError_t launch_expand_noalloc(const uint64_t* keys, const uint8_t* codes, int64_t n,
                                  uint64_t* child_keys, int32_t* child_parent, int64_t cap_children,

@@ -14,66 +14,114 @@ namespace {
 
 // Scale b0 from int32 xyz and codes, strictly ascending in (frame, Morton)
 // order; a frame batch gives each voxel's frame id (key f << 3b0 | Morton).
-__global__ void __launch_bounds__(256) k_set_base(const int32_t* __restrict__ xyz,
-                                                  const int32_t* __restrict__ frame_of, int frames,
-                                                  const uint8_t* __restrict__ codes, int64_t n,
-                                                  int b0, uint64_t* __restrict__ key,
-                                                  uint8_t* __restrict__ code,
-                                                  int32_t* __restrict__ parent, int32_t* count,
-                                                  int32_t* moff, uint64_t* __restrict__ hreg, int hash_lg,
-                                                  uint32_t* err) {
-  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+struct BaseArgs {
+  const int32_t* xyz;
+  const int32_t* frame_of;  // null: one frame
+  int frames;
+  const uint8_t* codes;
+  int64_t n;
+  int b0;
+  uint64_t* key;
+  uint8_t* code;
+  int32_t* parent;
+  int32_t* count;
+  int32_t* moff;
+  uint64_t* hreg;
+  int hash_lg;
+  uint32_t* err;
+};
+
+// Thread i of the base scale: voxel i for i < n; i == n closes the hash
+// region table of a frame batch.
+__device__ __forceinline__ void set_base_voxel(const BaseArgs& a, int64_t i) {
+  const int64_t n = a.n;
+  const int b0 = a.b0;
   if (i == 0) {
-    count[b0] = (int32_t)n;
-    moff[b0 + 1] = 0;
+    a.count[b0] = (int32_t)n;
+    a.moff[b0 + 1] = 0;
   }
   // hash regions of a frame batch in proportion to each frame's base voxels:
   // the thread of the first voxel of a frame (ids ascending; out-of-range ids
   // clamped, they are latched below) writes the starts of the frames since
   // the previous voxel's frame
-  if (frame_of && i <= n) {
-    const uint64_t T = 1ull << hash_lg;
+  if (a.frame_of && i <= n) {
+    const uint64_t T = 1ull << a.hash_lg;
     auto fid = [&](int64_t j) {
-      const int32_t f = frame_of[j];
-      return f < 0 ? 0 : (f >= frames ? frames - 1 : f);
+      const int32_t f = a.frame_of[j];
+      return f < 0 ? 0 : (f >= a.frames ? a.frames - 1 : f);
     };
-    const int f_hi = i < n ? fid(i) : frames;            // frames f_lo+1 .. f_hi start at voxel i
+    const int f_hi = i < n ? fid(i) : a.frames;          // frames f_lo+1 .. f_hi start at voxel i
     const int f_lo = i > 0 ? fid(i - 1) : -1;
     const uint64_t st = n > 0 ? (uint64_t)i * T / (uint64_t)n : 0ull;
-    for (int f = f_lo + 1; f <= f_hi; ++f) hreg[f] = f == frames ? T : st;
+    for (int f = f_lo + 1; f <= f_hi; ++f) a.hreg[f] = f == a.frames ? T : st;
   }
   if (i >= n) return;
   const int32_t lim = 1 << b0;
   uint32_t q[3], qp[3];
   bool range_ok = true;
-  for (int a = 0; a < 3; ++a) {
-    const int32_t v = xyz[3 * i + a];
+  for (int ax = 0; ax < 3; ++ax) {
+    const int32_t v = a.xyz[3 * i + ax];
     range_ok = range_ok && v >= 0 && v < lim;
-    q[a] = (uint32_t)v & (uint32_t)(lim - 1);
+    q[ax] = (uint32_t)v & (uint32_t)(lim - 1);
   }
-  if (!range_ok) latch(err, ERR_BASE_RANGE);
+  if (!range_ok) latch(a.err, ERR_BASE_RANGE);
   int32_t f = 0, fp = 0;
-  if (frame_of) {
-    f = frame_of[i];
-    if (f < 0 || f >= frames) {
-      latch(err, ERR_FRAMES);
+  if (a.frame_of) {
+    f = a.frame_of[i];
+    if (f < 0 || f >= a.frames) {
+      latch(a.err, ERR_FRAMES);
       f = 0;
     }
     if (i > 0) {
-      fp = frame_of[i - 1];
-      fp = (fp < 0 || fp >= frames) ? 0 : fp;
+      fp = a.frame_of[i - 1];
+      fp = (fp < 0 || fp >= a.frames) ? 0 : fp;
     }
   }
   const uint64_t k = morton3(q[0], q[1], q[2]) | ((uint64_t)f << (3 * b0));
   if (i > 0) {
-    for (int a = 0; a < 3; ++a) qp[a] = (uint32_t)xyz[3 * (i - 1) + a] & (uint32_t)(lim - 1);
-    if ((morton3(qp[0], qp[1], qp[2]) | ((uint64_t)fp << (3 * b0))) >= k) latch(err, ERR_BASE_ORDER);
+    for (int ax = 0; ax < 3; ++ax) qp[ax] = (uint32_t)a.xyz[3 * (i - 1) + ax] & (uint32_t)(lim - 1);
+    if ((morton3(qp[0], qp[1], qp[2]) | ((uint64_t)fp << (3 * b0))) >= k) latch(a.err, ERR_BASE_ORDER);
   }
-  const uint8_t c = codes[i];
-  if (c == 0) latch(err, ERR_ZERO_CODE);
-  key[i] = k;
-  code[i] = c;
-  parent[i] = -1;
+  const uint8_t c = a.codes[i];
+  if (c == 0) latch(a.err, ERR_ZERO_CODE);
+  a.key[i] = k;
+  a.code[i] = c;
+  a.parent[i] = -1;
+}
+
+__global__ void __launch_bounds__(256) k_set_base(BaseArgs a) {
+  set_base_voxel(a, (int64_t)blockIdx.x * blockDim.x + threadIdx.x);
+}
+
+// A new decoder frame whose base scale fits one block (n < 256): the frame's
+// clear and the base scale in one launch.  Every block zeroes its share of
+// the large ranges; block 0 alone clears the error word, the scale counts and
+// the row offsets and then, after a barrier, writes the base scale (which
+// sets a count and an offset and may latch errors), so no other block touches
+// a word that block 0 writes.
+constexpr int BASE_ONE_BLOCK = 256;
+struct ClearBaseArgs {
+  uint4* p[8];        // ranges every block zeroes
+  uint64_t n16[8];
+  int n;
+  uint4* s[CLEAR_SMALL];  // ranges block 0 zeroes before the base scale
+  uint32_t s16[CLEAR_SMALL];
+  BaseArgs base;
+};
+
+__global__ void __launch_bounds__(BASE_ONE_BLOCK) k_clear_set_base(ClearBaseArgs a) {
+  const uint64_t stride = (uint64_t)gridDim.x * blockDim.x;
+  const uint64_t g = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  for (int r = 0; r < a.n; ++r) {
+    uint4* p = a.p[r];
+    const uint64_t n = a.n16[r];
+    for (uint64_t i = g; i < n; i += stride) p[i] = make_uint4(0u, 0u, 0u, 0u);
+  }
+  if (blockIdx.x != 0) return;
+  for (int r = 0; r < CLEAR_SMALL; ++r)
+    for (uint32_t i = threadIdx.x; i < a.s16[r]; i += blockDim.x) a.s[r][i] = make_uint4(0u, 0u, 0u, 0u);
+  __syncthreads();
+  set_base_voxel(a.base, threadIdx.x);
 }
 
 struct ExpArgs {
@@ -311,16 +359,49 @@ hipError_t launch_expand_noalloc(const uint64_t* keys, const uint8_t* codes, int
   return hipGetLastError();
 }
 
+BaseArgs base_args(Ctx& c, const int32_t* xyz, const int32_t* frame_of, const uint8_t* codes, int64_t n) {
+  const int b0 = c.b0();
+  return BaseArgs{xyz, frame_of, c.frames, codes, n, b0, c.lv_key + c.lv(b0), c.lv_code + c.lv(b0),
+                  c.lv_parent + c.lv(b0), c.d_count, c.d_moff, c.d_hreg, c.hash_lg, c.d_err};
+}
+
 hipError_t launch_set_base(Ctx& c, const int32_t* xyz, const int32_t* frame_of, const uint8_t* codes, int64_t n,
                            int B) {
   ProfScope ps_(c, RENO_K_SET_BASE);
   (void)B;
-  const int b0 = c.b0();
   int64_t blocks = (n + 1 + 255) / 256;   // thread n closes the hash region table
   if (blocks < 1) blocks = 1;
-  hipLaunchKernelGGL(k_set_base, dim3((unsigned)blocks), dim3(256), 0, c.stream, xyz, frame_of, c.frames, codes, n, b0,
-                     c.lv_key + c.lv(b0), c.lv_code + c.lv(b0), c.lv_parent + c.lv(b0), c.d_count,
-                     c.d_moff, c.d_hreg, c.hash_lg, c.d_err);
+  hipLaunchKernelGGL(k_set_base, dim3((unsigned)blocks), dim3(256), 0, c.stream,
+                     base_args(c, xyz, frame_of, codes, n));
+  return hipGetLastError();
+}
+
+bool clear_set_base_fits(int64_t n) { return n >= 0 && n < BASE_ONE_BLOCK; }
+
+hipError_t launch_clear_set_base(Ctx& c, const int32_t* xyz, const int32_t* frame_of, const uint8_t* codes,
+                                 int64_t n) {
+  if (!clear_set_base_fits(n)) return hipErrorInvalidValue;
+  ProfScope ps_(c, RENO_K_SET_BASE);
+  void* ptr[8];
+  size_t bytes[8];
+  const int k = frame_clear(c, ptr, bytes);
+  ClearBaseArgs a{};
+  uint64_t most = 0;
+  for (int i = 0; i < CLEAR_SMALL; ++i) {
+    a.s[i] = static_cast<uint4*>(ptr[i]);
+    a.s16[i] = (uint32_t)((bytes[i] + 15) / 16);
+  }
+  a.n = 0;
+  for (int i = CLEAR_SMALL; i < k && a.n < 8; ++i, ++a.n) {
+    a.p[a.n] = static_cast<uint4*>(ptr[i]);
+    a.n16[a.n] = (bytes[i] + 15) / 16;
+    if (a.n16[a.n] > most) most = a.n16[a.n];
+  }
+  a.base = base_args(c, xyz, frame_of, codes, n);
+  uint64_t blocks = (most + BASE_ONE_BLOCK - 1) / BASE_ONE_BLOCK;
+  if (blocks > 2048) blocks = 2048;
+  if (blocks < 1) blocks = 1;
+  hipLaunchKernelGGL(k_clear_set_base, dim3((unsigned)blocks), dim3(BASE_ONE_BLOCK), 0, c.stream, a);
   return hipGetLastError();
 }
 
