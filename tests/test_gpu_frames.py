@@ -104,14 +104,12 @@ def test_frame_batch_encoder_matches_oracle_per_frame(ci, scan_cache):
     ctx.close()
 
 
-@pytest.mark.parametrize("two,top", [(False, False), (True, False), (False, True)])
-def test_frame_batch_decoder_bit_identical(two, top, scan_cache):
-    cfg = CONFIGS[1]
+def _decoder_round(cfg, frames, two, top):
+    """Batched encoder, then the batched decoder from its base scale and codes:
+    every logit, bit, total and scale identical.  Returns the base-scale count."""
     B, b0 = cfg.bit_depth, cfg.min_bit_depth
-    frames = _frames(scan_cache(1))
     pts, start = _batch(frames)
     w = gen_weights(cfg.channels, cfg.layers, seed=cfg.weight_seed + 9, bias_std=0.1, two_stage=two, top=top)
-    say("frame batch decoder two-stage", two, "full predictor", top)
     enc = _ctx(cfg, len(pts), two_stage=two, top=top)
     enc.set_weights(reno.weights_to_device(w))
     enc.build_pyramid_frames(to_dev(pts), to_dev(start), B)
@@ -144,6 +142,34 @@ def test_frame_batch_decoder_bit_identical(two, top, scan_cache):
         np.testing.assert_array_equal(dec.coords(b)[1].cpu().numpy(), enc.coords(b)[1].cpu().numpy())
     enc.close()
     dec.close()
+    return counts[b0]
+
+
+@pytest.mark.parametrize("two,top", [(False, False), (True, False), (False, True)])
+def test_frame_batch_decoder_bit_identical(two, top, scan_cache):
+    say("frame batch decoder two-stage", two, "full predictor", top)
+    _decoder_round(CONFIGS[1], _frames(scan_cache(1)), two, top)
+
+
+@pytest.mark.parametrize("small", [True, False])
+def test_frame_batch_decoder_base_paths(small, scan_cache):
+    """A batch whose base scale has fewer than 256 voxels in all (the decoder
+    clears its frame and writes the base scale, hash regions included, in one
+    launch) and one with more (a clear, then the base-scale kernel)."""
+    scan = scan_cache(0)
+    if small:
+        f1 = scan[:300].copy()
+        f1[:, 1] += np.float32(2.0)
+        frames = [scan[:300], f1, scan[:0], scan[:40]]
+    else:
+        frames = []
+        for k in range(4):
+            f = scan.copy()
+            f[:, 0] += np.float32(0.7 * k)
+            frames.append(f)
+    say("frame batch decoder, base scale", "small" if small else "large")
+    n0 = _decoder_round(CONFIGS[0], frames, False, False)
+    assert (0 < n0 < 256) if small else n0 >= 256, n0
 
 
 def test_frame_batch_errors(scan_cache):
