@@ -239,9 +239,9 @@ reno_status reno_create(const reno_params* p, void* hip_stream, reno_ctx** out) 
     delete c;
     return fail(nullptr, e == hipErrorOutOfMemory ? RENO_E_NOMEM : RENO_E_HIP, msg);
   }
-  // reduction done-counters start at zero and reset themselves after use; the
-  // reserved zero row of each feature buffer and the zero input-bit entry are
-  // never written afterwards
+  // tickets start at zero (every frame clears them again); the reserved zero
+  // row of each feature buffer and the zero input-bit entry are never written
+  // afterwards
   e = hipMemsetAsync(c->d_ticket, 0, sizeof(uint32_t) * reno::TICKETS, c->stream);
   if (e == hipSuccess)
     e = hipMemsetAsync(c->h_a + (size_t)cap_model * C, 0, sizeof(float) * C, c->stream);

@@ -38,7 +38,6 @@ constexpr int NBR_STRIDE = 32;                  // neighbour-map row: 27 offsets
 constexpr int TK_SORT = 0;        // + pass
 constexpr int TK_PYR = 16;
 constexpr int TK_EXPAND = 17;     // + scale (decoder: one per expand call)
-constexpr int TK_RED = 40;        // + scale slot (reduction done-counters, self-resetting)
 
 struct ProfRec {
   int kind;
