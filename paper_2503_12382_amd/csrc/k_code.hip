@@ -31,7 +31,6 @@ constexpr int kDecWaves = 4;           // decoder: wavefronts (streams) per work
 constexpr int kLayThreads = 1024;
 
 __device__ __forceinline__ int64_t streams_of(int64_t n, int L) { return n > 0 ? (n + L - 1) / L : 1; }
-__device__ __forceinline__ int64_t nonneg(int64_t v) { return v > 0 ? v : 0; }
 
 // Section t and stream j of global stream index g (sections in bitstream
 // order: scale b_lo first, stages inner); false past the last stream.
@@ -66,9 +65,6 @@ struct EncArgs {
 __device__ __forceinline__ uint32_t rfl(uint32_t v) { return (uint32_t)__builtin_amdgcn_readfirstlane((int)v); }
 __device__ __forceinline__ uint32_t rdl(uint32_t v, int lane) {
   return (uint32_t)__builtin_amdgcn_readlane((int)v, lane);
-}
-__device__ __forceinline__ int64_t opaque(int64_t v) {
-  return (int64_t)(((uint64_t)rfl((uint32_t)((uint64_t)v >> 32)) << 32) | rfl((uint32_t)v));
 }
 
 // v into lane `at` of a register whose other lanes keep old (at uniform)
@@ -370,8 +366,8 @@ __device__ __forceinline__ Table<K> load_table(const uint32_t* tab, int64_t i, i
 // <= slot" names the lane holding s (starts ascend across the lanes), and
 // two lane reads bring that lane's pick out.
 template <int K>
-__device__ __forceinline__ void find_symbol(const Table<K>& tb, uint32_t slot, int lane, uint32_t* sym,
-                                            uint32_t* lo_s, uint32_t* f_s) {
+__device__ __forceinline__ void find_symbol(const Table<K>& tb, uint32_t slot, uint32_t* sym, uint32_t* lo_s,
+                                            uint32_t* f_s) {
   if constexpr (K == 256) {
     const bool c1 = (tb.e[1] & 0xFFFFu) <= slot, c2 = (tb.e[2] & 0xFFFFu) <= slot,
                c3 = (tb.e[3] & 0xFFFFu) <= slot;
@@ -495,7 +491,7 @@ __global__ void __launch_bounds__(64 * kDecWaves) k_rans_decode(DecArgs a, const
       if (!GUARD || k0 + u < m) {
         const uint32_t slot = (uint32_t)x & ((1u << kProb) - 1u);
         uint32_t sym, lo_s, f_s;
-        find_symbol<K>(cur, slot, lane, &sym, &lo_s, &f_s);
+        find_symbol<K>(cur, slot, &sym, &lo_s, &f_s);
         x = (uint64_t)f_s * (x >> kProb) + slot - lo_s;
         if ((uint32_t)(x >> 31) == 0) {  // x < 2^31 (x < 2^63 always)
           const int q = p - wb;          // below 128 inside a trip
