@@ -6,7 +6,7 @@ a spinning multi-beam sensor over a ground plane with boxes and poles.
 """
 from __future__ import annotations
 
-from dataclasses import dataclass, field
+from dataclasses import dataclass
 
 
 @dataclass(frozen=True)

@@ -1,12 +1,12 @@
-"""Shared drivers for the GPU tests: run the HIP path through the C ABI and the
-oracle on the same seeded inputs.  Every GPU step prints what it runs first."""
+"""Shared drivers for the GPU tests: run the HIP path through the C ABI on the
+seeded inputs the tests also hand to the oracle, and compare levels with it.
+Every GPU step prints what it runs first."""
 from __future__ import annotations
 
 import sys
 
 import numpy as np
 
-import oracle
 import paper_2503_12382_amd as reno
 
 LOGIT_TOL = 1e-3         # absolute, fp32 path vs fp64 oracle

@@ -2,7 +2,6 @@
 frames, each with its own encoder and decoder context on its own stream,
 interleaved call by call and replayed as HIP graphs, give bit-identical totals
 to running them one after the other, and the decoders match the encoders."""
-import numpy as np
 import pytest
 import torch
 
